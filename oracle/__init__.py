@@ -1,0 +1,215 @@
+"""fp64 CPU oracle for the Gorila DQN learner step.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  The product path
+(the HIP library and its binding) never imports, links or calls it, and the
+oracle shares no code with it.
+
+The arithmetic lives in ``gorila_oracle.c`` (plain C, fp64, OpenMP over
+samples); this module only marshals numpy arrays through ctypes.  Each function
+cites the passage of Nair et al. 2015 it follows; the readings used where the
+paper is silent are listed at the top of the C source.
+
+Pins: every function here is pinned by tests in ``tests/test_oracle_*.py``
+(finite differences, closed forms, a hand-enumerated replay-ring fixture, a
+published SplitMix64 output, torch fp64 convolutions as a library special
+case, batch invariants).  The whole learner step at full size has no value
+printed in the paper to compare against: beyond those pins it is parity
+unpinned.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from dataclasses import dataclass
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "gorila_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP, no BLAS)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
+             "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Net(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "in_c", "in_h", "in_w", "c1", "k1", "s1", "c2", "k2", "s2",
+        "c3", "k3", "s3", "hidden", "n_actions")]
+
+
+@dataclass(frozen=True)
+class Net:
+    """Q-network topology (Section 4.1: 84x84x4 input, conv 32@8x8/4,
+    conv 64@4x4/2, conv 64@3x3/1, FC 512, linear FC with one unit per action).
+    Tiny topologies exist only for finite-difference tests."""
+    in_c: int = 4
+    in_h: int = 84
+    in_w: int = 84
+    c1: int = 32
+    k1: int = 8
+    s1: int = 4
+    c2: int = 64
+    k2: int = 4
+    s2: int = 2
+    c3: int = 64
+    k3: int = 3
+    s3: int = 1
+    hidden: int = 512
+    n_actions: int = 18
+
+    def c(self) -> _Net:
+        return _Net(*[getattr(self, name) for name, _ in _Net._fields_])
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.POINTER
+        net_p = P(_Net)
+        dp, u8p, i32p, i64p, f32p = (ctypes.c_void_p,) * 5
+        L.oracle_param_count.argtypes = [net_p]
+        L.oracle_param_count.restype = ctypes.c_int64
+        L.oracle_param_offsets.argtypes = [net_p, i64p]
+        L.oracle_num_threads.restype = ctypes.c_int
+        L.oracle_q_forward.argtypes = [net_p, dp, u8p, ctypes.c_int32, dp]
+        L.oracle_act.argtypes = [net_p, dp, u8p, ctypes.c_int32, ctypes.c_double,
+                                 ctypes.c_uint64, i32p, dp]
+        L.oracle_learner_step.argtypes = [
+            net_p, dp, dp, u8p, u8p, i32p, dp, u8p, ctypes.c_int32,
+            ctypes.c_double, ctypes.c_double, dp, dp, dp, dp]
+        L.oracle_gather.argtypes = [
+            u8p, u8p, i32p, f32p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
+            ctypes.c_int64, i64p, ctypes.c_int32, u8p, u8p, i64p, i32p, f32p, u8p]
+        for f in ("oracle_param_offsets", "oracle_q_forward", "oracle_act",
+                  "oracle_learner_step", "oracle_gather"):
+            getattr(L, f).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray | None):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"]
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _c(a, dtype) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise ValueError(f"{what}: oracle rejected the arguments (rc={rc})")
+
+
+def param_count(net: Net) -> int:
+    """Length of the flat parameter vector (layout in gorila_oracle.h)."""
+    return int(lib().oracle_param_count(ctypes.byref(net.c())))
+
+
+def param_offsets(net: Net) -> list[int]:
+    """Offsets of W1,b1,W2,b2,W3,b3,W4,b4,W5,b5 and the total."""
+    off = np.zeros(11, np.int64)
+    _check(lib().oracle_param_offsets(ctypes.byref(net.c()), _ptr(off)), "param_offsets")
+    return [int(x) for x in off]
+
+
+def num_threads() -> int:
+    return int(lib().oracle_num_threads())
+
+
+def q_forward(net: Net, theta, states) -> np.ndarray:
+    """Q(s, .; theta) for a batch of uint8 states (Section 4.1 network)."""
+    theta = _c(theta, np.float64)
+    states = _c(states, np.uint8)
+    n = states.shape[0]
+    q = np.zeros((n, net.n_actions), np.float64)
+    _check(lib().oracle_q_forward(ctypes.byref(net.c()), _ptr(theta), _ptr(states),
+                                  n, _ptr(q)), "q_forward")
+    return q
+
+
+def act(net: Net, theta, states, eps: float, seed: int):
+    """epsilon-greedy behaviour (Algorithm 1); returns (actions i32, Q f64).
+    eps is taken as a float32 value promoted exactly to fp64."""
+    theta = _c(theta, np.float64)
+    states = _c(states, np.uint8)
+    n = states.shape[0]
+    acts = np.zeros(n, np.int32)
+    q = np.zeros((n, net.n_actions), np.float64)
+    _check(lib().oracle_act(ctypes.byref(net.c()), _ptr(theta), _ptr(states), n,
+                            float(np.float32(eps)), ctypes.c_uint64(seed & (2**64 - 1)),
+                            _ptr(acts), _ptr(q)), "act")
+    return acts, q
+
+
+def learner_step(net: Net, theta, theta_target, s, s2, a, r, term, gamma: float,
+                 clip: float = 1.0):
+    """DQN loss (eq. (1)) and its gradient (eq. (2)) on one minibatch.
+
+    Returns dict(grads [P] f64, loss f64, q [B,A], q2 [B,A]).  gamma, r and clip
+    are float32 values promoted exactly to fp64 (clip may be +inf)."""
+    theta = _c(theta, np.float64)
+    theta_target = _c(theta_target, np.float64)
+    s = _c(s, np.uint8)
+    s2 = _c(s2, np.uint8)
+    a = _c(a, np.int32)
+    r = _c(np.asarray(r, np.float32), np.float64)
+    term = _c(term, np.uint8)
+    B = s.shape[0]
+    P = param_count(net)
+    grads = np.zeros(P, np.float64)
+    loss = np.zeros(1, np.float64)
+    q = np.zeros((B, net.n_actions), np.float64)
+    q2 = np.zeros((B, net.n_actions), np.float64)
+    _check(lib().oracle_learner_step(
+        ctypes.byref(net.c()), _ptr(theta), _ptr(theta_target), _ptr(s), _ptr(s2),
+        _ptr(a), _ptr(r), _ptr(term), B, float(np.float32(gamma)),
+        float(np.float32(clip)), _ptr(grads), _ptr(loss), _ptr(q), _ptr(q2)),
+        "learner_step")
+    return dict(grads=grads, loss=float(loss[0]), q=q, q2=q2)
+
+
+def gather(frames, ep_start, action, reward, head: int, idx, hist: int = 4):
+    """Frame stacking out of the replay ring (Section 3 replay memory,
+    Section 4.1 four-frame input).  frames is [capacity, ...] uint8.
+
+    Returns dict(s, s2 [n, hist, ...] u8, frame_map [n, 2, hist] i64,
+    a i32, r f32, term u8)."""
+    frames = np.asarray(frames)
+    assert frames.dtype == np.uint8 and frames.flags["C_CONTIGUOUS"]
+    cap = frames.shape[0]
+    fshape = frames.shape[1:]
+    fbytes = int(np.prod(fshape)) if fshape else 1
+    ep_start = _c(ep_start, np.uint8)
+    action = _c(action, np.int32)
+    reward = _c(reward, np.float32)
+    idx = _c(idx, np.int64)
+    n = idx.shape[0]
+    s = np.zeros((n, hist) + fshape, np.uint8)
+    s2 = np.zeros((n, hist) + fshape, np.uint8)
+    fmap = np.zeros((n, 2, hist), np.int64)
+    a = np.zeros(n, np.int32)
+    r = np.zeros(n, np.float32)
+    t = np.zeros(n, np.uint8)
+    _check(lib().oracle_gather(_ptr(frames), _ptr(ep_start), _ptr(action), _ptr(reward),
+                               cap, head, hist, fbytes, _ptr(idx), n, _ptr(s), _ptr(s2),
+                               _ptr(fmap), _ptr(a), _ptr(r), _ptr(t)), "gather")
+    return dict(s=s, s2=s2, frame_map=fmap, a=a, r=r, term=t)

@@ -1,0 +1,95 @@
+/*
+ * Gorila DQN learner step -- plain fp64 CPU oracle (declarations).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may include, link
+ * or call this code: only the tests, the package smoke check and the CPU
+ * baseline leg of the benchmark use it.  It shares no code with the HIP
+ * library (this header is the oracle's own, written independently of
+ * include/gorila.h).
+ *
+ * What it computes (Nair et al. 2015, "Massively Parallel Methods for Deep
+ * Reinforcement Learning"):
+ *   - the Q-network of the experimental set-up section (three convolutions,
+ *     a 512-unit fully connected layer, a linear action head, ReLU after
+ *     every hidden layer), here with a configurable topology so that tiny
+ *     networks can be finite-differenced;
+ *   - the DQN loss of eq. (1) and its gradient, eq. (2), with the terminal
+ *     case of Algorithm 1 and a Huber/clipped TD error (clip = +inf gives
+ *     eq. (1) exactly);
+ *   - the epsilon-greedy behaviour policy of Algorithm 1;
+ *   - frame stacking of the four most recent frames out of a replay ring.
+ *
+ * All arithmetic is IEEE fp64.  Every entry point returns 0 on success and
+ * a negative value on a bad argument (nothing is written in that case).
+ */
+#ifndef GORILA_ORACLE_H
+#define GORILA_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Network topology.  Input is in_c x in_h x in_w uint8, scaled by 1/255.
+ * Layer l is a valid (unpadded) cross-correlation with c_l filters of size
+ * c_{l-1} x k_l x k_l and stride s_l, followed by ReLU.  Then a ReLU fully
+ * connected layer of `hidden` units and a linear layer of n_actions units.
+ * The Atari network is {4,84,84, 32,8,4, 64,4,2, 64,3,1, 512, A}. */
+typedef struct {
+    int32_t in_c, in_h, in_w;
+    int32_t c1, k1, s1;
+    int32_t c2, k2, s2;
+    int32_t c3, k3, s3;
+    int32_t hidden;
+    int32_t n_actions;
+} oracle_net;
+
+/* Number of parameters.  The flat layout is, in this order, W1 [c1,in_c,k1,k1],
+ * b1 [c1], W2 [c2,c1,k2,k2], b2, W3 [c3,c2,k3,k3], b3, W4 [hidden, c3*h3*w3],
+ * b4 [hidden], W5 [A, hidden], b5 [A]; the flatten of conv3's output is
+ * channel-major (c, i, j).  Returns -1 for an invalid topology. */
+int64_t oracle_param_count(const oracle_net* net);
+
+/* Offsets of the ten tensors inside the flat vector; off has 11 entries
+ * (the 11th is the total). */
+int oracle_param_offsets(const oracle_net* net, int64_t* off);
+
+/* Threads the OpenMP loops use. */
+int oracle_num_threads(void);
+
+/* Q(s, .; theta) for n states [n, in_c, in_h, in_w] -> q_out [n, A]. */
+int oracle_q_forward(const oracle_net* net, const double* theta,
+                     const uint8_t* states, int32_t n, double* q_out);
+
+/* epsilon-greedy actions (Algorithm 1) with the SplitMix64 draws described
+ * in the source; q_out may be NULL. */
+int oracle_act(const oracle_net* net, const double* theta,
+               const uint8_t* states, int32_t n, double eps, uint64_t seed,
+               int32_t* actions_out, double* q_out);
+
+/* One learner step on B stacked transitions (s, a, r, s', terminal).
+ * grads_out [P] = d loss / d theta, loss_out [1] = mean Huber loss.
+ * q_out / q2_out [B, A] (may be NULL) receive Q(s;theta), Q(s';theta-). */
+int oracle_learner_step(const oracle_net* net, const double* theta,
+                        const double* theta_target, const uint8_t* s,
+                        const uint8_t* s2, const int32_t* a, const double* r,
+                        const uint8_t* term, int32_t B, double gamma,
+                        double clip, double* grads_out, double* loss_out,
+                        double* q_out, double* q2_out);
+
+/* Replay gather: for logical positions idx[n] build s = stack(k) and
+ * s' = stack(k+1) (each hist frames of frame_bytes bytes, oldest first),
+ * the frame map [n, 2, hist] (physical slot, or -1 where zero-filled),
+ * a = action[p(k)], r = reward[p(k)], term = ep_start[p(k+1)]. */
+int oracle_gather(const uint8_t* frames, const uint8_t* ep_start,
+                  const int32_t* action, const float* reward,
+                  int64_t capacity, int64_t head, int32_t hist,
+                  int64_t frame_bytes, const int64_t* idx, int32_t n,
+                  uint8_t* s_out, uint8_t* s2_out, int64_t* frame_map_out,
+                  int32_t* a_out, float* r_out, uint8_t* term_out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
