@@ -1,0 +1,186 @@
+#!/usr/bin/env python3
+"""Benchmark of the Gorila DQN learner step on one MI355X.
+
+A step is one whole learner step (Algorithm 1 of Nair et al. 2015): gather the
+minibatch out of replay, online and target Q forward passes, TD target and
+Huber-clipped TD error, loss, and backprop to every parameter gradient.  The
+timed workload is the batch-512, 6-action fp32 step on seeded synthetic
+Atari-shaped data (uint8 4x84x84 stacks); inputs sit in HBM before timing.
+
+Prints one JSON line: transitions/s, the fraction of fp32 MFMA peak the whole
+step reaches, the roofline of the dominant kernel (timed live with HIP events
+on the stream the kernels run on) and the fp64 CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+FP32_MFMA_PEAK_TFLOPS = 157.3   # MI355X dense fp32 matrix peak
+HBM_PEAK_GBS = 8000.0
+
+# Algorithmic multiply-accumulates per sample of each layer (Section 4.1 net).
+MAC_CONV1 = 400 * 32 * 256
+MAC_CONV2 = 81 * 64 * 512
+MAC_CONV3 = 49 * 64 * 576
+MAC_FC1 = 3136 * 512
+
+
+def step_flops_per_transition(A: int) -> int:
+    """Online + target forward, data gradients of layers 2-5, weight gradients
+    of layers 1-5; the action head's backward counted at the chosen action."""
+    fwd = MAC_CONV1 + MAC_CONV2 + MAC_CONV3 + MAC_FC1 + 512 * A
+    bwd = 2 * 512 + 2 * MAC_FC1 + 2 * MAC_CONV3 + 2 * MAC_CONV2 + MAC_CONV1
+    return 2 * (2 * fwd + bwd)
+
+
+def stage_flops(stage: str, B: int, A: int) -> float:
+    """Algorithmic FLOPs of one launch of a stage of the learner step at batch B."""
+    two = 2 * B  # online + target rows in the forward stages
+    table = {
+        "conv1_fwd": two * MAC_CONV1, "conv2_fwd": two * MAC_CONV2, "conv3_fwd": two * MAC_CONV3,
+        "fc1_fwd": two * MAC_FC1, "head": two * 512 * A + B * 512, "head_reduce": B * 512,
+        "fc1_dgrad": B * MAC_FC1, "fc1_wgrad": B * MAC_FC1, "conv3_dgrad": B * MAC_CONV3,
+        "conv3_wgrad": B * MAC_CONV3, "conv2_dgrad": B * MAC_CONV2, "conv2_wgrad": B * MAC_CONV2,
+        "conv1_wgrad": B * MAC_CONV1,
+    }
+    return 2.0 * table.get(stage, 0)
+
+
+def run_learner(torch, g, datagen, B, A, seed, steps, warmup, timed_stage=None):
+    inp = datagen.learner_inputs(seed, B, A)
+    dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    theta, tgt, idx = t(inp.theta), t(inp.theta_target), t(inp.idx)
+    rep = g.Replay.stacked(t(inp.s), t(inp.s2), t(inp.a), t(inp.r), t(inp.term))
+    ctx = g.Context(B, A, device=dev)
+    grads = torch.empty(g.param_count(A), dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    step = lambda: g.gorila_learner_step(ctx, theta, tgt, A, rep, idx, inp.gamma, 1.0, grads, loss)
+    for _ in range(warmup):
+        step()
+    ctx.check()
+
+    # per-stage profile (separate pass, every stage bracketed by events)
+    names = g.stage_names()
+    ctx.timing_begin(names, max_records=len(names) * max(steps, 1))
+    for _ in range(max(steps // 2, 1)):
+        step()
+    prof = ctx.timing_end()
+
+    dominant = timed_stage or max((k for k in prof if stage_flops(k, B, A) > 0),
+                                  key=lambda k: prof[k][0])
+    # timed region: events only around the dominant kernel
+    torch.cuda.synchronize()
+    ctx.timing_begin([dominant], max_records=steps)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dom = ctx.timing_end()[dominant]
+    ctx.check()
+    ms_total = start.elapsed_time(stop)
+    ctx.close()
+    return dict(inp=inp, ms_per_step=ms_total / steps, wall_s=wall, prof=prof, dominant=dominant,
+                dominant_ms=dom[0] / max(dom[1], 1), dominant_launches=dom[1])
+
+
+def cpu_baseline(datagen, B, A, seed, sample):
+    import oracle
+    inp = datagen.learner_inputs(seed, B, A)
+    n = min(sample, B)
+    net = oracle.Net(n_actions=A)
+    t0 = time.perf_counter()
+    oracle.learner_step(net, inp.theta, inp.theta_target, inp.s[:n], inp.s2[:n], inp.a[:n],
+                        inp.r[:n], inp.term[:n], inp.gamma, 1.0)
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "transitions/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"one fp64 learner step over the first {n} transitions of the "
+                      f"batch-{B} workload ({dt:.1f} s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--batch", type=int, default=512)
+    ap.add_argument("--actions", type=int, default=6)
+    ap.add_argument("--cpu-sample", type=int, default=128)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-b32", action="store_true", help="skip the batch-32 companion line")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_1507_04296_amd as g
+    from paper_1507_04296_amd import datagen
+    if not torch.cuda.is_available():
+        print("bench.py needs a ROCm GPU", file=sys.stderr)
+        sys.exit(2)
+    g.lib()  # fails loudly if the HIP library is missing
+
+    B, A = args.batch, args.actions
+    seed = datagen.SEED_BASE + 2
+    r = run_learner(torch, g, datagen, B, A, seed, args.steps, args.warmup)
+    fpt = step_flops_per_transition(A)
+    step_tflops = B * fpt / (r["ms_per_step"] * 1e-3) / 1e12
+    dom_flops = stage_flops(r["dominant"], B, A)
+    dom_tflops = dom_flops / (r["dominant_ms"] * 1e-3) / 1e12
+    stages = {k: {"ms": round(v[0] / max(v[1], 1), 4),
+                  "tflops": round(stage_flops(k, B, A) / (v[0] / max(v[1], 1) * 1e-3) / 1e12, 2)}
+              for k, v in r["prof"].items()}
+    out = {
+        "metric": "learner transitions/sec (DQN fwd+bwd) and % MFMA peak at batch 32/512",
+        "value": round(B / (r["ms_per_step"] * 1e-3), 1),
+        "unit": "transitions/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(r["ms_per_step"], 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"learner_b{B}_a{A}_f32", "batch": B, "n_actions": A,
+                   "replay": "stacked uint8 4x84x84", "gamma": 0.99, "clip_delta": 1.0,
+                   "parallelism": "single GPU"},
+        "tflops": round(step_tflops, 2),
+        "pct_mfma_peak": round(100 * step_tflops / FP32_MFMA_PEAK_TFLOPS, 2),
+        "flops_per_transition": fpt,
+        "roofline": {"bound": "mfma", "kernel": r["dominant"], "achieved": round(dom_tflops, 2),
+                     "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(dom_tflops / FP32_MFMA_PEAK_TFLOPS, 4), "traffic": None,
+                     "avg_launch_ms": round(r["dominant_ms"], 4),
+                     "flops_per_launch": dom_flops},
+        "stages": stages,
+    }
+    if not args.no_b32:
+        r32 = run_learner(torch, g, datagen, 32, 18, datagen.SEED_BASE + 0, max(args.steps, 50),
+                          args.warmup)
+        t32 = 32 * step_flops_per_transition(18) / (r32["ms_per_step"] * 1e-3) / 1e12
+        out["batch32"] = {"workload": "learner_b32_a18_f32",
+                          "value": round(32 / (r32["ms_per_step"] * 1e-3), 1),
+                          "ms_per_step": round(r32["ms_per_step"], 4), "tflops": round(t32, 3),
+                          "pct_mfma_peak": round(100 * t32 / FP32_MFMA_PEAK_TFLOPS, 2)}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(datagen, B, A, seed, args.cpu_sample)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,184 @@
+/*
+ * libgorila -- the Gorila DQN learner step and actor inference on one MI355X.
+ *
+ * Method: Nair et al. 2015, "Massively Parallel Methods for Deep
+ * Reinforcement Learning".  The learner's job (Section 3, Learners;
+ * Algorithm 1) is: sample a minibatch of transitions (s, a, r, s') from
+ * replay memory, form the target y = r for terminal s' and
+ * y = r + gamma * max_a' Q(s', a'; theta-) otherwise, take the squared TD
+ * error of eq. (1) and compute its gradient, eq. (2), with respect to theta.
+ * Actors (Section 3, Actors; Algorithm 1) choose epsilon-greedy actions on
+ * Q(s, a; theta).  The Q-network is the one of Section 4.1.
+ *
+ * Conventions for every call below:
+ *  - All array arguments are DEVICE pointers owned by the caller (normally
+ *    torch tensors), C-contiguous, on the device the context was made on.
+ *    Nothing is allocated or freed inside a call.  Inputs are never modified.
+ *  - All work is enqueued on the context's HIP stream and is asynchronous;
+ *    outputs are valid once that stream has been synchronised.
+ *  - Return value 0 = success; a negative GORILA_E* code otherwise.  Argument
+ *    errors are detected on the host before anything is enqueued.  Errors
+ *    that only the device can see (an index or an action out of range) set
+ *    a sticky flag in the workspace; the kernels then read a zero frame /
+ *    action 0 instead of touching memory out of bounds, and the error is
+ *    returned by gorila_ctx_check() (or by the next call on the context).
+ *  - States are uint8 [n, 4, 84, 84]: four 84x84 luminance frames, oldest
+ *    first (Section 4.1).  Network input is state / 255.
+ *  - Parameters are one flat vector in this order (weights OIHW / [out, in]):
+ *    W1 [32,4,8,8], b1 [32], W2 [64,32,4,4], b2 [64], W3 [64,64,3,3], b3 [64],
+ *    W4 [512,3136], b4 [512], W5 [A,512], b5 [A]; the FC input is conv3's
+ *    output flattened channel-major.  gorila_param_count(A) elements.
+ *  - Not thread-safe per context: calls on one context must not overlap.
+ */
+#ifndef GORILA_H
+#define GORILA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    GORILA_OK = 0,
+    GORILA_EINVAL = -1,        /* bad pointer, size, dtype or action count      */
+    GORILA_ERANGE = -2,        /* device saw an index or action out of range    */
+    GORILA_EWORKSPACE = -3,    /* workspace too small for this call             */
+    GORILA_EHIP = -4,          /* HIP runtime or launch error                   */
+    GORILA_EUNSUPPORTED = -5   /* valid request this build does not implement   */
+};
+
+enum { GORILA_F32 = 0, GORILA_BF16 = 1 };
+enum { GORILA_REPLAY_STACKED = 0, GORILA_REPLAY_RING = 1 };
+
+/* A parameter set theta (device pointer to the flat layout above). */
+typedef struct {
+    const void* data;     /* fp32 (GORILA_F32) or bf16 bit patterns (GORILA_BF16) */
+    int32_t n_actions;    /* A, 1 .. 32 (the Atari action set has 18)             */
+    int32_t dtype;
+} gorila_params;
+
+/* Replay memory D (Section 3, Experience replay memory).
+ *
+ * STACKED: `rows` whole transitions; a minibatch index k in [0, rows) names
+ *   s = s[k] and s' = s2[k] (uint8 [rows,4,84,84]), action[k], reward[k] and
+ *   term[k] (nonzero = s' is terminal).
+ * RING: a ring of `capacity` single uint8 84x84 frames; `head` is the slot of
+ *   the oldest frame and logical position k lives in slot
+ *   (head + k) mod capacity.  ep_start[slot] != 0 marks the first frame of an
+ *   episode; logical 0 also counts as one.  A minibatch index is a logical
+ *   position k in [0, capacity-2]: s is the stack of frames k-3 .. k and s'
+ *   of frames k-2 .. k+1 (oldest first), where any frame before the latest
+ *   episode start at or before the stack's newest frame is all zeros (the
+ *   paper concatenates the four most recent frames, Section 4.1; zero-fill at
+ *   episode starts is this library's reading).  The transition's action and
+ *   reward are action[slot(k)], reward[slot(k)]; it is terminal iff k+1
+ *   starts an episode.  s, s2 and term are unused. */
+typedef struct {
+    int32_t kind;
+    int32_t reserved;
+    const uint8_t* s;
+    const uint8_t* s2;
+    const uint8_t* term;
+    int64_t rows;
+    const uint8_t* frames;
+    const uint8_t* ep_start;
+    int64_t capacity;
+    int64_t head;
+    const int32_t* action;   /* [rows] or [capacity] */
+    const float* reward;     /* [rows] or [capacity] */
+} gorila_replay;
+
+typedef struct gorila_ctx gorila_ctx;
+
+/* Number of elements of a flat parameter vector with A actions, or -1. */
+int64_t gorila_param_count(int32_t n_actions);
+
+/* Device workspace bytes needed by calls with batch <= max_batch on
+ * `groups` parameter sets (1 for the single-learner and actor calls).
+ * The caller allocates it; the context keeps only the pointer. */
+size_t gorila_workspace_bytes(int32_t max_batch, int32_t n_actions, int32_t dtype,
+                              int32_t groups);
+
+/* Bind a stream (hipStream_t, may be NULL for the null stream) and a device
+ * workspace of ws_bytes (>= gorila_workspace_bytes(1,1,0,1), 256-byte
+ * aligned) to a new context on the current device.  The context owns only
+ * host bookkeeping; destroy it before freeing the workspace. */
+int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_t ws_bytes);
+int gorila_ctx_destroy(gorila_ctx* ctx);
+/* Point the context at another stream (subsequent calls enqueue there). */
+int gorila_ctx_set_stream(gorila_ctx* ctx, void* hip_stream);
+/* Synchronise the context's stream and report (then clear) the sticky device
+ * error: GORILA_ERANGE if an index or action was out of range. */
+int gorila_ctx_check(gorila_ctx* ctx);
+const char* gorila_strerror(int code);
+
+/* Kernel timing for benchmarks and profiling.  After
+ * gorila_ctx_timing_begin(ctx, stage_mask, max_records), every learner step,
+ * forward or act call records a HIP event pair on the context's stream
+ * around each stage whose bit (1u << stage) is set in stage_mask, up to
+ * max_records pairs in total (events are created here, not in the calls).
+ * gorila_ctx_timing_end synchronises the stream, writes for each of the first
+ * n_stages stages the summed milliseconds (total_ms) and the number of
+ * recorded launches (count), and stops recording.  Stage numbers and names:
+ * gorila_stage_name(i) (NULL past the last stage).  Timing does not change
+ * any result. */
+int gorila_ctx_timing_begin(gorila_ctx* ctx, uint32_t stage_mask, int32_t max_records);
+int gorila_ctx_timing_end(gorila_ctx* ctx, double* total_ms, int32_t* count, int32_t n_stages);
+const char* gorila_stage_name(int32_t stage);
+
+/* Replay gather (Section 3 replay memory, Section 4.1 frame stacking).
+ * For n minibatch indices idx [n] (int64) write s_out, s2_out
+ * [n,4,84,84] uint8, frame_map_out [n,2,4] int64 (RING: the slot each
+ * channel was copied from, -1 = zero-filled; STACKED: row*4 + channel),
+ * a_out [n] int32, r_out [n] float, term_out [n] uint8.  frame_map_out may be
+ * NULL.  Uses no workspace beyond the context's header. */
+int gorila_gather(const gorila_replay* replay, const int64_t* idx, int32_t n,
+                  uint8_t* s_out, uint8_t* s2_out, int64_t* frame_map_out,
+                  int32_t* a_out, float* r_out, uint8_t* term_out, gorila_ctx* ctx);
+
+/* Q(s, .; theta) (Section 4.1 network) for states [n,4,84,84] -> q_out [n,A]
+ * fp32.  Needs gorila_workspace_bytes(n, A, dtype, 1). */
+int gorila_q_forward(const gorila_params* params, const uint8_t* states_u8, int32_t n,
+                     float* q_out, gorila_ctx* ctx);
+
+/* epsilon-greedy actions (Algorithm 1): for env e, with probability eps a
+ * uniformly random action, else the lowest-index argmax of Q(s_e, .; theta).
+ * The two uniform draws per env are u = mix(seed + (2e+1)G) and
+ * v = mix(seed + (2e+2)G), G = 0x9E3779B97F4A7C15, mix = the SplitMix64
+ * output function (Steele, Lea and Flood 2014), all mod 2^64; explore iff
+ * (u >> 11) < floor(eps * 2^53), random action = ((v >> 32) * A) >> 32.
+ * actions_out [n] int32; q_out [n,A] fp32 may be NULL.  eps in [0, 1]. */
+int gorila_act(const gorila_params* params, const uint8_t* states_u8, int32_t n, float eps,
+               uint64_t seed, int32_t* actions_out, float* q_out, gorila_ctx* ctx);
+
+/* One DQN learner step (Algorithm 1; eq. (1) and (2)) on the minibatch
+ * idx [batch] drawn from `replay`:
+ *   q = Q(s; theta), q' = Q(s'; theta-), y = r + gamma (1 - term) max q',
+ *   delta = y - q[a], loss = mean_b huber(delta_b) with threshold clip_delta
+ *   (0.5 delta^2 for |delta| <= clip_delta, clip_delta |delta| - 0.5
+ *   clip_delta^2 beyond; clip_delta = +INFINITY gives eq. (1) times 1/2),
+ *   grads_out [P] fp32 = d loss / d theta (for |delta| <= clip_delta this is
+ *   minus the minibatch mean of eq. (2)'s g), loss_out [1] fp32.
+ * No gradient flows into theta-.  params and target_params must have the
+ * same A and dtype GORILA_F32.  Needs gorila_workspace_bytes(batch, A, 0, 1). */
+int gorila_learner_step(const gorila_params* params, const gorila_params* target_params,
+                        const gorila_replay* replay, const int64_t* idx, int32_t batch,
+                        float gamma, float clip_delta, float* grads_out, float* loss_out,
+                        gorila_ctx* ctx);
+
+/* `groups` independent learner steps (Section 3: many learners, each with
+ * its own, possibly stale, replica of theta) sharing one target theta-.
+ * params points to `groups` parameter sets; group g uses minibatch indices
+ * idx[g*batch .. g*batch+batch-1] and writes grads_out[g*P .. g*P+P-1] and
+ * loss_out[g].  Returns GORILA_EUNSUPPORTED in this build. */
+int gorila_learner_step_grouped(const gorila_params* params, int32_t groups,
+                                const gorila_params* target_params, const gorila_replay* replay,
+                                const int64_t* idx, int32_t batch, float gamma, float clip_delta,
+                                float* grads_out, float* loss_out, gorila_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,1 +1,290 @@
-"""Gorila DQN learner step on MI355X (gfx950): HIP kernels behind a C-ABI."""
+"""Gorila DQN learner step on MI355X (gfx950): HIP kernels behind a C-ABI.
+
+This module is the thin Python binding of ``libgorila.so`` (declared in
+``include/gorila.h``): it only marshals torch tensors (device pointers) and the
+current HIP stream into the C calls.  Every step of the computation runs in the
+library's kernels; there is no Python or CPU fallback.  If the library is not
+built, every call raises.
+
+Method: Nair et al. 2015, "Massively Parallel Methods for Deep Reinforcement
+Learning" -- the learner's DQN gradient step (Algorithm 1, eq. (1) and (2)) and
+the actors' epsilon-greedy inference (Algorithm 1), on the Q-network of
+Section 4.1.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libgorila.so")
+
+GORILA_F32, GORILA_BF16 = 0, 1
+REPLAY_STACKED, REPLAY_RING = 0, 1
+ERRORS = {0: "OK", -1: "EINVAL", -2: "ERANGE", -3: "EWORKSPACE", -4: "EHIP", -5: "EUNSUPPORTED"}
+
+# Every function declared in include/gorila.h.
+EXPORTS = (
+    "gorila_param_count", "gorila_workspace_bytes", "gorila_ctx_create", "gorila_ctx_destroy",
+    "gorila_ctx_set_stream", "gorila_ctx_check", "gorila_strerror", "gorila_gather",
+    "gorila_q_forward", "gorila_act", "gorila_learner_step", "gorila_learner_step_grouped",
+    "gorila_ctx_timing_begin", "gorila_ctx_timing_end", "gorila_stage_name",
+)
+
+
+class GorilaError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        self.code = code
+        super().__init__(f"{what}: {ERRORS.get(code, code)} ({strerror(code)})")
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("n_actions", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class _Replay(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("s", ctypes.c_void_p), ("s2", ctypes.c_void_p), ("term", ctypes.c_void_p),
+                ("rows", ctypes.c_int64), ("frames", ctypes.c_void_p),
+                ("ep_start", ctypes.c_void_p), ("capacity", ctypes.c_int64),
+                ("head", ctypes.c_int64), ("action", ctypes.c_void_p),
+                ("reward", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libgorila.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                           "(there is no fallback implementation)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, u64, f32 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64,
+                              ctypes.c_float)
+    P, R = ctypes.POINTER(_Params), ctypes.POINTER(_Replay)
+    sig = {
+        "gorila_param_count": (i64, [i32]),
+        "gorila_workspace_bytes": (ctypes.c_size_t, [i32, i32, i32, i32]),
+        "gorila_ctx_create": (ctypes.c_int, [ctypes.POINTER(vp), vp, vp, ctypes.c_size_t]),
+        "gorila_ctx_destroy": (ctypes.c_int, [vp]),
+        "gorila_ctx_set_stream": (ctypes.c_int, [vp, vp]),
+        "gorila_ctx_check": (ctypes.c_int, [vp]),
+        "gorila_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+        "gorila_gather": (ctypes.c_int, [R, vp, i32, vp, vp, vp, vp, vp, vp, vp]),
+        "gorila_q_forward": (ctypes.c_int, [P, vp, i32, vp, vp]),
+        "gorila_act": (ctypes.c_int, [P, vp, i32, f32, u64, vp, vp, vp]),
+        "gorila_learner_step": (ctypes.c_int, [P, P, R, vp, i32, f32, f32, vp, vp, vp]),
+        "gorila_learner_step_grouped": (ctypes.c_int, [P, i32, P, R, vp, i32, f32, f32, vp, vp, vp]),
+        "gorila_ctx_timing_begin": (ctypes.c_int, [vp, ctypes.c_uint32, i32]),
+        "gorila_ctx_timing_end": (ctypes.c_int, [vp, vp, vp, i32]),
+        "gorila_stage_name": (ctypes.c_char_p, [i32]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype, fn.argtypes = res, args
+    _lib = L
+    return L
+
+
+def strerror(code: int) -> str:
+    return lib().gorila_strerror(code).decode()
+
+
+def stage_names() -> list:
+    out, i = [], 0
+    while True:
+        name = lib().gorila_stage_name(i)
+        if name is None:
+            return out
+        out.append(name.decode())
+        i += 1
+
+
+def param_count(n_actions: int) -> int:
+    return int(lib().gorila_param_count(n_actions))
+
+
+def workspace_bytes(max_batch: int, n_actions: int, dtype: int = GORILA_F32, groups: int = 1) -> int:
+    return int(lib().gorila_workspace_bytes(max_batch, n_actions, dtype, groups))
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise GorilaError(rc, what)
+
+
+class Context:
+    """A gorila_ctx bound to a torch-allocated device workspace.
+
+    The workspace is sized for calls with batch <= max_batch (learner step) or
+    n <= 2 * max_batch states (forward / act)."""
+
+    def __init__(self, max_batch: int, n_actions: int, groups: int = 1, device=None):
+        import torch
+        self.device = torch.device(device if device is not None else "cuda")
+        self.ws_bytes = workspace_bytes(max_batch, n_actions, GORILA_F32, groups)
+        if self.ws_bytes == 0:
+            raise ValueError("invalid workspace request")
+        with torch.cuda.device(self.device):
+            self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+            h = ctypes.c_void_p()
+            _check(lib().gorila_ctx_create(ctypes.byref(h), self._stream(), self.workspace.data_ptr(),
+                                           self.ws_bytes), "gorila_ctx_create")
+        self.handle = h
+
+    def _stream(self):
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream)
+
+    def bind_stream(self):
+        _check(lib().gorila_ctx_set_stream(self.handle, self._stream()), "gorila_ctx_set_stream")
+        return self.handle
+
+    def check(self) -> None:
+        """Synchronise and raise GorilaError(ERANGE) if the device saw a bad index/action."""
+        _check(lib().gorila_ctx_check(self.handle), "gorila_ctx_check")
+
+    def timing_begin(self, stages, max_records: int = 4096):
+        """Record HIP events around the named stages of the following calls."""
+        mask = 0
+        for name in stages:
+            mask |= 1 << stage_names().index(name)
+        _check(lib().gorila_ctx_timing_begin(self.handle, mask, max_records), "timing_begin")
+
+    def timing_end(self) -> dict:
+        """{stage: (total_ms, launches)} for the stages timed since timing_begin."""
+        import numpy as np
+        names = stage_names()
+        ms = np.zeros(len(names), np.float64)
+        cnt = np.zeros(len(names), np.int32)
+        _check(lib().gorila_ctx_timing_end(self.handle, ms.ctypes.data, cnt.ctypes.data, len(names)),
+               "timing_end")
+        return {n: (float(ms[i]), int(cnt[i])) for i, n in enumerate(names) if cnt[i]}
+
+    def close(self):
+        if getattr(self, "handle", None) is not None:
+            lib().gorila_ctx_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def params(theta, n_actions: int, dtype: int = GORILA_F32) -> _Params:
+    """gorila_params over a flat device tensor (fp32, or bf16 bits as int16/uint16/bfloat16)."""
+    return _Params(theta.data_ptr(), n_actions, dtype)
+
+
+@dataclass
+class Replay:
+    """Device tensors of a replay memory (see gorila_replay in include/gorila.h)."""
+    kind: int
+    action: object
+    reward: object
+    s: object = None
+    s2: object = None
+    term: object = None
+    frames: object = None
+    ep_start: object = None
+    head: int = 0
+
+    @staticmethod
+    def stacked(s, s2, action, reward, term) -> "Replay":
+        return Replay(REPLAY_STACKED, action, reward, s=s, s2=s2, term=term)
+
+    @staticmethod
+    def ring(frames, ep_start, action, reward, head: int) -> "Replay":
+        return Replay(REPLAY_RING, action, reward, frames=frames, ep_start=ep_start, head=head)
+
+    def c(self) -> _Replay:
+        rows = self.s.shape[0] if self.s is not None else 0
+        cap = self.frames.shape[0] if self.frames is not None else 0
+        return _Replay(self.kind, 0, _ptr(self.s), _ptr(self.s2), _ptr(self.term), rows,
+                       _ptr(self.frames), _ptr(self.ep_start), cap, int(self.head),
+                       _ptr(self.action), _ptr(self.reward))
+
+
+def gorila_gather(ctx: Context, replay: Replay, idx, s_out, s2_out, frame_map_out, a_out, r_out,
+                  term_out) -> None:
+    rv = replay.c()
+    _check(lib().gorila_gather(ctypes.byref(rv), _ptr(idx), idx.shape[0], _ptr(s_out), _ptr(s2_out),
+                               _ptr(frame_map_out), _ptr(a_out), _ptr(r_out), _ptr(term_out),
+                               ctx.bind_stream()), "gorila_gather")
+
+
+def gorila_q_forward(ctx: Context, theta, n_actions: int, states, q_out) -> None:
+    p = params(theta, n_actions)
+    _check(lib().gorila_q_forward(ctypes.byref(p), _ptr(states), states.shape[0], _ptr(q_out),
+                                  ctx.bind_stream()), "gorila_q_forward")
+
+
+def gorila_act(ctx: Context, theta, n_actions: int, states, eps: float, seed: int, actions_out,
+               q_out=None) -> None:
+    p = params(theta, n_actions)
+    _check(lib().gorila_act(ctypes.byref(p), _ptr(states), states.shape[0], eps,
+                            ctypes.c_uint64(seed & (2 ** 64 - 1)), _ptr(actions_out), _ptr(q_out),
+                            ctx.bind_stream()), "gorila_act")
+
+
+def gorila_learner_step(ctx: Context, theta, theta_target, n_actions: int, replay: Replay, idx,
+                        gamma: float, clip_delta: float, grads_out, loss_out) -> None:
+    p, pt, rv = params(theta, n_actions), params(theta_target, n_actions), replay.c()
+    _check(lib().gorila_learner_step(ctypes.byref(p), ctypes.byref(pt), ctypes.byref(rv), _ptr(idx),
+                                     idx.shape[0], gamma, clip_delta, _ptr(grads_out),
+                                     _ptr(loss_out), ctx.bind_stream()), "gorila_learner_step")
+
+
+# Convenience wrappers that allocate the outputs (torch) and return them.
+def q_forward(ctx: Context, theta, n_actions: int, states):
+    import torch
+    q = torch.empty((states.shape[0], n_actions), dtype=torch.float32, device=states.device)
+    gorila_q_forward(ctx, theta, n_actions, states, q)
+    return q
+
+
+def act(ctx: Context, theta, n_actions: int, states, eps: float, seed: int, with_q: bool = False):
+    import torch
+    n = states.shape[0]
+    actions = torch.empty(n, dtype=torch.int32, device=states.device)
+    q = torch.empty((n, n_actions), dtype=torch.float32, device=states.device) if with_q else None
+    gorila_act(ctx, theta, n_actions, states, eps, seed, actions, q)
+    return (actions, q) if with_q else actions
+
+
+def learner_step(ctx: Context, theta, theta_target, n_actions: int, replay: Replay, idx,
+                 gamma: float = 0.99, clip_delta: float = 1.0):
+    import torch
+    grads = torch.empty(param_count(n_actions), dtype=torch.float32, device=theta.device)
+    loss = torch.empty(1, dtype=torch.float32, device=theta.device)
+    gorila_learner_step(ctx, theta, theta_target, n_actions, replay, idx, gamma, clip_delta,
+                        grads, loss)
+    return grads, loss
+
+
+def gather(ctx: Context, replay: Replay, idx):
+    import torch
+    n, dev = idx.shape[0], idx.device
+    s = torch.empty((n, 4, 84, 84), dtype=torch.uint8, device=dev)
+    s2 = torch.empty_like(s)
+    fmap = torch.empty((n, 2, 4), dtype=torch.int64, device=dev)
+    a = torch.empty(n, dtype=torch.int32, device=dev)
+    r = torch.empty(n, dtype=torch.float32, device=dev)
+    t = torch.empty(n, dtype=torch.uint8, device=dev)
+    gorila_gather(ctx, replay, idx, s, s2, fmap, a, r, t)
+    return dict(s=s, s2=s2, frame_map=fmap, a=a, r=r, term=t)
+
+
+INF = math.inf

@@ -1,0 +1,452 @@
+// C-ABI entry points of libgorila (declared in include/gorila.h): argument
+// validation, the workspace plan and the launch sequence of each call.
+#include <math.h>
+#include <string.h>
+
+#include <new>
+#include <vector>
+
+#include "common.h"
+#include "kernels.h"
+
+using namespace gorila;
+
+namespace {
+// Stages of the calls, in launch order (bits of the timing mask).
+enum Stage {
+    ST_RESOLVE, ST_PREP, ST_CONV1_FWD, ST_CONV2_FWD, ST_CONV3_FWD, ST_FC1_FWD, ST_HEAD,
+    ST_HEAD_REDUCE, ST_FC1_DGRAD, ST_FC1_WGRAD, ST_CONV3_DGRAD, ST_CONV3_WGRAD, ST_CONV2_DGRAD,
+    ST_CONV2_WGRAD, ST_CONV1_WGRAD, ST_GRAD_REDUCE, ST_COUNT
+};
+const char* const STAGE_NAMES[ST_COUNT] = {
+    "resolve", "prep_weights", "conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "head",
+    "head_reduce", "fc1_dgrad", "fc1_wgrad", "conv3_dgrad", "conv3_wgrad", "conv2_dgrad",
+    "conv2_wgrad", "conv1_wgrad", "grad_reduce"};
+struct TimingRecord {
+    int stage;
+    hipEvent_t start, stop;
+};
+}  // namespace
+
+struct gorila_ctx {
+    hipStream_t stream;
+    char* ws;
+    size_t ws_bytes;
+    int device;
+    uint32_t timing_mask = 0;
+    std::vector<TimingRecord> records;  // events created by timing_begin
+    size_t used = 0;
+};
+
+namespace {
+// Records an event pair around one stage when its timing bit is set.
+struct StageTimer {
+    gorila_ctx* c;
+    TimingRecord* rec = nullptr;
+    StageTimer(gorila_ctx* ctx, int stage) : c(ctx) {
+        if ((c->timing_mask >> stage) & 1u && c->used < c->records.size()) {
+            rec = &c->records[c->used++];
+            rec->stage = stage;
+            (void)hipEventRecord(rec->start, c->stream);
+        }
+    }
+    ~StageTimer() {
+        if (rec) (void)hipEventRecord(rec->stop, c->stream);
+    }
+};
+}  // namespace
+
+namespace {
+
+constexpr size_t ALIGN = 256;
+size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+// Byte offsets of every workspace region for fwd_rows forward rows (all
+// parameter sets together) and bwd_rows learner rows.
+struct Plan {
+    size_t err, ftab, a, r, term;
+    size_t w2t[2], w3t[2], w3d, w2d;
+    size_t h1, h2, h3, h4, q, ell, coef;
+    size_t dz4, dz3, dz2, dz1;
+    size_t fc1part, part1, part2, part3, bpart;
+    size_t total;
+};
+
+Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A) {
+    Plan p{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) { size_t at = o; o += up(bytes); return at; };
+    const int64_t F = fwd_rows, B = bwd_rows;
+    p.err = take(ALIGN);
+    p.ftab = take(sizeof(void*) * 2 * (size_t)(F > 2 * B ? F : 2 * B) * 4);
+    p.a = take(4 * (size_t)B);
+    p.r = take(4 * (size_t)B);
+    p.term = take((size_t)B);
+    for (int g = 0; g < 2; ++g) {
+        p.w2t[g] = take(4 * 16 * 64 * 32);
+        p.w3t[g] = take(4 * 9 * 64 * 64);
+    }
+    p.w3d = take(4 * 9 * 64 * 64);
+    p.w2d = take(4 * 16 * 32 * 64);
+    p.h1 = take(4 * (size_t)F * P1 * C1);
+    p.h2 = take(4 * (size_t)F * P2 * C2);
+    p.h3 = take(4 * (size_t)F * FLAT);
+    p.h4 = take(4 * (size_t)F * HID);
+    p.q = take(4 * (size_t)F * A);
+    p.fc1part = take(4 * (size_t)F * HID * FC1_MAX_SPLITS);
+    p.ell = take(4 * (size_t)B);
+    p.coef = take(4 * (size_t)B);
+    p.dz4 = take(4 * (size_t)B * HID);
+    p.dz3 = take(4 * (size_t)B * FLAT);
+    p.dz2 = take(4 * (size_t)B * P2 * C2);
+    p.dz1 = take(4 * (size_t)B * P1 * C1);
+    p.part1 = B ? take(4 * (size_t)CONV1_WG_MAX_SPLITS * C1 * 256) : o;
+    p.part2 = B ? take(4 * (size_t)WG_MAX_SPLITS * C2 * 16 * C1) : o;
+    p.part3 = B ? take(4 * (size_t)WG_MAX_SPLITS * C3 * 9 * C2) : o;
+    p.bpart = B ? take(4 * (size_t)3 * BIAS_BLOCKS * 64) : o;
+    p.total = o;
+    return p;
+}
+
+template <class T>
+T* at(gorila_ctx* c, size_t off) { return (T*)(c->ws + off); }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+int check_launch() {
+    return hipGetLastError() == hipSuccess ? GORILA_OK : GORILA_EHIP;
+}
+
+int check_ctx(gorila_ctx* c) {
+    if (!c) return GORILA_EINVAL;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return GORILA_EHIP;
+    return dev == c->device ? GORILA_OK : GORILA_EINVAL;
+}
+
+int check_params(const gorila_params* p) {
+    if (!p || !p->data || !aligned16(p->data)) return GORILA_EINVAL;
+    if (p->n_actions < 1 || p->n_actions > MAX_ACTIONS) return GORILA_EINVAL;
+    if (p->dtype != GORILA_F32) return p->dtype == GORILA_BF16 ? GORILA_EUNSUPPORTED : GORILA_EINVAL;
+    return GORILA_OK;
+}
+
+int check_replay(const gorila_replay* rv) {
+    if (!rv || !rv->action || !rv->reward) return GORILA_EINVAL;
+    if (rv->kind == GORILA_REPLAY_STACKED) {
+        if (!rv->s || !rv->s2 || !rv->term || rv->rows < 1) return GORILA_EINVAL;
+        if (!aligned16(rv->s) || !aligned16(rv->s2)) return GORILA_EINVAL;
+        return GORILA_OK;
+    }
+    if (rv->kind == GORILA_REPLAY_RING) {
+        if (!rv->frames || !rv->ep_start || rv->capacity < 2) return GORILA_EINVAL;
+        if (rv->head < 0 || rv->head >= rv->capacity || !aligned16(rv->frames)) return GORILA_EINVAL;
+        return GORILA_OK;
+    }
+    return GORILA_EINVAL;
+}
+
+ReplayView view_of(const gorila_replay* rv) {
+    return ReplayView{rv->kind,     rv->s,        rv->s2,       rv->term,
+                      rv->rows,     rv->frames,   rv->ep_start, rv->capacity,
+                      rv->head,     rv->action,   rv->reward};
+}
+
+// Frame table for a batch of stacked states (forward-only calls).
+__global__ void states_table_kernel(const uint8_t* states, int n, const uint8_t** ftab) {
+    const int e = blockIdx.x * blockDim.x + threadIdx.x;
+    if (e < n * 4) ftab[e] = states + (int64_t)(e >> 2) * STATE_BYTES + (int64_t)(e & 3) * FRAME_BYTES;
+}
+
+// Forward pass of n states through one parameter set up to h4.
+int forward_one(gorila_ctx* c, const Plan& p, const float* theta, const uint8_t* states, int n) {
+    hipStream_t st = c->stream;
+    const uint8_t** ftab = at<const uint8_t*>(c, p.ftab);
+    { StageTimer t(c, ST_RESOLVE); states_table_kernel<<<(n * 4 + 255) / 256, 256, 0, st>>>(states, n, ftab); }
+    WeightViews wv{theta, at<float>(c, p.w2t[0]), at<float>(c, p.w3t[0]), nullptr, nullptr};
+    { StageTimer t(c, ST_PREP); launch_prep_weights(&wv, 1, st); }
+    GroupPtrs th{}, w2t{}, w3t{};
+    th.p[0] = theta;
+    w2t.p[0] = wv.w2t;
+    w3t.p[0] = wv.w3t;
+    { StageTimer t(c, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 1, n, at<float>(c, p.h1), st); }
+    { StageTimer t(c, ST_CONV2_FWD); launch_conv2_fwd(at<float>(c, p.h1), w2t, th, 1, n, at<float>(c, p.h2), st); }
+    { StageTimer t(c, ST_CONV3_FWD); launch_conv3_fwd(at<float>(c, p.h2), w3t, th, 1, n, at<float>(c, p.h3), st); }
+    { StageTimer t(c, ST_FC1_FWD); launch_fc1_fwd(at<float>(c, p.h3), th, 1, n, at<float>(c, p.fc1part), at<float>(c, p.h4), st); }
+    return check_launch();
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t gorila_param_count(int32_t n_actions) {
+    if (n_actions < 1 || n_actions > MAX_ACTIONS) return -1;
+    return param_count(n_actions);
+}
+
+size_t gorila_workspace_bytes(int32_t max_batch, int32_t n_actions, int32_t dtype, int32_t groups) {
+    if (max_batch < 1 || n_actions < 1 || n_actions > MAX_ACTIONS || groups < 1) return 0;
+    if (dtype != GORILA_F32 && dtype != GORILA_BF16) return 0;
+    const int64_t B = (int64_t)max_batch * groups;
+    return make_plan(2 * B, B, n_actions).total;
+}
+
+int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_t ws_bytes) {
+    if (!out || !workspace || !aligned16(workspace)) return GORILA_EINVAL;
+    if (ws_bytes < make_plan(1, 1, 1).err + ALIGN) return GORILA_EWORKSPACE;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return GORILA_EHIP;
+    gorila_ctx* c = new (std::nothrow) gorila_ctx;
+    if (c) {
+        c->stream = (hipStream_t)hip_stream;
+        c->ws = (char*)workspace;
+        c->ws_bytes = ws_bytes;
+        c->device = dev;
+    }
+    if (!c) return GORILA_EINVAL;
+    if (hipMemsetAsync(c->ws, 0, ALIGN, c->stream) != hipSuccess) {
+        delete c;
+        return GORILA_EHIP;
+    }
+    *out = c;
+    return GORILA_OK;
+}
+
+int gorila_ctx_destroy(gorila_ctx* ctx) {
+    if (!ctx) return GORILA_EINVAL;
+    for (auto& r : ctx->records) {
+        (void)hipEventDestroy(r.start);
+        (void)hipEventDestroy(r.stop);
+    }
+    delete ctx;
+    return GORILA_OK;
+}
+
+int gorila_ctx_set_stream(gorila_ctx* ctx, void* hip_stream) {
+    if (!ctx) return GORILA_EINVAL;
+    ctx->stream = (hipStream_t)hip_stream;
+    return GORILA_OK;
+}
+
+int gorila_ctx_check(gorila_ctx* ctx) {
+    int rc = check_ctx(ctx);
+    if (rc) return rc;
+    if (hipStreamSynchronize(ctx->stream) != hipSuccess) return GORILA_EHIP;
+    unsigned word = 0;
+    if (hipMemcpy(&word, ctx->ws, sizeof(word), hipMemcpyDeviceToHost) != hipSuccess) return GORILA_EHIP;
+    if (word == 0) return GORILA_OK;
+    if (hipMemset(ctx->ws, 0, sizeof(word)) != hipSuccess) return GORILA_EHIP;
+    return GORILA_ERANGE;
+}
+
+const char* gorila_strerror(int code) {
+    switch (code) {
+        case GORILA_OK: return "success";
+        case GORILA_EINVAL: return "invalid argument";
+        case GORILA_ERANGE: return "minibatch index or action out of range (seen on the device)";
+        case GORILA_EWORKSPACE: return "workspace too small";
+        case GORILA_EHIP: return "HIP runtime error";
+        case GORILA_EUNSUPPORTED: return "not supported by this build";
+        default: return "unknown error";
+    }
+}
+
+int gorila_ctx_timing_begin(gorila_ctx* ctx, uint32_t stage_mask, int32_t max_records) {
+    int rc = check_ctx(ctx);
+    if (rc) return rc;
+    if (max_records < 0) return GORILA_EINVAL;
+    for (auto& r : ctx->records) {
+        (void)hipEventDestroy(r.start);
+        (void)hipEventDestroy(r.stop);
+    }
+    ctx->records.clear();
+    ctx->used = 0;
+    ctx->timing_mask = 0;
+    for (int32_t i = 0; i < max_records; ++i) {
+        TimingRecord r{0, nullptr, nullptr};
+        if (hipEventCreate(&r.start) != hipSuccess) return GORILA_EHIP;
+        if (hipEventCreate(&r.stop) != hipSuccess) {
+            (void)hipEventDestroy(r.start);
+            return GORILA_EHIP;
+        }
+        ctx->records.push_back(r);
+    }
+    ctx->timing_mask = stage_mask;
+    return GORILA_OK;
+}
+
+int gorila_ctx_timing_end(gorila_ctx* ctx, double* total_ms, int32_t* count, int32_t n_stages) {
+    int rc = check_ctx(ctx);
+    if (rc) return rc;
+    if (n_stages < 0 || (n_stages > 0 && (!total_ms || !count))) return GORILA_EINVAL;
+    ctx->timing_mask = 0;
+    if (hipStreamSynchronize(ctx->stream) != hipSuccess) return GORILA_EHIP;
+    for (int32_t i = 0; i < n_stages; ++i) {
+        total_ms[i] = 0.0;
+        count[i] = 0;
+    }
+    for (size_t i = 0; i < ctx->used; ++i) {
+        const TimingRecord& r = ctx->records[i];
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess) return GORILA_EHIP;
+        if (r.stage < n_stages) {
+            total_ms[r.stage] += ms;
+            count[r.stage] += 1;
+        }
+    }
+    for (auto& r : ctx->records) {
+        (void)hipEventDestroy(r.start);
+        (void)hipEventDestroy(r.stop);
+    }
+    ctx->records.clear();
+    ctx->used = 0;
+    return GORILA_OK;
+}
+
+const char* gorila_stage_name(int32_t stage) {
+    return stage >= 0 && stage < ST_COUNT ? STAGE_NAMES[stage] : nullptr;
+}
+
+int gorila_gather(const gorila_replay* replay, const int64_t* idx, int32_t n, uint8_t* s_out,
+                  uint8_t* s2_out, int64_t* frame_map_out, int32_t* a_out, float* r_out,
+                  uint8_t* term_out, gorila_ctx* ctx) {
+    int rc = check_ctx(ctx);
+    if (rc) return rc;
+    if ((rc = check_replay(replay))) return rc;
+    if (n < 0 || (n > 0 && (!idx || !s_out || !s2_out || !a_out || !r_out || !term_out)))
+        return GORILA_EINVAL;
+    if (!aligned16(s_out) || !aligned16(s2_out)) return GORILA_EINVAL;
+    if (n == 0) return GORILA_OK;
+    const Plan p = make_plan(n, 0, 1);
+    if (p.ftab + sizeof(void*) * 8 * (size_t)n > ctx->ws_bytes) return GORILA_EWORKSPACE;
+    const uint8_t** ftab = at<const uint8_t*>(ctx, p.ftab);
+    launch_resolve(view_of(replay), idx, n, 0x7fffffff, ftab, a_out, r_out, term_out, frame_map_out,
+                   at<unsigned>(ctx, p.err), ctx->stream);
+    launch_materialize(ftab, n, s_out, s2_out, ctx->stream);
+    return check_launch();
+}
+
+int gorila_q_forward(const gorila_params* params, const uint8_t* states_u8, int32_t n,
+                     float* q_out, gorila_ctx* ctx) {
+    int rc = check_ctx(ctx);
+    if (rc) return rc;
+    if ((rc = check_params(params))) return rc;
+    if (n < 0 || (n > 0 && (!states_u8 || !q_out)) || !aligned16(states_u8)) return GORILA_EINVAL;
+    if (n == 0) return GORILA_OK;
+    const Plan p = make_plan(n, 0, params->n_actions);
+    if (p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
+    const float* theta = (const float*)params->data;
+    if ((rc = forward_one(ctx, p, theta, states_u8, n))) return rc;
+    { StageTimer t(ctx, ST_HEAD); launch_q_head(at<float>(ctx, p.h4), theta, n, params->n_actions, q_out, ctx->stream); }
+    return check_launch();
+}
+
+int gorila_act(const gorila_params* params, const uint8_t* states_u8, int32_t n, float eps,
+               uint64_t seed, int32_t* actions_out, float* q_out, gorila_ctx* ctx) {
+    int rc = check_ctx(ctx);
+    if (rc) return rc;
+    if ((rc = check_params(params))) return rc;
+    if (n < 0 || (n > 0 && (!states_u8 || !actions_out)) || !aligned16(states_u8)) return GORILA_EINVAL;
+    if (!(eps >= 0.0f && eps <= 1.0f)) return GORILA_EINVAL;
+    if (n == 0) return GORILA_OK;
+    const Plan p = make_plan(n, 0, params->n_actions);
+    if (p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
+    const float* theta = (const float*)params->data;
+    if ((rc = forward_one(ctx, p, theta, states_u8, n))) return rc;
+    {
+        StageTimer t(ctx, ST_HEAD);
+        launch_act_head(at<float>(ctx, p.h4), theta, n, params->n_actions, eps, seed, actions_out,
+                        q_out, ctx->stream);
+    }
+    return check_launch();
+}
+
+int gorila_learner_step(const gorila_params* params, const gorila_params* target_params,
+                        const gorila_replay* replay, const int64_t* idx, int32_t batch,
+                        float gamma, float clip_delta, float* grads_out, float* loss_out,
+                        gorila_ctx* ctx) {
+    int rc = check_ctx(ctx);
+    if (rc) return rc;
+    if ((rc = check_params(params)) || (rc = check_params(target_params))) return rc;
+    if (params->n_actions != target_params->n_actions) return GORILA_EINVAL;
+    if ((rc = check_replay(replay))) return rc;
+    if (batch < 1 || !idx || !grads_out || !loss_out) return GORILA_EINVAL;
+    if (!(gamma >= 0.0f && gamma <= 1.0f) || !(clip_delta > 0.0f)) return GORILA_EINVAL;
+    const int A = params->n_actions, B = batch;
+    const Plan p = make_plan(2 * (int64_t)B, B, A);
+    if (p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
+    hipStream_t st = ctx->stream;
+    const float* theta = (const float*)params->data;
+    const float* theta_t = (const float*)target_params->data;
+
+    const uint8_t** ftab = at<const uint8_t*>(ctx, p.ftab);
+    int32_t* a = at<int32_t>(ctx, p.a);
+    float* r = at<float>(ctx, p.r);
+    uint8_t* term = at<uint8_t>(ctx, p.term);
+    {
+        StageTimer t(ctx, ST_RESOLVE);
+        launch_resolve(view_of(replay), idx, B, A, ftab, a, r, term, nullptr, at<unsigned>(ctx, p.err), st);
+    }
+
+    WeightViews wv[2] = {
+        {theta, at<float>(ctx, p.w2t[0]), at<float>(ctx, p.w3t[0]), at<float>(ctx, p.w3d),
+         at<float>(ctx, p.w2d)},
+        {theta_t, at<float>(ctx, p.w2t[1]), at<float>(ctx, p.w3t[1]), nullptr, nullptr}};
+    { StageTimer t(ctx, ST_PREP); launch_prep_weights(wv, 2, st); }
+    GroupPtrs th{}, w2t{}, w3t{};
+    for (int g = 0; g < 2; ++g) {
+        th.p[g] = g ? theta_t : theta;
+        w2t.p[g] = wv[g].w2t;
+        w3t.p[g] = wv[g].w3t;
+    }
+    float* h1 = at<float>(ctx, p.h1);
+    float* h2 = at<float>(ctx, p.h2);
+    float* h3 = at<float>(ctx, p.h3);
+    float* h4 = at<float>(ctx, p.h4);
+    // online (group 0, on s) and target (group 1, on s') forward passes
+    { StageTimer t(ctx, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 2, B, h1, st); }
+    { StageTimer t(ctx, ST_CONV2_FWD); launch_conv2_fwd(h1, w2t, th, 2, B, h2, st); }
+    { StageTimer t(ctx, ST_CONV3_FWD); launch_conv3_fwd(h2, w3t, th, 2, B, h3, st); }
+    { StageTimer t(ctx, ST_FC1_FWD); launch_fc1_fwd(h3, th, 2, B, at<float>(ctx, p.fc1part), h4, st); }
+
+    float* dz4 = at<float>(ctx, p.dz4);
+    float* dz3 = at<float>(ctx, p.dz3);
+    float* dz2 = at<float>(ctx, p.dz2);
+    float* dz1 = at<float>(ctx, p.dz1);
+    float* ell = at<float>(ctx, p.ell);
+    float* coef = at<float>(ctx, p.coef);
+    {
+        StageTimer t(ctx, ST_HEAD);
+        launch_td_head(h4, theta, theta_t, B, A, a, r, term, gamma, clip_delta, at<float>(ctx, p.q),
+                       ell, coef, dz4, st);
+    }
+    { StageTimer t(ctx, ST_HEAD_REDUCE); launch_head_reduce(h4, dz4, a, coef, ell, B, A, grads_out, loss_out, st); }
+    { StageTimer t(ctx, ST_FC1_DGRAD); launch_fc1_dgrad(dz4, theta, h3, B, dz3, st); }
+    { StageTimer t(ctx, ST_FC1_WGRAD); launch_fc1_wgrad(dz4, h3, B, grads_out, st); }
+    int s1 = 0, s2 = 0, s3 = 0;
+    { StageTimer t(ctx, ST_CONV3_DGRAD); launch_conv3_dgrad(dz3, wv[0].w3d, h2, B, dz2, st); }
+    { StageTimer t(ctx, ST_CONV3_WGRAD); launch_conv3_wgrad(dz3, h2, B, at<float>(ctx, p.part3), WG_MAX_SPLITS, &s3, st); }
+    { StageTimer t(ctx, ST_CONV2_DGRAD); launch_conv2_dgrad(dz2, wv[0].w2d, h1, B, dz1, st); }
+    { StageTimer t(ctx, ST_CONV2_WGRAD); launch_conv2_wgrad(dz2, h1, B, at<float>(ctx, p.part2), WG_MAX_SPLITS, &s2, st); }
+    { StageTimer t(ctx, ST_CONV1_WGRAD); launch_conv1_wgrad(dz1, ftab, B, at<float>(ctx, p.part1), CONV1_WG_MAX_SPLITS, &s1, st); }
+    {
+        StageTimer t(ctx, ST_GRAD_REDUCE);
+        launch_bias_partials(dz1, dz2, dz3, B, at<float>(ctx, p.bpart), BIAS_BLOCKS, st);
+        launch_grad_reduce(at<float>(ctx, p.part1), s1, at<float>(ctx, p.part2), s2,
+                           at<float>(ctx, p.part3), s3, at<float>(ctx, p.bpart), BIAS_BLOCKS,
+                           grads_out, st);
+    }
+    return check_launch();
+}
+
+int gorila_learner_step_grouped(const gorila_params* params, int32_t groups,
+                                const gorila_params* target_params, const gorila_replay* replay,
+                                const int64_t* idx, int32_t batch, float gamma, float clip_delta,
+                                float* grads_out, float* loss_out, gorila_ctx* ctx) {
+    (void)params; (void)groups; (void)target_params; (void)replay; (void)idx; (void)batch;
+    (void)gamma; (void)clip_delta; (void)grads_out; (void)loss_out; (void)ctx;
+    return GORILA_EUNSUPPORTED;
+}
+
+}  // extern "C"

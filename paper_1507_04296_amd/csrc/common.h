@@ -1,0 +1,221 @@
+// Shared device-side definitions for the Gorila learner-step kernels (gfx950).
+//
+// Network (Nair et al. 2015, Section 4.1): 4x84x84 uint8 input scaled by
+// 1/255, conv 32@8x8 stride 4 -> 20x20, conv 64@4x4 stride 2 -> 9x9,
+// conv 64@3x3 stride 1 -> 7x7, FC 3136 -> 512, linear FC 512 -> A, ReLU after
+// every hidden layer.  Parameters are one flat fp32 vector: W1 [32,4,8,8],
+// b1, W2 [64,32,4,4], b2, W3 [64,64,3,3], b3, W4 [512,3136], b4, W5 [A,512], b5.
+//
+// Activation layouts in the workspace (chosen so every producer stores and
+// every consumer loads whole 16-byte vectors):
+//   h1, dz1 : [n][20][20][32]  pixel-major, channel-minor (NHWC)
+//   h2, dz2 : [n][9][9][64]    NHWC
+//   h3, dz3 : [n][64][49]      channel-major: the flatten order of the FC input
+//   h4, dz4 : [n][512]
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gorila {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int IN_C = 4, IN_H = 84, IN_W = 84;
+constexpr int FRAME_BYTES = IN_H * IN_W;          // 7056 = 441 x 16 bytes
+constexpr int STATE_BYTES = IN_C * FRAME_BYTES;   // 28224
+constexpr int C1 = 32, K1 = 8, S1 = 4, H1 = 20, P1 = H1 * H1;  // 400 pixels
+constexpr int C2 = 64, K2 = 4, S2 = 2, H2 = 9, P2 = H2 * H2;   // 81
+constexpr int C3 = 64, K3 = 3, H3 = 7, P3 = H3 * H3;           // 49
+constexpr int FLAT = C3 * P3;                                  // 3136
+constexpr int HID = 512;
+constexpr int MAX_ACTIONS = 32;
+
+constexpr int64_t OFF_W1 = 0, OFF_B1 = 8192, OFF_W2 = 8224, OFF_B2 = 40992,
+                  OFF_W3 = 41056, OFF_B3 = 77920, OFF_W4 = 77984,
+                  OFF_B4 = 1683616, OFF_W5 = 1684128;
+__host__ __device__ constexpr int64_t off_b5(int A) { return OFF_W5 + (int64_t)HID * A; }
+__host__ __device__ constexpr int64_t param_count(int A) { return off_b5(A) + A; }
+
+// Up to MAX_GROUPS parameter sets per launch, passed by value.
+constexpr int MAX_GROUPS = 32;
+struct GroupPtrs {
+    const float* p[MAX_GROUPS];
+};
+
+// Sticky device error bits (workspace word 0).
+constexpr unsigned ERR_IDX_RANGE = 1u, ERR_ACTION_RANGE = 2u;
+
+// ---------------------------------------------------------------------------
+// fp32 MFMA tile engine.
+//
+// One 256-thread workgroup (4 wave64s) computes a BM x BN tile of
+// C = sum_k A[row][k] * B[col][k] with v_mfma_f32_32x32x2_f32.  The reduction
+// runs in chunks of BK = 32 that are staged through LDS, double buffered, one
+// barrier per chunk.  Each operand tile lives in LDS in one of two layouts:
+//   KMAJ: [rows][BK + 4]   (reduction index contiguous; read as one b128)
+//   RMAJ: [BK][rows + 4]   (row index contiguous; read as four b32)
+// and is filled from global memory in 16-byte quads that are contiguous in
+// the operand's natural global layout: along k for KMAJ, along rows for RMAJ.
+//
+// Inside every group of 8 reduction indices, lane half h (lane / 32) feeds
+// indices 4h .. 4h+3 to four consecutive MFMAs, so a lane's four values are
+// one contiguous LDS vector.  A and B use the same permutation, so the sum is
+// unchanged.
+//
+// Accumulator element r of lane l in a 32x32 tile is row 8*(r/4) + 4*(l/32)
+// + r%4, column l%32, so each epilogue store of a wave writes two runs of 32
+// consecutive columns.
+// ---------------------------------------------------------------------------
+constexpr int BK = 32;
+enum { KMAJ = 0, RMAJ = 1 };
+
+template <int ROWS, int MODE>
+struct LdsTile {
+    static constexpr int LD = MODE == KMAJ ? BK + 4 : ROWS + 4;
+    static constexpr int SIZE = MODE == KMAJ ? ROWS * LD : BK * LD;  // floats
+    static constexpr int QUADS = ROWS * BK / 4;
+    static constexpr int NQ = (QUADS + 255) / 256;   // quads per thread
+
+    // Tile coordinates (row, k) of the first element of quad e.
+    __device__ static inline void quad_coord(int e, int& row, int& k) {
+        if (MODE == KMAJ) { row = e / (BK / 4); k = (e % (BK / 4)) * 4; }
+        else              { k = e / (ROWS / 4); row = (e % (ROWS / 4)) * 4; }
+    }
+    __device__ static inline void put(float* s, int row, int k, f32x4 v) {
+        if (MODE == KMAJ) *(f32x4*)(s + row * LD + k) = v;
+        else              *(f32x4*)(s + k * LD + row) = v;
+    }
+    // Values (row r, k = kb .. kb+3).
+    __device__ static inline f32x4 get(const float* s, int r, int kb) {
+        if (MODE == KMAJ) return *(const f32x4*)(s + r * LD + kb);
+        f32x4 v;
+        v[0] = s[(kb + 0) * LD + r];
+        v[1] = s[(kb + 1) * LD + r];
+        v[2] = s[(kb + 2) * LD + r];
+        v[3] = s[(kb + 3) * LD + r];
+        return v;
+    }
+};
+
+// Loaders keep per-quad state in arrays of MAXQ entries.
+constexpr int MAXQ = 4;
+
+template <int BM, int BN, int AMODE, int BMODE>
+struct GemmShape {
+    using LA = LdsTile<BM, AMODE>;
+    using LB = LdsTile<BN, BMODE>;
+    static constexpr int SMEM_FLOATS = 2 * (LA::SIZE + LB::SIZE);
+};
+
+// Loaders: `la.init(j, row, k)` is called once per quad slot j of this thread
+// with the quad's tile coordinates; `la.load(kc, j)` returns the quad for
+// reduction chunk kc (zeros where the operand is zero-padded).
+template <int BM, int BN, int WAVES_M, int AMODE, int BMODE, class LoadA, class LoadB, class Epi>
+__device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
+                                          LoadA& la, LoadB& lb, Epi& epi) {
+    using SH = GemmShape<BM, BN, AMODE, BMODE>;
+    using LA = typename SH::LA;
+    using LB = typename SH::LB;
+    constexpr int WAVES_N = 4 / WAVES_M;
+    constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
+    constexpr int TM = WM / 32, TN = WN / 32;
+    static_assert(TM * 32 == WM && TN * 32 == WN, "wave tile must be a multiple of 32");
+    static_assert(LA::NQ <= MAXQ && LB::NQ <= MAXQ, "loader state arrays hold MAXQ quads");
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave % WAVES_M, wn = wave / WAVES_M;
+    float* sa[2] = {smem, smem + LA::SIZE + LB::SIZE};
+    float* sb[2] = {smem + LA::SIZE, smem + 2 * LA::SIZE + LB::SIZE};
+
+    int qa_row[LA::NQ], qa_k[LA::NQ], qb_row[LB::NQ], qb_k[LB::NQ];
+#pragma unroll
+    for (int j = 0; j < LA::NQ; ++j) {
+        int e = tid + 256 * j;
+        if (e < LA::QUADS) { LA::quad_coord(e, qa_row[j], qa_k[j]); la.init(j, qa_row[j], qa_k[j]); }
+    }
+#pragma unroll
+    for (int j = 0; j < LB::NQ; ++j) {
+        int e = tid + 256 * j;
+        if (e < LB::QUADS) { LB::quad_coord(e, qb_row[j], qb_k[j]); lb.init(j, qb_row[j], qb_k[j]); }
+    }
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
+
+    f32x4 ra[LA::NQ], rb[LB::NQ];
+    auto gload = [&](int kc) {
+#pragma unroll
+        for (int j = 0; j < LA::NQ; ++j)
+            if (tid + 256 * j < LA::QUADS) ra[j] = la.load(kc, j);
+#pragma unroll
+        for (int j = 0; j < LB::NQ; ++j)
+            if (tid + 256 * j < LB::QUADS) rb[j] = lb.load(kc, j);
+    };
+    auto sstore = [&](int buf) {
+#pragma unroll
+        for (int j = 0; j < LA::NQ; ++j)
+            if (tid + 256 * j < LA::QUADS) LA::put(sa[buf], qa_row[j], qa_k[j], ra[j]);
+#pragma unroll
+        for (int j = 0; j < LB::NQ; ++j)
+            if (tid + 256 * j < LB::QUADS) LB::put(sb[buf], qb_row[j], qb_k[j], rb[j]);
+    };
+
+    if (kc_begin < kc_end) {
+        gload(kc_begin);
+        sstore(0);
+    }
+    __syncthreads();
+    for (int kc = kc_begin; kc < kc_end; ++kc) {
+        const int cur = (kc - kc_begin) & 1;
+        const bool more = kc + 1 < kc_end;
+        if (more) gload(kc + 1);
+#pragma unroll
+        for (int g = 0; g < BK / 8; ++g) {
+            const int kb = 8 * g + 4 * (lane >> 5);
+            f32x4 av[TM], bv[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) av[i] = LA::get(sa[cur], wm * WM + i * 32 + (lane & 31), kb);
+#pragma unroll
+            for (int j = 0; j < TN; ++j) bv[j] = LB::get(sb[cur], wn * WN + j * 32 + (lane & 31), kb);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][q], bv[j][q], acc[i][j], 0, 0, 0);
+        }
+        if (more) sstore(cur ^ 1);
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                int row = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                int col = wn * WN + j * 32 + (lane & 31);
+                epi(row, col, acc[i][j][r]);
+            }
+}
+
+// Epilogue writing scale * C into a row-major [rows][ld] buffer at column col0.
+struct PartialEpi {
+    float* out;
+    int ld, col0;
+    float scale;
+    __device__ void operator()(int row, int col, float v) const {
+        out[(int64_t)row * ld + col0 + col] = v * scale;
+    }
+};
+
+__device__ inline f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+__device__ inline f32x4 ld4(const float* p) { return *(const f32x4*)p; }
+
+}  // namespace gorila

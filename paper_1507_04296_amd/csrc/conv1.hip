@@ -1,0 +1,148 @@
+// First convolution (Section 4.1: 32 filters of 4x8x8, stride 4, ReLU) on the
+// raw uint8 frames, forward and weight gradient.
+//
+// Forward: one workgroup takes two samples, stages their 2 x 28224 input bytes
+// in LDS (16-byte copies straight from the replay frames), keeps W1 in
+// registers and runs the 800 x 32 x 256 product as 25 M-tiles of 32 pixels.
+// The reduction index is ordered (c, u, v) with lane half h feeding v = 4h..4h+3
+// of one filter row, so one aligned 4-byte LDS read gives a lane the four
+// input bytes of four consecutive MFMAs.  Bytes enter the MFMA as exact
+// integers; the 1/255 input scale is applied once in the epilogue.
+#include "common.h"
+#include "kernels.h"
+
+namespace gorila {
+
+__global__ __launch_bounds__(256, 2) void conv1_fwd_kernel(const uint8_t* const* __restrict__ ftab,
+                                                           GroupPtrs theta, int n,
+                                                           float* __restrict__ h1) {
+    __shared__ __attribute__((aligned(16))) uint8_t xs[2 * STATE_BYTES];
+    const int g = blockIdx.y, b0 = blockIdx.x * 2;
+    const int ns = min(2, n - b0);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+    constexpr int VEC = FRAME_BYTES / 16;  // 441 16-byte vectors per frame
+    for (int e = tid; e < 8 * VEC; e += 256) {
+        const int sc = e / VEC, q = e - sc * VEC;  // sc = sample * 4 + channel
+        const int s = sc >> 2, c = sc & 3;
+        const uint4* src = s < ns ? (const uint4*)ftab[((int64_t)g * n + b0 + s) * 4 + c] : nullptr;
+        ((uint4*)xs)[e] = src ? src[q] : make_uint4(0, 0, 0, 0);
+    }
+
+    const float* W1 = theta.p[g];
+    const int col = lane & 31, h = lane >> 5;
+    float w[128];  // w[4*(c*8+u) + q] = W1[col][c][u][4h+q]
+#pragma unroll
+    for (int cb = 0; cb < 32; ++cb) {
+        f32x4 v = ld4(W1 + OFF_W1 + col * 256 + cb * 8 + 4 * h);
+        w[4 * cb + 0] = v[0];
+        w[4 * cb + 1] = v[1];
+        w[4 * cb + 2] = v[2];
+        w[4 * cb + 3] = v[3];
+    }
+    const float bias = W1[OFF_B1 + col];
+    __syncthreads();
+
+    const int rows = ns * P1;
+    const int ntiles = (rows + 31) / 32;
+    float* out = h1 + ((int64_t)g * n + b0) * P1 * C1;
+    for (int t = wave; t < ntiles; t += 4) {
+        int m = t * 32 + (lane & 31);
+        if (m >= rows) m = 0;  // padding rows compute on a valid pixel, never stored
+        const int s = m / P1, p = m - s * P1, i = p / H1, j = p - i * H1;
+        const uint8_t* base = xs + s * STATE_BYTES + (S1 * i) * IN_W + S1 * j + 4 * h;
+        f32x16 acc = f32x16{};
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const uint32_t d = *(const uint32_t*)(base + c * FRAME_BYTES + u * IN_W);
+                const int cb = c * 8 + u;
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32((float)(d & 255u), w[4 * cb + 0], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32((float)((d >> 8) & 255u), w[4 * cb + 1], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32((float)((d >> 16) & 255u), w[4 * cb + 2], acc, 0, 0, 0);
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32((float)(d >> 24), w[4 * cb + 3], acc, 0, 0, 0);
+            }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int row = t * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (row < rows) out[(int64_t)row * C1 + col] = fmaxf(acc[r] * (1.0f / 255.0f) + bias, 0.0f);
+        }
+    }
+}
+
+void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int groups, int n,
+                      float* h1, hipStream_t st) {
+    if (n <= 0) return;
+    conv1_fwd_kernel<<<dim3((n + 1) / 2, groups), 256, 0, st>>>(ftab, theta, n, h1);
+}
+
+// Weight gradient: dW1[o][(c,u,v)] = (1/255) sum_pixels dz1[pixel][o] * x[c][4i+u][4j+v]
+// over every pixel of the n online samples.  Rows o (32), columns (c,u,v)
+// (256, two tiles of 128), reduction over pixels split across workgroups;
+// partial[split][o][k] is summed in a fixed order afterwards.
+struct Conv1WgradA {  // dz1 rows o, RMAJ quads along o at one pixel
+    const float* dz1;
+    int npix;
+    int o0[MAXQ];
+    int kk[MAXQ];
+    __device__ void init(int j, int row, int k) { o0[j] = row; kk[j] = k; }
+    __device__ f32x4 load(int kc, int j) const {
+        const int m = kc * BK + kk[j];
+        return m < npix ? ld4(dz1 + (int64_t)m * C1 + o0[j]) : zero4();
+    }
+};
+
+struct Conv1WgradB {  // input bytes rows (c,u,v), RMAJ quads along v at one pixel
+    const uint8_t* const* ftab;
+    int npix, col0;
+    int chan[MAXQ], off[MAXQ], kk[MAXQ];
+    __device__ void init(int j, int row, int k) {
+        const int kr = col0 + row;  // (c, u, v0) with v0 in {0, 4}
+        chan[j] = kr >> 6;
+        off[j] = ((kr >> 3) & 7) * IN_W + (kr & 7);
+        kk[j] = k;
+    }
+    __device__ f32x4 load(int kc, int j) const {
+        const int m = kc * BK + kk[j];
+        if (m >= npix) return zero4();
+        const int b = m / P1, p = m - b * P1, i = p / H1, jj = p - i * H1;
+        const uint8_t* f = ftab[(int64_t)b * 4 + chan[j]];
+        if (!f) return zero4();
+        const uint32_t d = *(const uint32_t*)(f + (S1 * i) * IN_W + S1 * jj + off[j]);
+        return f32x4{(float)(d & 255u), (float)((d >> 8) & 255u), (float)((d >> 16) & 255u),
+                     (float)(d >> 24)};
+    }
+};
+
+constexpr int C1W_BN = 128;
+
+__global__ __launch_bounds__(256) void conv1_wgrad_kernel(const float* __restrict__ dz1,
+                                                          const uint8_t* const* __restrict__ ftab,
+                                                          int n, int chunks_per_split,
+                                                          float* __restrict__ partial) {
+    using SH = GemmShape<32, C1W_BN, RMAJ, RMAJ>;
+    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
+    const int col0 = blockIdx.x * C1W_BN, split = blockIdx.y;
+    const int npix = n * P1;
+    const int nchunks = (npix + BK - 1) / BK;
+    const int kc0 = split * chunks_per_split;
+    const int kc1 = min(nchunks, kc0 + chunks_per_split);
+    Conv1WgradA la{dz1, npix};
+    Conv1WgradB lb{ftab, npix, col0};
+    PartialEpi epi{partial + (int64_t)split * C1 * 256, 256, col0, 1.0f / 255.0f};
+    mfma_gemm<32, C1W_BN, 1, RMAJ, RMAJ>(smem, kc0, kc1, la, lb, epi);
+}
+
+void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int n, float* partial,
+                        int max_splits, int* splits_out, hipStream_t st) {
+    const int nchunks = (n * P1 + BK - 1) / BK;
+    int splits = min(max_splits, max(1, 512 / (256 / C1W_BN)));
+    splits = min(splits, nchunks);
+    const int cps = (nchunks + splits - 1) / splits;
+    splits = (nchunks + cps - 1) / cps;
+    *splits_out = splits;
+    conv1_wgrad_kernel<<<dim3(256 / C1W_BN, splits), 256, 0, st>>>(dz1, ftab, n, cps, partial);
+}
+
+}  // namespace gorila

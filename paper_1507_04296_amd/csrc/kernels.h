@@ -1,0 +1,98 @@
+// Host-side launchers of the Gorila kernels (internal to libgorila).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/gorila.h"
+#include "common.h"
+
+namespace gorila {
+
+// Replay source as the kernels see it.
+struct ReplayView {
+    int kind;
+    const uint8_t* s;
+    const uint8_t* s2;
+    const uint8_t* term;
+    int64_t rows;
+    const uint8_t* frames;
+    const uint8_t* ep_start;
+    int64_t capacity;
+    int64_t head;
+    const int32_t* action;
+    const float* reward;
+};
+
+// Resolve minibatch indices: frame pointers ftab[2][n][4] (s then s'; null =
+// zero-filled channel), a/r/term per row, optional frame map [n][2][4].
+void launch_resolve(const ReplayView& rv, const int64_t* idx, int n, int n_actions,
+                    const uint8_t** ftab, int32_t* a, float* r, uint8_t* term,
+                    int64_t* frame_map, unsigned* err, hipStream_t st);
+
+// Copy the stacks named by ftab into s_out / s2_out [n][4][84][84].
+void launch_materialize(const uint8_t* const* ftab, int n, uint8_t* s_out, uint8_t* s2_out,
+                        hipStream_t st);
+
+// Transposed conv weights used as MFMA operands.
+//  w2t [16][64][32]: W2[o][c][u][v] at [(u,v)][o][c]   (conv2 forward)
+//  w3t [9][64][64]:  W3[o][c][u][v] at [(u,v)][o][c]   (conv3 forward)
+//  w3d [9][64][64]:  W3[o][c][u][v] at [(u,v)][c][o]   (conv3 data gradient)
+//  w2d [16][32][64]: W2[o][c][u][v] at [(u,v)][c][o]   (conv2 data gradient)
+struct WeightViews {
+    const float* theta;   // flat parameters
+    float* w2t;
+    float* w3t;
+    float* w3d;           // may be null (forward only)
+    float* w2d;           // may be null
+};
+void launch_prep_weights(const WeightViews* nets, int n_nets, hipStream_t st);
+
+// Forward layers.  `groups` parameter sets; group g owns rows [g*n, (g+1)*n)
+// of every activation buffer.
+void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int groups, int n,
+                      float* h1, hipStream_t st);
+void launch_conv2_fwd(const float* h1, const GroupPtrs& w2t, const GroupPtrs& theta, int groups,
+                      int n, float* h2, hipStream_t st);
+void launch_conv3_fwd(const float* h2, const GroupPtrs& w3t, const GroupPtrs& theta, int groups,
+                      int n, float* h3, hipStream_t st);
+void launch_fc1_fwd(const float* h3, const GroupPtrs& theta, int groups, int n, float* partial,
+                    float* h4, hipStream_t st);
+
+// Head: Q values, epsilon-greedy actions, TD error / Huber loss / dLoss.
+void launch_q_head(const float* h4, const float* theta, int n, int A, float* q, hipStream_t st);
+void launch_act_head(const float* h4, const float* theta, int n, int A, float eps, uint64_t seed,
+                     int32_t* actions, float* q_out, hipStream_t st);
+void launch_td_head(const float* h4, const float* theta, const float* theta_target, int n, int A,
+                    const int32_t* a, const float* r, const uint8_t* term, float gamma, float clip,
+                    float* q, float* ell, float* coef, float* dz4, hipStream_t st);
+void launch_head_reduce(const float* h4, const float* dz4, const int32_t* a, const float* coef,
+                        const float* ell, int n, int A, float* grads, float* loss_out,
+                        hipStream_t st);
+
+// Backward layers.
+void launch_fc1_dgrad(const float* dz4, const float* theta, const float* h3, int n, float* dz3,
+                      hipStream_t st);
+void launch_fc1_wgrad(const float* dz4, const float* h3, int n, float* grads, hipStream_t st);
+void launch_conv3_dgrad(const float* dz3, const float* w3d, const float* h2, int n, float* dz2,
+                        hipStream_t st);
+void launch_conv3_wgrad(const float* dz3, const float* h2, int n, float* partial, int max_splits,
+                        int* splits_out, hipStream_t st);
+void launch_conv2_dgrad(const float* dz2, const float* w2d, const float* h1, int n, float* dz1,
+                        hipStream_t st);
+void launch_conv2_wgrad(const float* dz2, const float* h1, int n, float* partial, int max_splits,
+                        int* splits_out, hipStream_t st);
+void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int n, float* partial,
+                        int max_splits, int* splits_out, hipStream_t st);
+void launch_bias_partials(const float* dz1, const float* dz2, const float* dz3, int n,
+                          float* bpart, int nblk, hipStream_t st);
+void launch_grad_reduce(const float* part1, int s1, const float* part2, int s2,
+                        const float* part3, int s3, const float* bpart, int nblk,
+                        float* grads, hipStream_t st);
+
+// Sizes of the split-K / partial buffers the launchers above may use.
+constexpr int FC1_MAX_SPLITS = 14;
+constexpr int WG_MAX_SPLITS = 128;
+constexpr int CONV1_WG_MAX_SPLITS = 256;
+constexpr int BIAS_BLOCKS = 64;
+
+}  // namespace gorila

@@ -1,0 +1,628 @@
+// Convolution 2/3 and FC-512 layers, forward and backward, as implicit GEMMs
+// on the fp32 MFMA tile engine (common.h).  Shapes follow Section 4.1 of the
+// paper; the backward pass is the exact gradient of those layers (eq. (2)
+// needs grad_theta Q(s, a; theta)).
+//
+// Every layer below is written as C[row][col] = sum_k A[row][k] * B[col][k]
+// plus an epilogue.  Reduction indices of convolutions are ordered
+// (tap (u,v), channel): one reduction chunk of 32 is one tap and 32 channels,
+// so activation quads are 16 contiguous bytes of an NHWC pixel.
+#include "common.h"
+#include "kernels.h"
+
+namespace gorila {
+
+// ---------------------------------------------------------------------------
+// Weight transposes (run once per call, small: < 0.3 MB)
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void prep_weights_kernel(WeightViews v0, WeightViews v1,
+                                                           int n_nets) {
+    const WeightViews v = blockIdx.y == 0 ? v0 : v1;
+    if ((int)blockIdx.y >= n_nets) return;
+    const float* W2 = v.theta + OFF_W2;
+    const float* W3 = v.theta + OFF_W3;
+    for (int e = blockIdx.x * 256 + threadIdx.x; e < 16 * 64 * 32; e += gridDim.x * 256) {
+        // e = ((o*32 + c)*4 + u)*4 + v  ->  W2[o][c][u][v]
+        const int vv = e & 3, u = (e >> 2) & 3, c = (e >> 4) & 31, o = e >> 9;
+        const float x = W2[e];
+        const int t = u * 4 + vv;
+        v.w2t[(t * 64 + o) * 32 + c] = x;
+        if (v.w2d) v.w2d[(t * 32 + c) * 64 + o] = x;
+    }
+    for (int e = blockIdx.x * 256 + threadIdx.x; e < 9 * 64 * 64; e += gridDim.x * 256) {
+        // e = ((o*64 + c)*3 + u)*3 + v
+        const int vv = e % 3, u = (e / 3) % 3, c = (e / 9) % 64, o = e / 576;
+        const float x = W3[e];
+        const int t = u * 3 + vv;
+        v.w3t[(t * 64 + o) * 64 + c] = x;
+        if (v.w3d) v.w3d[(t * 64 + c) * 64 + o] = x;
+    }
+}
+
+void launch_prep_weights(const WeightViews* nets, int n_nets, hipStream_t st) {
+    prep_weights_kernel<<<dim3(64, n_nets), 256, 0, st>>>(nets[0], n_nets > 1 ? nets[1] : nets[0],
+                                                          n_nets);
+}
+
+// ---------------------------------------------------------------------------
+// conv2 forward: h2[m][o] = relu(b2[o] + sum_{u,v,c} W2[o][c][u][v] h1[b][2i+u][2j+v][c])
+// rows m = (b,i,j) of one group, cols o; 16 chunks = 16 taps x 32 channels.
+// ---------------------------------------------------------------------------
+struct Conv2FwdA {
+    const float* h1;
+    int rows, m0;
+    const float* base[MAXQ];
+    __device__ void init(int j, int row, int k) {
+        const int m = m0 + row;
+        const int mm = m < rows ? m : 0;
+        const int b = mm / P2, p = mm - b * P2, i = p / H2, jj = p - i * H2;
+        const float* ptr = h1 + (((int64_t)b * H1 + S2 * i) * H1 + S2 * jj) * C1 + k;
+        base[j] = m < rows ? ptr : nullptr;
+    }
+    __device__ f32x4 load(int kc, int j) const {
+        if (!base[j]) return zero4();
+        const int u = kc >> 2, v = kc & 3;
+        return ld4(base[j] + (u * H1 + v) * C1);
+    }
+};
+struct WtapB {  // transposed weights w[tap][row][k]; per_tap chunks of 32 k per tap
+    const float* w;
+    int ldk;      // k extent of one row
+    int per_tap;  // chunks per tap
+    int rows;     // rows per tap
+    const float* base[MAXQ];
+    __device__ void init(int j, int row, int k) { base[j] = w + (int64_t)row * ldk + k; }
+    __device__ f32x4 load(int kc, int j) const {
+        const int t = kc / per_tap, part = kc - t * per_tap;
+        return ld4(base[j] + (int64_t)t * rows * ldk + part * BK);
+    }
+};
+struct BiasReluStore {
+    float* out;
+    const float* bias;
+    int rows, m0, ld;
+    __device__ void operator()(int row, int col, float v) const {
+        const int m = m0 + row;
+        if (m < rows) out[(int64_t)m * ld + col] = fmaxf(v + bias[col], 0.0f);
+    }
+};
+
+__global__ __launch_bounds__(256) void conv2_fwd_kernel(const float* __restrict__ h1, GroupPtrs w2t,
+                                                        GroupPtrs theta, int n,
+                                                        float* __restrict__ h2) {
+    using SH = GemmShape<64, 64, KMAJ, KMAJ>;
+    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
+    const int g = blockIdx.y, m0 = blockIdx.x * 64;
+    const int rows = n * P2;
+    Conv2FwdA la{h1 + (int64_t)g * n * P1 * C1, rows, m0};
+    WtapB lb{w2t.p[g], C1, 1, C2};
+    BiasReluStore epi{h2 + (int64_t)g * n * P2 * C2, theta.p[g] + OFF_B2, rows, m0, C2};
+    mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, 0, 16, la, lb, epi);
+}
+
+void launch_conv2_fwd(const float* h1, const GroupPtrs& w2t, const GroupPtrs& theta, int groups,
+                      int n, float* h2, hipStream_t st) {
+    if (n <= 0) return;
+    conv2_fwd_kernel<<<dim3((n * P2 + 63) / 64, groups), 256, 0, st>>>(h1, w2t, theta, n, h2);
+}
+
+// ---------------------------------------------------------------------------
+// conv3 forward, computed transposed so the channel-major (flatten-order)
+// output is stored along pixels: h3[b][o][p] = relu(b3[o] + sum W3 h2[b][i+u][j+v][c]).
+// rows o (64), cols m = (b,p) of one group; 18 chunks = 9 taps x 2 halves of c.
+// ---------------------------------------------------------------------------
+struct Conv3FwdB {
+    const float* h2;
+    int rows, m0;
+    const float* base[MAXQ];
+    __device__ void init(int j, int row, int k) {
+        const int m = m0 + row;
+        const int mm = m < rows ? m : 0;
+        const int b = mm / P3, p = mm - b * P3, i = p / H3, jj = p - i * H3;
+        const float* ptr = h2 + (((int64_t)b * H2 + i) * H2 + jj) * C2 + k;
+        base[j] = m < rows ? ptr : nullptr;
+    }
+    __device__ f32x4 load(int kc, int j) const {
+        if (!base[j]) return zero4();
+        const int t = kc >> 1, u = t / 3, v = t - u * 3;
+        return ld4(base[j] + (u * H2 + v) * C2 + (kc & 1) * BK);
+    }
+};
+struct Conv3FwdStore {  // row = o, col = pixel index within the tile
+    float* out;
+    const float* bias;
+    int rows, m0;
+    __device__ void operator()(int row, int col, float v) const {
+        const int m = m0 + col;
+        if (m >= rows) return;
+        const int b = m / P3, p = m - b * P3;
+        out[(int64_t)b * FLAT + row * P3 + p] = fmaxf(v + bias[row], 0.0f);
+    }
+};
+
+__global__ __launch_bounds__(256) void conv3_fwd_kernel(const float* __restrict__ h2, GroupPtrs w3t,
+                                                        GroupPtrs theta, int n,
+                                                        float* __restrict__ h3) {
+    using SH = GemmShape<64, 64, KMAJ, KMAJ>;
+    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
+    const int g = blockIdx.y, m0 = blockIdx.x * 64;
+    const int rows = n * P3;
+    WtapB la{w3t.p[g], C2, 2, C3};
+    Conv3FwdB lb{h2 + (int64_t)g * n * P2 * C2, rows, m0};
+    Conv3FwdStore epi{h3 + (int64_t)g * n * FLAT, theta.p[g] + OFF_B3, rows, m0};
+    mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, 0, 18, la, lb, epi);
+}
+
+void launch_conv3_fwd(const float* h2, const GroupPtrs& w3t, const GroupPtrs& theta, int groups,
+                      int n, float* h3, hipStream_t st) {
+    if (n <= 0) return;
+    conv3_fwd_kernel<<<dim3((n * P3 + 63) / 64, groups), 256, 0, st>>>(h2, w3t, theta, n, h3);
+}
+
+// ---------------------------------------------------------------------------
+// fc1 forward, split over the 3136-long reduction: partial[g][s][b][o];
+// a second pass adds the splits in order, the bias and the ReLU.
+// ---------------------------------------------------------------------------
+struct RowMajorK {  // rows of a row-major [rows][ld] matrix, quads along k
+    const float* a;
+    int rows, r0, ld;
+    const float* base[MAXQ];
+    __device__ void init(int j, int row, int k) {
+        base[j] = r0 + row < rows ? a + (int64_t)(r0 + row) * ld + k : nullptr;
+    }
+    __device__ f32x4 load(int kc, int j) const { return base[j] ? ld4(base[j] + kc * BK) : zero4(); }
+};
+struct PlainStore {
+    float* out;
+    int rows, r0, c0, ld;
+    __device__ void operator()(int row, int col, float v) const {
+        if (r0 + row < rows) out[(int64_t)(r0 + row) * ld + c0 + col] = v;
+    }
+};
+
+constexpr int FC1_CHUNKS = FLAT / BK;  // 98
+
+__global__ __launch_bounds__(256) void fc1_fwd_kernel(const float* __restrict__ h3, GroupPtrs theta,
+                                                      int n, int splits, int cps,
+                                                      float* __restrict__ partial) {
+    using SH = GemmShape<64, 64, KMAJ, KMAJ>;
+    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
+    const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+    const int g = blockIdx.z / splits, s = blockIdx.z - g * splits;
+    RowMajorK la{h3 + (int64_t)g * n * FLAT, n, r0, FLAT};
+    RowMajorK lb{theta.p[g] + OFF_W4, HID, c0, FLAT};
+    PlainStore epi{partial + ((int64_t)g * splits + s) * n * HID, n, r0, c0, HID};
+    const int kc0 = s * cps, kc1 = min(FC1_CHUNKS, kc0 + cps);
+    mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, kc0, kc1, la, lb, epi);
+}
+
+__global__ __launch_bounds__(256) void fc1_fwd_reduce_kernel(const float* __restrict__ partial,
+                                                             GroupPtrs theta, int n, int splits,
+                                                             float* __restrict__ h4) {
+    const int g = blockIdx.y;
+    const int64_t per = (int64_t)n * HID;
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < per; e += (int64_t)gridDim.x * 256) {
+        const float* p = partial + (int64_t)g * splits * per + e;
+        float acc = 0.0f;
+        for (int s = 0; s < splits; ++s) acc += p[s * per];
+        const int o = (int)(e % HID);
+        h4[(int64_t)g * per + e] = fmaxf(acc + theta.p[g][OFF_B4 + o], 0.0f);
+    }
+}
+
+void launch_fc1_fwd(const float* h3, const GroupPtrs& theta, int groups, int n, float* partial,
+                    float* h4, hipStream_t st) {
+    if (n <= 0) return;
+    const int mt = (n + 63) / 64, tiles = mt * (HID / 64) * groups;
+    int splits = min(FC1_MAX_SPLITS, max(1, (512 + tiles - 1) / tiles));
+    const int cps = (FC1_CHUNKS + splits - 1) / splits;
+    splits = (FC1_CHUNKS + cps - 1) / cps;
+    fc1_fwd_kernel<<<dim3(mt, HID / 64, groups * splits), 256, 0, st>>>(h3, theta, n, splits, cps,
+                                                                         partial);
+    const int64_t want = ((int64_t)n * HID + 255) / 256;
+    const int blocks = (int)(want < 1024 ? want : 1024);
+    fc1_fwd_reduce_kernel<<<dim3(blocks, groups), 256, 0, st>>>(partial, theta, n, splits, h4);
+}
+
+// ---------------------------------------------------------------------------
+// fc1 data gradient: dz3[b][k] = [h3[b][k] > 0] * sum_o dz4[b][o] W4[o][k]
+// rows b, cols k (3136 = 49 tiles), reduction o (16 chunks).
+// ---------------------------------------------------------------------------
+struct RowMajorR {  // B[col][k] = M[k][c0 + col] of a row-major [k][ld] matrix (RMAJ quads)
+    const float* a;
+    int c0, ld, kmax;
+    const float* base[MAXQ];
+    int kk[MAXQ];
+    __device__ void init(int j, int row, int k) { base[j] = a + c0 + row; kk[j] = k; }
+    __device__ f32x4 load(int kc, int j) const {
+        const int k = kc * BK + kk[j];
+        return k < kmax ? ld4(base[j] + (int64_t)k * ld) : zero4();
+    }
+};
+struct ReluMaskStore {  // out[r][c] = mask[r][c] > 0 ? v : 0
+    float* out;
+    const float* mask;
+    int rows, r0, c0, ld;
+    __device__ void operator()(int row, int col, float v) const {
+        const int r = r0 + row;
+        if (r >= rows) return;
+        const int64_t e = (int64_t)r * ld + c0 + col;
+        out[e] = mask[e] > 0.0f ? v : 0.0f;
+    }
+};
+
+__global__ __launch_bounds__(256) void fc1_dgrad_kernel(const float* __restrict__ dz4,
+                                                        const float* __restrict__ W4,
+                                                        const float* __restrict__ h3, int n,
+                                                        float* __restrict__ dz3) {
+    using SH = GemmShape<64, 64, KMAJ, RMAJ>;
+    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
+    const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+    RowMajorK la{dz4, n, r0, HID};
+    RowMajorR lb{W4, c0, FLAT, HID};
+    ReluMaskStore epi{dz3, h3, n, r0, c0, FLAT};
+    mfma_gemm<64, 64, 2, KMAJ, RMAJ>(smem, 0, HID / BK, la, lb, epi);
+}
+
+void launch_fc1_dgrad(const float* dz4, const float* theta, const float* h3, int n, float* dz3,
+                      hipStream_t st) {
+    if (n <= 0) return;
+    fc1_dgrad_kernel<<<dim3((n + 63) / 64, FLAT / 64), 256, 0, st>>>(dz4, theta + OFF_W4, h3, n, dz3);
+}
+
+// ---------------------------------------------------------------------------
+// fc1 weight gradient: dW4[o][k] = sum_b dz4[b][o] h3[b][k]  (written in place)
+// rows o (512), cols k (3136), reduction b.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void fc1_wgrad_kernel(const float* __restrict__ dz4,
+                                                        const float* __restrict__ h3, int n,
+                                                        float* __restrict__ gW4) {
+    using SH = GemmShape<64, 64, RMAJ, RMAJ>;
+    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
+    const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+    RowMajorR la{dz4, r0, HID, n};
+    RowMajorR lb{h3, c0, FLAT, n};
+    PlainStore epi{gW4, HID, r0, c0, FLAT};
+    mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, 0, (n + BK - 1) / BK, la, lb, epi);
+}
+
+void launch_fc1_wgrad(const float* dz4, const float* h3, int n, float* grads, hipStream_t st) {
+    if (n <= 0) return;
+    fc1_wgrad_kernel<<<dim3(HID / 64, FLAT / 64), 256, 0, st>>>(dz4, h3, n, grads + OFF_W4);
+}
+
+// ---------------------------------------------------------------------------
+// conv3 data gradient (stride 1): dh2[b][y][x][c] = sum_{u,v,o} W3[o][c][u][v]
+// dz3[b][o][y-u][x-v] over in-range (y-u, x-v); then dz2 = dh2 * [h2 > 0].
+// rows m = (b,y,x), cols c (64), reduction (tap, o) = 18 chunks.
+// ---------------------------------------------------------------------------
+struct Conv3DgradA {  // RMAJ quads: 4 consecutive output pixels at one (tap, o)
+    const float* dz3;
+    int rows, m0;
+    int pb[MAXQ][4], py[MAXQ][4], px[MAXQ][4];
+    int kk[MAXQ];
+    __device__ void init(int j, int row, int k) {
+        kk[j] = k;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int m = m0 + row + q;
+            const int mm = m < rows ? m : 0;
+            const int b = mm / P2, p = mm - b * P2;
+            pb[j][q] = m < rows ? b : -1;
+            py[j][q] = p / H2;
+            px[j][q] = p - (p / H2) * H2;
+        }
+    }
+    __device__ f32x4 load(int kc, int j) const {
+        const int t = kc >> 1, u = t / 3, v = t - u * 3;
+        const int o = (kc & 1) * BK + kk[j];
+        f32x4 r;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int i = py[j][q] - u, jj = px[j][q] - v;
+            const bool ok = pb[j][q] >= 0 && i >= 0 && i < H3 && jj >= 0 && jj < H3;
+            r[q] = ok ? dz3[(int64_t)pb[j][q] * FLAT + o * P3 + i * H3 + jj] : 0.0f;
+        }
+        return r;
+    }
+};
+
+__global__ __launch_bounds__(256) void conv3_dgrad_kernel(const float* __restrict__ dz3,
+                                                          const float* __restrict__ w3d,
+                                                          const float* __restrict__ h2, int n,
+                                                          float* __restrict__ dz2) {
+    using SH = GemmShape<64, 64, RMAJ, KMAJ>;
+    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
+    const int m0 = blockIdx.x * 64;
+    const int rows = n * P2;
+    Conv3DgradA la{dz3, rows, m0};
+    WtapB lb{w3d, C3, 2, C2};
+    ReluMaskStore epi{dz2, h2, rows, m0, 0, C2};
+    mfma_gemm<64, 64, 2, RMAJ, KMAJ>(smem, 0, 18, la, lb, epi);
+}
+
+void launch_conv3_dgrad(const float* dz3, const float* w3d, const float* h2, int n, float* dz2,
+                        hipStream_t st) {
+    if (n <= 0) return;
+    conv3_dgrad_kernel<<<(n * P2 + 63) / 64, 256, 0, st>>>(dz3, w3d, h2, n, dz2);
+}
+
+// ---------------------------------------------------------------------------
+// conv3 weight gradient: dW3[o][c][u][v] = sum_{b,i,j} dz3[b][o][i][j] h2[b][i+u][j+v][c]
+// rows o (64), cols (tap, c): one tap of 64 channels per column tile,
+// reduction over the n*49 output pixels, split across workgroups.
+// partial[s][o][tap*64 + c].
+// ---------------------------------------------------------------------------
+struct Conv3WgradA {  // KMAJ quads: 4 consecutive output pixels of channel o
+    const float* dz3;
+    int npix;
+    int o[MAXQ], kk[MAXQ];
+    __device__ void init(int j, int row, int k) { o[j] = row; kk[j] = k; }
+    __device__ f32x4 load(int kc, int j) const {
+        f32x4 r;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int m = kc * BK + kk[j] + q;
+            const int mm = m < npix ? m : 0;
+            const int b = mm / P3, p = mm - b * P3;
+            const float x = dz3[(int64_t)b * FLAT + o[j] * P3 + p];
+            r[q] = m < npix ? x : 0.0f;
+        }
+        return r;
+    }
+};
+struct Conv3WgradB {  // RMAJ quads: 4 channels of h2 at one (pixel, tap)
+    const float* h2;
+    int npix, tap;
+    int c0[MAXQ], kk[MAXQ];
+    __device__ void init(int j, int row, int k) { c0[j] = row; kk[j] = k; }
+    __device__ f32x4 load(int kc, int j) const {
+        const int m = kc * BK + kk[j];
+        if (m >= npix) return zero4();
+        const int b = m / P3, p = m - b * P3, i = p / H3, jj = p - i * H3;
+        const int u = tap / 3, v = tap - u * 3;
+        return ld4(h2 + (((int64_t)b * H2 + i + u) * H2 + jj + v) * C2 + c0[j]);
+    }
+};
+
+__global__ __launch_bounds__(256) void conv3_wgrad_kernel(const float* __restrict__ dz3,
+                                                          const float* __restrict__ h2, int n,
+                                                          int cps, float* __restrict__ partial) {
+    using SH = GemmShape<64, 64, KMAJ, RMAJ>;
+    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
+    const int tap = blockIdx.x, s = blockIdx.y;
+    const int npix = n * P3, nchunks = (npix + BK - 1) / BK;
+    Conv3WgradA la{dz3, npix};
+    Conv3WgradB lb{h2, npix, tap};
+    PartialEpi epi{partial + (int64_t)s * C3 * 9 * C2, 9 * C2, tap * C2, 1.0f};
+    mfma_gemm<64, 64, 2, KMAJ, RMAJ>(smem, s * cps, min(nchunks, (s + 1) * cps), la, lb, epi);
+}
+
+void launch_conv3_wgrad(const float* dz3, const float* h2, int n, float* partial, int max_splits,
+                        int* splits_out, hipStream_t st) {
+    const int nchunks = (n * P3 + BK - 1) / BK;
+    int splits = min(min(max_splits, nchunks), max(1, (512 + 8) / 9));
+    const int cps = (nchunks + splits - 1) / splits;
+    splits = (nchunks + cps - 1) / cps;
+    *splits_out = splits;
+    conv3_wgrad_kernel<<<dim3(9, splits), 256, 0, st>>>(dz3, h2, n, cps, partial);
+}
+
+// ---------------------------------------------------------------------------
+// conv2 data gradient (stride 2), split by output phase (y mod 2, x mod 2) so
+// that no inserted zeros are multiplied: output (2y'+py, 2x'+px) receives taps
+// u = py + 2du, v = px + 2dv from dz2[y'-du][x'-dv], du, dv in {0, 1}.
+// rows m = (b, y', x') (10 x 10 per sample), cols c (32),
+// reduction (du, dv, o) = 8 chunks; dz1 = dh1 * [h1 > 0].
+// ---------------------------------------------------------------------------
+struct Conv2DgradA {
+    const float* dz2;
+    int rows, m0;
+    int pb[MAXQ], yy[MAXQ], xx[MAXQ], kk[MAXQ];
+    __device__ void init(int j, int row, int k) {
+        const int m = m0 + row;
+        const int mm = m < rows ? m : 0;
+        const int b = mm / 100, p = mm - b * 100;
+        kk[j] = k;
+        pb[j] = m < rows ? b : -1;
+        yy[j] = p / 10;
+        xx[j] = p - (p / 10) * 10;
+    }
+    __device__ f32x4 load(int kc, int j) const {
+        const int t = kc >> 1, du = t >> 1, dv = t & 1;
+        const int i = yy[j] - du, jj = xx[j] - dv;
+        if (pb[j] < 0 || i < 0 || i >= H2 || jj < 0 || jj >= H2) return zero4();
+        return ld4(dz2 + (((int64_t)pb[j] * H2 + i) * H2 + jj) * C2 + (kc & 1) * BK + kk[j]);
+    }
+};
+struct Conv2DgradB {  // w2d[(u,v)][c][o], rows c, quads along o
+    const float* w2d;
+    int py, px;
+    const float* base[MAXQ];
+    __device__ void init(int j, int row, int k) { base[j] = w2d + row * C2 + k; }
+    __device__ f32x4 load(int kc, int j) const {
+        const int t = kc >> 1, u = py + 2 * (t >> 1), v = px + 2 * (t & 1);
+        return ld4(base[j] + (u * K2 + v) * C1 * C2 + (kc & 1) * BK);
+    }
+};
+struct Conv2DgradStore {
+    float* dz1;
+    const float* h1;
+    int rows, m0, py, px;
+    __device__ void operator()(int row, int col, float v) const {
+        const int m = m0 + row;
+        if (m >= rows) return;
+        const int b = m / 100, p = m - b * 100, y = 2 * (p / 10) + py, x = 2 * (p % 10) + px;
+        const int64_t e = (((int64_t)b * H1 + y) * H1 + x) * C1 + col;
+        dz1[e] = h1[e] > 0.0f ? v : 0.0f;
+    }
+};
+
+__global__ __launch_bounds__(256) void conv2_dgrad_kernel(const float* __restrict__ dz2,
+                                                          const float* __restrict__ w2d,
+                                                          const float* __restrict__ h1, int n,
+                                                          float* __restrict__ dz1) {
+    using SH = GemmShape<128, 32, KMAJ, KMAJ>;
+    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
+    const int m0 = blockIdx.x * 128, py = blockIdx.y >> 1, px = blockIdx.y & 1;
+    const int rows = n * 100;
+    Conv2DgradA la{dz2, rows, m0};
+    Conv2DgradB lb{w2d, py, px};
+    Conv2DgradStore epi{dz1, h1, rows, m0, py, px};
+    mfma_gemm<128, 32, 4, KMAJ, KMAJ>(smem, 0, 8, la, lb, epi);
+}
+
+void launch_conv2_dgrad(const float* dz2, const float* w2d, const float* h1, int n, float* dz1,
+                        hipStream_t st) {
+    if (n <= 0) return;
+    conv2_dgrad_kernel<<<dim3((n * 100 + 127) / 128, 4), 256, 0, st>>>(dz2, w2d, h1, n, dz1);
+}
+
+// ---------------------------------------------------------------------------
+// conv2 weight gradient: dW2[o][c][u][v] = sum_{b,i,j} dz2[b][i][j][o] h1[b][2i+u][2j+v][c]
+// rows o (64), cols (tap, c) with two taps per 64-column tile, reduction over
+// the n*81 output pixels split across workgroups.  partial[s][o][tap*32 + c].
+// ---------------------------------------------------------------------------
+struct Conv2WgradA {  // dz2 quads along o at one pixel
+    const float* dz2;
+    int npix;
+    int o0[MAXQ], kk[MAXQ];
+    __device__ void init(int j, int row, int k) { o0[j] = row; kk[j] = k; }
+    __device__ f32x4 load(int kc, int j) const {
+        const int m = kc * BK + kk[j];
+        return m < npix ? ld4(dz2 + (int64_t)m * C2 + o0[j]) : zero4();
+    }
+};
+struct Conv2WgradB {  // h1 quads along c at one (pixel, tap)
+    const float* h1;
+    int npix, tap0;
+    int off[MAXQ], kk[MAXQ];
+    __device__ void init(int j, int row, int k) {
+        const int t = tap0 + (row >> 5), c0 = row & 31;
+        off[j] = ((t >> 2) * H1 + (t & 3)) * C1 + c0;
+        kk[j] = k;
+    }
+    __device__ f32x4 load(int kc, int j) const {
+        const int m = kc * BK + kk[j];
+        if (m >= npix) return zero4();
+        const int b = m / P2, p = m - b * P2, i = p / H2, jj = p - i * H2;
+        return ld4(h1 + (((int64_t)b * H1 + S2 * i) * H1 + S2 * jj) * C1 + off[j]);
+    }
+};
+
+__global__ __launch_bounds__(256) void conv2_wgrad_kernel(const float* __restrict__ dz2,
+                                                          const float* __restrict__ h1, int n,
+                                                          int cps, float* __restrict__ partial) {
+    using SH = GemmShape<64, 64, RMAJ, RMAJ>;
+    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
+    const int tap0 = blockIdx.x * 2, s = blockIdx.y;
+    const int npix = n * P2, nchunks = (npix + BK - 1) / BK;
+    Conv2WgradA la{dz2, npix};
+    Conv2WgradB lb{h1, npix, tap0};
+    PartialEpi epi{partial + (int64_t)s * C2 * 16 * C1, 16 * C1, tap0 * C1, 1.0f};
+    mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, s * cps, min(nchunks, (s + 1) * cps), la, lb, epi);
+}
+
+void launch_conv2_wgrad(const float* dz2, const float* h1, int n, float* partial, int max_splits,
+                        int* splits_out, hipStream_t st) {
+    const int nchunks = (n * P2 + BK - 1) / BK;
+    int splits = min(min(max_splits, nchunks), 512 / 8);
+    const int cps = (nchunks + splits - 1) / splits;
+    splits = (nchunks + cps - 1) / cps;
+    *splits_out = splits;
+    conv2_wgrad_kernel<<<dim3(8, splits), 256, 0, st>>>(dz2, h1, n, cps, partial);
+}
+
+// ---------------------------------------------------------------------------
+// Bias gradients of the convolutions: db_l[o] = sum over samples and pixels of
+// dz_l.  Block (blk, layer) sums a contiguous share of the rows in a fixed
+// order; bpart[layer][blk][64].
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void bias_partials_kernel(const float* __restrict__ dz1,
+                                                            const float* __restrict__ dz2,
+                                                            const float* __restrict__ dz3, int n,
+                                                            float* __restrict__ bpart, int nblk) {
+    __shared__ float red[256];
+    const int blk = blockIdx.x, layer = blockIdx.y, tid = threadIdx.x;
+    float acc = 0.0f;
+    int C, lanes;
+    if (layer == 0) {
+        C = C1; lanes = 256 / C1;
+        const int64_t rows = (int64_t)n * P1;
+        const int64_t r0 = rows * blk / nblk, r1 = rows * (blk + 1) / nblk;
+        for (int64_t r = r0 + tid / C; r < r1; r += lanes) acc += dz1[r * C1 + tid % C];
+    } else if (layer == 1) {
+        C = C2; lanes = 256 / C2;
+        const int64_t rows = (int64_t)n * P2;
+        const int64_t r0 = rows * blk / nblk, r1 = rows * (blk + 1) / nblk;
+        for (int64_t r = r0 + tid / C; r < r1; r += lanes) acc += dz2[r * C2 + tid % C];
+    } else {
+        C = C3; lanes = 256 / C3;
+        const int b0 = (int)((int64_t)n * blk / nblk), b1 = (int)((int64_t)n * (blk + 1) / nblk);
+        for (int b = b0 + tid / C; b < b1; b += lanes) {
+            const float* p = dz3 + (int64_t)b * FLAT + (tid % C) * P3;
+            for (int q = 0; q < P3; ++q) acc += p[q];
+        }
+    }
+    red[tid] = acc;
+    __syncthreads();
+    if (tid < C) {
+        float s = 0.0f;
+        for (int l = 0; l < lanes; ++l) s += red[l * C + tid];
+        bpart[((int64_t)layer * nblk + blk) * 64 + tid] = s;
+    }
+}
+
+void launch_bias_partials(const float* dz1, const float* dz2, const float* dz3, int n,
+                          float* bpart, int nblk, hipStream_t st) {
+    bias_partials_kernel<<<dim3(nblk, 3), 256, 0, st>>>(dz1, dz2, dz3, n, bpart, nblk);
+}
+
+// ---------------------------------------------------------------------------
+// Sum the split partials in split order and scatter into the OIHW gradient
+// layout; add up the bias partials.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void grad_reduce_kernel(const float* __restrict__ part1, int s1,
+                                                          const float* __restrict__ part2, int s2,
+                                                          const float* __restrict__ part3, int s3,
+                                                          const float* __restrict__ bpart, int nblk,
+                                                          float* __restrict__ grads) {
+    constexpr int N1 = C1 * 256, N2 = C2 * 16 * C1, N3 = C3 * 9 * C2;
+    const int e = blockIdx.x * 256 + threadIdx.x;
+    if (e < N1) {  // partial1 is already [o][c][u][v]
+        float acc = 0.0f;
+        for (int s = 0; s < s1; ++s) acc += part1[(int64_t)s * N1 + e];
+        grads[OFF_W1 + e] = acc;
+    } else if (e < N1 + N2) {  // partial2 [o][(u*4+v)*32 + c]
+        const int p = e - N1;
+        float acc = 0.0f;
+        for (int s = 0; s < s2; ++s) acc += part2[(int64_t)s * N2 + p];
+        const int o = p >> 9, t = (p >> 5) & 15, c = p & 31;
+        grads[OFF_W2 + ((o * C1 + c) * K2 + (t >> 2)) * K2 + (t & 3)] = acc;
+    } else if (e < N1 + N2 + N3) {  // partial3 [o][(u*3+v)*64 + c]
+        const int p = e - N1 - N2;
+        float acc = 0.0f;
+        for (int s = 0; s < s3; ++s) acc += part3[(int64_t)s * N3 + p];
+        const int o = p / 576, t = (p / 64) % 9, c = p & 63;
+        grads[OFF_W3 + ((o * C2 + c) * K3 + t / 3) * K3 + t % 3] = acc;
+    } else if (e < N1 + N2 + N3 + C1 + C2 + C3) {
+        int q = e - N1 - N2 - N3, layer, o;
+        int64_t off;
+        if (q < C1) { layer = 0; o = q; off = OFF_B1; }
+        else if (q < C1 + C2) { layer = 1; o = q - C1; off = OFF_B2; }
+        else { layer = 2; o = q - C1 - C2; off = OFF_B3; }
+        float acc = 0.0f;
+        for (int b = 0; b < nblk; ++b) acc += bpart[((int64_t)layer * nblk + b) * 64 + o];
+        grads[off + o] = acc;
+    }
+}
+
+void launch_grad_reduce(const float* part1, int s1, const float* part2, int s2,
+                        const float* part3, int s3, const float* bpart, int nblk, float* grads,
+                        hipStream_t st) {
+    const int total = C1 * 256 + C2 * 16 * C1 + C3 * 9 * C2 + C1 + C2 + C3;
+    grad_reduce_kernel<<<(total + 255) / 256, 256, 0, st>>>(part1, s1, part2, s2, part3, s3, bpart,
+                                                            nblk, grads);
+}
+
+}  // namespace gorila
