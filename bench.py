@@ -43,6 +43,10 @@ def step_flops_per_transition(A: int) -> int:
     return 2 * (2 * fwd + bwd)
 
 
+MFMA_STAGES = ("conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "fc1_dgrad", "fc1_wgrad",
+               "conv3_dgrad", "conv3_wgrad", "conv2_dgrad", "conv2_wgrad", "conv1_wgrad")
+
+
 def stage_flops(stage: str, B: int, A: int) -> float:
     """Algorithmic FLOPs of one launch of a stage of the learner step at batch B."""
     two = 2 * B  # online + target rows in the forward stages
@@ -77,8 +81,7 @@ def run_learner(torch, g, datagen, B, A, seed, steps, warmup, timed_stage=None):
         step()
     prof = ctx.timing_end()
 
-    dominant = timed_stage or max((k for k in prof if stage_flops(k, B, A) > 0),
-                                  key=lambda k: prof[k][0])
+    dominant = timed_stage or max((k for k in prof if k in MFMA_STAGES), key=lambda k: prof[k][0])
     # timed region: events only around the dominant kernel
     torch.cuda.synchronize()
     ctx.timing_begin([dominant], max_records=steps)
@@ -98,19 +101,24 @@ def run_learner(torch, g, datagen, B, A, seed, steps, warmup, timed_stage=None):
                 dominant_ms=dom[0] / max(dom[1], 1), dominant_launches=dom[1])
 
 
-def cpu_baseline(datagen, B, A, seed, sample):
+def cpu_baseline(datagen, B, A, seed, seconds):
+    """The fp64 oracle (as it stands) running whole learner steps of the same
+    batch-B workload on the host cores until `seconds` have passed."""
     import oracle
     inp = datagen.learner_inputs(seed, B, A)
-    n = min(sample, B)
     net = oracle.Net(n_actions=A)
-    t0 = time.perf_counter()
-    oracle.learner_step(net, inp.theta, inp.theta_target, inp.s[:n], inp.s2[:n], inp.a[:n],
-                        inp.r[:n], inp.term[:n], inp.gamma, 1.0)
-    dt = time.perf_counter() - t0
-    return {"value": n / dt, "unit": "transitions/s", "cores": oracle.num_threads(),
+    steps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.learner_step(net, inp.theta, inp.theta_target, inp.s, inp.s2, inp.a, inp.r,
+                            inp.term, inp.gamma, 1.0)
+        steps += 1
+        dt = time.perf_counter() - t0
+        if dt >= seconds:
+            break
+    return {"value": steps * B / dt, "unit": "transitions/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"one fp64 learner step over the first {n} transitions of the "
-                      f"batch-{B} workload ({dt:.1f} s)"}
+            "sample": f"{steps} fp64 learner steps of the batch-{B} workload "
+                      f"({steps * B} transitions, {dt:.1f} s)"}
 
 
 def main():
@@ -120,7 +128,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--batch", type=int, default=512)
     ap.add_argument("--actions", type=int, default=6)
-    ap.add_argument("--cpu-sample", type=int, default=128)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-b32", action="store_true", help="skip the batch-32 companion line")
     args = ap.parse_args()
@@ -178,7 +186,7 @@ def main():
                           "ms_per_step": round(r32["ms_per_step"], 4), "tflops": round(t32, 3),
                           "pct_mfma_peak": round(100 * t32 / FP32_MFMA_PEAK_TFLOPS, 2)}
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(datagen, B, A, seed, args.cpu_sample)
+        out["cpu_baseline"] = cpu_baseline(datagen, B, A, seed, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 

@@ -68,7 +68,7 @@ struct Plan {
     size_t w2t[2], w3t[2], w3d, w2d;
     size_t h1, h2, h3, h4, q, ell, coef;
     size_t dz4, dz3, dz2, dz1;
-    size_t fc1part, part1, part2, part3, bpart;
+    size_t fc1part, part1, part2, part3, bpart, hpart;
     size_t total;
 };
 
@@ -103,7 +103,8 @@ Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A) {
     p.part1 = B ? take(4 * (size_t)CONV1_WG_MAX_SPLITS * C1 * 256) : o;
     p.part2 = B ? take(4 * (size_t)WG_MAX_SPLITS * C2 * 16 * C1) : o;
     p.part3 = B ? take(4 * (size_t)WG_MAX_SPLITS * C3 * 9 * C2) : o;
-    p.bpart = B ? take(4 * (size_t)3 * BIAS_BLOCKS * 64) : o;
+    p.bpart = B ? take(4 * (size_t)3 * BIAS_PART_STRIDE) : o;
+    p.hpart = B ? take(4 * (size_t)HEAD_MAX_BLOCKS * HP_STRIDE) : o;
     p.total = o;
     return p;
 }
@@ -421,21 +422,26 @@ int gorila_learner_step(const gorila_params* params, const gorila_params* target
         launch_td_head(h4, theta, theta_t, B, A, a, r, term, gamma, clip_delta, at<float>(ctx, p.q),
                        ell, coef, dz4, st);
     }
-    { StageTimer t(ctx, ST_HEAD_REDUCE); launch_head_reduce(h4, dz4, a, coef, ell, B, A, grads_out, loss_out, st); }
+    int head_blocks = 0;
+    {
+        StageTimer t(ctx, ST_HEAD_REDUCE);
+        head_blocks = launch_head_partial(h4, a, coef, ell, B, A, at<float>(ctx, p.hpart), st);
+    }
     { StageTimer t(ctx, ST_FC1_DGRAD); launch_fc1_dgrad(dz4, theta, h3, B, dz3, st); }
     { StageTimer t(ctx, ST_FC1_WGRAD); launch_fc1_wgrad(dz4, h3, B, grads_out, st); }
     int s1 = 0, s2 = 0, s3 = 0;
+    float* bpart = at<float>(ctx, p.bpart);
     { StageTimer t(ctx, ST_CONV3_DGRAD); launch_conv3_dgrad(dz3, wv[0].w3d, h2, B, dz2, st); }
-    { StageTimer t(ctx, ST_CONV3_WGRAD); launch_conv3_wgrad(dz3, h2, B, at<float>(ctx, p.part3), WG_MAX_SPLITS, &s3, st); }
+    { StageTimer t(ctx, ST_CONV3_WGRAD); launch_conv3_wgrad(dz3, h2, B, at<float>(ctx, p.part3), bpart + 2 * BIAS_PART_STRIDE, WG_MAX_SPLITS, &s3, st); }
     { StageTimer t(ctx, ST_CONV2_DGRAD); launch_conv2_dgrad(dz2, wv[0].w2d, h1, B, dz1, st); }
-    { StageTimer t(ctx, ST_CONV2_WGRAD); launch_conv2_wgrad(dz2, h1, B, at<float>(ctx, p.part2), WG_MAX_SPLITS, &s2, st); }
-    { StageTimer t(ctx, ST_CONV1_WGRAD); launch_conv1_wgrad(dz1, ftab, B, at<float>(ctx, p.part1), CONV1_WG_MAX_SPLITS, &s1, st); }
+    { StageTimer t(ctx, ST_CONV2_WGRAD); launch_conv2_wgrad(dz2, h1, B, at<float>(ctx, p.part2), bpart + BIAS_PART_STRIDE, WG_MAX_SPLITS, &s2, st); }
+    { StageTimer t(ctx, ST_CONV1_WGRAD); launch_conv1_wgrad(dz1, ftab, B, at<float>(ctx, p.part1), bpart, CONV1_WG_MAX_SPLITS, &s1, st); }
     {
         StageTimer t(ctx, ST_GRAD_REDUCE);
-        launch_bias_partials(dz1, dz2, dz3, B, at<float>(ctx, p.bpart), BIAS_BLOCKS, st);
-        launch_grad_reduce(at<float>(ctx, p.part1), s1, at<float>(ctx, p.part2), s2,
-                           at<float>(ctx, p.part3), s3, at<float>(ctx, p.bpart), BIAS_BLOCKS,
-                           grads_out, st);
+        ReduceArgs ra{at<float>(ctx, p.part1), at<float>(ctx, p.part2), at<float>(ctx, p.part3),
+                      bpart, at<float>(ctx, p.hpart), s1, s2, s3, head_blocks, B, A, grads_out,
+                      loss_out};
+        launch_grad_reduce(ra, st);
     }
     return check_launch();
 }

@@ -111,33 +111,41 @@ struct GemmShape {
 // Loaders: `la.init(j, row, k)` is called once per quad slot j of this thread
 // with the quad's tile coordinates; `la.load(kc, j)` returns the quad for
 // reduction chunk kc (zeros where the operand is zero-padded).
+// If rowsum_out is not null, thread t < BM also writes sum_k A[t][k] over this
+// workgroup's reduction range (in chunk order) to rowsum_out[t].
+//
+// The chunk loop is unrolled by two so that the LDS buffer and the register
+// set of every access are compile-time constants: LDS is then addressed with
+// ds_read/ds_write, and each global load is waited for only where its data is
+// stored to LDS, one chunk later.
 template <int BM, int BN, int WAVES_M, int AMODE, int BMODE, class LoadA, class LoadB, class Epi>
 __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
-                                          LoadA& la, LoadB& lb, Epi& epi) {
+                                          LoadA& la, LoadB& lb, Epi& epi,
+                                          float* rowsum_out = nullptr) {
     using SH = GemmShape<BM, BN, AMODE, BMODE>;
     using LA = typename SH::LA;
     using LB = typename SH::LB;
     constexpr int WAVES_N = 4 / WAVES_M;
     constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
     constexpr int TM = WM / 32, TN = WN / 32;
+    constexpr int STAGE = LA::SIZE + LB::SIZE;  // floats per LDS buffer
     static_assert(TM * 32 == WM && TN * 32 == WN, "wave tile must be a multiple of 32");
     static_assert(LA::NQ <= MAXQ && LB::NQ <= MAXQ, "loader state arrays hold MAXQ quads");
+    static_assert(LA::QUADS % 256 == 0 && LB::QUADS % 256 == 0, "every thread owns whole quads");
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WAVES_M, wn = wave / WAVES_M;
-    float* sa[2] = {smem, smem + LA::SIZE + LB::SIZE};
-    float* sb[2] = {smem + LA::SIZE, smem + 2 * LA::SIZE + LB::SIZE};
 
     int qa_row[LA::NQ], qa_k[LA::NQ], qb_row[LB::NQ], qb_k[LB::NQ];
 #pragma unroll
     for (int j = 0; j < LA::NQ; ++j) {
-        int e = tid + 256 * j;
-        if (e < LA::QUADS) { LA::quad_coord(e, qa_row[j], qa_k[j]); la.init(j, qa_row[j], qa_k[j]); }
+        LA::quad_coord(tid + 256 * j, qa_row[j], qa_k[j]);
+        la.init(j, qa_row[j], qa_k[j]);
     }
 #pragma unroll
     for (int j = 0; j < LB::NQ; ++j) {
-        int e = tid + 256 * j;
-        if (e < LB::QUADS) { LB::quad_coord(e, qb_row[j], qb_k[j]); lb.init(j, qb_row[j], qb_k[j]); }
+        LB::quad_coord(tid + 256 * j, qb_row[j], qb_k[j]);
+        lb.init(j, qb_row[j], qb_k[j]);
     }
 
     f32x16 acc[TM][TN];
@@ -146,41 +154,35 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
 
-    f32x4 ra[LA::NQ], rb[LB::NQ];
-    auto gload = [&](int kc) {
+    // Register sets 0/1 hold chunks fetched ahead; set s always holds chunks
+    // with (kc - kc_begin) % 2 == s.
+    f32x4 ra0[LA::NQ], rb0[LB::NQ], ra1[LA::NQ], rb1[LB::NQ];
+    auto gload = [&](int kc, f32x4* ra, f32x4* rb) {
 #pragma unroll
-        for (int j = 0; j < LA::NQ; ++j)
-            if (tid + 256 * j < LA::QUADS) ra[j] = la.load(kc, j);
+        for (int j = 0; j < LA::NQ; ++j) ra[j] = la.load(kc, j);
 #pragma unroll
-        for (int j = 0; j < LB::NQ; ++j)
-            if (tid + 256 * j < LB::QUADS) rb[j] = lb.load(kc, j);
+        for (int j = 0; j < LB::NQ; ++j) rb[j] = lb.load(kc, j);
     };
-    auto sstore = [&](int buf) {
+    auto sstore = [&](float* buf, const f32x4* ra, const f32x4* rb) {
 #pragma unroll
-        for (int j = 0; j < LA::NQ; ++j)
-            if (tid + 256 * j < LA::QUADS) LA::put(sa[buf], qa_row[j], qa_k[j], ra[j]);
+        for (int j = 0; j < LA::NQ; ++j) LA::put(buf, qa_row[j], qa_k[j], ra[j]);
 #pragma unroll
-        for (int j = 0; j < LB::NQ; ++j)
-            if (tid + 256 * j < LB::QUADS) LB::put(sb[buf], qb_row[j], qb_k[j], rb[j]);
+        for (int j = 0; j < LB::NQ; ++j) LB::put(buf + LA::SIZE, qb_row[j], qb_k[j], rb[j]);
     };
 
-    if (kc_begin < kc_end) {
-        gload(kc_begin);
-        sstore(0);
-    }
-    __syncthreads();
-    for (int kc = kc_begin; kc < kc_end; ++kc) {
-        const int cur = (kc - kc_begin) & 1;
-        const bool more = kc + 1 < kc_end;
-        if (more) gload(kc + 1);
+    const bool do_rowsum = rowsum_out != nullptr && tid < BM;
+    float rowsum = 0.0f;
+    auto compute = [&](const float* buf) {
+        const float* sa = buf;
+        const float* sb = buf + LA::SIZE;
 #pragma unroll
         for (int g = 0; g < BK / 8; ++g) {
             const int kb = 8 * g + 4 * (lane >> 5);
             f32x4 av[TM], bv[TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i) av[i] = LA::get(sa[cur], wm * WM + i * 32 + (lane & 31), kb);
+            for (int i = 0; i < TM; ++i) av[i] = LA::get(sa, wm * WM + i * 32 + (lane & 31), kb);
 #pragma unroll
-            for (int j = 0; j < TN; ++j) bv[j] = LB::get(sb[cur], wn * WN + j * 32 + (lane & 31), kb);
+            for (int j = 0; j < TN; ++j) bv[j] = LB::get(sb, wn * WN + j * 32 + (lane & 31), kb);
 #pragma unroll
             for (int q = 0; q < 4; ++q)
 #pragma unroll
@@ -189,9 +191,35 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
                     for (int j = 0; j < TN; ++j)
                         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][q], bv[j][q], acc[i][j], 0, 0, 0);
         }
-        if (more) sstore(cur ^ 1);
+        if (do_rowsum) {
+#pragma unroll
+            for (int k = 0; k < BK; k += 4) {
+                const f32x4 v = LA::get(sa, tid, k);
+                rowsum += ((v[0] + v[1]) + v[2]) + v[3];
+            }
+        }
+    };
+
+    if (kc_begin < kc_end) {
+        gload(kc_begin, ra0, rb0);
+        if (kc_begin + 1 < kc_end) gload(kc_begin + 1, ra1, rb1);
+        sstore(smem, ra0, rb0);
+    }
+    __syncthreads();
+    for (int kc = kc_begin; kc < kc_end; kc += 2) {
+        // even chunk: LDS buffer 0, refill register set 0 with chunk kc+2
+        if (kc + 2 < kc_end) gload(kc + 2, ra0, rb0);
+        compute(smem);
+        if (kc + 1 < kc_end) sstore(smem + STAGE, ra1, rb1);
+        __syncthreads();
+        if (kc + 1 >= kc_end) break;
+        // odd chunk: LDS buffer 1, refill register set 1 with chunk kc+3
+        if (kc + 3 < kc_end) gload(kc + 3, ra1, rb1);
+        compute(smem + STAGE);
+        if (kc + 2 < kc_end) sstore(smem, ra0, rb0);
         __syncthreads();
     }
+    if (do_rowsum) rowsum_out[tid] = rowsum;
 
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -216,6 +244,9 @@ struct PartialEpi {
 };
 
 __device__ inline f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+__device__ inline f32x4 sel4(bool ok, f32x4 v) {
+    return f32x4{ok ? v[0] : 0.f, ok ? v[1] : 0.f, ok ? v[2] : 0.f, ok ? v[3] : 0.f};
+}
 __device__ inline f32x4 ld4(const float* p) { return *(const f32x4*)p; }
 
 }  // namespace gorila

@@ -89,12 +89,13 @@ struct Conv1WgradA {  // dz1 rows o, RMAJ quads along o at one pixel
     __device__ void init(int j, int row, int k) { o0[j] = row; kk[j] = k; }
     __device__ f32x4 load(int kc, int j) const {
         const int m = kc * BK + kk[j];
-        return m < npix ? ld4(dz1 + (int64_t)m * C1 + o0[j]) : zero4();
+        return sel4(m < npix, ld4(dz1 + (int64_t)(m < npix ? m : 0) * C1 + o0[j]));
     }
 };
 
 struct Conv1WgradB {  // input bytes rows (c,u,v), RMAJ quads along v at one pixel
     const uint8_t* const* ftab;
+    const uint8_t* safe;  // any readable 7056 bytes, read in place of a zero-filled frame
     int npix, col0;
     int chan[MAXQ], off[MAXQ], kk[MAXQ];
     __device__ void init(int j, int row, int k) {
@@ -105,13 +106,13 @@ struct Conv1WgradB {  // input bytes rows (c,u,v), RMAJ quads along v at one pix
     }
     __device__ f32x4 load(int kc, int j) const {
         const int m = kc * BK + kk[j];
-        if (m >= npix) return zero4();
-        const int b = m / P1, p = m - b * P1, i = p / H1, jj = p - i * H1;
+        const int mm = m < npix ? m : 0;
+        const int b = mm / P1, p = mm - b * P1, i = p / H1, jj = p - i * H1;
         const uint8_t* f = ftab[(int64_t)b * 4 + chan[j]];
-        if (!f) return zero4();
-        const uint32_t d = *(const uint32_t*)(f + (S1 * i) * IN_W + S1 * jj + off[j]);
-        return f32x4{(float)(d & 255u), (float)((d >> 8) & 255u), (float)((d >> 16) & 255u),
-                     (float)(d >> 24)};
+        const bool ok = m < npix && f != nullptr;
+        const uint32_t d = *(const uint32_t*)((ok ? f : safe) + (S1 * i) * IN_W + S1 * jj + off[j]);
+        return sel4(ok, f32x4{(float)(d & 255u), (float)((d >> 8) & 255u),
+                              (float)((d >> 16) & 255u), (float)(d >> 24)});
     }
 };
 
@@ -120,7 +121,8 @@ constexpr int C1W_BN = 128;
 __global__ __launch_bounds__(256) void conv1_wgrad_kernel(const float* __restrict__ dz1,
                                                           const uint8_t* const* __restrict__ ftab,
                                                           int n, int chunks_per_split,
-                                                          float* __restrict__ partial) {
+                                                          float* __restrict__ partial,
+                                                          float* __restrict__ bias_part) {
     using SH = GemmShape<32, C1W_BN, RMAJ, RMAJ>;
     __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
     const int col0 = blockIdx.x * C1W_BN, split = blockIdx.y;
@@ -129,20 +131,22 @@ __global__ __launch_bounds__(256) void conv1_wgrad_kernel(const float* __restric
     const int kc0 = split * chunks_per_split;
     const int kc1 = min(nchunks, kc0 + chunks_per_split);
     Conv1WgradA la{dz1, npix};
-    Conv1WgradB lb{ftab, npix, col0};
+    Conv1WgradB lb{ftab, (const uint8_t*)dz1, npix, col0};
     PartialEpi epi{partial + (int64_t)split * C1 * 256, 256, col0, 1.0f / 255.0f};
-    mfma_gemm<32, C1W_BN, 1, RMAJ, RMAJ>(smem, kc0, kc1, la, lb, epi);
+    float* rs = blockIdx.x == 0 ? bias_part + (int64_t)split * 64 : nullptr;
+    mfma_gemm<32, C1W_BN, 1, RMAJ, RMAJ>(smem, kc0, kc1, la, lb, epi, rs);
 }
 
 void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int n, float* partial,
-                        int max_splits, int* splits_out, hipStream_t st) {
+                        float* bias_part, int max_splits, int* splits_out, hipStream_t st) {
     const int nchunks = (n * P1 + BK - 1) / BK;
     int splits = min(max_splits, max(1, 512 / (256 / C1W_BN)));
     splits = min(splits, nchunks);
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
     *splits_out = splits;
-    conv1_wgrad_kernel<<<dim3(256 / C1W_BN, splits), 256, 0, st>>>(dz1, ftab, n, cps, partial);
+    conv1_wgrad_kernel<<<dim3(256 / C1W_BN, splits), 256, 0, st>>>(dz1, ftab, n, cps, partial,
+                                                                    bias_part);
 }
 
 }  // namespace gorila

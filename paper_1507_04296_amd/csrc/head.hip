@@ -142,46 +142,59 @@ void launch_td_head(const float* h4, const float* theta, const float* theta_targ
                                                 clip, q, ell, coef, dz4);
 }
 
-// dW5[k][:] = sum_{b: a_b = k} coef_b h4[b][:], db5[k] = sum_{b: a_b = k} coef_b,
-// db4 = sum_b dz4[b][:], loss = mean_b ell_b.  Block k < A does row k of dW5;
-// block A does db4, db5 and the loss.  Every sum runs over b in order.
-__global__ __launch_bounds__(256) void head_reduce_kernel(
-    const float* __restrict__ h4, const float* __restrict__ dz4, const int32_t* __restrict__ a,
-    const float* __restrict__ coef, const float* __restrict__ ell, int n, int A,
-    float* __restrict__ grads, float* __restrict__ loss_out) {
-    const int blk = blockIdx.x, tid = threadIdx.x;
-    if (blk < A) {
-        for (int k = tid; k < HID; k += 256) {
+// Partial sums of the action-head gradients and the loss over blocks of rows:
+//   hpart[bb][a*512 + k] = sum_{b in block bb, a_b = a} coef_b h4[b][k]   (dW5)
+//   hpart[bb][HP_DB5 + a] = sum_{b in block bb, a_b = a} coef_b           (db5)
+//   hpart[bb][HP_LOSS]    = sum_{b in block bb} ell_b                     (loss)
+// Grid (8 column tiles, row blocks).  Thread (column kl, lane group bq) adds
+// rows bq, bq+4, ... of its block in order into its own LDS slots; the four
+// lane groups are added in order, so every sum is deterministic.  The blocks
+// are summed in order by the final gradient reduction.
+__global__ __launch_bounds__(256) void head_partial_kernel(
+    const float* __restrict__ h4, const int32_t* __restrict__ a, const float* __restrict__ coef,
+    const float* __restrict__ ell, int n, int A, int rows_per_block, float* __restrict__ hpart) {
+    __shared__ float sacc[4][MAX_ACTIONS][64];
+    const int tid = threadIdx.x, kl = tid & 63, bq = tid >> 6;
+    const int k = blockIdx.x * 64 + kl, bb = blockIdx.y;
+    const int b0 = bb * rows_per_block, b1 = min(n, b0 + rows_per_block);
+    float* out = hpart + (int64_t)bb * HP_STRIDE;
+    for (int j = 0; j < A; ++j) sacc[bq][j][kl] = 0.0f;
+    for (int b = b0 + bq; b < b1; b += 4) {
+        const int ab = a[b];
+        sacc[bq][ab][kl] = fmaf(coef[b], h4[(int64_t)b * HID + k], sacc[bq][ab][kl]);
+    }
+    __syncthreads();
+    for (int e = tid; e < A * 64; e += 256) {
+        const int j = e >> 6, kk = e & 63;
+        out[j * HID + blockIdx.x * 64 + kk] =
+            ((sacc[0][j][kk] + sacc[1][j][kk]) + sacc[2][j][kk]) + sacc[3][j][kk];
+    }
+    if (blockIdx.x == 0) {
+        // wave w: actions j = w, w+4, ...; lane l: rows b0+l, b0+l+64, ...
+        const int lane = tid & 63, w = tid >> 6;
+        for (int j = w; j < A; j += 4) {
             float s = 0.0f;
-            for (int b = 0; b < n; ++b)
-                if (a[b] == blk) s = fmaf(coef[b], h4[(int64_t)b * HID + k], s);
-            grads[OFF_W5 + (int64_t)blk * HID + k] = s;
+            for (int b = b0 + lane; b < b1; b += 64)
+                if (a[b] == j) s += coef[b];
+            s = wave_sum(s);
+            if (lane == 0) out[HP_DB5 + j] = s;
         }
-        return;
-    }
-    for (int k = tid; k < HID; k += 256) {
-        float s = 0.0f;
-        for (int b = 0; b < n; ++b) s += dz4[(int64_t)b * HID + k];
-        grads[OFF_B4 + k] = s;
-    }
-    if (tid < A) {
-        float s = 0.0f;
-        for (int b = 0; b < n; ++b)
-            if (a[b] == tid) s += coef[b];
-        grads[off_b5(A) + tid] = s;
-    }
-    if (tid == 255) {
-        double s = 0.0;
-        for (int b = 0; b < n; ++b) s += (double)ell[b];
-        loss_out[0] = (float)(s / (double)n);
+        if (w == 0) {
+            float s = 0.0f;
+            for (int b = b0 + lane; b < b1; b += 64) s += ell[b];
+            s = wave_sum(s);
+            if (lane == 0) out[HP_LOSS] = s;
+        }
     }
 }
 
-void launch_head_reduce(const float* h4, const float* dz4, const int32_t* a, const float* coef,
-                        const float* ell, int n, int A, float* grads, float* loss_out,
-                        hipStream_t st) {
-    if (n <= 0) return;
-    head_reduce_kernel<<<A + 1, 256, 0, st>>>(h4, dz4, a, coef, ell, n, A, grads, loss_out);
+int launch_head_partial(const float* h4, const int32_t* a, const float* coef, const float* ell,
+                        int n, int A, float* hpart, hipStream_t st) {
+    if (n <= 0) return 0;
+    int rows = max(32, (n + HEAD_MAX_BLOCKS - 1) / HEAD_MAX_BLOCKS);
+    const int blocks = (n + rows - 1) / rows;
+    head_partial_kernel<<<dim3(HID / 64, blocks), 256, 0, st>>>(h4, a, coef, ell, n, A, rows, hpart);
+    return blocks;
 }
 
 }  // namespace gorila

@@ -65,34 +65,50 @@ void launch_act_head(const float* h4, const float* theta, int n, int A, float ep
 void launch_td_head(const float* h4, const float* theta, const float* theta_target, int n, int A,
                     const int32_t* a, const float* r, const uint8_t* term, float gamma, float clip,
                     float* q, float* ell, float* coef, float* dz4, hipStream_t st);
-void launch_head_reduce(const float* h4, const float* dz4, const int32_t* a, const float* coef,
-                        const float* ell, int n, int A, float* grads, float* loss_out,
-                        hipStream_t st);
+// Row-block partials of dW5, db5 and the loss (see head.hip); returns the
+// number of row blocks written.
+int launch_head_partial(const float* h4, const int32_t* a, const float* coef, const float* ell,
+                        int n, int A, float* hpart, hipStream_t st);
 
 // Backward layers.
 void launch_fc1_dgrad(const float* dz4, const float* theta, const float* h3, int n, float* dz3,
                       hipStream_t st);
+// dW4 and (as row sums of dz4) db4, written straight into grads.
 void launch_fc1_wgrad(const float* dz4, const float* h3, int n, float* grads, hipStream_t st);
 void launch_conv3_dgrad(const float* dz3, const float* w3d, const float* h2, int n, float* dz2,
                         hipStream_t st);
-void launch_conv3_wgrad(const float* dz3, const float* h2, int n, float* partial, int max_splits,
-                        int* splits_out, hipStream_t st);
+void launch_conv3_wgrad(const float* dz3, const float* h2, int n, float* partial, float* bias_part,
+                        int max_splits, int* splits_out, hipStream_t st);
 void launch_conv2_dgrad(const float* dz2, const float* w2d, const float* h1, int n, float* dz1,
                         hipStream_t st);
-void launch_conv2_wgrad(const float* dz2, const float* h1, int n, float* partial, int max_splits,
-                        int* splits_out, hipStream_t st);
-void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int n, float* partial,
+void launch_conv2_wgrad(const float* dz2, const float* h1, int n, float* partial, float* bias_part,
                         int max_splits, int* splits_out, hipStream_t st);
-void launch_bias_partials(const float* dz1, const float* dz2, const float* dz3, int n,
-                          float* bpart, int nblk, hipStream_t st);
-void launch_grad_reduce(const float* part1, int s1, const float* part2, int s2,
-                        const float* part3, int s3, const float* bpart, int nblk,
-                        float* grads, hipStream_t st);
+void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int n, float* partial,
+                        float* bias_part, int max_splits, int* splits_out, hipStream_t st);
+// Conv weight-gradient partials [split][o][(tap, c)], bias partials
+// bias_part[layer][split][64] (one row per split, written by the weight-gradient
+// workgroups of column tile 0) and the head partials hpart[block][HP_STRIDE],
+// each summed in split / block order into grads and loss_out.
+struct ReduceArgs {
+    const float* part1;
+    const float* part2;
+    const float* part3;
+    const float* bias_part;
+    const float* hpart;
+    int s1, s2, s3, head_blocks, n, A;
+    float* grads;
+    float* loss_out;
+};
+void launch_grad_reduce(const ReduceArgs& ra, hipStream_t st);
 
 // Sizes of the split-K / partial buffers the launchers above may use.
 constexpr int FC1_MAX_SPLITS = 14;
 constexpr int WG_MAX_SPLITS = 128;
 constexpr int CONV1_WG_MAX_SPLITS = 256;
-constexpr int BIAS_BLOCKS = 64;
+constexpr int BIAS_PART_STRIDE = 256 * 64;  // floats per layer in bias_part
+constexpr int HEAD_MAX_BLOCKS = 16;          // row blocks of the head partials
+constexpr int HP_DB5 = MAX_ACTIONS * HID;    // offsets inside one head partial
+constexpr int HP_LOSS = HP_DB5 + MAX_ACTIONS;
+constexpr int HP_STRIDE = HP_LOSS + 32;
 
 }  // namespace gorila

@@ -52,17 +52,17 @@ struct Conv2FwdA {
     const float* h1;
     int rows, m0;
     const float* base[MAXQ];
+    bool ok[MAXQ];
     __device__ void init(int j, int row, int k) {
         const int m = m0 + row;
         const int mm = m < rows ? m : 0;
         const int b = mm / P2, p = mm - b * P2, i = p / H2, jj = p - i * H2;
-        const float* ptr = h1 + (((int64_t)b * H1 + S2 * i) * H1 + S2 * jj) * C1 + k;
-        base[j] = m < rows ? ptr : nullptr;
+        base[j] = h1 + (((int64_t)b * H1 + S2 * i) * H1 + S2 * jj) * C1 + k;
+        ok[j] = m < rows;
     }
     __device__ f32x4 load(int kc, int j) const {
-        if (!base[j]) return zero4();
         const int u = kc >> 2, v = kc & 3;
-        return ld4(base[j] + (u * H1 + v) * C1);
+        return sel4(ok[j], ld4(base[j] + (u * H1 + v) * C1));
     }
 };
 struct WtapB {  // transposed weights w[tap][row][k]; per_tap chunks of 32 k per tap
@@ -115,17 +115,17 @@ struct Conv3FwdB {
     const float* h2;
     int rows, m0;
     const float* base[MAXQ];
+    bool ok[MAXQ];
     __device__ void init(int j, int row, int k) {
         const int m = m0 + row;
         const int mm = m < rows ? m : 0;
         const int b = mm / P3, p = mm - b * P3, i = p / H3, jj = p - i * H3;
-        const float* ptr = h2 + (((int64_t)b * H2 + i) * H2 + jj) * C2 + k;
-        base[j] = m < rows ? ptr : nullptr;
+        base[j] = h2 + (((int64_t)b * H2 + i) * H2 + jj) * C2 + k;
+        ok[j] = m < rows;
     }
     __device__ f32x4 load(int kc, int j) const {
-        if (!base[j]) return zero4();
         const int t = kc >> 1, u = t / 3, v = t - u * 3;
-        return ld4(base[j] + (u * H2 + v) * C2 + (kc & 1) * BK);
+        return sel4(ok[j], ld4(base[j] + (u * H2 + v) * C2 + (kc & 1) * BK));
     }
 };
 struct Conv3FwdStore {  // row = o, col = pixel index within the tile
@@ -167,10 +167,12 @@ struct RowMajorK {  // rows of a row-major [rows][ld] matrix, quads along k
     const float* a;
     int rows, r0, ld;
     const float* base[MAXQ];
+    bool ok[MAXQ];
     __device__ void init(int j, int row, int k) {
-        base[j] = r0 + row < rows ? a + (int64_t)(r0 + row) * ld + k : nullptr;
+        ok[j] = r0 + row < rows;
+        base[j] = a + (int64_t)(ok[j] ? r0 + row : 0) * ld + k;
     }
-    __device__ f32x4 load(int kc, int j) const { return base[j] ? ld4(base[j] + kc * BK) : zero4(); }
+    __device__ f32x4 load(int kc, int j) const { return sel4(ok[j], ld4(base[j] + kc * BK)); }
 };
 struct PlainStore {
     float* out;
@@ -236,7 +238,7 @@ struct RowMajorR {  // B[col][k] = M[k][c0 + col] of a row-major [k][ld] matrix 
     __device__ void init(int j, int row, int k) { base[j] = a + c0 + row; kk[j] = k; }
     __device__ f32x4 load(int kc, int j) const {
         const int k = kc * BK + kk[j];
-        return k < kmax ? ld4(base[j] + (int64_t)k * ld) : zero4();
+        return sel4(k < kmax, ld4(base[j] + (int64_t)(k < kmax ? k : 0) * ld));
     }
 };
 struct ReluMaskStore {  // out[r][c] = mask[r][c] > 0 ? v : 0
@@ -276,19 +278,23 @@ void launch_fc1_dgrad(const float* dz4, const float* theta, const float* h3, int
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void fc1_wgrad_kernel(const float* __restrict__ dz4,
                                                         const float* __restrict__ h3, int n,
-                                                        float* __restrict__ gW4) {
+                                                        float* __restrict__ gW4,
+                                                        float* __restrict__ gb4) {
     using SH = GemmShape<64, 64, RMAJ, RMAJ>;
     __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
     const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
     RowMajorR la{dz4, r0, HID, n};
     RowMajorR lb{h3, c0, FLAT, n};
     PlainStore epi{gW4, HID, r0, c0, FLAT};
-    mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, 0, (n + BK - 1) / BK, la, lb, epi);
+    // db4[o] = sum_b dz4[b][o]: the row sums of this GEMM's A operand
+    float* rs = blockIdx.y == 0 ? gb4 + r0 : nullptr;
+    mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, 0, (n + BK - 1) / BK, la, lb, epi, rs);
 }
 
 void launch_fc1_wgrad(const float* dz4, const float* h3, int n, float* grads, hipStream_t st) {
     if (n <= 0) return;
-    fc1_wgrad_kernel<<<dim3(HID / 64, FLAT / 64), 256, 0, st>>>(dz4, h3, n, grads + OFF_W4);
+    fc1_wgrad_kernel<<<dim3(HID / 64, FLAT / 64), 256, 0, st>>>(dz4, h3, n, grads + OFF_W4,
+                                                                grads + OFF_B4);
 }
 
 // ---------------------------------------------------------------------------
@@ -321,7 +327,9 @@ struct Conv3DgradA {  // RMAJ quads: 4 consecutive output pixels at one (tap, o)
         for (int q = 0; q < 4; ++q) {
             const int i = py[j][q] - u, jj = px[j][q] - v;
             const bool ok = pb[j][q] >= 0 && i >= 0 && i < H3 && jj >= 0 && jj < H3;
-            r[q] = ok ? dz3[(int64_t)pb[j][q] * FLAT + o * P3 + i * H3 + jj] : 0.0f;
+            const int64_t e = ok ? (int64_t)pb[j][q] * FLAT + o * P3 + i * H3 + jj : 0;
+            const float x = dz3[e];
+            r[q] = ok ? x : 0.0f;
         }
         return r;
     }
@@ -378,16 +386,17 @@ struct Conv3WgradB {  // RMAJ quads: 4 channels of h2 at one (pixel, tap)
     __device__ void init(int j, int row, int k) { c0[j] = row; kk[j] = k; }
     __device__ f32x4 load(int kc, int j) const {
         const int m = kc * BK + kk[j];
-        if (m >= npix) return zero4();
-        const int b = m / P3, p = m - b * P3, i = p / H3, jj = p - i * H3;
+        const int mm = m < npix ? m : 0;
+        const int b = mm / P3, p = mm - b * P3, i = p / H3, jj = p - i * H3;
         const int u = tap / 3, v = tap - u * 3;
-        return ld4(h2 + (((int64_t)b * H2 + i + u) * H2 + jj + v) * C2 + c0[j]);
+        return sel4(m < npix, ld4(h2 + (((int64_t)b * H2 + i + u) * H2 + jj + v) * C2 + c0[j]));
     }
 };
 
 __global__ __launch_bounds__(256) void conv3_wgrad_kernel(const float* __restrict__ dz3,
                                                           const float* __restrict__ h2, int n,
-                                                          int cps, float* __restrict__ partial) {
+                                                          int cps, float* __restrict__ partial,
+                                                          float* __restrict__ bias_part) {
     using SH = GemmShape<64, 64, KMAJ, RMAJ>;
     __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
     const int tap = blockIdx.x, s = blockIdx.y;
@@ -395,17 +404,18 @@ __global__ __launch_bounds__(256) void conv3_wgrad_kernel(const float* __restric
     Conv3WgradA la{dz3, npix};
     Conv3WgradB lb{h2, npix, tap};
     PartialEpi epi{partial + (int64_t)s * C3 * 9 * C2, 9 * C2, tap * C2, 1.0f};
-    mfma_gemm<64, 64, 2, KMAJ, RMAJ>(smem, s * cps, min(nchunks, (s + 1) * cps), la, lb, epi);
+    float* rs = tap == 0 ? bias_part + (int64_t)s * 64 : nullptr;
+    mfma_gemm<64, 64, 2, KMAJ, RMAJ>(smem, s * cps, min(nchunks, (s + 1) * cps), la, lb, epi, rs);
 }
 
-void launch_conv3_wgrad(const float* dz3, const float* h2, int n, float* partial, int max_splits,
-                        int* splits_out, hipStream_t st) {
+void launch_conv3_wgrad(const float* dz3, const float* h2, int n, float* partial, float* bias_part,
+                        int max_splits, int* splits_out, hipStream_t st) {
     const int nchunks = (n * P3 + BK - 1) / BK;
     int splits = min(min(max_splits, nchunks), max(1, (512 + 8) / 9));
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
     *splits_out = splits;
-    conv3_wgrad_kernel<<<dim3(9, splits), 256, 0, st>>>(dz3, h2, n, cps, partial);
+    conv3_wgrad_kernel<<<dim3(9, splits), 256, 0, st>>>(dz3, h2, n, cps, partial, bias_part);
 }
 
 // ---------------------------------------------------------------------------
@@ -431,8 +441,9 @@ struct Conv2DgradA {
     __device__ f32x4 load(int kc, int j) const {
         const int t = kc >> 1, du = t >> 1, dv = t & 1;
         const int i = yy[j] - du, jj = xx[j] - dv;
-        if (pb[j] < 0 || i < 0 || i >= H2 || jj < 0 || jj >= H2) return zero4();
-        return ld4(dz2 + (((int64_t)pb[j] * H2 + i) * H2 + jj) * C2 + (kc & 1) * BK + kk[j]);
+        const bool ok = pb[j] >= 0 && i >= 0 && i < H2 && jj >= 0 && jj < H2;
+        const int64_t e = ok ? (((int64_t)pb[j] * H2 + i) * H2 + jj) * C2 : 0;
+        return sel4(ok, ld4(dz2 + e + (kc & 1) * BK + kk[j]));
     }
 };
 struct Conv2DgradB {  // w2d[(u,v)][c][o], rows c, quads along o
@@ -490,7 +501,7 @@ struct Conv2WgradA {  // dz2 quads along o at one pixel
     __device__ void init(int j, int row, int k) { o0[j] = row; kk[j] = k; }
     __device__ f32x4 load(int kc, int j) const {
         const int m = kc * BK + kk[j];
-        return m < npix ? ld4(dz2 + (int64_t)m * C2 + o0[j]) : zero4();
+        return sel4(m < npix, ld4(dz2 + (int64_t)(m < npix ? m : 0) * C2 + o0[j]));
     }
 };
 struct Conv2WgradB {  // h1 quads along c at one (pixel, tap)
@@ -504,15 +515,16 @@ struct Conv2WgradB {  // h1 quads along c at one (pixel, tap)
     }
     __device__ f32x4 load(int kc, int j) const {
         const int m = kc * BK + kk[j];
-        if (m >= npix) return zero4();
-        const int b = m / P2, p = m - b * P2, i = p / H2, jj = p - i * H2;
-        return ld4(h1 + (((int64_t)b * H1 + S2 * i) * H1 + S2 * jj) * C1 + off[j]);
+        const int mm = m < npix ? m : 0;
+        const int b = mm / P2, p = mm - b * P2, i = p / H2, jj = p - i * H2;
+        return sel4(m < npix, ld4(h1 + (((int64_t)b * H1 + S2 * i) * H1 + S2 * jj) * C1 + off[j]));
     }
 };
 
 __global__ __launch_bounds__(256) void conv2_wgrad_kernel(const float* __restrict__ dz2,
                                                           const float* __restrict__ h1, int n,
-                                                          int cps, float* __restrict__ partial) {
+                                                          int cps, float* __restrict__ partial,
+                                                          float* __restrict__ bias_part) {
     using SH = GemmShape<64, 64, RMAJ, RMAJ>;
     __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
     const int tap0 = blockIdx.x * 2, s = blockIdx.y;
@@ -520,109 +532,92 @@ __global__ __launch_bounds__(256) void conv2_wgrad_kernel(const float* __restric
     Conv2WgradA la{dz2, npix};
     Conv2WgradB lb{h1, npix, tap0};
     PartialEpi epi{partial + (int64_t)s * C2 * 16 * C1, 16 * C1, tap0 * C1, 1.0f};
-    mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, s * cps, min(nchunks, (s + 1) * cps), la, lb, epi);
+    float* rs = blockIdx.x == 0 ? bias_part + (int64_t)s * 64 : nullptr;
+    mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, s * cps, min(nchunks, (s + 1) * cps), la, lb, epi, rs);
 }
 
-void launch_conv2_wgrad(const float* dz2, const float* h1, int n, float* partial, int max_splits,
-                        int* splits_out, hipStream_t st) {
+void launch_conv2_wgrad(const float* dz2, const float* h1, int n, float* partial, float* bias_part,
+                        int max_splits, int* splits_out, hipStream_t st) {
     const int nchunks = (n * P2 + BK - 1) / BK;
     int splits = min(min(max_splits, nchunks), 512 / 8);
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
     *splits_out = splits;
-    conv2_wgrad_kernel<<<dim3(8, splits), 256, 0, st>>>(dz2, h1, n, cps, partial);
+    conv2_wgrad_kernel<<<dim3(8, splits), 256, 0, st>>>(dz2, h1, n, cps, partial, bias_part);
 }
 
 // ---------------------------------------------------------------------------
-// Bias gradients of the convolutions: db_l[o] = sum over samples and pixels of
-// dz_l.  Block (blk, layer) sums a contiguous share of the rows in a fixed
-// order; bpart[layer][blk][64].
+// Final reduction.  Every output element is a sum of partials (split partials
+// of the conv weight gradients, bias partials, row-block partials of dW5, db5
+// and the loss) added in split / block order and scattered to its place.  A
+// block owns 64 consecutive elements of the list below; its four waves each add
+// every fourth partial, then one wave adds the four sums in wave order.
+//   [0, N1)            dW1   (partials already in [o][c][u][v] order)
+//   [.., +N2)          dW2   (partials [o][(u*4+v)*32 + c])
+//   [.., +N3)          dW3   (partials [o][(u*3+v)*64 + c])
+//   [.., +160)         db1, db2, db3
+//   [.., +A*512)       dW5
+//   [.., +A)           db5
+//   [.., +1)           loss (divided by the batch size)
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void bias_partials_kernel(const float* __restrict__ dz1,
-                                                            const float* __restrict__ dz2,
-                                                            const float* __restrict__ dz3, int n,
-                                                            float* __restrict__ bpart, int nblk) {
-    __shared__ float red[256];
-    const int blk = blockIdx.x, layer = blockIdx.y, tid = threadIdx.x;
-    float acc = 0.0f;
-    int C, lanes;
-    if (layer == 0) {
-        C = C1; lanes = 256 / C1;
-        const int64_t rows = (int64_t)n * P1;
-        const int64_t r0 = rows * blk / nblk, r1 = rows * (blk + 1) / nblk;
-        for (int64_t r = r0 + tid / C; r < r1; r += lanes) acc += dz1[r * C1 + tid % C];
-    } else if (layer == 1) {
-        C = C2; lanes = 256 / C2;
-        const int64_t rows = (int64_t)n * P2;
-        const int64_t r0 = rows * blk / nblk, r1 = rows * (blk + 1) / nblk;
-        for (int64_t r = r0 + tid / C; r < r1; r += lanes) acc += dz2[r * C2 + tid % C];
-    } else {
-        C = C3; lanes = 256 / C3;
-        const int b0 = (int)((int64_t)n * blk / nblk), b1 = (int)((int64_t)n * (blk + 1) / nblk);
-        for (int b = b0 + tid / C; b < b1; b += lanes) {
-            const float* p = dz3 + (int64_t)b * FLAT + (tid % C) * P3;
-            for (int q = 0; q < P3; ++q) acc += p[q];
-        }
-    }
-    red[tid] = acc;
-    __syncthreads();
-    if (tid < C) {
-        float s = 0.0f;
-        for (int l = 0; l < lanes; ++l) s += red[l * C + tid];
-        bpart[((int64_t)layer * nblk + blk) * 64 + tid] = s;
-    }
-}
-
-void launch_bias_partials(const float* dz1, const float* dz2, const float* dz3, int n,
-                          float* bpart, int nblk, hipStream_t st) {
-    bias_partials_kernel<<<dim3(nblk, 3), 256, 0, st>>>(dz1, dz2, dz3, n, bpart, nblk);
-}
-
-// ---------------------------------------------------------------------------
-// Sum the split partials in split order and scatter into the OIHW gradient
-// layout; add up the bias partials.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void grad_reduce_kernel(const float* __restrict__ part1, int s1,
-                                                          const float* __restrict__ part2, int s2,
-                                                          const float* __restrict__ part3, int s3,
-                                                          const float* __restrict__ bpart, int nblk,
-                                                          float* __restrict__ grads) {
+__global__ __launch_bounds__(256) void grad_reduce_kernel(ReduceArgs ra) {
     constexpr int N1 = C1 * 256, N2 = C2 * 16 * C1, N3 = C3 * 9 * C2;
-    const int e = blockIdx.x * 256 + threadIdx.x;
-    if (e < N1) {  // partial1 is already [o][c][u][v]
-        float acc = 0.0f;
-        for (int s = 0; s < s1; ++s) acc += part1[(int64_t)s * N1 + e];
-        grads[OFF_W1 + e] = acc;
-    } else if (e < N1 + N2) {  // partial2 [o][(u*4+v)*32 + c]
+    constexpr int E0 = N1 + N2 + N3, E1 = E0 + C1 + C2 + C3;
+    const int E2 = E1 + ra.A * HID, E3 = E2 + ra.A;
+    __shared__ float red[4][64];
+    const int el = threadIdx.x & 63, sq = threadIdx.x >> 6;
+    const int e = blockIdx.x * 64 + el;
+    const float* src = nullptr;
+    int nsplit = 0, stride = 0;
+    float* dst = nullptr;
+    float scale = 1.0f;
+    if (e < N1) {
+        src = ra.part1 + e; nsplit = ra.s1; stride = N1; dst = ra.grads + OFF_W1 + e;
+    } else if (e < N1 + N2) {
         const int p = e - N1;
-        float acc = 0.0f;
-        for (int s = 0; s < s2; ++s) acc += part2[(int64_t)s * N2 + p];
+        src = ra.part2 + p; nsplit = ra.s2; stride = N2;
         const int o = p >> 9, t = (p >> 5) & 15, c = p & 31;
-        grads[OFF_W2 + ((o * C1 + c) * K2 + (t >> 2)) * K2 + (t & 3)] = acc;
-    } else if (e < N1 + N2 + N3) {  // partial3 [o][(u*3+v)*64 + c]
+        dst = ra.grads + OFF_W2 + ((o * C1 + c) * K2 + (t >> 2)) * K2 + (t & 3);
+    } else if (e < E0) {
         const int p = e - N1 - N2;
-        float acc = 0.0f;
-        for (int s = 0; s < s3; ++s) acc += part3[(int64_t)s * N3 + p];
+        src = ra.part3 + p; nsplit = ra.s3; stride = N3;
         const int o = p / 576, t = (p / 64) % 9, c = p & 63;
-        grads[OFF_W3 + ((o * C2 + c) * K3 + t / 3) * K3 + t % 3] = acc;
-    } else if (e < N1 + N2 + N3 + C1 + C2 + C3) {
-        int q = e - N1 - N2 - N3, layer, o;
-        int64_t off;
-        if (q < C1) { layer = 0; o = q; off = OFF_B1; }
-        else if (q < C1 + C2) { layer = 1; o = q - C1; off = OFF_B2; }
-        else { layer = 2; o = q - C1 - C2; off = OFF_B3; }
-        float acc = 0.0f;
-        for (int b = 0; b < nblk; ++b) acc += bpart[((int64_t)layer * nblk + b) * 64 + o];
-        grads[off + o] = acc;
+        dst = ra.grads + OFF_W3 + ((o * C2 + c) * K3 + t / 3) * K3 + t % 3;
+    } else if (e < E1) {
+        const int q = e - E0;
+        int layer = 2, o = q - C1 - C2;
+        if (q < C1) { layer = 0; o = q; }
+        else if (q < C1 + C2) { layer = 1; o = q - C1; }
+        src = ra.bias_part + (int64_t)layer * BIAS_PART_STRIDE + o;
+        nsplit = layer == 0 ? ra.s1 : layer == 1 ? ra.s2 : ra.s3;
+        stride = 64;
+        dst = ra.grads + (layer == 0 ? OFF_B1 : layer == 1 ? OFF_B2 : OFF_B3) + o;
+    } else if (e < E2) {
+        const int q = e - E1;
+        src = ra.hpart + q; nsplit = ra.head_blocks; stride = HP_STRIDE;
+        dst = ra.grads + OFF_W5 + q;
+    } else if (e < E3) {
+        const int q = e - E2;
+        src = ra.hpart + HP_DB5 + q; nsplit = ra.head_blocks; stride = HP_STRIDE;
+        dst = ra.grads + off_b5(ra.A) + q;
+    } else if (e == E3) {
+        src = ra.hpart + HP_LOSS; nsplit = ra.head_blocks; stride = HP_STRIDE;
+        dst = ra.loss_out;
+        scale = 1.0f / (float)ra.n;
     }
+    float acc = 0.0f;
+    if (dst) {
+#pragma unroll 4
+        for (int s = sq; s < nsplit; s += 4) acc += src[(int64_t)s * stride];
+    }
+    red[sq][el] = acc;
+    __syncthreads();
+    if (sq == 0 && dst) *dst = (((red[0][el] + red[1][el]) + red[2][el]) + red[3][el]) * scale;
 }
 
-void launch_grad_reduce(const float* part1, int s1, const float* part2, int s2,
-                        const float* part3, int s3, const float* bpart, int nblk, float* grads,
-                        hipStream_t st) {
-    const int total = C1 * 256 + C2 * 16 * C1 + C3 * 9 * C2 + C1 + C2 + C3;
-    grad_reduce_kernel<<<(total + 255) / 256, 256, 0, st>>>(part1, s1, part2, s2, part3, s3, bpart,
-                                                            nblk, grads);
+void launch_grad_reduce(const ReduceArgs& ra, hipStream_t st) {
+    const int total = C1 * 256 + C2 * 16 * C1 + C3 * 9 * C2 + C1 + C2 + C3 + ra.A * HID + ra.A + 1;
+    grad_reduce_kernel<<<(total + 63) / 64, 256, 0, st>>>(ra);
 }
 
 }  // namespace gorila
