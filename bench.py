@@ -43,19 +43,19 @@ def step_flops_per_transition(A: int) -> int:
     return 2 * (2 * fwd + bwd)
 
 
-MFMA_STAGES = ("conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "fc1_dgrad", "fc1_wgrad",
-               "conv3_dgrad", "conv3_wgrad", "conv2_dgrad", "conv2_wgrad", "conv1_wgrad")
+MFMA_STAGES = ("conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "fc1_bwd", "conv3_bwd",
+               "conv2_bwd", "conv1_wgrad")
 
 
 def stage_flops(stage: str, B: int, A: int) -> float:
-    """Algorithmic FLOPs of one launch of a stage of the learner step at batch B."""
+    """Algorithmic FLOPs of one launch of a stage of the learner step at batch B
+    (the backward stages each hold a data gradient and a weight gradient)."""
     two = 2 * B  # online + target rows in the forward stages
     table = {
         "conv1_fwd": two * MAC_CONV1, "conv2_fwd": two * MAC_CONV2, "conv3_fwd": two * MAC_CONV3,
-        "fc1_fwd": two * MAC_FC1, "head": two * 512 * A + B * 512, "head_reduce": B * 512,
-        "fc1_dgrad": B * MAC_FC1, "fc1_wgrad": B * MAC_FC1, "conv3_dgrad": B * MAC_CONV3,
-        "conv3_wgrad": B * MAC_CONV3, "conv2_dgrad": B * MAC_CONV2, "conv2_wgrad": B * MAC_CONV2,
-        "conv1_wgrad": B * MAC_CONV1,
+        "fc1_fwd": two * MAC_FC1, "head": two * 512 * A + B * 512,
+        "fc1_bwd": 2 * B * MAC_FC1 + B * 512, "conv3_bwd": 2 * B * MAC_CONV3,
+        "conv2_bwd": 2 * B * MAC_CONV2, "conv1_wgrad": B * MAC_CONV1,
     }
     return 2.0 * table.get(stage, 0)
 

@@ -15,13 +15,11 @@ namespace {
 // Stages of the calls, in launch order (bits of the timing mask).
 enum Stage {
     ST_RESOLVE, ST_PREP, ST_CONV1_FWD, ST_CONV2_FWD, ST_CONV3_FWD, ST_FC1_FWD, ST_HEAD,
-    ST_HEAD_REDUCE, ST_FC1_DGRAD, ST_FC1_WGRAD, ST_CONV3_DGRAD, ST_CONV3_WGRAD, ST_CONV2_DGRAD,
-    ST_CONV2_WGRAD, ST_CONV1_WGRAD, ST_GRAD_REDUCE, ST_COUNT
+    ST_FC1_BWD, ST_CONV3_BWD, ST_CONV2_BWD, ST_CONV1_WGRAD, ST_GRAD_REDUCE, ST_COUNT
 };
 const char* const STAGE_NAMES[ST_COUNT] = {
     "resolve", "prep_weights", "conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "head",
-    "head_reduce", "fc1_dgrad", "fc1_wgrad", "conv3_dgrad", "conv3_wgrad", "conv2_dgrad",
-    "conv2_wgrad", "conv1_wgrad", "grad_reduce"};
+    "fc1_bwd", "conv3_bwd", "conv2_bwd", "conv1_wgrad", "grad_reduce"};
 struct TimingRecord {
     int stage;
     hipEvent_t start, stop;
@@ -160,7 +158,8 @@ __global__ void states_table_kernel(const uint8_t* states, int n, const uint8_t*
 }
 
 // Forward pass of n states through one parameter set up to h4.
-int forward_one(gorila_ctx* c, const Plan& p, const float* theta, const uint8_t* states, int n) {
+int forward_one(gorila_ctx* c, const Plan& p, const float* theta, const uint8_t* states, int n,
+                int* fc1_splits) {
     hipStream_t st = c->stream;
     const uint8_t** ftab = at<const uint8_t*>(c, p.ftab);
     { StageTimer t(c, ST_RESOLVE); states_table_kernel<<<(n * 4 + 255) / 256, 256, 0, st>>>(states, n, ftab); }
@@ -173,7 +172,7 @@ int forward_one(gorila_ctx* c, const Plan& p, const float* theta, const uint8_t*
     { StageTimer t(c, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 1, n, at<float>(c, p.h1), st); }
     { StageTimer t(c, ST_CONV2_FWD); launch_conv2_fwd(at<float>(c, p.h1), w2t, th, 1, n, at<float>(c, p.h2), st); }
     { StageTimer t(c, ST_CONV3_FWD); launch_conv3_fwd(at<float>(c, p.h2), w3t, th, 1, n, at<float>(c, p.h3), st); }
-    { StageTimer t(c, ST_FC1_FWD); launch_fc1_fwd(at<float>(c, p.h3), th, 1, n, at<float>(c, p.fc1part), at<float>(c, p.h4), st); }
+    { StageTimer t(c, ST_FC1_FWD); *fc1_splits = launch_fc1_fwd(at<float>(c, p.h3), th, 1, n, at<float>(c, p.fc1part), st); }
     return check_launch();
 }
 
@@ -338,8 +337,13 @@ int gorila_q_forward(const gorila_params* params, const uint8_t* states_u8, int3
     const Plan p = make_plan(n, 0, params->n_actions);
     if (p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
     const float* theta = (const float*)params->data;
-    if ((rc = forward_one(ctx, p, theta, states_u8, n))) return rc;
-    { StageTimer t(ctx, ST_HEAD); launch_q_head(at<float>(ctx, p.h4), theta, n, params->n_actions, q_out, ctx->stream); }
+    int splits = 0;
+    if ((rc = forward_one(ctx, p, theta, states_u8, n, &splits))) return rc;
+    {
+        StageTimer t(ctx, ST_HEAD);
+        launch_q_head(at<float>(ctx, p.fc1part), splits, theta, n, params->n_actions, q_out,
+                      ctx->stream);
+    }
     return check_launch();
 }
 
@@ -354,11 +358,12 @@ int gorila_act(const gorila_params* params, const uint8_t* states_u8, int32_t n,
     const Plan p = make_plan(n, 0, params->n_actions);
     if (p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
     const float* theta = (const float*)params->data;
-    if ((rc = forward_one(ctx, p, theta, states_u8, n))) return rc;
+    int splits = 0;
+    if ((rc = forward_one(ctx, p, theta, states_u8, n, &splits))) return rc;
     {
         StageTimer t(ctx, ST_HEAD);
-        launch_act_head(at<float>(ctx, p.h4), theta, n, params->n_actions, eps, seed, actions_out,
-                        q_out, ctx->stream);
+        launch_act_head(at<float>(ctx, p.fc1part), splits, theta, n, params->n_actions, eps, seed,
+                        actions_out, q_out, ctx->stream);
     }
     return check_launch();
 }
@@ -409,7 +414,11 @@ int gorila_learner_step(const gorila_params* params, const gorila_params* target
     { StageTimer t(ctx, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 2, B, h1, st); }
     { StageTimer t(ctx, ST_CONV2_FWD); launch_conv2_fwd(h1, w2t, th, 2, B, h2, st); }
     { StageTimer t(ctx, ST_CONV3_FWD); launch_conv3_fwd(h2, w3t, th, 2, B, h3, st); }
-    { StageTimer t(ctx, ST_FC1_FWD); launch_fc1_fwd(h3, th, 2, B, at<float>(ctx, p.fc1part), h4, st); }
+    int fc1_splits = 0;
+    {
+        StageTimer t(ctx, ST_FC1_FWD);
+        fc1_splits = launch_fc1_fwd(h3, th, 2, B, at<float>(ctx, p.fc1part), st);
+    }
 
     float* dz4 = at<float>(ctx, p.dz4);
     float* dz3 = at<float>(ctx, p.dz3);
@@ -419,23 +428,30 @@ int gorila_learner_step(const gorila_params* params, const gorila_params* target
     float* coef = at<float>(ctx, p.coef);
     {
         StageTimer t(ctx, ST_HEAD);
-        launch_td_head(h4, theta, theta_t, B, A, a, r, term, gamma, clip_delta, at<float>(ctx, p.q),
-                       ell, coef, dz4, st);
+        launch_td_head(at<float>(ctx, p.fc1part), fc1_splits, theta, theta_t, B, A, a, r, term,
+                       gamma, clip_delta, h4, at<float>(ctx, p.q), ell, coef, dz4, st);
     }
-    int head_blocks = 0;
-    {
-        StageTimer t(ctx, ST_HEAD_REDUCE);
-        head_blocks = launch_head_partial(h4, a, coef, ell, B, A, at<float>(ctx, p.hpart), st);
-    }
-    { StageTimer t(ctx, ST_FC1_DGRAD); launch_fc1_dgrad(dz4, theta, h3, B, dz3, st); }
-    { StageTimer t(ctx, ST_FC1_WGRAD); launch_fc1_wgrad(dz4, h3, B, grads_out, st); }
-    int s1 = 0, s2 = 0, s3 = 0;
+    int head_blocks = 0, s1 = 0, s2 = 0, s3 = 0;
     float* bpart = at<float>(ctx, p.bpart);
-    { StageTimer t(ctx, ST_CONV3_DGRAD); launch_conv3_dgrad(dz3, wv[0].w3d, h2, B, dz2, st); }
-    { StageTimer t(ctx, ST_CONV3_WGRAD); launch_conv3_wgrad(dz3, h2, B, at<float>(ctx, p.part3), bpart + 2 * BIAS_PART_STRIDE, WG_MAX_SPLITS, &s3, st); }
-    { StageTimer t(ctx, ST_CONV2_DGRAD); launch_conv2_dgrad(dz2, wv[0].w2d, h1, B, dz1, st); }
-    { StageTimer t(ctx, ST_CONV2_WGRAD); launch_conv2_wgrad(dz2, h1, B, at<float>(ctx, p.part2), bpart + BIAS_PART_STRIDE, WG_MAX_SPLITS, &s2, st); }
-    { StageTimer t(ctx, ST_CONV1_WGRAD); launch_conv1_wgrad(dz1, ftab, B, at<float>(ctx, p.part1), bpart, CONV1_WG_MAX_SPLITS, &s1, st); }
+    {
+        StageTimer t(ctx, ST_FC1_BWD);
+        head_blocks = launch_fc1_backward(dz4, theta, h3, h4, a, coef, ell, B, A, dz3, grads_out,
+                                          at<float>(ctx, p.hpart), st);
+    }
+    {
+        StageTimer t(ctx, ST_CONV3_BWD);
+        s3 = launch_conv3_backward(dz3, wv[0].w3d, h2, B, dz2, at<float>(ctx, p.part3),
+                                   bpart + 2 * BIAS_PART_STRIDE, st);
+    }
+    {
+        StageTimer t(ctx, ST_CONV2_BWD);
+        s2 = launch_conv2_backward(dz2, wv[0].w2d, h1, B, dz1, at<float>(ctx, p.part2),
+                                   bpart + BIAS_PART_STRIDE, st);
+    }
+    {
+        StageTimer t(ctx, ST_CONV1_WGRAD);
+        launch_conv1_wgrad(dz1, ftab, B, at<float>(ctx, p.part1), bpart, CONV1_WG_MAX_SPLITS, &s1, st);
+    }
     {
         StageTimer t(ctx, ST_GRAD_REDUCE);
         ReduceArgs ra{at<float>(ctx, p.part1), at<float>(ctx, p.part2), at<float>(ctx, p.part3),

@@ -10,7 +10,8 @@
 // every consumer loads whole 16-byte vectors):
 //   h1, dz1 : [n][20][20][32]  pixel-major, channel-minor (NHWC)
 //   h2, dz2 : [n][9][9][64]    NHWC
-//   h3, dz3 : [n][64][49]      channel-major: the flatten order of the FC input
+//   h3      : [n][64][49]      channel-major: the flatten order of the FC input
+//   dz3     : [n][49][64]      NHWC
 //   h4, dz4 : [n][512]
 #pragma once
 #include <hip/hip_runtime.h>
@@ -242,6 +243,39 @@ struct PartialEpi {
         out[(int64_t)row * ld + col0 + col] = v * scale;
     }
 };
+
+// Butterfly sum over a wave64: every lane ends with the same bit pattern.
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+// Several independent jobs in one launch: blocks [0, a.blocks()) run job a,
+// the next b.blocks() run job b, the rest job c.  A job is a struct with
+// SMEM (floats of shared memory), blocks() and run(block, smem).
+struct NoJob {
+    static constexpr int SMEM = 1;
+    __host__ __device__ int blocks() const { return 0; }
+    __device__ void run(int, float*) const {}
+};
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+template <class J1, class J2, class J3>
+__global__ __launch_bounds__(256) void jobs_kernel(J1 a, J2 b, J3 c) {
+    __shared__ __attribute__((aligned(16))) float smem[cmax(J1::SMEM, cmax(J2::SMEM, J3::SMEM))];
+    int bid = blockIdx.x;
+    const int na = a.blocks();
+    if (bid < na) { a.run(bid, smem); return; }
+    bid -= na;
+    const int nb = b.blocks();
+    if (bid < nb) { b.run(bid, smem); return; }
+    c.run(bid - nb, smem);
+}
+template <class J1, class J2 = NoJob, class J3 = NoJob>
+inline void launch_jobs(hipStream_t st, const J1& a, const J2& b = J2{}, const J3& c = J3{}) {
+    const int blocks = a.blocks() + b.blocks() + c.blocks();
+    if (blocks > 0) jobs_kernel<J1, J2, J3><<<blocks, 256, 0, st>>>(a, b, c);
+}
 
 __device__ inline f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 __device__ inline f32x4 sel4(bool ok, f32x4 v) {

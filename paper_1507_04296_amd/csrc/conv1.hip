@@ -140,7 +140,7 @@ __global__ __launch_bounds__(256) void conv1_wgrad_kernel(const float* __restric
 void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int n, float* partial,
                         float* bias_part, int max_splits, int* splits_out, hipStream_t st) {
     const int nchunks = (n * P1 + BK - 1) / BK;
-    int splits = min(max_splits, max(1, 512 / (256 / C1W_BN)));
+    int splits = min(max_splits, max(1, TARGET_WGS / (256 / C1W_BN)));
     splits = min(splits, nchunks);
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;

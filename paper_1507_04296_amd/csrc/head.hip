@@ -5,19 +5,15 @@
 //    TD error delta = y - Q(s, a; theta), Huber loss and dLoss/dQ (eq. (1),
 //    (2); Algorithm 1's terminal case), fused with the action-head backward
 //    dz4 = dLoss/dQ(s,a) * W5[a][:] * [h4 > 0].
-// One wave64 per sample: lane l holds h4[8l .. 8l+7]; each of the A dot
-// products is a butterfly sum over the wave, so every lane ends with the same
-// bit pattern and the result does not depend on scheduling.
+// One wave64 per sample.  The FC-512 layer arrives as split-K partial sums
+// fc1part[g][s][b][512]; lane l adds its 8 columns over the splits in order,
+// adds the bias and applies the ReLU, so h4 is finished here.  Each of the A
+// dot products is a butterfly sum over the wave, so every lane ends with the
+// same bit pattern and nothing depends on scheduling.
 #include "common.h"
 #include "kernels.h"
 
 namespace gorila {
-
-__device__ inline float wave_sum(float v) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
-    return v;
-}
 
 __device__ inline float dot8(const float* h, const float* w) {
     const f32x4 w0 = ld4(w), w1 = ld4(w + 4);
@@ -32,10 +28,20 @@ __device__ inline float dot8(const float* h, const float* w) {
     return s;
 }
 
-__device__ inline void load8(const float* p, float* h) {
-    const f32x4 a = ld4(p), b = ld4(p + 4);
-    h[0] = a[0]; h[1] = a[1]; h[2] = a[2]; h[3] = a[3];
-    h[4] = b[0]; h[5] = b[1]; h[6] = b[2]; h[7] = b[3];
+// h[0..7] = relu(b4[8l..] + sum_s part[s][b][8l..]) for one row b.
+__device__ inline void finish_h4(const float* part, int splits, int64_t split_stride,
+                                 const float* b4, int lane, float* h) {
+    f32x4 a = ld4(part + lane * 8), c = ld4(part + lane * 8 + 4);
+    for (int s = 1; s < splits; ++s) {
+        const float* p = part + s * split_stride + lane * 8;
+        a += ld4(p);
+        c += ld4(p + 4);
+    }
+    const f32x4 ba = ld4(b4 + lane * 8), bc = ld4(b4 + lane * 8 + 4);
+    h[0] = fmaxf(a[0] + ba[0], 0.f); h[1] = fmaxf(a[1] + ba[1], 0.f);
+    h[2] = fmaxf(a[2] + ba[2], 0.f); h[3] = fmaxf(a[3] + ba[3], 0.f);
+    h[4] = fmaxf(c[0] + bc[0], 0.f); h[5] = fmaxf(c[1] + bc[1], 0.f);
+    h[6] = fmaxf(c[2] + bc[2], 0.f); h[7] = fmaxf(c[3] + bc[3], 0.f);
 }
 
 // SplitMix64 output function (Steele, Lea and Flood 2014).
@@ -45,7 +51,7 @@ __device__ inline uint64_t splitmix64_mix(uint64_t z) {
     return z ^ (z >> 31);
 }
 
-__global__ __launch_bounds__(256) void q_head_kernel(const float* __restrict__ h4,
+__global__ __launch_bounds__(256) void q_head_kernel(const float* __restrict__ fc1part, int splits,
                                                      const float* __restrict__ theta, int n, int A,
                                                      float* __restrict__ q,
                                                      int32_t* __restrict__ actions,
@@ -53,7 +59,7 @@ __global__ __launch_bounds__(256) void q_head_kernel(const float* __restrict__ h
     const int lane = threadIdx.x & 63, b = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (b >= n) return;
     float h[8];
-    load8(h4 + (int64_t)b * HID + lane * 8, h);
+    finish_h4(fc1part + (int64_t)b * HID, splits, (int64_t)n * HID, theta + OFF_B4, lane, h);
     const float* W5 = theta + OFF_W5;
     const float* b5 = theta + off_b5(A);
     float best = 0.0f;
@@ -72,32 +78,38 @@ __global__ __launch_bounds__(256) void q_head_kernel(const float* __restrict__ h
     }
 }
 
-void launch_q_head(const float* h4, const float* theta, int n, int A, float* q, hipStream_t st) {
+void launch_q_head(const float* fc1part, int splits, const float* theta, int n, int A, float* q,
+                   hipStream_t st) {
     if (n <= 0) return;
-    q_head_kernel<<<(n + 3) / 4, 256, 0, st>>>(h4, theta, n, A, q, nullptr, 0, 0);
+    q_head_kernel<<<(n + 3) / 4, 256, 0, st>>>(fc1part, splits, theta, n, A, q, nullptr, 0, 0);
 }
 
-void launch_act_head(const float* h4, const float* theta, int n, int A, float eps, uint64_t seed,
-                     int32_t* actions, float* q_out, hipStream_t st) {
+void launch_act_head(const float* fc1part, int splits, const float* theta, int n, int A, float eps,
+                     uint64_t seed, int32_t* actions, float* q_out, hipStream_t st) {
     if (n <= 0) return;
     // explore iff a uniform 53-bit integer is below floor(eps * 2^53); eps is
     // exact in double and the scaling by 2^53 is exact.
     const uint64_t below = (uint64_t)floor((double)eps * 9007199254740992.0);
-    q_head_kernel<<<(n + 3) / 4, 256, 0, st>>>(h4, theta, n, A, q_out, actions, below, seed);
+    q_head_kernel<<<(n + 3) / 4, 256, 0, st>>>(fc1part, splits, theta, n, A, q_out, actions, below,
+                                               seed);
 }
 
-// h4 holds 2n rows: online rows [0, n) on s, target rows [n, 2n) on s'.
+// fc1part holds [2][splits][n][512]: group 0 (online, on s), group 1 (target, on s').
 __global__ __launch_bounds__(256) void td_head_kernel(
-    const float* __restrict__ h4, const float* __restrict__ theta,
+    const float* __restrict__ fc1part, int splits, const float* __restrict__ theta,
     const float* __restrict__ theta_t, int n, int A, const int32_t* __restrict__ a,
     const float* __restrict__ r, const uint8_t* __restrict__ term, float gamma, float clip,
-    float* __restrict__ q, float* __restrict__ ell, float* __restrict__ coef,
-    float* __restrict__ dz4) {
+    float* __restrict__ h4, float* __restrict__ q, float* __restrict__ ell,
+    float* __restrict__ coef, float* __restrict__ dz4) {
     const int lane = threadIdx.x & 63, b = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (b >= n) return;
+    const int64_t ss = (int64_t)n * HID;
     float h[8], ht[8];
-    load8(h4 + (int64_t)b * HID + lane * 8, h);
-    load8(h4 + (int64_t)(n + b) * HID + lane * 8, ht);
+    finish_h4(fc1part + (int64_t)b * HID, splits, ss, theta + OFF_B4, lane, h);
+    finish_h4(fc1part + splits * ss + (int64_t)b * HID, splits, ss, theta_t + OFF_B4, lane, ht);
+    float* h4row = h4 + (int64_t)b * HID + lane * 8;
+    *(f32x4*)h4row = f32x4{h[0], h[1], h[2], h[3]};
+    *(f32x4*)(h4row + 4) = f32x4{h[4], h[5], h[6], h[7]};
     const float* W5 = theta + OFF_W5;
     const float* b5 = theta + off_b5(A);
     const float* W5t = theta_t + OFF_W5;
@@ -134,67 +146,13 @@ __global__ __launch_bounds__(256) void td_head_kernel(
     *(f32x4*)(out + 4) = o1;
 }
 
-void launch_td_head(const float* h4, const float* theta, const float* theta_target, int n, int A,
-                    const int32_t* a, const float* r, const uint8_t* term, float gamma, float clip,
-                    float* q, float* ell, float* coef, float* dz4, hipStream_t st) {
+void launch_td_head(const float* fc1part, int splits, const float* theta, const float* theta_target,
+                    int n, int A, const int32_t* a, const float* r, const uint8_t* term, float gamma,
+                    float clip, float* h4, float* q, float* ell, float* coef, float* dz4,
+                    hipStream_t st) {
     if (n <= 0) return;
-    td_head_kernel<<<(n + 3) / 4, 256, 0, st>>>(h4, theta, theta_target, n, A, a, r, term, gamma,
-                                                clip, q, ell, coef, dz4);
-}
-
-// Partial sums of the action-head gradients and the loss over blocks of rows:
-//   hpart[bb][a*512 + k] = sum_{b in block bb, a_b = a} coef_b h4[b][k]   (dW5)
-//   hpart[bb][HP_DB5 + a] = sum_{b in block bb, a_b = a} coef_b           (db5)
-//   hpart[bb][HP_LOSS]    = sum_{b in block bb} ell_b                     (loss)
-// Grid (8 column tiles, row blocks).  Thread (column kl, lane group bq) adds
-// rows bq, bq+4, ... of its block in order into its own LDS slots; the four
-// lane groups are added in order, so every sum is deterministic.  The blocks
-// are summed in order by the final gradient reduction.
-__global__ __launch_bounds__(256) void head_partial_kernel(
-    const float* __restrict__ h4, const int32_t* __restrict__ a, const float* __restrict__ coef,
-    const float* __restrict__ ell, int n, int A, int rows_per_block, float* __restrict__ hpart) {
-    __shared__ float sacc[4][MAX_ACTIONS][64];
-    const int tid = threadIdx.x, kl = tid & 63, bq = tid >> 6;
-    const int k = blockIdx.x * 64 + kl, bb = blockIdx.y;
-    const int b0 = bb * rows_per_block, b1 = min(n, b0 + rows_per_block);
-    float* out = hpart + (int64_t)bb * HP_STRIDE;
-    for (int j = 0; j < A; ++j) sacc[bq][j][kl] = 0.0f;
-    for (int b = b0 + bq; b < b1; b += 4) {
-        const int ab = a[b];
-        sacc[bq][ab][kl] = fmaf(coef[b], h4[(int64_t)b * HID + k], sacc[bq][ab][kl]);
-    }
-    __syncthreads();
-    for (int e = tid; e < A * 64; e += 256) {
-        const int j = e >> 6, kk = e & 63;
-        out[j * HID + blockIdx.x * 64 + kk] =
-            ((sacc[0][j][kk] + sacc[1][j][kk]) + sacc[2][j][kk]) + sacc[3][j][kk];
-    }
-    if (blockIdx.x == 0) {
-        // wave w: actions j = w, w+4, ...; lane l: rows b0+l, b0+l+64, ...
-        const int lane = tid & 63, w = tid >> 6;
-        for (int j = w; j < A; j += 4) {
-            float s = 0.0f;
-            for (int b = b0 + lane; b < b1; b += 64)
-                if (a[b] == j) s += coef[b];
-            s = wave_sum(s);
-            if (lane == 0) out[HP_DB5 + j] = s;
-        }
-        if (w == 0) {
-            float s = 0.0f;
-            for (int b = b0 + lane; b < b1; b += 64) s += ell[b];
-            s = wave_sum(s);
-            if (lane == 0) out[HP_LOSS] = s;
-        }
-    }
-}
-
-int launch_head_partial(const float* h4, const int32_t* a, const float* coef, const float* ell,
-                        int n, int A, float* hpart, hipStream_t st) {
-    if (n <= 0) return 0;
-    int rows = max(32, (n + HEAD_MAX_BLOCKS - 1) / HEAD_MAX_BLOCKS);
-    const int blocks = (n + rows - 1) / rows;
-    head_partial_kernel<<<dim3(HID / 64, blocks), 256, 0, st>>>(h4, a, coef, ell, n, A, rows, hpart);
-    return blocks;
+    td_head_kernel<<<(n + 3) / 4, 256, 0, st>>>(fc1part, splits, theta, theta_target, n, A, a, r,
+                                                term, gamma, clip, h4, q, ell, coef, dz4);
 }
 
 }  // namespace gorila

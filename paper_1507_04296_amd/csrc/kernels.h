@@ -55,34 +55,35 @@ void launch_conv2_fwd(const float* h1, const GroupPtrs& w2t, const GroupPtrs& th
                       int n, float* h2, hipStream_t st);
 void launch_conv3_fwd(const float* h2, const GroupPtrs& w3t, const GroupPtrs& theta, int groups,
                       int n, float* h3, hipStream_t st);
-void launch_fc1_fwd(const float* h3, const GroupPtrs& theta, int groups, int n, float* partial,
-                    float* h4, hipStream_t st);
+// fc1 forward as split-K partial sums partial[g][s][b][512]; returns the
+// number of splits s (the head kernels finish the layer).
+int launch_fc1_fwd(const float* h3, const GroupPtrs& theta, int groups, int n, float* partial,
+                   hipStream_t st);
 
 // Head: Q values, epsilon-greedy actions, TD error / Huber loss / dLoss.
-void launch_q_head(const float* h4, const float* theta, int n, int A, float* q, hipStream_t st);
-void launch_act_head(const float* h4, const float* theta, int n, int A, float eps, uint64_t seed,
-                     int32_t* actions, float* q_out, hipStream_t st);
-void launch_td_head(const float* h4, const float* theta, const float* theta_target, int n, int A,
-                    const int32_t* a, const float* r, const uint8_t* term, float gamma, float clip,
-                    float* q, float* ell, float* coef, float* dz4, hipStream_t st);
-// Row-block partials of dW5, db5 and the loss (see head.hip); returns the
-// number of row blocks written.
-int launch_head_partial(const float* h4, const int32_t* a, const float* coef, const float* ell,
-                        int n, int A, float* hpart, hipStream_t st);
+// Each first finishes the FC-512 layer (splits in order, bias, ReLU).
+void launch_q_head(const float* fc1part, int splits, const float* theta, int n, int A, float* q,
+                   hipStream_t st);
+void launch_act_head(const float* fc1part, int splits, const float* theta, int n, int A, float eps,
+                     uint64_t seed, int32_t* actions, float* q_out, hipStream_t st);
+// Writes h4 (online rows), q [2n][A], ell, coef = dLoss/dQ(s,a) and dz4.
+void launch_td_head(const float* fc1part, int splits, const float* theta, const float* theta_target,
+                    int n, int A, const int32_t* a, const float* r, const uint8_t* term, float gamma,
+                    float clip, float* h4, float* q, float* ell, float* coef, float* dz4,
+                    hipStream_t st);
 
-// Backward layers.
-void launch_fc1_dgrad(const float* dz4, const float* theta, const float* h3, int n, float* dz3,
-                      hipStream_t st);
-// dW4 and (as row sums of dz4) db4, written straight into grads.
-void launch_fc1_wgrad(const float* dz4, const float* h3, int n, float* grads, hipStream_t st);
-void launch_conv3_dgrad(const float* dz3, const float* w3d, const float* h2, int n, float* dz2,
-                        hipStream_t st);
-void launch_conv3_wgrad(const float* dz3, const float* h2, int n, float* partial, float* bias_part,
-                        int max_splits, int* splits_out, hipStream_t st);
-void launch_conv2_dgrad(const float* dz2, const float* w2d, const float* h1, int n, float* dz1,
-                        hipStream_t st);
-void launch_conv2_wgrad(const float* dz2, const float* h1, int n, float* partial, float* bias_part,
-                        int max_splits, int* splits_out, hipStream_t st);
+// Backward, three launches of independent jobs each:
+//  fc1: dz3 = [h3 > 0] W4^T dz4 (stored [b][p][o]), dW4 and db4 into grads,
+//       and row-block partials of dW5, db5 and the loss (returns #row blocks);
+//  conv3: dz2 and split partials of dW3 / db3 (returns #splits);
+//  conv2: dz1 and split partials of dW2 / db2 (returns #splits).
+int launch_fc1_backward(const float* dz4, const float* theta, const float* h3, const float* h4,
+                        const int32_t* a, const float* coef, const float* ell, int n, int A,
+                        float* dz3, float* grads, float* hpart, hipStream_t st);
+int launch_conv3_backward(const float* dz3, const float* w3d, const float* h2, int n, float* dz2,
+                          float* partial, float* bias_part, hipStream_t st);
+int launch_conv2_backward(const float* dz2, const float* w2d, const float* h1, int n, float* dz1,
+                          float* partial, float* bias_part, hipStream_t st);
 void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int n, float* partial,
                         float* bias_part, int max_splits, int* splits_out, hipStream_t st);
 // Conv weight-gradient partials [split][o][(tap, c)], bias partials
@@ -102,10 +103,13 @@ struct ReduceArgs {
 void launch_grad_reduce(const ReduceArgs& ra, hipStream_t st);
 
 // Sizes of the split-K / partial buffers the launchers above may use.
+constexpr int TARGET_WGS = 1024;             // split-K launches aim at ~4 workgroups per CU
 constexpr int FC1_MAX_SPLITS = 14;
-constexpr int WG_MAX_SPLITS = 128;
-constexpr int CONV1_WG_MAX_SPLITS = 256;
-constexpr int BIAS_PART_STRIDE = 256 * 64;  // floats per layer in bias_part
+constexpr int WG_MAX_SPLITS = 256;
+constexpr int CONV3_WG_SPLITS = 114;         // 9 column tiles x 114 splits ~ 1024 workgroups
+constexpr int CONV2_WG_SPLITS = 64;          // 8 column tiles x 64 splits
+constexpr int CONV1_WG_MAX_SPLITS = 512;
+constexpr int BIAS_PART_STRIDE = 512 * 64;  // floats per layer in bias_part
 constexpr int HEAD_MAX_BLOCKS = 16;          // row blocks of the head partials
 constexpr int HP_DB5 = MAX_ACTIONS * HID;    // offsets inside one head partial
 constexpr int HP_LOSS = HP_DB5 + MAX_ACTIONS;

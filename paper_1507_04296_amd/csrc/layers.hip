@@ -160,8 +160,8 @@ void launch_conv3_fwd(const float* h2, const GroupPtrs& w3t, const GroupPtrs& th
 }
 
 // ---------------------------------------------------------------------------
-// fc1 forward, split over the 3136-long reduction: partial[g][s][b][o];
-// a second pass adds the splits in order, the bias and the ReLU.
+// fc1 forward, split over the 3136-long reduction: partial[g][s][b][o].  The
+// action-head kernel adds the splits in order, the bias and the ReLU.
 // ---------------------------------------------------------------------------
 struct RowMajorK {  // rows of a row-major [rows][ld] matrix, quads along k
     const float* a;
@@ -198,37 +198,21 @@ __global__ __launch_bounds__(256) void fc1_fwd_kernel(const float* __restrict__ 
     mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, kc0, kc1, la, lb, epi);
 }
 
-__global__ __launch_bounds__(256) void fc1_fwd_reduce_kernel(const float* __restrict__ partial,
-                                                             GroupPtrs theta, int n, int splits,
-                                                             float* __restrict__ h4) {
-    const int g = blockIdx.y;
-    const int64_t per = (int64_t)n * HID;
-    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < per; e += (int64_t)gridDim.x * 256) {
-        const float* p = partial + (int64_t)g * splits * per + e;
-        float acc = 0.0f;
-        for (int s = 0; s < splits; ++s) acc += p[s * per];
-        const int o = (int)(e % HID);
-        h4[(int64_t)g * per + e] = fmaxf(acc + theta.p[g][OFF_B4 + o], 0.0f);
-    }
-}
-
-void launch_fc1_fwd(const float* h3, const GroupPtrs& theta, int groups, int n, float* partial,
-                    float* h4, hipStream_t st) {
-    if (n <= 0) return;
+int launch_fc1_fwd(const float* h3, const GroupPtrs& theta, int groups, int n, float* partial,
+                   hipStream_t st) {
+    if (n <= 0) return 0;
     const int mt = (n + 63) / 64, tiles = mt * (HID / 64) * groups;
-    int splits = min(FC1_MAX_SPLITS, max(1, (512 + tiles - 1) / tiles));
+    int splits = min(FC1_MAX_SPLITS, max(1, (TARGET_WGS + tiles - 1) / tiles));
     const int cps = (FC1_CHUNKS + splits - 1) / splits;
     splits = (FC1_CHUNKS + cps - 1) / cps;
     fc1_fwd_kernel<<<dim3(mt, HID / 64, groups * splits), 256, 0, st>>>(h3, theta, n, splits, cps,
                                                                          partial);
-    const int64_t want = ((int64_t)n * HID + 255) / 256;
-    const int blocks = (int)(want < 1024 ? want : 1024);
-    fc1_fwd_reduce_kernel<<<dim3(blocks, groups), 256, 0, st>>>(partial, theta, n, splits, h4);
+    return splits;
 }
 
 // ---------------------------------------------------------------------------
-// fc1 data gradient: dz3[b][k] = [h3[b][k] > 0] * sum_o dz4[b][o] W4[o][k]
-// rows b, cols k (3136 = 49 tiles), reduction o (16 chunks).
+// fc1 data gradient: dz3 = [h3 > 0] * (W4^T dz4), rows b, cols k (3136 = 49
+// tiles), reduction o (16 chunks); dz3 is written as [b][p][o].
 // ---------------------------------------------------------------------------
 struct RowMajorR {  // B[col][k] = M[k][c0 + col] of a row-major [k][ld] matrix (RMAJ quads)
     const float* a;
@@ -253,130 +237,212 @@ struct ReluMaskStore {  // out[r][c] = mask[r][c] > 0 ? v : 0
     }
 };
 
-__global__ __launch_bounds__(256) void fc1_dgrad_kernel(const float* __restrict__ dz4,
-                                                        const float* __restrict__ W4,
-                                                        const float* __restrict__ h3, int n,
-                                                        float* __restrict__ dz3) {
-    using SH = GemmShape<64, 64, KMAJ, RMAJ>;
-    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
-    const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
-    RowMajorK la{dz4, n, r0, HID};
-    RowMajorR lb{W4, c0, FLAT, HID};
-    ReluMaskStore epi{dz3, h3, n, r0, c0, FLAT};
-    mfma_gemm<64, 64, 2, KMAJ, RMAJ>(smem, 0, HID / BK, la, lb, epi);
-}
+// df is produced in the FC input's flatten order k = o*49 + p; dz3 is stored
+// pixel-major ([b][p][o], like the other activation gradients) so that the
+// conv3 backward kernels read it in 16-byte quads.
+struct Dz3NhwcStore {
+    float* dz3;
+    const float* h3;
+    int rows, r0, c0;
+    __device__ void operator()(int row, int col, float v) const {
+        const int b = r0 + row;
+        if (b >= rows) return;
+        const int k = c0 + col, o = k / P3, p = k - o * P3;
+        const float m = h3[(int64_t)b * FLAT + k];
+        dz3[(int64_t)b * FLAT + p * C3 + o] = m > 0.0f ? v : 0.0f;
+    }
+};
 
-void launch_fc1_dgrad(const float* dz4, const float* theta, const float* h3, int n, float* dz3,
-                      hipStream_t st) {
-    if (n <= 0) return;
-    fc1_dgrad_kernel<<<dim3((n + 63) / 64, FLAT / 64), 256, 0, st>>>(dz4, theta + OFF_W4, h3, n, dz3);
-}
+struct Fc1DgradJob {
+    const float* dz4;
+    const float* W4;
+    const float* h3;
+    float* dz3;
+    int n;
+    using SH = GemmShape<64, 64, KMAJ, RMAJ>;
+    static constexpr int SMEM = SH::SMEM_FLOATS;
+    __host__ __device__ int blocks() const { return ((n + 63) / 64) * (FLAT / 64); }
+    __device__ void run(int bid, float* smem) const {
+        const int mt = (n + 63) / 64;
+        const int r0 = (bid % mt) * 64, c0 = (bid / mt) * 64;
+        RowMajorK la{dz4, n, r0, HID};
+        RowMajorR lb{W4, c0, FLAT, HID};
+        Dz3NhwcStore epi{dz3, h3, n, r0, c0};
+        mfma_gemm<64, 64, 2, KMAJ, RMAJ>(smem, 0, HID / BK, la, lb, epi);
+    }
+};
 
 // ---------------------------------------------------------------------------
 // fc1 weight gradient: dW4[o][k] = sum_b dz4[b][o] h3[b][k]  (written in place)
 // rows o (512), cols k (3136), reduction b.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void fc1_wgrad_kernel(const float* __restrict__ dz4,
-                                                        const float* __restrict__ h3, int n,
-                                                        float* __restrict__ gW4,
-                                                        float* __restrict__ gb4) {
+struct Fc1WgradJob {
+    const float* dz4;
+    const float* h3;
+    float* gW4;
+    float* gb4;
+    int n;
     using SH = GemmShape<64, 64, RMAJ, RMAJ>;
-    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
-    const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
-    RowMajorR la{dz4, r0, HID, n};
-    RowMajorR lb{h3, c0, FLAT, n};
-    PlainStore epi{gW4, HID, r0, c0, FLAT};
-    // db4[o] = sum_b dz4[b][o]: the row sums of this GEMM's A operand
-    float* rs = blockIdx.y == 0 ? gb4 + r0 : nullptr;
-    mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, 0, (n + BK - 1) / BK, la, lb, epi, rs);
-}
+    static constexpr int SMEM = SH::SMEM_FLOATS;
+    __host__ __device__ int blocks() const { return (HID / 64) * (FLAT / 64); }
+    __device__ void run(int bid, float* smem) const {
+        const int r0 = (bid % (HID / 64)) * 64, c0 = (bid / (HID / 64)) * 64;
+        RowMajorR la{dz4, r0, HID, n};
+        RowMajorR lb{h3, c0, FLAT, n};
+        PlainStore epi{gW4, HID, r0, c0, FLAT};
+        // db4[o] = sum_b dz4[b][o]: the row sums of this GEMM's A operand
+        float* rs = c0 == 0 ? gb4 + r0 : nullptr;
+        mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, 0, (n + BK - 1) / BK, la, lb, epi, rs);
+    }
+};
 
-void launch_fc1_wgrad(const float* dz4, const float* h3, int n, float* grads, hipStream_t st) {
-    if (n <= 0) return;
-    fc1_wgrad_kernel<<<dim3(HID / 64, FLAT / 64), 256, 0, st>>>(dz4, h3, n, grads + OFF_W4,
-                                                                grads + OFF_B4);
+// Row-block partial sums of the action-head gradients and of the loss:
+//   hpart[bb][a*512 + k] = sum_{b in block bb, a_b = a} coef_b h4[b][k]   (dW5)
+//   hpart[bb][HP_DB5 + a] = sum_{b in block bb, a_b = a} coef_b           (db5)
+//   hpart[bb][HP_LOSS]    = sum_{b in block bb} ell_b                     (loss)
+// Block (column tile kt, row block bb).  Thread (column kl, lane group bq)
+// adds rows bq, bq+4, ... of its block in order into its own LDS slots; the
+// four lane groups are added in order, so every sum is deterministic.  The row
+// blocks are summed in order by the final gradient reduction.
+struct HeadPartialJob {
+    const float* h4;
+    const int32_t* a;
+    const float* coef;
+    const float* ell;
+    float* hpart;
+    int n, A, rows_per_block, row_blocks;
+    static constexpr int SMEM = 4 * MAX_ACTIONS * 64;
+    __host__ __device__ int blocks() const { return (HID / 64) * row_blocks; }
+    __device__ void run(int bid, float* smem) const {
+        float (*sacc)[MAX_ACTIONS][64] = (float (*)[MAX_ACTIONS][64])smem;
+        const int tid = threadIdx.x, kl = tid & 63, bq = tid >> 6;
+        const int kt = bid % (HID / 64), bb = bid / (HID / 64);
+        const int k = kt * 64 + kl;
+        const int b0 = bb * rows_per_block, b1 = min(n, b0 + rows_per_block);
+        float* out = hpart + (int64_t)bb * HP_STRIDE;
+        for (int j = 0; j < A; ++j) sacc[bq][j][kl] = 0.0f;
+        for (int b = b0 + bq; b < b1; b += 4) {
+            const int ab = a[b];
+            sacc[bq][ab][kl] = fmaf(coef[b], h4[(int64_t)b * HID + k], sacc[bq][ab][kl]);
+        }
+        __syncthreads();
+        for (int e = tid; e < A * 64; e += 256) {
+            const int j = e >> 6, kk = e & 63;
+            out[j * HID + kt * 64 + kk] =
+                ((sacc[0][j][kk] + sacc[1][j][kk]) + sacc[2][j][kk]) + sacc[3][j][kk];
+        }
+        if (kt == 0) {
+            // wave w: actions j = w, w+4, ...; lane l: rows b0+l, b0+l+64, ...
+            const int lane = tid & 63, w = tid >> 6;
+            for (int j = w; j < A; j += 4) {
+                float s = 0.0f;
+                for (int b = b0 + lane; b < b1; b += 64)
+                    if (a[b] == j) s += coef[b];
+                s = wave_sum(s);
+                if (lane == 0) out[HP_DB5 + j] = s;
+            }
+            if (w == 0) {
+                float s = 0.0f;
+                for (int b = b0 + lane; b < b1; b += 64) s += ell[b];
+                s = wave_sum(s);
+                if (lane == 0) out[HP_LOSS] = s;
+            }
+        }
+    }
+};
+
+int launch_fc1_backward(const float* dz4, const float* theta, const float* h3, const float* h4,
+                        const int32_t* a, const float* coef, const float* ell, int n, int A,
+                        float* dz3, float* grads, float* hpart, hipStream_t st) {
+    if (n <= 0) return 0;
+    const int rows = max(32, (n + HEAD_MAX_BLOCKS - 1) / HEAD_MAX_BLOCKS);
+    const int row_blocks = (n + rows - 1) / rows;
+    launch_jobs(st, Fc1DgradJob{dz4, theta + OFF_W4, h3, dz3, n},
+                Fc1WgradJob{dz4, h3, grads + OFF_W4, grads + OFF_B4, n},
+                HeadPartialJob{h4, a, coef, ell, hpart, n, A, rows, row_blocks});
+    return row_blocks;
 }
 
 // ---------------------------------------------------------------------------
 // conv3 data gradient (stride 1): dh2[b][y][x][c] = sum_{u,v,o} W3[o][c][u][v]
-// dz3[b][o][y-u][x-v] over in-range (y-u, x-v); then dz2 = dh2 * [h2 > 0].
-// rows m = (b,y,x), cols c (64), reduction (tap, o) = 18 chunks.
+// dz3[b][y-u][x-v][o] over in-range (y-u, x-v); then dz2 = dh2 * [h2 > 0].
+// A workgroup owns one output position (y, x) for 64 samples, so the taps that
+// fall outside the 7x7 input are the same for every row and are left out of
+// the reduction: only the 1..9 valid taps x 64 channels are multiplied.
+// rows b, cols c (64), reduction (valid tap, o) in chunks of 32 o.
 // ---------------------------------------------------------------------------
-struct Conv3DgradA {  // RMAJ quads: 4 consecutive output pixels at one (tap, o)
+struct Conv3DgradA {  // KMAJ quads dz3[b][p][o..o+3] at p = (y-u)*7 + (x-v)
     const float* dz3;
-    int rows, m0;
-    int pb[MAXQ][4], py[MAXQ][4], px[MAXQ][4];
-    int kk[MAXQ];
+    int n, b0, y, x, u0, v0, nv;
+    const float* base[MAXQ];
+    bool ok[MAXQ];
     __device__ void init(int j, int row, int k) {
-        kk[j] = k;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int m = m0 + row + q;
-            const int mm = m < rows ? m : 0;
-            const int b = mm / P2, p = mm - b * P2;
-            pb[j][q] = m < rows ? b : -1;
-            py[j][q] = p / H2;
-            px[j][q] = p - (p / H2) * H2;
-        }
+        const int b = b0 + row;
+        ok[j] = b < n;
+        base[j] = dz3 + (int64_t)(ok[j] ? b : 0) * FLAT + k;
     }
     __device__ f32x4 load(int kc, int j) const {
-        const int t = kc >> 1, u = t / 3, v = t - u * 3;
-        const int o = (kc & 1) * BK + kk[j];
-        f32x4 r;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int i = py[j][q] - u, jj = px[j][q] - v;
-            const bool ok = pb[j][q] >= 0 && i >= 0 && i < H3 && jj >= 0 && jj < H3;
-            const int64_t e = ok ? (int64_t)pb[j][q] * FLAT + o * P3 + i * H3 + jj : 0;
-            const float x = dz3[e];
-            r[q] = ok ? x : 0.0f;
-        }
-        return r;
+        const int t = kc >> 1, u = u0 + t / nv, v = v0 + t % nv;
+        return sel4(ok[j], ld4(base[j] + ((y - u) * H3 + (x - v)) * C3 + (kc & 1) * BK));
+    }
+};
+struct Conv3DgradB {  // w3d[(u,v)][c][o], rows c, quads along o
+    const float* w3d;
+    int u0, v0, nv;
+    const float* base[MAXQ];
+    __device__ void init(int j, int row, int k) { base[j] = w3d + row * C3 + k; }
+    __device__ f32x4 load(int kc, int j) const {
+        const int t = kc >> 1, tap = (u0 + t / nv) * K3 + v0 + t % nv;
+        return ld4(base[j] + tap * C2 * C3 + (kc & 1) * BK);
+    }
+};
+struct Conv3DgradStore {
+    float* dz2;
+    const float* h2;
+    int n, b0, pos;
+    __device__ void operator()(int row, int col, float v) const {
+        const int b = b0 + row;
+        if (b >= n) return;
+        const int64_t e = ((int64_t)b * P2 + pos) * C2 + col;
+        dz2[e] = h2[e] > 0.0f ? v : 0.0f;
     }
 };
 
-__global__ __launch_bounds__(256) void conv3_dgrad_kernel(const float* __restrict__ dz3,
-                                                          const float* __restrict__ w3d,
-                                                          const float* __restrict__ h2, int n,
-                                                          float* __restrict__ dz2) {
-    using SH = GemmShape<64, 64, RMAJ, KMAJ>;
-    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
-    const int m0 = blockIdx.x * 64;
-    const int rows = n * P2;
-    Conv3DgradA la{dz3, rows, m0};
-    WtapB lb{w3d, C3, 2, C2};
-    ReluMaskStore epi{dz2, h2, rows, m0, 0, C2};
-    mfma_gemm<64, 64, 2, RMAJ, KMAJ>(smem, 0, 18, la, lb, epi);
-}
-
-void launch_conv3_dgrad(const float* dz3, const float* w3d, const float* h2, int n, float* dz2,
-                        hipStream_t st) {
-    if (n <= 0) return;
-    conv3_dgrad_kernel<<<(n * P2 + 63) / 64, 256, 0, st>>>(dz3, w3d, h2, n, dz2);
-}
+struct Conv3DgradJob {
+    const float* dz3;
+    const float* w3d;
+    const float* h2;
+    float* dz2;
+    int n;
+    using SH = GemmShape<64, 64, KMAJ, KMAJ>;
+    static constexpr int SMEM = SH::SMEM_FLOATS;
+    __host__ __device__ int blocks() const { return P2 * ((n + 63) / 64); }
+    __device__ void run(int bid, float* smem) const {
+        const int pos = bid % P2, y = pos / H2, x = pos - y * H2, b0 = (bid / P2) * 64;
+        const int u0 = max(0, y - (H3 - 1)), u1 = min(K3 - 1, y);
+        const int v0 = max(0, x - (H3 - 1)), v1 = min(K3 - 1, x);
+        const int nv = v1 - v0 + 1, taps = (u1 - u0 + 1) * nv;
+        Conv3DgradA la{dz3, n, b0, y, x, u0, v0, nv};
+        Conv3DgradB lb{w3d, u0, v0, nv};
+        Conv3DgradStore epi{dz2, h2, n, b0, pos};
+        mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, 0, 2 * taps, la, lb, epi);
+    }
+};
 
 // ---------------------------------------------------------------------------
-// conv3 weight gradient: dW3[o][c][u][v] = sum_{b,i,j} dz3[b][o][i][j] h2[b][i+u][j+v][c]
+// conv3 weight gradient: dW3[o][c][u][v] = sum_{b,i,j} dz3[b][i][j][o] h2[b][i+u][j+v][c]
 // rows o (64), cols (tap, c): one tap of 64 channels per column tile,
 // reduction over the n*49 output pixels, split across workgroups.
 // partial[s][o][tap*64 + c].
 // ---------------------------------------------------------------------------
-struct Conv3WgradA {  // KMAJ quads: 4 consecutive output pixels of channel o
+struct Conv3WgradA {  // RMAJ quads dz3[b][p][o0..o0+3] at one output pixel m = (b, p)
     const float* dz3;
     int npix;
-    int o[MAXQ], kk[MAXQ];
-    __device__ void init(int j, int row, int k) { o[j] = row; kk[j] = k; }
+    int o0[MAXQ], kk[MAXQ];
+    __device__ void init(int j, int row, int k) { o0[j] = row; kk[j] = k; }
     __device__ f32x4 load(int kc, int j) const {
-        f32x4 r;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int m = kc * BK + kk[j] + q;
-            const int mm = m < npix ? m : 0;
-            const int b = mm / P3, p = mm - b * P3;
-            const float x = dz3[(int64_t)b * FLAT + o[j] * P3 + p];
-            r[q] = m < npix ? x : 0.0f;
-        }
-        return r;
+        const int m = kc * BK + kk[j];
+        return sel4(m < npix, ld4(dz3 + (int64_t)(m < npix ? m : 0) * C3 + o0[j]));
     }
 };
 struct Conv3WgradB {  // RMAJ quads: 4 channels of h2 at one (pixel, tap)
@@ -393,101 +459,106 @@ struct Conv3WgradB {  // RMAJ quads: 4 channels of h2 at one (pixel, tap)
     }
 };
 
-__global__ __launch_bounds__(256) void conv3_wgrad_kernel(const float* __restrict__ dz3,
-                                                          const float* __restrict__ h2, int n,
-                                                          int cps, float* __restrict__ partial,
-                                                          float* __restrict__ bias_part) {
-    using SH = GemmShape<64, 64, KMAJ, RMAJ>;
-    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
-    const int tap = blockIdx.x, s = blockIdx.y;
-    const int npix = n * P3, nchunks = (npix + BK - 1) / BK;
-    Conv3WgradA la{dz3, npix};
-    Conv3WgradB lb{h2, npix, tap};
-    PartialEpi epi{partial + (int64_t)s * C3 * 9 * C2, 9 * C2, tap * C2, 1.0f};
-    float* rs = tap == 0 ? bias_part + (int64_t)s * 64 : nullptr;
-    mfma_gemm<64, 64, 2, KMAJ, RMAJ>(smem, s * cps, min(nchunks, (s + 1) * cps), la, lb, epi, rs);
-}
+struct Conv3WgradJob {
+    const float* dz3;
+    const float* h2;
+    float* partial;
+    float* bias_part;
+    int n, splits, cps;
+    using SH = GemmShape<64, 64, RMAJ, RMAJ>;
+    static constexpr int SMEM = SH::SMEM_FLOATS;
+    __host__ __device__ int blocks() const { return 9 * splits; }
+    __device__ void run(int bid, float* smem) const {
+        const int tap = bid % 9, s = bid / 9;
+        const int npix = n * P3, nchunks = (npix + BK - 1) / BK;
+        Conv3WgradA la{dz3, npix};
+        Conv3WgradB lb{h2, npix, tap};
+        PartialEpi epi{partial + (int64_t)s * C3 * 9 * C2, 9 * C2, tap * C2, 1.0f};
+        float* rs = tap == 0 ? bias_part + (int64_t)s * 64 : nullptr;
+        mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, s * cps, min(nchunks, (s + 1) * cps), la, lb, epi, rs);
+    }
+};
 
-void launch_conv3_wgrad(const float* dz3, const float* h2, int n, float* partial, float* bias_part,
-                        int max_splits, int* splits_out, hipStream_t st) {
+int launch_conv3_backward(const float* dz3, const float* w3d, const float* h2, int n, float* dz2,
+                          float* partial, float* bias_part, hipStream_t st) {
+    if (n <= 0) return 0;
     const int nchunks = (n * P3 + BK - 1) / BK;
-    int splits = min(min(max_splits, nchunks), max(1, (512 + 8) / 9));
+    int splits = min(min(WG_MAX_SPLITS, nchunks), CONV3_WG_SPLITS);
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
-    *splits_out = splits;
-    conv3_wgrad_kernel<<<dim3(9, splits), 256, 0, st>>>(dz3, h2, n, cps, partial, bias_part);
+    launch_jobs(st, Conv3DgradJob{dz3, w3d, h2, dz2, n},
+                Conv3WgradJob{dz3, h2, partial, bias_part, n, splits, cps});
+    return splits;
 }
 
 // ---------------------------------------------------------------------------
 // conv2 data gradient (stride 2), split by output phase (y mod 2, x mod 2) so
 // that no inserted zeros are multiplied: output (2y'+py, 2x'+px) receives taps
 // u = py + 2du, v = px + 2dv from dz2[y'-du][x'-dv], du, dv in {0, 1}.
-// rows m = (b, y', x') (10 x 10 per sample), cols c (32),
-// reduction (du, dv, o) = 8 chunks; dz1 = dh1 * [h1 > 0].
+// A workgroup owns one (phase, y', x') for 128 samples; taps that fall outside
+// the 9x9 input are the same for all its rows and are skipped.
+// rows b, cols c (32), reduction (valid tap, o) in chunks of 32 o;
+// dz1 = dh1 * [h1 > 0].
 // ---------------------------------------------------------------------------
-struct Conv2DgradA {
+struct Conv2DgradA {  // KMAJ quads dz2[b][i][j][o..o+3]
     const float* dz2;
-    int rows, m0;
-    int pb[MAXQ], yy[MAXQ], xx[MAXQ], kk[MAXQ];
+    int n, b0, yy, xx, du0, dv0, ndv;
+    const float* base[MAXQ];
+    bool ok[MAXQ];
     __device__ void init(int j, int row, int k) {
-        const int m = m0 + row;
-        const int mm = m < rows ? m : 0;
-        const int b = mm / 100, p = mm - b * 100;
-        kk[j] = k;
-        pb[j] = m < rows ? b : -1;
-        yy[j] = p / 10;
-        xx[j] = p - (p / 10) * 10;
+        const int b = b0 + row;
+        ok[j] = b < n;
+        base[j] = dz2 + (int64_t)(ok[j] ? b : 0) * P2 * C2 + k;
     }
     __device__ f32x4 load(int kc, int j) const {
-        const int t = kc >> 1, du = t >> 1, dv = t & 1;
-        const int i = yy[j] - du, jj = xx[j] - dv;
-        const bool ok = pb[j] >= 0 && i >= 0 && i < H2 && jj >= 0 && jj < H2;
-        const int64_t e = ok ? (((int64_t)pb[j] * H2 + i) * H2 + jj) * C2 : 0;
-        return sel4(ok, ld4(dz2 + e + (kc & 1) * BK + kk[j]));
+        const int t = kc >> 1, du = du0 + t / ndv, dv = dv0 + t % ndv;
+        return sel4(ok[j], ld4(base[j] + ((yy - du) * H2 + (xx - dv)) * C2 + (kc & 1) * BK));
     }
 };
 struct Conv2DgradB {  // w2d[(u,v)][c][o], rows c, quads along o
     const float* w2d;
-    int py, px;
+    int py, px, du0, dv0, ndv;
     const float* base[MAXQ];
     __device__ void init(int j, int row, int k) { base[j] = w2d + row * C2 + k; }
     __device__ f32x4 load(int kc, int j) const {
-        const int t = kc >> 1, u = py + 2 * (t >> 1), v = px + 2 * (t & 1);
+        const int t = kc >> 1, u = py + 2 * (du0 + t / ndv), v = px + 2 * (dv0 + t % ndv);
         return ld4(base[j] + (u * K2 + v) * C1 * C2 + (kc & 1) * BK);
     }
 };
 struct Conv2DgradStore {
     float* dz1;
     const float* h1;
-    int rows, m0, py, px;
+    int n, b0, y, x;
     __device__ void operator()(int row, int col, float v) const {
-        const int m = m0 + row;
-        if (m >= rows) return;
-        const int b = m / 100, p = m - b * 100, y = 2 * (p / 10) + py, x = 2 * (p % 10) + px;
+        const int b = b0 + row;
+        if (b >= n) return;
         const int64_t e = (((int64_t)b * H1 + y) * H1 + x) * C1 + col;
         dz1[e] = h1[e] > 0.0f ? v : 0.0f;
     }
 };
 
-__global__ __launch_bounds__(256) void conv2_dgrad_kernel(const float* __restrict__ dz2,
-                                                          const float* __restrict__ w2d,
-                                                          const float* __restrict__ h1, int n,
-                                                          float* __restrict__ dz1) {
+struct Conv2DgradJob {
+    const float* dz2;
+    const float* w2d;
+    const float* h1;
+    float* dz1;
+    int n;
     using SH = GemmShape<128, 32, KMAJ, KMAJ>;
-    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
-    const int m0 = blockIdx.x * 128, py = blockIdx.y >> 1, px = blockIdx.y & 1;
-    const int rows = n * 100;
-    Conv2DgradA la{dz2, rows, m0};
-    Conv2DgradB lb{w2d, py, px};
-    Conv2DgradStore epi{dz1, h1, rows, m0, py, px};
-    mfma_gemm<128, 32, 4, KMAJ, KMAJ>(smem, 0, 8, la, lb, epi);
-}
-
-void launch_conv2_dgrad(const float* dz2, const float* w2d, const float* h1, int n, float* dz1,
-                        hipStream_t st) {
-    if (n <= 0) return;
-    conv2_dgrad_kernel<<<dim3((n * 100 + 127) / 128, 4), 256, 0, st>>>(dz2, w2d, h1, n, dz1);
-}
+    static constexpr int SMEM = SH::SMEM_FLOATS;
+    __host__ __device__ int blocks() const { return 400 * ((n + 127) / 128); }
+    __device__ void run(int bid, float* smem) const {
+        const int cell = bid % 400, b0 = (bid / 400) * 128;
+        const int phase = cell / 100, yy = (cell % 100) / 10, xx = cell % 10;
+        const int py = phase >> 1, px = phase & 1;
+        const int du0 = max(0, yy - (H2 - 1)), du1 = min(1, yy);
+        const int dv0 = max(0, xx - (H2 - 1)), dv1 = min(1, xx);
+        const int ndv = dv1 - dv0 + 1, taps = (du1 - du0 + 1) * ndv;
+        Conv2DgradA la{dz2, n, b0, yy, xx, du0, dv0, ndv};
+        Conv2DgradB lb{w2d, py, px, du0, dv0, ndv};
+        Conv2DgradStore epi{dz1, h1, n, b0, 2 * yy + py, 2 * xx + px};
+        mfma_gemm<128, 32, 4, KMAJ, KMAJ>(smem, 0, 2 * taps, la, lb, epi);
+    }
+};
 
 // ---------------------------------------------------------------------------
 // conv2 weight gradient: dW2[o][c][u][v] = sum_{b,i,j} dz2[b][i][j][o] h1[b][2i+u][2j+v][c]
@@ -521,29 +592,36 @@ struct Conv2WgradB {  // h1 quads along c at one (pixel, tap)
     }
 };
 
-__global__ __launch_bounds__(256) void conv2_wgrad_kernel(const float* __restrict__ dz2,
-                                                          const float* __restrict__ h1, int n,
-                                                          int cps, float* __restrict__ partial,
-                                                          float* __restrict__ bias_part) {
+struct Conv2WgradJob {
+    const float* dz2;
+    const float* h1;
+    float* partial;
+    float* bias_part;
+    int n, splits, cps;
     using SH = GemmShape<64, 64, RMAJ, RMAJ>;
-    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
-    const int tap0 = blockIdx.x * 2, s = blockIdx.y;
-    const int npix = n * P2, nchunks = (npix + BK - 1) / BK;
-    Conv2WgradA la{dz2, npix};
-    Conv2WgradB lb{h1, npix, tap0};
-    PartialEpi epi{partial + (int64_t)s * C2 * 16 * C1, 16 * C1, tap0 * C1, 1.0f};
-    float* rs = blockIdx.x == 0 ? bias_part + (int64_t)s * 64 : nullptr;
-    mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, s * cps, min(nchunks, (s + 1) * cps), la, lb, epi, rs);
-}
+    static constexpr int SMEM = SH::SMEM_FLOATS;
+    __host__ __device__ int blocks() const { return 8 * splits; }
+    __device__ void run(int bid, float* smem) const {
+        const int tap0 = (bid % 8) * 2, s = bid / 8;
+        const int npix = n * P2, nchunks = (npix + BK - 1) / BK;
+        Conv2WgradA la{dz2, npix};
+        Conv2WgradB lb{h1, npix, tap0};
+        PartialEpi epi{partial + (int64_t)s * C2 * 16 * C1, 16 * C1, tap0 * C1, 1.0f};
+        float* rs = tap0 == 0 ? bias_part + (int64_t)s * 64 : nullptr;
+        mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, s * cps, min(nchunks, (s + 1) * cps), la, lb, epi, rs);
+    }
+};
 
-void launch_conv2_wgrad(const float* dz2, const float* h1, int n, float* partial, float* bias_part,
-                        int max_splits, int* splits_out, hipStream_t st) {
+int launch_conv2_backward(const float* dz2, const float* w2d, const float* h1, int n, float* dz1,
+                          float* partial, float* bias_part, hipStream_t st) {
+    if (n <= 0) return 0;
     const int nchunks = (n * P2 + BK - 1) / BK;
-    int splits = min(min(max_splits, nchunks), 512 / 8);
+    int splits = min(min(WG_MAX_SPLITS, nchunks), CONV2_WG_SPLITS);
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
-    *splits_out = splits;
-    conv2_wgrad_kernel<<<dim3(8, splits), 256, 0, st>>>(dz2, h1, n, cps, partial, bias_part);
+    launch_jobs(st, Conv2DgradJob{dz2, w2d, h1, dz1, n},
+                Conv2WgradJob{dz2, h1, partial, bias_part, n, splits, cps});
+    return splits;
 }
 
 // ---------------------------------------------------------------------------
