@@ -2,13 +2,13 @@
  * libgorila -- the Gorila DQN learner step and actor inference on one MI355X.
  *
  * Method: Nair et al. 2015, "Massively Parallel Methods for Deep
- * Reinforcement Learning".  The learner's job (Section 3, Learners;
+ * Reinforcement Learning".  The learner's job (Section 4, Learners;
  * Algorithm 1) is: sample a minibatch of transitions (s, a, r, s') from
  * replay memory, form the target y = r for terminal s' and
  * y = r + gamma * max_a' Q(s', a'; theta-) otherwise, take the squared TD
  * error of eq. (1) and compute its gradient, eq. (2), with respect to theta.
- * Actors (Section 3, Actors; Algorithm 1) choose epsilon-greedy actions on
- * Q(s, a; theta).  The Q-network is the one of Section 4.1.
+ * Actors (Section 4, Actors; Algorithm 1) choose epsilon-greedy actions on
+ * Q(s, a; theta).  The Q-network is the one of Section 5.1.
  *
  * Conventions for every call below:
  *  - All array arguments are DEVICE pointers owned by the caller (normally
@@ -23,7 +23,7 @@
  *    action 0 instead of touching memory out of bounds, and the error is
  *    returned by gorila_ctx_check() (or by the next call on the context).
  *  - States are uint8 [n, 4, 84, 84]: four 84x84 luminance frames, oldest
- *    first (Section 4.1).  Network input is state / 255.
+ *    first (Section 5.1).  Network input is state / 255.
  *  - Parameters are one flat vector in this order (weights OIHW / [out, in]):
  *    W1 [32,4,8,8], b1 [32], W2 [64,32,4,4], b2 [64], W3 [64,64,3,3], b3 [64],
  *    W4 [512,3136], b4 [512], W5 [A,512], b5 [A]; the FC input is conv3's
@@ -59,7 +59,7 @@ typedef struct {
     int32_t dtype;
 } gorila_params;
 
-/* Replay memory D (Section 3, Experience replay memory).
+/* Replay memory D (Section 4, Experience replay memory).
  *
  * STACKED: `rows` whole transitions; a minibatch index k in [0, rows) names
  *   s = s[k] and s' = s2[k] (uint8 [rows,4,84,84]), action[k], reward[k] and
@@ -71,7 +71,7 @@ typedef struct {
  *   position k in [0, capacity-2]: s is the stack of frames k-3 .. k and s'
  *   of frames k-2 .. k+1 (oldest first), where any frame before the latest
  *   episode start at or before the stack's newest frame is all zeros (the
- *   paper concatenates the four most recent frames, Section 4.1; zero-fill at
+ *   paper concatenates the four most recent frames, Section 5.1; zero-fill at
  *   episode starts is this library's reading).  The transition's action and
  *   reward are action[slot(k)], reward[slot(k)]; it is terminal iff k+1
  *   starts an episode.  s, s2 and term are unused. */
@@ -128,7 +128,7 @@ int gorila_ctx_timing_begin(gorila_ctx* ctx, uint32_t stage_mask, int32_t max_re
 int gorila_ctx_timing_end(gorila_ctx* ctx, double* total_ms, int32_t* count, int32_t n_stages);
 const char* gorila_stage_name(int32_t stage);
 
-/* Replay gather (Section 3 replay memory, Section 4.1 frame stacking).
+/* Replay gather (Section 4 replay memory, Section 5.1 frame stacking).
  * For n minibatch indices idx [n] (int64) write s_out, s2_out
  * [n,4,84,84] uint8, frame_map_out [n,2,4] int64 (RING: the slot each
  * channel was copied from, -1 = zero-filled; STACKED: row*4 + channel),
@@ -138,7 +138,7 @@ int gorila_gather(const gorila_replay* replay, const int64_t* idx, int32_t n,
                   uint8_t* s_out, uint8_t* s2_out, int64_t* frame_map_out,
                   int32_t* a_out, float* r_out, uint8_t* term_out, gorila_ctx* ctx);
 
-/* Q(s, .; theta) (Section 4.1 network) for states [n,4,84,84] -> q_out [n,A]
+/* Q(s, .; theta) (Section 5.1 network) for states [n,4,84,84] -> q_out [n,A]
  * fp32.  Needs gorila_workspace_bytes(n, A, dtype, 1). */
 int gorila_q_forward(const gorila_params* params, const uint8_t* states_u8, int32_t n,
                      float* q_out, gorila_ctx* ctx);
@@ -168,7 +168,7 @@ int gorila_learner_step(const gorila_params* params, const gorila_params* target
                         float gamma, float clip_delta, float* grads_out, float* loss_out,
                         gorila_ctx* ctx);
 
-/* `groups` independent learner steps (Section 3: many learners, each with
+/* `groups` independent learner steps (Section 4: many learners, each with
  * its own, possibly stale, replica of theta) sharing one target theta-.
  * params points to `groups` parameter sets; group g uses minibatch indices
  * idx[g*batch .. g*batch+batch-1] and writes grads_out[g*P .. g*P+P-1] and

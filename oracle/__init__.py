@@ -50,7 +50,7 @@ class _Net(ctypes.Structure):
 
 @dataclass(frozen=True)
 class Net:
-    """Q-network topology (Section 4.1: 84x84x4 input, conv 32@8x8/4,
+    """Q-network topology (Section 5.1: 84x84x4 input, conv 32@8x8/4,
     conv 64@4x4/2, conv 64@3x3/1, FC 512, linear FC with one unit per action).
     Tiny topologies exist only for finite-difference tests."""
     in_c: int = 4
@@ -136,7 +136,7 @@ def num_threads() -> int:
 
 
 def q_forward(net: Net, theta, states) -> np.ndarray:
-    """Q(s, .; theta) for a batch of uint8 states (Section 4.1 network)."""
+    """Q(s, .; theta) for a batch of uint8 states (Section 5.1 network)."""
     theta = _c(theta, np.float64)
     states = _c(states, np.uint8)
     n = states.shape[0]
@@ -188,8 +188,8 @@ def learner_step(net: Net, theta, theta_target, s, s2, a, r, term, gamma: float,
 
 
 def gather(frames, ep_start, action, reward, head: int, idx, hist: int = 4):
-    """Frame stacking out of the replay ring (Section 3 replay memory,
-    Section 4.1 four-frame input).  frames is [capacity, ...] uint8.
+    """Frame stacking out of the replay ring (Section 4 replay memory,
+    Section 5.1 four-frame input).  frames is [capacity, ...] uint8.
 
     Returns dict(s, s2 [n, hist, ...] u8, frame_map [n, 2, hist] i64,
     a i32, r f32, term u8)."""

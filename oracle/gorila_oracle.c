@@ -9,7 +9,7 @@
  * library.
  *
  * Readings of the paper used here (the paper is silent or garbled on them):
- *  - Network (Section 4.1, experimental set-up): valid cross-correlations,
+ *  - Network (Section 5.1, experimental set-up): valid cross-correlations,
  *    OIHW weights, biases present, flatten of the last conv in (c, i, j)
  *    order, input bytes scaled by 1/255, ReLU'(0) = 0.
  *  - Loss (eq. (1), Algorithm 1): the target is y = r for a terminal next
@@ -27,9 +27,9 @@
  *    environment come from the SplitMix64 output function (Steele, Lea and
  *    Flood, OOPSLA 2014) evaluated at seed + (2e+1)*G and seed + (2e+2)*G,
  *    G = 0x9E3779B97F4A7C15, all mod 2^64.
- *  - Frame stacking (Section 4.1): the state is the four most recent frames,
+ *  - Frame stacking (Section 5.1): the state is the four most recent frames,
  *    oldest in channel 0; a frame that lies before the start of the current
- *    episode is replaced by zeros.  The replay ring (Section 3, replay
+ *    episode is replaced by zeros.  The replay ring (Section 4, replay
  *    memory) has `capacity` slots, `head` is the physical slot of the oldest
  *    frame, and logical position k lives in slot (head + k) mod capacity.
  *    ep_start flags the first frame of an episode; logical 0 counts as one.
@@ -202,7 +202,7 @@ static void carve(const oracle_net* n, const layout* L, double* base,
     S->dq = p;  p += n->n_actions;
 }
 
-/* Q-network forward pass of one state (Section 4.1). */
+/* Q-network forward pass of one state (Section 5.1). */
 static void forward(const oracle_net* n, const layout* L, const double* th,
                     const uint8_t* state, sample_state* S) {
     const int64_t* o = L->off;

@@ -9,7 +9,7 @@ built, every call raises.
 Method: Nair et al. 2015, "Massively Parallel Methods for Deep Reinforcement
 Learning" -- the learner's DQN gradient step (Algorithm 1, eq. (1) and (2)) and
 the actors' epsilon-greedy inference (Algorithm 1), on the Q-network of
-Section 4.1.
+Section 5.1.
 """
 from __future__ import annotations
 

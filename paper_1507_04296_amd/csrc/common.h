@@ -1,6 +1,6 @@
 // Shared device-side definitions for the Gorila learner-step kernels (gfx950).
 //
-// Network (Nair et al. 2015, Section 4.1): 4x84x84 uint8 input scaled by
+// Network (Nair et al. 2015, Section 5.1): 4x84x84 uint8 input scaled by
 // 1/255, conv 32@8x8 stride 4 -> 20x20, conv 64@4x4 stride 2 -> 9x9,
 // conv 64@3x3 stride 1 -> 7x7, FC 3136 -> 512, linear FC 512 -> A, ReLU after
 // every hidden layer.  Parameters are one flat fp32 vector: W1 [32,4,8,8],

@@ -1,4 +1,4 @@
-// First convolution (Section 4.1: 32 filters of 4x8x8, stride 4, ReLU) on the
+// First convolution (Section 5.1: 32 filters of 4x8x8, stride 4, ReLU) on the
 // raw uint8 frames, forward and weight gradient.
 //
 // Forward: one workgroup takes two samples, stages their 2 x 28224 input bytes

@@ -1,4 +1,4 @@
-// Action head (linear FC 512 -> A, Section 4.1) and what follows it:
+// Action head (linear FC 512 -> A, Section 5.1) and what follows it:
 //  - Q values;
 //  - epsilon-greedy actions (Algorithm 1);
 //  - the DQN TD target y = r + gamma (1 - term) max_a' Q(s', a'; theta-),

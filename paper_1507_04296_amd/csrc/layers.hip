@@ -1,5 +1,5 @@
 // Convolution 2/3 and FC-512 layers, forward and backward, as implicit GEMMs
-// on the fp32 MFMA tile engine (common.h).  Shapes follow Section 4.1 of the
+// on the fp32 MFMA tile engine (common.h).  Shapes follow Section 5.1 of the
 // paper; the backward pass is the exact gradient of those layers (eq. (2)
 // needs grad_theta Q(s, a; theta)).
 //

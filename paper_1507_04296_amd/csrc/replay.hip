@@ -1,6 +1,6 @@
 // Replay minibatch resolution and the materialising gather.
 //
-// Frame stacking (Section 4.1): a state is the four most recent frames,
+// Frame stacking (Section 5.1): a state is the four most recent frames,
 // oldest in channel 0.  Out of a ring of single frames, channel j of the
 // stack ending at logical frame k holds frame l = k - 3 + j, or zeros when l
 // lies before the latest episode start at or before k (logical 0 counts as a

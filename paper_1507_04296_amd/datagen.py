@@ -6,7 +6,7 @@ code that both the HIP path (through the tests and the benchmark) and the fp64
 oracle consume.  Everything comes from numpy's PCG64 (``default_rng``), so an
 input is fixed by its seed.
 
-The paper trains on Atari 2600 frames (Section 4.1: 84x84 luminance, four-frame
+The paper trains on Atari 2600 frames (Section 5.1: 84x84 luminance, four-frame
 stacks, up to 18 actions, rewards clipped as in DQN); those frames are not
 available here, so these generators stand in for them with the same shapes,
 value ranges and structure.
@@ -170,7 +170,7 @@ def actor_inputs(seed: int, n: int, n_actions: int, eps: float = 0.05) -> ActorI
 
 @dataclass
 class RingInputs:
-    """A replay ring of single frames (Section 3 replay memory, 1M frames)."""
+    """A replay ring of single frames (Section 4 replay memory, 1M frames)."""
     frames: np.ndarray    # u8 [capacity, 84, 84] (or [capacity, fh, fw])
     ep_start: np.ndarray  # u8 [capacity], physical slots
     action: np.ndarray    # i32 [capacity]

@@ -3,8 +3,8 @@ same seeded inputs.  Bars: gathers, frame maps and actions bit-exact; Q within
 1e-4 relative; loss within 1e-4 relative; every gradient tensor within 1e-3
 relative L2 (fp32 path).
 
-Workloads are the paper's shapes (Section 4.1 network, four-frame 84x84 uint8
-states, one-million-frame replay, Section 4.1 / Algorithm 1): single learner
+Workloads are the paper's shapes (Section 5.1 network, four-frame 84x84 uint8
+states, one-million-frame replay, Section 5.1 / Algorithm 1): single learner
 steps at batch 32 (18 actions) and 512 (6 actions), a batch of 256 drawn from a
 one-million-frame replay ring, and actor inference on 1024 environments, plus
 ragged and degenerate cases.
