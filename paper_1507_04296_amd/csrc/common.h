@@ -251,6 +251,18 @@ __device__ inline float wave_sum(float v) {
     return v;
 }
 
+// Workgroups are dispatched to the eight XCDs round-robin by workgroup id, and
+// each XCD has its own L2.  Every job pads its block count to a multiple of 8
+// (so every job starts at a multiple of 8 in its launch) and maps its block
+// index through xcd_tile, which sends logical tiles [k*n/8, (k+1)*n/8) to XCD
+// k: tiles that are neighbours in logical order, and share operands, then
+// share an L2.  Logical tiles >= the real count are idle.
+constexpr int NUM_XCD = 8;
+__host__ __device__ inline int pad_xcd(int n) { return (n + NUM_XCD - 1) / NUM_XCD * NUM_XCD; }
+__device__ inline int xcd_tile(int bid, int padded) {
+    return (bid % NUM_XCD) * (padded / NUM_XCD) + bid / NUM_XCD;
+}
+
 // Several independent jobs in one launch: blocks [0, a.blocks()) run job a,
 // the next b.blocks() run job b, the rest job c.  A job is a struct with
 // SMEM (floats of shared memory), blocks() and run(block, smem).

@@ -118,24 +118,30 @@ struct Conv1WgradB {  // input bytes rows (c,u,v), RMAJ quads along v at one pix
 
 constexpr int C1W_BN = 128;
 
-__global__ __launch_bounds__(256) void conv1_wgrad_kernel(const float* __restrict__ dz1,
-                                                          const uint8_t* const* __restrict__ ftab,
-                                                          int n, int chunks_per_split,
-                                                          float* __restrict__ partial,
-                                                          float* __restrict__ bias_part) {
+struct Conv1WgradJob {
+    const float* dz1;
+    const uint8_t* const* ftab;
+    float* partial;
+    float* bias_part;
+    int n, splits, cps;
     using SH = GemmShape<32, C1W_BN, RMAJ, RMAJ>;
-    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
-    const int col0 = blockIdx.x * C1W_BN, split = blockIdx.y;
-    const int npix = n * P1;
-    const int nchunks = (npix + BK - 1) / BK;
-    const int kc0 = split * chunks_per_split;
-    const int kc1 = min(nchunks, kc0 + chunks_per_split);
-    Conv1WgradA la{dz1, npix};
-    Conv1WgradB lb{ftab, (const uint8_t*)dz1, npix, col0};
-    PartialEpi epi{partial + (int64_t)split * C1 * 256, 256, col0, 1.0f / 255.0f};
-    float* rs = blockIdx.x == 0 ? bias_part + (int64_t)split * 64 : nullptr;
-    mfma_gemm<32, C1W_BN, 1, RMAJ, RMAJ>(smem, kc0, kc1, la, lb, epi, rs);
-}
+    static constexpr int SMEM = SH::SMEM_FLOATS;
+    static constexpr int NCT = 256 / C1W_BN;
+    __host__ __device__ int blocks() const { return pad_xcd(NCT * splits); }
+    __device__ void run(int bid, float* smem) const {
+        const int t = xcd_tile(bid, blocks());
+        if (t >= NCT * splits) return;
+        const int col0 = (t % NCT) * C1W_BN, split = t / NCT;  // column tiles of a split adjacent
+        const int npix = n * P1;
+        const int nchunks = (npix + BK - 1) / BK;
+        const int kc0 = split * cps, kc1 = min(nchunks, kc0 + cps);
+        Conv1WgradA la{dz1, npix};
+        Conv1WgradB lb{ftab, (const uint8_t*)dz1, npix, col0};
+        PartialEpi epi{partial + (int64_t)split * C1 * 256, 256, col0, 1.0f / 255.0f};
+        float* rs = col0 == 0 ? bias_part + (int64_t)split * 64 : nullptr;
+        mfma_gemm<32, C1W_BN, 1, RMAJ, RMAJ>(smem, kc0, kc1, la, lb, epi, rs);
+    }
+};
 
 void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int n, float* partial,
                         float* bias_part, int max_splits, int* splits_out, hipStream_t st) {
@@ -145,8 +151,7 @@ void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int n, flo
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
     *splits_out = splits;
-    conv1_wgrad_kernel<<<dim3(256 / C1W_BN, splits), 256, 0, st>>>(dz1, ftab, n, cps, partial,
-                                                                    bias_part);
+    launch_jobs(st, Conv1WgradJob{dz1, ftab, partial, bias_part, n, splits, cps});
 }
 
 }  // namespace gorila

@@ -87,23 +87,31 @@ struct BiasReluStore {
     }
 };
 
-__global__ __launch_bounds__(256) void conv2_fwd_kernel(const float* __restrict__ h1, GroupPtrs w2t,
-                                                        GroupPtrs theta, int n,
-                                                        float* __restrict__ h2) {
+struct Conv2FwdJob {
+    const float* h1;
+    GroupPtrs w2t, theta;
+    float* h2;
+    int n, groups;
     using SH = GemmShape<64, 64, KMAJ, KMAJ>;
-    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
-    const int g = blockIdx.y, m0 = blockIdx.x * 64;
-    const int rows = n * P2;
-    Conv2FwdA la{h1 + (int64_t)g * n * P1 * C1, rows, m0};
-    WtapB lb{w2t.p[g], C1, 1, C2};
-    BiasReluStore epi{h2 + (int64_t)g * n * P2 * C2, theta.p[g] + OFF_B2, rows, m0, C2};
-    mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, 0, 16, la, lb, epi);
-}
+    static constexpr int SMEM = SH::SMEM_FLOATS;
+    __host__ __device__ int tiles() const { return (n * P2 + 63) / 64; }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
+    __device__ void run(int bid, float* smem) const {
+        const int t = xcd_tile(bid, blocks());
+        if (t >= tiles() * groups) return;
+        const int g = t / tiles(), m0 = (t % tiles()) * 64;
+        const int rows = n * P2;
+        Conv2FwdA la{h1 + (int64_t)g * n * P1 * C1, rows, m0};
+        WtapB lb{w2t.p[g], C1, 1, C2};
+        BiasReluStore epi{h2 + (int64_t)g * n * P2 * C2, theta.p[g] + OFF_B2, rows, m0, C2};
+        mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, 0, 16, la, lb, epi);
+    }
+};
 
 void launch_conv2_fwd(const float* h1, const GroupPtrs& w2t, const GroupPtrs& theta, int groups,
                       int n, float* h2, hipStream_t st) {
     if (n <= 0) return;
-    conv2_fwd_kernel<<<dim3((n * P2 + 63) / 64, groups), 256, 0, st>>>(h1, w2t, theta, n, h2);
+    launch_jobs(st, Conv2FwdJob{h1, w2t, theta, h2, n, groups});
 }
 
 // ---------------------------------------------------------------------------
@@ -140,23 +148,31 @@ struct Conv3FwdStore {  // row = o, col = pixel index within the tile
     }
 };
 
-__global__ __launch_bounds__(256) void conv3_fwd_kernel(const float* __restrict__ h2, GroupPtrs w3t,
-                                                        GroupPtrs theta, int n,
-                                                        float* __restrict__ h3) {
+struct Conv3FwdJob {
+    const float* h2;
+    GroupPtrs w3t, theta;
+    float* h3;
+    int n, groups;
     using SH = GemmShape<64, 64, KMAJ, KMAJ>;
-    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
-    const int g = blockIdx.y, m0 = blockIdx.x * 64;
-    const int rows = n * P3;
-    WtapB la{w3t.p[g], C2, 2, C3};
-    Conv3FwdB lb{h2 + (int64_t)g * n * P2 * C2, rows, m0};
-    Conv3FwdStore epi{h3 + (int64_t)g * n * FLAT, theta.p[g] + OFF_B3, rows, m0};
-    mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, 0, 18, la, lb, epi);
-}
+    static constexpr int SMEM = SH::SMEM_FLOATS;
+    __host__ __device__ int tiles() const { return (n * P3 + 63) / 64; }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
+    __device__ void run(int bid, float* smem) const {
+        const int t = xcd_tile(bid, blocks());
+        if (t >= tiles() * groups) return;
+        const int g = t / tiles(), m0 = (t % tiles()) * 64;
+        const int rows = n * P3;
+        WtapB la{w3t.p[g], C2, 2, C3};
+        Conv3FwdB lb{h2 + (int64_t)g * n * P2 * C2, rows, m0};
+        Conv3FwdStore epi{h3 + (int64_t)g * n * FLAT, theta.p[g] + OFF_B3, rows, m0};
+        mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, 0, 18, la, lb, epi);
+    }
+};
 
 void launch_conv3_fwd(const float* h2, const GroupPtrs& w3t, const GroupPtrs& theta, int groups,
                       int n, float* h3, hipStream_t st) {
     if (n <= 0) return;
-    conv3_fwd_kernel<<<dim3((n * P3 + 63) / 64, groups), 256, 0, st>>>(h2, w3t, theta, n, h3);
+    launch_jobs(st, Conv3FwdJob{h2, w3t, theta, h3, n, groups});
 }
 
 // ---------------------------------------------------------------------------
@@ -184,19 +200,33 @@ struct PlainStore {
 
 constexpr int FC1_CHUNKS = FLAT / BK;  // 98
 
-__global__ __launch_bounds__(256) void fc1_fwd_kernel(const float* __restrict__ h3, GroupPtrs theta,
-                                                      int n, int splits, int cps,
-                                                      float* __restrict__ partial) {
+// Logical tile order (group, split, column tile, row tile): the row tiles that
+// share a block of W4 are neighbours and so share an XCD's L2.
+struct Fc1FwdJob {
+    const float* h3;
+    GroupPtrs theta;
+    float* partial;
+    int n, groups, splits, cps;
     using SH = GemmShape<64, 64, KMAJ, KMAJ>;
-    __shared__ __attribute__((aligned(16))) float smem[SH::SMEM_FLOATS];
-    const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
-    const int g = blockIdx.z / splits, s = blockIdx.z - g * splits;
-    RowMajorK la{h3 + (int64_t)g * n * FLAT, n, r0, FLAT};
-    RowMajorK lb{theta.p[g] + OFF_W4, HID, c0, FLAT};
-    PlainStore epi{partial + ((int64_t)g * splits + s) * n * HID, n, r0, c0, HID};
-    const int kc0 = s * cps, kc1 = min(FC1_CHUNKS, kc0 + cps);
-    mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, kc0, kc1, la, lb, epi);
-}
+    static constexpr int SMEM = SH::SMEM_FLOATS;
+    __host__ __device__ int mt() const { return (n + 63) / 64; }
+    __host__ __device__ int tiles() const { return mt() * (HID / 64) * groups * splits; }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles()); }
+    __device__ void run(int bid, float* smem) const {
+        int t = xcd_tile(bid, blocks());
+        if (t >= tiles()) return;
+        const int r0 = (t % mt()) * 64;
+        t /= mt();
+        const int c0 = (t % (HID / 64)) * 64;
+        t /= HID / 64;
+        const int s = t % splits, g = t / splits;
+        RowMajorK la{h3 + (int64_t)g * n * FLAT, n, r0, FLAT};
+        RowMajorK lb{theta.p[g] + OFF_W4, HID, c0, FLAT};
+        PlainStore epi{partial + ((int64_t)g * splits + s) * n * HID, n, r0, c0, HID};
+        const int kc0 = s * cps, kc1 = min(FC1_CHUNKS, kc0 + cps);
+        mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, kc0, kc1, la, lb, epi);
+    }
+};
 
 int launch_fc1_fwd(const float* h3, const GroupPtrs& theta, int groups, int n, float* partial,
                    hipStream_t st) {
@@ -205,8 +235,7 @@ int launch_fc1_fwd(const float* h3, const GroupPtrs& theta, int groups, int n, f
     int splits = min(FC1_MAX_SPLITS, max(1, (TARGET_WGS + tiles - 1) / tiles));
     const int cps = (FC1_CHUNKS + splits - 1) / splits;
     splits = (FC1_CHUNKS + cps - 1) / cps;
-    fc1_fwd_kernel<<<dim3(mt, HID / 64, groups * splits), 256, 0, st>>>(h3, theta, n, splits, cps,
-                                                                         partial);
+    launch_jobs(st, Fc1FwdJob{h3, theta, partial, n, groups, splits, cps});
     return splits;
 }
 
@@ -261,10 +290,13 @@ struct Fc1DgradJob {
     int n;
     using SH = GemmShape<64, 64, KMAJ, RMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
-    __host__ __device__ int blocks() const { return ((n + 63) / 64) * (FLAT / 64); }
+    __host__ __device__ int tiles() const { return ((n + 63) / 64) * (FLAT / 64); }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles()); }
     __device__ void run(int bid, float* smem) const {
+        const int t = xcd_tile(bid, blocks());
+        if (t >= tiles()) return;
         const int mt = (n + 63) / 64;
-        const int r0 = (bid % mt) * 64, c0 = (bid / mt) * 64;
+        const int r0 = (t % mt) * 64, c0 = (t / mt) * 64;  // row tiles of one W4 column block adjacent
         RowMajorK la{dz4, n, r0, HID};
         RowMajorR lb{W4, c0, FLAT, HID};
         Dz3NhwcStore epi{dz3, h3, n, r0, c0};
@@ -284,9 +316,12 @@ struct Fc1WgradJob {
     int n;
     using SH = GemmShape<64, 64, RMAJ, RMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
-    __host__ __device__ int blocks() const { return (HID / 64) * (FLAT / 64); }
+    __host__ __device__ int tiles() const { return (HID / 64) * (FLAT / 64); }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles()); }
     __device__ void run(int bid, float* smem) const {
-        const int r0 = (bid % (HID / 64)) * 64, c0 = (bid / (HID / 64)) * 64;
+        const int t = xcd_tile(bid, blocks());
+        if (t >= tiles()) return;
+        const int r0 = (t % (HID / 64)) * 64, c0 = (t / (HID / 64)) * 64;
         RowMajorR la{dz4, r0, HID, n};
         RowMajorR lb{h3, c0, FLAT, n};
         PlainStore epi{gW4, HID, r0, c0, FLAT};
@@ -312,8 +347,9 @@ struct HeadPartialJob {
     float* hpart;
     int n, A, rows_per_block, row_blocks;
     static constexpr int SMEM = 4 * MAX_ACTIONS * 64;
-    __host__ __device__ int blocks() const { return (HID / 64) * row_blocks; }
+    __host__ __device__ int blocks() const { return pad_xcd((HID / 64) * row_blocks); }
     __device__ void run(int bid, float* smem) const {
+        if (bid >= (HID / 64) * row_blocks) return;
         float (*sacc)[MAX_ACTIONS][64] = (float (*)[MAX_ACTIONS][64])smem;
         const int tid = threadIdx.x, kl = tid & 63, bq = tid >> 6;
         const int kt = bid % (HID / 64), bb = bid / (HID / 64);
@@ -416,9 +452,12 @@ struct Conv3DgradJob {
     int n;
     using SH = GemmShape<64, 64, KMAJ, KMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
-    __host__ __device__ int blocks() const { return P2 * ((n + 63) / 64); }
+    __host__ __device__ int tiles() const { return P2 * ((n + 63) / 64); }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles()); }
     __device__ void run(int bid, float* smem) const {
-        const int pos = bid % P2, y = pos / H2, x = pos - y * H2, b0 = (bid / P2) * 64;
+        const int t = xcd_tile(bid, blocks());
+        if (t >= tiles()) return;
+        const int pos = t % P2, y = pos / H2, x = pos - y * H2, b0 = (t / P2) * 64;
         const int u0 = max(0, y - (H3 - 1)), u1 = min(K3 - 1, y);
         const int v0 = max(0, x - (H3 - 1)), v1 = min(K3 - 1, x);
         const int nv = v1 - v0 + 1, taps = (u1 - u0 + 1) * nv;
@@ -467,9 +506,11 @@ struct Conv3WgradJob {
     int n, splits, cps;
     using SH = GemmShape<64, 64, RMAJ, RMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
-    __host__ __device__ int blocks() const { return 9 * splits; }
+    __host__ __device__ int blocks() const { return pad_xcd(9 * splits); }
     __device__ void run(int bid, float* smem) const {
-        const int tap = bid % 9, s = bid / 9;
+        const int t = xcd_tile(bid, blocks());
+        if (t >= 9 * splits) return;
+        const int tap = t % 9, s = t / 9;  // the nine taps of one split share dz3 rows
         const int npix = n * P3, nchunks = (npix + BK - 1) / BK;
         Conv3WgradA la{dz3, npix};
         Conv3WgradB lb{h2, npix, tap};
@@ -545,10 +586,13 @@ struct Conv2DgradJob {
     int n;
     using SH = GemmShape<128, 32, KMAJ, KMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
-    __host__ __device__ int blocks() const { return 400 * ((n + 127) / 128); }
+    __host__ __device__ int tiles() const { return 400 * ((n + 127) / 128); }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles()); }
     __device__ void run(int bid, float* smem) const {
-        const int cell = bid % 400, b0 = (bid / 400) * 128;
-        const int phase = cell / 100, yy = (cell % 100) / 10, xx = cell % 10;
+        const int t = xcd_tile(bid, blocks());
+        if (t >= tiles()) return;
+        const int cell = t % 400, b0 = (t / 400) * 128;
+        const int phase = cell & 3, yy = (cell >> 2) / 10, xx = (cell >> 2) % 10;
         const int py = phase >> 1, px = phase & 1;
         const int du0 = max(0, yy - (H2 - 1)), du1 = min(1, yy);
         const int dv0 = max(0, xx - (H2 - 1)), dv1 = min(1, xx);
@@ -600,9 +644,11 @@ struct Conv2WgradJob {
     int n, splits, cps;
     using SH = GemmShape<64, 64, RMAJ, RMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
-    __host__ __device__ int blocks() const { return 8 * splits; }
+    __host__ __device__ int blocks() const { return pad_xcd(8 * splits); }
     __device__ void run(int bid, float* smem) const {
-        const int tap0 = (bid % 8) * 2, s = bid / 8;
+        const int t = xcd_tile(bid, blocks());
+        if (t >= 8 * splits) return;
+        const int tap0 = (t % 8) * 2, s = t / 8;  // the column tiles of one split share dz2 rows
         const int npix = n * P2, nchunks = (npix + BK - 1) / BK;
         Conv2WgradA la{dz2, npix};
         Conv2WgradB lb{h1, npix, tap0};
