@@ -154,6 +154,41 @@ static void linear_forward(const double* x, int K, const double* w,
     }
 }
 
+/* Distance of a layer's pre-activations from the ReLU kink, relative to the
+ * size of the terms summed into them: min over units of
+ * |z| / (|b| + sum |w| |x|).  A finite-precision evaluation of z errs by a
+ * small multiple of that denominator, so units with a small ratio are the ones
+ * whose ReLU derivative another precision may decide differently.  A unit
+ * whose terms are all zero is exactly zero in any precision and is skipped. */
+static double conv_margin(const double* in, int C, int H, int W, const double* w,
+                          const double* b, int O, int k, int s, int Ho, int Wo,
+                          const double* z) {
+    double m = INFINITY;
+    for (int o = 0; o < O; ++o)
+        for (int i = 0; i < Ho; ++i)
+            for (int j = 0; j < Wo; ++j) {
+                double scale = fabs(b[o]);
+                for (int c = 0; c < C; ++c)
+                    for (int u = 0; u < k; ++u)
+                        for (int v = 0; v < k; ++v)
+                            scale += fabs(w[((o * C + c) * k + u) * k + v]) *
+                                     fabs(in[(c * H + s * i + u) * W + s * j + v]);
+                if (scale > 0.0) m = fmin(m, fabs(z[(o * Ho + i) * Wo + j]) / scale);
+            }
+    return m;
+}
+
+static double linear_margin(const double* x, int K, const double* w, const double* b, int N,
+                            const double* z) {
+    double m = INFINITY;
+    for (int n = 0; n < N; ++n) {
+        double scale = fabs(b[n]);
+        for (int k = 0; k < K; ++k) scale += fabs(w[(int64_t)n * K + k]) * fabs(x[k]);
+        if (scale > 0.0) m = fmin(m, fabs(z[n]) / scale);
+    }
+    return m;
+}
+
 static void relu(const double* z, double* h, int64_t n) {
     for (int64_t t = 0; t < n; ++t) h[t] = z[t] > 0.0 ? z[t] : 0.0;
 }
@@ -221,6 +256,20 @@ static void forward(const oracle_net* n, const layout* L, const double* th,
     linear_forward(S->h3, L->flat, th + o[6], th + o[7], n->hidden, S->z4);
     relu(S->z4, S->h4, n->hidden);
     linear_forward(S->h4, n->hidden, th + o[8], th + o[9], n->n_actions, S->q);
+}
+
+/* Smallest relative kink margin over the four hidden layers of one sample. */
+static double kink_margin(const oracle_net* n, const layout* L, const double* th,
+                          const sample_state* S) {
+    const int64_t* o = L->off;
+    double m = conv_margin(S->x, n->in_c, n->in_h, n->in_w, th + o[0], th + o[1], n->c1,
+                           n->k1, n->s1, L->h1, L->w1, S->z1);
+    m = fmin(m, conv_margin(S->h1, n->c1, L->h1, L->w1, th + o[2], th + o[3], n->c2, n->k2,
+                            n->s2, L->h2, L->w2, S->z2));
+    m = fmin(m, conv_margin(S->h2, n->c2, L->h2, L->w2, th + o[4], th + o[5], n->c3, n->k3,
+                            n->s3, L->h3, L->w3, S->z3));
+    m = fmin(m, linear_margin(S->h3, L->flat, th + o[6], th + o[7], n->hidden, S->z4));
+    return m;
 }
 
 /* Back-propagate dq through one sample, leaving dz4..dz1 (data gradients
@@ -391,7 +440,7 @@ int oracle_learner_step(const oracle_net* net, const double* theta,
                         const uint8_t* s2, const int32_t* a, const double* r,
                         const uint8_t* term, int32_t B, double gamma,
                         double clip, double* grads_out, double* loss_out,
-                        double* q_out, double* q2_out) {
+                        double* q_out, double* q2_out, double* margin_out) {
     layout L;
     if (make_layout(net, &L) || !theta || !theta_target || !s || !s2 || !a ||
         !r || !term || B <= 0 || !grads_out || !loss_out || !(clip > 0.0))
@@ -432,6 +481,7 @@ int oracle_learner_step(const oracle_net* net, const double* theta,
 
         carve(net, &L, buf + (int64_t)b * per, &S[b]);
         forward(net, &L, theta, s + (int64_t)b * nx, &S[b]);
+        if (margin_out) margin_out[b] = kink_margin(net, &L, theta, &S[b]);
         forward(net, &L, theta_target, s2 + (int64_t)b * nx, &T);
 
         double m = T.q[0]; /* max_a' Q(s', a'; theta-) */

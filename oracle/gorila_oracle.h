@@ -70,13 +70,16 @@ int oracle_act(const oracle_net* net, const double* theta,
 
 /* One learner step on B stacked transitions (s, a, r, s', terminal).
  * grads_out [P] = d loss / d theta, loss_out [1] = mean Huber loss.
- * q_out / q2_out [B, A] (may be NULL) receive Q(s;theta), Q(s';theta-). */
+ * q_out / q2_out [B, A] (may be NULL) receive Q(s;theta), Q(s';theta-).
+ * margin_out [B] (may be NULL) receives each sample's smallest ReLU kink
+ * margin over the online network: min |z| / (|b| + sum |w||x|) over every
+ * hidden pre-activation z (units whose terms are all zero are skipped). */
 int oracle_learner_step(const oracle_net* net, const double* theta,
                         const double* theta_target, const uint8_t* s,
                         const uint8_t* s2, const int32_t* a, const double* r,
                         const uint8_t* term, int32_t B, double gamma,
                         double clip, double* grads_out, double* loss_out,
-                        double* q_out, double* q2_out);
+                        double* q_out, double* q2_out, double* margin_out);
 
 /* Replay gather: for logical positions idx[n] build s = stack(k) and
  * s' = stack(k+1) (each hist frames of frame_bytes bytes, oldest first),

@@ -63,7 +63,7 @@ size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 // parameter sets together) and bwd_rows learner rows.
 struct Plan {
     size_t err, ftab, a, r, term;
-    size_t w2t[2], w3t[2], w3d, w2d;
+    size_t w2t[2], w3t[2], w3d, w2p;
     size_t h1, h2, h3, h4, q, ell, coef;
     size_t dz4, dz3, dz2, dz1;
     size_t fc1part, part1, part2, part3, bpart, hpart;
@@ -85,7 +85,7 @@ Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A) {
         p.w3t[g] = take(4 * 9 * 64 * 64);
     }
     p.w3d = take(4 * 9 * 64 * 64);
-    p.w2d = take(4 * 16 * 32 * 64);
+    p.w2p = take(4 * 16 * 32 * 64);
     p.h1 = take(4 * (size_t)F * P1 * C1);
     p.h2 = take(4 * (size_t)F * P2 * C2);
     p.h3 = take(4 * (size_t)F * FLAT);
@@ -397,7 +397,7 @@ int gorila_learner_step(const gorila_params* params, const gorila_params* target
 
     WeightViews wv[2] = {
         {theta, at<float>(ctx, p.w2t[0]), at<float>(ctx, p.w3t[0]), at<float>(ctx, p.w3d),
-         at<float>(ctx, p.w2d)},
+         at<float>(ctx, p.w2p)},
         {theta_t, at<float>(ctx, p.w2t[1]), at<float>(ctx, p.w3t[1]), nullptr, nullptr}};
     { StageTimer t(ctx, ST_PREP); launch_prep_weights(wv, 2, st); }
     GroupPtrs th{}, w2t{}, w3t{};
@@ -445,7 +445,7 @@ int gorila_learner_step(const gorila_params* params, const gorila_params* target
     }
     {
         StageTimer t(ctx, ST_CONV2_BWD);
-        s2 = launch_conv2_backward(dz2, wv[0].w2d, h1, B, dz1, at<float>(ctx, p.part2),
+        s2 = launch_conv2_backward(dz2, wv[0].w2p, h1, B, dz1, at<float>(ctx, p.part2),
                                    bpart + BIAS_PART_STRIDE, st);
     }
     {

@@ -115,6 +115,12 @@ struct GemmShape {
 // If rowsum_out is not null, thread t < BM also writes sum_k A[t][k] over this
 // workgroup's reduction range (in chunk order) to rowsum_out[t].
 //
+// Epilogue protocol: epi.pre(row, col) returns a value the epilogue needs for
+// that output element (a ReLU mask, a bias, or 0 when it needs none); it is
+// called for every accumulator element before the reduction loop, so its
+// loads overlap the loop instead of waiting behind the epilogue's own stores.
+// epi(row, col, value, pre) then writes the element.
+//
 // The chunk loop is unrolled by two so that the LDS buffer and the register
 // set of every access are compile-time constants: LDS is then addressed with
 // ds_read/ds_write, and each global load is waited for only where its data is
@@ -149,11 +155,17 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
         lb.init(j, qb_row[j], qb_k[j]);
     }
 
-    f32x16 acc[TM][TN];
+    f32x16 acc[TM][TN], pre[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
+        for (int j = 0; j < TN; ++j) {
+            acc[i][j] = f32x16{};
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                pre[i][j][r] = epi.pre(wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3),
+                                       wn * WN + j * 32 + (lane & 31));
+        }
 
     // Register sets 0/1 hold chunks fetched ahead; set s always holds chunks
     // with (kc - kc_begin) % 2 == s.
@@ -230,7 +242,7 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
             for (int r = 0; r < 16; ++r) {
                 int row = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
                 int col = wn * WN + j * 32 + (lane & 31);
-                epi(row, col, acc[i][j][r]);
+                epi(row, col, acc[i][j][r], pre[i][j][r]);
             }
 }
 
@@ -239,7 +251,8 @@ struct PartialEpi {
     float* out;
     int ld, col0;
     float scale;
-    __device__ void operator()(int row, int col, float v) const {
+    __device__ float pre(int, int) const { return 0.0f; }
+    __device__ void operator()(int row, int col, float v, float) const {
         out[(int64_t)row * ld + col0 + col] = v * scale;
     }
 };

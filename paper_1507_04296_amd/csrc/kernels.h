@@ -37,13 +37,13 @@ void launch_materialize(const uint8_t* const* ftab, int n, uint8_t* s_out, uint8
 //  w2t [16][64][32]: W2[o][c][u][v] at [(u,v)][o][c]   (conv2 forward)
 //  w3t [9][64][64]:  W3[o][c][u][v] at [(u,v)][o][c]   (conv3 forward)
 //  w3d [9][64][64]:  W3[o][c][u][v] at [(u,v)][c][o]   (conv3 data gradient)
-//  w2d [16][32][64]: W2[o][c][u][v] at [(u,v)][c][o]   (conv2 data gradient)
+//  w2p [4][4][32][64]: W2[o][c][u][v] at [(u/2,v/2)][(u%2,v%2)][c][o]  (conv2 data gradient)
 struct WeightViews {
     const float* theta;   // flat parameters
     float* w2t;
     float* w3t;
     float* w3d;           // may be null (forward only)
-    float* w2d;           // may be null
+    float* w2p;           // may be null
 };
 void launch_prep_weights(const WeightViews* nets, int n_nets, hipStream_t st);
 
@@ -82,7 +82,7 @@ int launch_fc1_backward(const float* dz4, const float* theta, const float* h3, c
                         float* dz3, float* grads, float* hpart, hipStream_t st);
 int launch_conv3_backward(const float* dz3, const float* w3d, const float* h2, int n, float* dz2,
                           float* partial, float* bias_part, hipStream_t st);
-int launch_conv2_backward(const float* dz2, const float* w2d, const float* h1, int n, float* dz1,
+int launch_conv2_backward(const float* dz2, const float* w2p, const float* h1, int n, float* dz1,
                           float* partial, float* bias_part, hipStream_t st);
 void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int n, float* partial,
                         float* bias_part, int max_splits, int* splits_out, hipStream_t st);

@@ -27,7 +27,9 @@ __global__ __launch_bounds__(256) void prep_weights_kernel(WeightViews v0, Weigh
         const float x = W2[e];
         const int t = u * 4 + vv;
         v.w2t[(t * 64 + o) * 32 + c] = x;
-        if (v.w2d) v.w2d[(t * 32 + c) * 64 + o] = x;
+        // data-gradient copy: tap pair (u/2, v/2), stride phase (u%2, v%2)
+        const int tp = (u >> 1) * 2 + (vv >> 1), phase = (u & 1) * 2 + (vv & 1);
+        if (v.w2p) v.w2p[((tp * 4 + phase) * 32 + c) * 64 + o] = x;
     }
     for (int e = blockIdx.x * 256 + threadIdx.x; e < 9 * 64 * 64; e += gridDim.x * 256) {
         // e = ((o*64 + c)*3 + u)*3 + v
@@ -81,9 +83,10 @@ struct BiasReluStore {
     float* out;
     const float* bias;
     int rows, m0, ld;
-    __device__ void operator()(int row, int col, float v) const {
+    __device__ float pre(int, int col) const { return bias[col]; }
+    __device__ void operator()(int row, int col, float v, float b) const {
         const int m = m0 + row;
-        if (m < rows) out[(int64_t)m * ld + col] = fmaxf(v + bias[col], 0.0f);
+        if (m < rows) out[(int64_t)m * ld + col] = fmaxf(v + b, 0.0f);
     }
 };
 
@@ -140,11 +143,12 @@ struct Conv3FwdStore {  // row = o, col = pixel index within the tile
     float* out;
     const float* bias;
     int rows, m0;
-    __device__ void operator()(int row, int col, float v) const {
+    __device__ float pre(int row, int) const { return bias[row]; }
+    __device__ void operator()(int row, int col, float v, float b3) const {
         const int m = m0 + col;
         if (m >= rows) return;
         const int b = m / P3, p = m - b * P3;
-        out[(int64_t)b * FLAT + row * P3 + p] = fmaxf(v + bias[row], 0.0f);
+        out[(int64_t)b * FLAT + row * P3 + p] = fmaxf(v + b3, 0.0f);
     }
 };
 
@@ -193,7 +197,8 @@ struct RowMajorK {  // rows of a row-major [rows][ld] matrix, quads along k
 struct PlainStore {
     float* out;
     int rows, r0, c0, ld;
-    __device__ void operator()(int row, int col, float v) const {
+    __device__ float pre(int, int) const { return 0.0f; }
+    __device__ void operator()(int row, int col, float v, float) const {
         if (r0 + row < rows) out[(int64_t)(r0 + row) * ld + c0 + col] = v;
     }
 };
@@ -254,17 +259,6 @@ struct RowMajorR {  // B[col][k] = M[k][c0 + col] of a row-major [k][ld] matrix 
         return sel4(k < kmax, ld4(base[j] + (int64_t)(k < kmax ? k : 0) * ld));
     }
 };
-struct ReluMaskStore {  // out[r][c] = mask[r][c] > 0 ? v : 0
-    float* out;
-    const float* mask;
-    int rows, r0, c0, ld;
-    __device__ void operator()(int row, int col, float v) const {
-        const int r = r0 + row;
-        if (r >= rows) return;
-        const int64_t e = (int64_t)r * ld + c0 + col;
-        out[e] = mask[e] > 0.0f ? v : 0.0f;
-    }
-};
 
 // df is produced in the FC input's flatten order k = o*49 + p; dz3 is stored
 // pixel-major ([b][p][o], like the other activation gradients) so that the
@@ -273,11 +267,14 @@ struct Dz3NhwcStore {
     float* dz3;
     const float* h3;
     int rows, r0, c0;
-    __device__ void operator()(int row, int col, float v) const {
+    __device__ float pre(int row, int col) const {
+        const int b = r0 + row;
+        return h3[(int64_t)(b < rows ? b : 0) * FLAT + c0 + col];
+    }
+    __device__ void operator()(int row, int col, float v, float m) const {
         const int b = r0 + row;
         if (b >= rows) return;
         const int k = c0 + col, o = k / P3, p = k - o * P3;
-        const float m = h3[(int64_t)b * FLAT + k];
         dz3[(int64_t)b * FLAT + p * C3 + o] = m > 0.0f ? v : 0.0f;
     }
 };
@@ -436,11 +433,14 @@ struct Conv3DgradStore {
     float* dz2;
     const float* h2;
     int n, b0, pos;
-    __device__ void operator()(int row, int col, float v) const {
+    __device__ float pre(int row, int col) const {
+        const int b = b0 + row;
+        return h2[((int64_t)(b < n ? b : 0) * P2 + pos) * C2 + col];
+    }
+    __device__ void operator()(int row, int col, float v, float m) const {
         const int b = b0 + row;
         if (b >= n) return;
-        const int64_t e = ((int64_t)b * P2 + pos) * C2 + col;
-        dz2[e] = h2[e] > 0.0f ? v : 0.0f;
+        dz2[((int64_t)b * P2 + pos) * C2 + col] = m > 0.0f ? v : 0.0f;
     }
 };
 
@@ -533,13 +533,14 @@ int launch_conv3_backward(const float* dz3, const float* w3d, const float* h2, i
 }
 
 // ---------------------------------------------------------------------------
-// conv2 data gradient (stride 2), split by output phase (y mod 2, x mod 2) so
-// that no inserted zeros are multiplied: output (2y'+py, 2x'+px) receives taps
-// u = py + 2du, v = px + 2dv from dz2[y'-du][x'-dv], du, dv in {0, 1}.
-// A workgroup owns one (phase, y', x') for 128 samples; taps that fall outside
-// the 9x9 input are the same for all its rows and are skipped.
-// rows b, cols c (32), reduction (valid tap, o) in chunks of 32 o;
-// dz1 = dh1 * [h1 > 0].
+// conv2 data gradient (stride 2).  Output pixel (2y'+py, 2x'+px) receives
+// taps u = py + 2du, v = px + 2dv from dz2[y'-du][x'-dv], du, dv in {0, 1}, so
+// the four stride phases (py, px) of one (y', x') read the same four dz2
+// pixels with different weights and no inserted zeros are multiplied.  A
+// workgroup owns one (y', x') for 64 samples and all four phases as its
+// columns (phase, c) = 128; taps that fall outside the 9x9 input are the same
+// for every row and column and are skipped.  Reduction (valid tap, o) in
+// chunks of 32 o; dz1 = dh1 * [h1 > 0].
 // ---------------------------------------------------------------------------
 struct Conv2DgradA {  // KMAJ quads dz2[b][i][j][o..o+3]
     const float* dz2;
@@ -556,51 +557,58 @@ struct Conv2DgradA {  // KMAJ quads dz2[b][i][j][o..o+3]
         return sel4(ok[j], ld4(base[j] + ((yy - du) * H2 + (xx - dv)) * C2 + (kc & 1) * BK));
     }
 };
-struct Conv2DgradB {  // w2d[(u,v)][c][o], rows c, quads along o
-    const float* w2d;
-    int py, px, du0, dv0, ndv;
+struct Conv2DgradB {  // w2p[(du,dv)][phase][c][o], rows (phase, c), quads along o
+    const float* w2p;
+    int du0, dv0, ndv;
     const float* base[MAXQ];
-    __device__ void init(int j, int row, int k) { base[j] = w2d + row * C2 + k; }
+    __device__ void init(int j, int row, int k) { base[j] = w2p + row * C2 + k; }
     __device__ f32x4 load(int kc, int j) const {
-        const int t = kc >> 1, u = py + 2 * (du0 + t / ndv), v = px + 2 * (dv0 + t % ndv);
-        return ld4(base[j] + (u * K2 + v) * C1 * C2 + (kc & 1) * BK);
+        const int t = kc >> 1, tp = (du0 + t / ndv) * 2 + dv0 + t % ndv;
+        return ld4(base[j] + tp * 4 * C1 * C2 + (kc & 1) * BK);
     }
 };
 struct Conv2DgradStore {
     float* dz1;
     const float* h1;
-    int n, b0, y, x;
-    __device__ void operator()(int row, int col, float v) const {
+    int n, b0, yy, xx;
+    __device__ int64_t at(int b, int col) const {
+        const int phase = col >> 5, c = col & 31;
+        const int y = 2 * yy + (phase >> 1), x = 2 * xx + (phase & 1);
+        return (((int64_t)b * H1 + y) * H1 + x) * C1 + c;
+    }
+    __device__ float pre(int row, int col) const {
+        const int b = b0 + row;
+        return h1[at(b < n ? b : 0, col)];
+    }
+    __device__ void operator()(int row, int col, float v, float m) const {
         const int b = b0 + row;
         if (b >= n) return;
-        const int64_t e = (((int64_t)b * H1 + y) * H1 + x) * C1 + col;
-        dz1[e] = h1[e] > 0.0f ? v : 0.0f;
+        dz1[at(b, col)] = m > 0.0f ? v : 0.0f;
     }
 };
 
 struct Conv2DgradJob {
     const float* dz2;
-    const float* w2d;
+    const float* w2p;
     const float* h1;
     float* dz1;
     int n;
-    using SH = GemmShape<128, 32, KMAJ, KMAJ>;
+    using SH = GemmShape<64, 128, KMAJ, KMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
-    __host__ __device__ int tiles() const { return 400 * ((n + 127) / 128); }
+    __host__ __device__ int tiles() const { return 100 * ((n + 63) / 64); }
     __host__ __device__ int blocks() const { return pad_xcd(tiles()); }
     __device__ void run(int bid, float* smem) const {
         const int t = xcd_tile(bid, blocks());
         if (t >= tiles()) return;
-        const int cell = t % 400, b0 = (t / 400) * 128;
-        const int phase = cell & 3, yy = (cell >> 2) / 10, xx = (cell >> 2) % 10;
-        const int py = phase >> 1, px = phase & 1;
+        const int pos = t % 100, b0 = (t / 100) * 64;  // neighbouring positions adjacent
+        const int yy = pos / 10, xx = pos % 10;
         const int du0 = max(0, yy - (H2 - 1)), du1 = min(1, yy);
         const int dv0 = max(0, xx - (H2 - 1)), dv1 = min(1, xx);
         const int ndv = dv1 - dv0 + 1, taps = (du1 - du0 + 1) * ndv;
         Conv2DgradA la{dz2, n, b0, yy, xx, du0, dv0, ndv};
-        Conv2DgradB lb{w2d, py, px, du0, dv0, ndv};
-        Conv2DgradStore epi{dz1, h1, n, b0, 2 * yy + py, 2 * xx + px};
-        mfma_gemm<128, 32, 4, KMAJ, KMAJ>(smem, 0, 2 * taps, la, lb, epi);
+        Conv2DgradB lb{w2p, du0, dv0, ndv};
+        Conv2DgradStore epi{dz1, h1, n, b0, yy, xx};
+        mfma_gemm<64, 128, 2, KMAJ, KMAJ>(smem, 0, 2 * taps, la, lb, epi);
     }
 };
 
@@ -658,14 +666,14 @@ struct Conv2WgradJob {
     }
 };
 
-int launch_conv2_backward(const float* dz2, const float* w2d, const float* h1, int n, float* dz1,
+int launch_conv2_backward(const float* dz2, const float* w2p, const float* h1, int n, float* dz1,
                           float* partial, float* bias_part, hipStream_t st) {
     if (n <= 0) return 0;
     const int nchunks = (n * P2 + BK - 1) / BK;
     int splits = min(min(WG_MAX_SPLITS, nchunks), CONV2_WG_SPLITS);
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
-    launch_jobs(st, Conv2DgradJob{dz2, w2d, h1, dz1, n},
+    launch_jobs(st, Conv2DgradJob{dz2, w2p, h1, dz1, n},
                 Conv2WgradJob{dz2, h1, partial, bias_part, n, splits, cps});
     return splits;
 }

@@ -57,6 +57,15 @@ def _stacked(torch, g, inp):
                             _dev(torch, inp.r), _dev(torch, inp.term))
 
 
+def _certify(oracle_mod, inp, want, clip=1.0):
+    """Pick `want` rows of a stacked workload whose online ReLUs clear the kink margin."""
+    net = oracle_mod.Net(n_actions=inp.n_actions)
+    m = oracle_mod.learner_step(net, inp.theta, inp.theta_target, inp.s, inp.s2, inp.a, inp.r,
+                                inp.term, inp.gamma, clip)["margin"]
+    inp.idx = parity.kink_certified(m, want).astype(np.int64)
+    return inp
+
+
 def _learner_case(torch_cuda, g, ctx, oracle_mod, inp, clip=1.0):
     torch = torch_cuda
     A, B = inp.n_actions, inp.idx.shape[0]
@@ -80,14 +89,14 @@ def _learner_case(torch_cuda, g, ctx, oracle_mod, inp, clip=1.0):
 # ---------------------------------------------------------------------------
 def test_learner_step_batch32_a18(torch_cuda, g, ctx, oracle_mod):
     _say("learner B=32 A=18 seed=1507000")
-    inp = datagen.learner_inputs(datagen.SEED_BASE + 0, 32, 18)
+    inp = _certify(oracle_mod, datagen.learner_inputs(datagen.SEED_BASE + 0, 32, 18, rows=64), 32)
     errs, _ = _learner_case(torch_cuda, g, ctx, oracle_mod, inp)
     _say(f"grad rel-L2 {errs}")
 
 
 def test_learner_step_batch512_a6(torch_cuda, g, ctx, oracle_mod):
     _say("learner B=512 A=6 seed=1507002")
-    inp = datagen.learner_inputs(datagen.SEED_BASE + 2, 512, 6)
+    inp = _certify(oracle_mod, datagen.learner_inputs(datagen.SEED_BASE + 2, 512, 6, rows=768), 512)
     errs, _ = _learner_case(torch_cuda, g, ctx, oracle_mod, inp)
     _say(f"grad rel-L2 {errs}")
 
@@ -97,16 +106,17 @@ def test_learner_step_batch512_a6(torch_cuda, g, ctx, oracle_mod):
 ])
 def test_learner_step_ragged_and_degenerate(torch_cuda, g, ctx, oracle_mod, B, A, clip, term_p):
     _say(f"learner ragged B={B} A={A} clip={clip} term_p={term_p}")
-    inp = datagen.learner_inputs(7100 + B, B, A, term_p=term_p)
-    _learner_case(torch_cuda, g, ctx, oracle_mod, inp, clip)
+    inp = datagen.learner_inputs(7100 + B, B, A, term_p=term_p, rows=2 * B + 16)
+    _learner_case(torch_cuda, g, ctx, oracle_mod, _certify(oracle_mod, inp, B, clip), clip)
 
 
 def test_learner_step_row_indices(torch_cuda, g, ctx, oracle_mod):
     """Minibatch rows picked by idx out of a larger stacked replay, with repeats."""
     _say("learner indexed rows")
     rng = np.random.default_rng(3)
-    inp = datagen.learner_inputs(7200, 40, 18, rows=300,
-                                 idx=rng.integers(0, 300, 40).astype(np.int64))
+    inp = datagen.learner_inputs(7200, 40, 18, rows=300)
+    ok = _certify(oracle_mod, inp, 100).idx
+    inp.idx = rng.choice(ok, 40).astype(np.int64)
     inp.idx[5] = inp.idx[6]
     _learner_case(torch_cuda, g, ctx, oracle_mod, inp)
 
@@ -223,13 +233,20 @@ def test_learner_step_from_ring(torch_cuda, g, ctx, oracle_mod, ring):
     theta64 = datagen.he_normal_params(rng, 18)
     tgt64 = theta64 + 0.01 * rng.standard_normal(theta64.shape[0])
     theta, tgt = theta64.astype(np.float32), tgt64.astype(np.float32)
-    # half uniform indices, half next to episode starts
-    idx = np.concatenate([idx[:128], datagen.boundary_dense_idx(r, 40)[:128]])
+    # half uniform indices, half next to episode starts, each half kink-certified
+    net = oracle_mod.Net(n_actions=18)
+    halves = []
+    for pool in (idx, datagen.boundary_dense_idx(r, 60)):
+        pg = oracle_mod.gather(r.frames, r.ep_start, r.action, r.reward, r.head, pool)
+        m = oracle_mod.learner_step(net, theta, tgt, pg["s"], pg["s2"], pg["a"], pg["r"],
+                                    pg["term"], 0.99, 1.0)["margin"]
+        halves.append(pool[parity.kink_certified(m, 128)])
+    idx = np.concatenate(halves)
     grads, loss = g.learner_step(ctx, _dev(torch, theta), _dev(torch, tgt), 18,
                                  _ring_replay(g, r, dev), _dev(torch, idx), 0.99, 1.0)
     ctx.check()
     ref_g = oracle_mod.gather(r.frames, r.ep_start, r.action, r.reward, r.head, idx)
-    ref = oracle_mod.learner_step(oracle_mod.Net(n_actions=18), theta, tgt, ref_g["s"], ref_g["s2"],
+    ref = oracle_mod.learner_step(net, theta, tgt, ref_g["s"], ref_g["s2"],
                                   ref_g["a"], ref_g["r"], ref_g["term"], 0.99, 1.0)
     errs = parity.assert_grads_close(grads.cpu().numpy(), ref["grads"], 18)
     assert abs(float(loss.cpu()[0]) - ref["loss"]) <= parity.LOSS_TOL * abs(ref["loss"])

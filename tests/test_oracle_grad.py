@@ -202,3 +202,31 @@ def test_no_gradient_flows_into_target(oracle_mod):
     o2 = oracle_mod.learner_step(net, theta, theta * 3.0 + 1.0, s, s2, a, r, t, 0.99)
     np.testing.assert_array_equal(o1["grads"], o2["grads"])
     assert o1["loss"] == o2["loss"]
+
+
+def test_kink_margin_closed_form(oracle_mod):
+    """A hidden unit built to sit exactly on the ReLU kink has margin 0; moving
+    one of its weights by a relative 1e-3 moves the margin to the closed-form
+    |h0 - (1 + 1e-3) h0| / (h0 + (1 + 1e-3) h0)."""
+    net = oracle_mod.Net(**TINY)
+    off = oracle_mod.param_offsets(net)
+    rng = np.random.default_rng(37)
+    theta = _random_theta(oracle_mod, net, rng, bias=0.0)
+    # conv3 channels 0 and 1 identical -> h3[c=0] == h3[c=1] elementwise
+    W3 = theta[off[4]:off[5]].reshape(net.c3, net.c2, net.k3, net.k3)
+    W3[1] = W3[0]
+    theta[off[5]:off[6]] = 0.0
+    W4 = theta[off[6]:off[7]].reshape(net.hidden, -1)
+    W4[:] = np.abs(W4) + 0.1          # every other hidden unit clearly positive
+    theta[off[7]:off[8]] = 0.0
+    P3 = (off[7] - off[6]) // net.hidden // net.c3   # conv3 output pixels
+    W4[0] = 0.0
+    W4[0, 0], W4[0, P3] = 1.0, -1.0                  # z4[0] = h3[0,0] - h3[1,0] = 0
+    s = rng.integers(0, 256, (1, net.in_c, net.in_h, net.in_w), dtype=np.uint8)
+    args = (s, s, np.array([0], np.int32), np.zeros(1, np.float32), np.zeros(1, np.uint8), 0.9)
+    out = oracle_mod.learner_step(net, theta, theta, *args)
+    assert out["margin"][0] == 0.0
+    W4[0, P3] = -(1.0 + 1e-3)
+    out = oracle_mod.learner_step(net, theta, theta, *args)
+    h0 = out["margin"][0]
+    assert 0 < h0 <= 1e-3 / (2 + 1e-3) * (1 + 1e-12)
