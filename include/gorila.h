@@ -52,7 +52,10 @@ enum {
 enum { GORILA_F32 = 0, GORILA_BF16 = 1 };
 enum { GORILA_REPLAY_STACKED = 0, GORILA_REPLAY_RING = 1 };
 
-/* A parameter set theta (device pointer to the flat layout above). */
+/* A parameter set theta (device pointer to the flat layout above).  fp32
+ * sets must be 16-byte aligned, bf16 sets 2-byte aligned (so the rows of a
+ * [groups, P] bf16 array qualify); states and frame buffers 16-byte aligned.
+ * Misalignment is GORILA_EINVAL. */
 typedef struct {
     const void* data;     /* fp32 (GORILA_F32) or bf16 bit patterns (GORILA_BF16) */
     int32_t n_actions;    /* A, 1 .. 32 (the Atari action set has 18)             */
@@ -95,9 +98,12 @@ typedef struct gorila_ctx gorila_ctx;
 /* Number of elements of a flat parameter vector with A actions, or -1. */
 int64_t gorila_param_count(int32_t n_actions);
 
-/* Device workspace bytes needed by calls with batch <= max_batch on
- * `groups` parameter sets (1 for the single-learner and actor calls).
- * The caller allocates it; the context keeps only the pointer. */
+/* Device workspace bytes needed by learner calls with batch <= max_batch on
+ * `groups` parameter sets (1 for the single-learner call), and by forward and
+ * act calls on n <= 2 * max_batch * groups states; dtype GORILA_BF16 adds room
+ * for fp32 copies of groups + 1 bf16 parameter sets.  0 for invalid
+ * arguments (groups outside 1 .. 16 included).  The caller allocates it; the
+ * context keeps only the pointer. */
 size_t gorila_workspace_bytes(int32_t max_batch, int32_t n_actions, int32_t dtype,
                               int32_t groups);
 
@@ -139,7 +145,8 @@ int gorila_gather(const gorila_replay* replay, const int64_t* idx, int32_t n,
                   int32_t* a_out, float* r_out, uint8_t* term_out, gorila_ctx* ctx);
 
 /* Q(s, .; theta) (Section 5.1 network) for states [n,4,84,84] -> q_out [n,A]
- * fp32.  Needs gorila_workspace_bytes(n, A, dtype, 1). */
+ * fp32.  theta may be GORILA_F32 or GORILA_BF16 (widened exactly to fp32).
+ * Needs gorila_workspace_bytes(ceil(n/2), A, dtype, 1). */
 int gorila_q_forward(const gorila_params* params, const uint8_t* states_u8, int32_t n,
                      float* q_out, gorila_ctx* ctx);
 
@@ -170,9 +177,14 @@ int gorila_learner_step(const gorila_params* params, const gorila_params* target
 
 /* `groups` independent learner steps (Section 4: many learners, each with
  * its own, possibly stale, replica of theta) sharing one target theta-.
- * params points to `groups` parameter sets; group g uses minibatch indices
- * idx[g*batch .. g*batch+batch-1] and writes grads_out[g*P .. g*P+P-1] and
- * loss_out[g].  Returns GORILA_EUNSUPPORTED in this build. */
+ * params points to `groups` (1 .. 16) host-side parameter descriptors, each
+ * GORILA_F32 or GORILA_BF16 and all with the target's A; group g is the
+ * learner step of gorila_learner_step on params[g] and the minibatch
+ * idx[g*batch .. g*batch+batch-1], and writes grads_out[g*P .. g*P+P-1] and
+ * loss_out[g] (fp32).  bf16 parameters are widened exactly to fp32 and the
+ * step runs in fp32.  The forward passes of all groups share launches.
+ * Needs gorila_workspace_bytes(batch, A, GORILA_BF16 if any set is bf16 else
+ * GORILA_F32, groups); EINVAL for groups outside 1 .. 16. */
 int gorila_learner_step_grouped(const gorila_params* params, int32_t groups,
                                 const gorila_params* target_params, const gorila_replay* replay,
                                 const int64_t* idx, int32_t batch, float gamma, float clip_delta,

@@ -129,10 +129,11 @@ class Context:
     The workspace is sized for calls with batch <= max_batch (learner step) or
     n <= 2 * max_batch states (forward / act)."""
 
-    def __init__(self, max_batch: int, n_actions: int, groups: int = 1, device=None):
+    def __init__(self, max_batch: int, n_actions: int, groups: int = 1, device=None,
+                 dtype: int = GORILA_F32):
         import torch
         self.device = torch.device(device if device is not None else "cuda")
-        self.ws_bytes = workspace_bytes(max_batch, n_actions, GORILA_F32, groups)
+        self.ws_bytes = workspace_bytes(max_batch, n_actions, dtype, groups)
         if self.ws_bytes == 0:
             raise ValueError("invalid workspace request")
         with torch.cuda.device(self.device):
@@ -183,9 +184,19 @@ class Context:
             pass
 
 
-def params(theta, n_actions: int, dtype: int = GORILA_F32) -> _Params:
+def dtype_of(theta) -> int:
+    """GORILA_F32 for a float32 tensor, GORILA_BF16 for bfloat16 or 16-bit integer bit patterns."""
+    import torch
+    if theta.dtype == torch.float32:
+        return GORILA_F32
+    if theta.dtype in (torch.bfloat16, torch.int16, torch.uint16):
+        return GORILA_BF16
+    raise TypeError(f"parameters must be float32 or bf16 (bits), got {theta.dtype}")
+
+
+def params(theta, n_actions: int, dtype: int | None = None) -> _Params:
     """gorila_params over a flat device tensor (fp32, or bf16 bits as int16/uint16/bfloat16)."""
-    return _Params(theta.data_ptr(), n_actions, dtype)
+    return _Params(theta.data_ptr(), n_actions, dtype_of(theta) if dtype is None else dtype)
 
 
 @dataclass
@@ -247,6 +258,19 @@ def gorila_learner_step(ctx: Context, theta, theta_target, n_actions: int, repla
                                      _ptr(loss_out), ctx.bind_stream()), "gorila_learner_step")
 
 
+def gorila_learner_step_grouped(ctx: Context, thetas, theta_target, n_actions: int,
+                                replay: Replay, idx, batch: int, gamma: float, clip_delta: float,
+                                grads_out, loss_out) -> None:
+    """thetas: a [G, P] tensor or a sequence of G flat tensors; idx [G * batch]."""
+    rows = [thetas[g] for g in range(len(thetas))]
+    arr = (_Params * len(rows))(*[params(t, n_actions) for t in rows])
+    pt, rv = params(theta_target, n_actions), replay.c()
+    _check(lib().gorila_learner_step_grouped(arr, len(rows), ctypes.byref(pt), ctypes.byref(rv),
+                                             _ptr(idx), batch, gamma, clip_delta, _ptr(grads_out),
+                                             _ptr(loss_out), ctx.bind_stream()),
+           "gorila_learner_step_grouped")
+
+
 # Convenience wrappers that allocate the outputs (torch) and return them.
 def q_forward(ctx: Context, theta, n_actions: int, states):
     import torch
@@ -271,6 +295,19 @@ def learner_step(ctx: Context, theta, theta_target, n_actions: int, replay: Repl
     loss = torch.empty(1, dtype=torch.float32, device=theta.device)
     gorila_learner_step(ctx, theta, theta_target, n_actions, replay, idx, gamma, clip_delta,
                         grads, loss)
+    return grads, loss
+
+
+def learner_step_grouped(ctx: Context, thetas, theta_target, n_actions: int, replay: Replay, idx,
+                         gamma: float = 0.99, clip_delta: float = 1.0):
+    """G learner steps sharing theta_target; returns grads [G, P] fp32 and loss [G]."""
+    import torch
+    G = len(thetas)
+    batch = idx.shape[0] // G
+    grads = torch.empty((G, param_count(n_actions)), dtype=torch.float32, device=idx.device)
+    loss = torch.empty(G, dtype=torch.float32, device=idx.device)
+    gorila_learner_step_grouped(ctx, thetas, theta_target, n_actions, replay, idx, batch, gamma,
+                                clip_delta, grads, loss)
     return grads, loss
 
 

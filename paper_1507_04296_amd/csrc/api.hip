@@ -60,17 +60,20 @@ constexpr size_t ALIGN = 256;
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 // Byte offsets of every workspace region for fwd_rows forward rows (all
-// parameter sets together) and bwd_rows learner rows.
+// parameter sets together), bwd_rows learner rows, `online` learner parameter
+// sets plus one target set, and `widened` fp32 copies of bf16 parameter sets.
+constexpr size_t W2T_BYTES = 4 * 16 * 64 * 32, W3T_BYTES = 4 * 9 * 64 * 64;
 struct Plan {
     size_t err, ftab, a, r, term;
-    size_t w2t[2], w3t[2], w3d, w2p;
+    size_t theta32, theta32_stride;
+    size_t w2t, w3t, w3d, w2p;  // bases of per-set arrays (stride W2T_BYTES / W3T_BYTES)
     size_t h1, h2, h3, h4, q, ell, coef;
     size_t dz4, dz3, dz2, dz1;
     size_t fc1part, part1, part2, part3, bpart, hpart;
     size_t total;
 };
 
-Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A) {
+Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online = 1, int widened = 0) {
     Plan p{};
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t at = o; o += up(bytes); return at; };
@@ -80,12 +83,12 @@ Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A) {
     p.a = take(4 * (size_t)B);
     p.r = take(4 * (size_t)B);
     p.term = take((size_t)B);
-    for (int g = 0; g < 2; ++g) {
-        p.w2t[g] = take(4 * 16 * 64 * 32);
-        p.w3t[g] = take(4 * 9 * 64 * 64);
-    }
-    p.w3d = take(4 * 9 * 64 * 64);
-    p.w2p = take(4 * 16 * 32 * 64);
+    p.theta32_stride = up(4 * (size_t)param_count(A));
+    p.theta32 = take(p.theta32_stride * (size_t)widened);
+    p.w2t = take(W2T_BYTES * (size_t)(online + 1));
+    p.w3t = take(W3T_BYTES * (size_t)(online + 1));
+    p.w3d = take(W3T_BYTES * (size_t)online);
+    p.w2p = take(W2T_BYTES * (size_t)online);
     p.h1 = take(4 * (size_t)F * P1 * C1);
     p.h2 = take(4 * (size_t)F * P2 * C2);
     p.h3 = take(4 * (size_t)F * FLAT);
@@ -123,11 +126,28 @@ int check_ctx(gorila_ctx* c) {
     return dev == c->device ? GORILA_OK : GORILA_EINVAL;
 }
 
-int check_params(const gorila_params* p) {
-    if (!p || !p->data || !aligned16(p->data)) return GORILA_EINVAL;
+// fp32 sets are read with 16-byte loads; bf16 sets only by the widening kernel.
+int check_params(const gorila_params* p, bool allow_bf16) {
+    if (!p || !p->data) return GORILA_EINVAL;
     if (p->n_actions < 1 || p->n_actions > MAX_ACTIONS) return GORILA_EINVAL;
-    if (p->dtype != GORILA_F32) return p->dtype == GORILA_BF16 ? GORILA_EUNSUPPORTED : GORILA_EINVAL;
+    if (p->dtype == GORILA_BF16) {
+        if ((uintptr_t)p->data & 1u) return GORILA_EINVAL;
+        return allow_bf16 ? GORILA_OK : GORILA_EUNSUPPORTED;
+    }
+    if (p->dtype != GORILA_F32 || !aligned16(p->data)) return GORILA_EINVAL;
     return GORILA_OK;
+}
+
+// fp32 view of a parameter set: the caller's vector, or its exact widening
+// into the next free fp32 slot of the workspace (queued on the stream).
+const float* fp32_params(gorila_ctx* c, const Plan& p, const gorila_params* prm, WidenSet& ws,
+                         int& n_widen) {
+    if (prm->dtype == GORILA_F32) return (const float*)prm->data;
+    float* dst = at<float>(c, p.theta32 + (size_t)n_widen * p.theta32_stride);
+    ws.src[n_widen] = (const uint16_t*)prm->data;
+    ws.dst[n_widen] = dst;
+    ++n_widen;
+    return dst;
 }
 
 int check_replay(const gorila_replay* rv) {
@@ -157,14 +177,23 @@ __global__ void states_table_kernel(const uint8_t* states, int n, const uint8_t*
     if (e < n * 4) ftab[e] = states + (int64_t)(e >> 2) * STATE_BYTES + (int64_t)(e & 3) * FRAME_BYTES;
 }
 
-// Forward pass of n states through one parameter set up to h4.
-int forward_one(gorila_ctx* c, const Plan& p, const float* theta, const uint8_t* states, int n,
-                int* fc1_splits) {
+// Forward pass of n states through one parameter set up to h4; *theta32
+// receives the fp32 parameters the head must use.
+int forward_one(gorila_ctx* c, const Plan& p, const gorila_params* prm, const uint8_t* states,
+                int n, const float** theta32, int* fc1_splits) {
     hipStream_t st = c->stream;
     const uint8_t** ftab = at<const uint8_t*>(c, p.ftab);
     { StageTimer t(c, ST_RESOLVE); states_table_kernel<<<(n * 4 + 255) / 256, 256, 0, st>>>(states, n, ftab); }
-    WeightViews wv{theta, at<float>(c, p.w2t[0]), at<float>(c, p.w3t[0]), nullptr, nullptr};
-    { StageTimer t(c, ST_PREP); launch_prep_weights(&wv, 1, st); }
+    WidenSet ws{};
+    int n_widen = 0;
+    const float* theta = fp32_params(c, p, prm, ws, n_widen);
+    *theta32 = theta;
+    WeightViews wv{theta, at<float>(c, p.w2t), at<float>(c, p.w3t), nullptr, nullptr};
+    {
+        StageTimer t(c, ST_PREP);
+        if (n_widen) launch_widen_bf16(ws, n_widen, param_count(prm->n_actions), st);
+        launch_prep_weights(&wv, 1, st);
+    }
     GroupPtrs th{}, w2t{}, w3t{};
     th.p[0] = theta;
     w2t.p[0] = wv.w2t;
@@ -188,8 +217,10 @@ int64_t gorila_param_count(int32_t n_actions) {
 size_t gorila_workspace_bytes(int32_t max_batch, int32_t n_actions, int32_t dtype, int32_t groups) {
     if (max_batch < 1 || n_actions < 1 || n_actions > MAX_ACTIONS || groups < 1) return 0;
     if (dtype != GORILA_F32 && dtype != GORILA_BF16) return 0;
+    if (groups > MAX_LEARNER_GROUPS) return 0;
     const int64_t B = (int64_t)max_batch * groups;
-    return make_plan(2 * B, B, n_actions).total;
+    const int widened = dtype == GORILA_BF16 ? groups + 1 : 0;
+    return make_plan(2 * B, B, n_actions, groups, widened).total;
 }
 
 int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_t ws_bytes) {
@@ -331,14 +362,14 @@ int gorila_q_forward(const gorila_params* params, const uint8_t* states_u8, int3
                      float* q_out, gorila_ctx* ctx) {
     int rc = check_ctx(ctx);
     if (rc) return rc;
-    if ((rc = check_params(params))) return rc;
+    if ((rc = check_params(params, true))) return rc;
     if (n < 0 || (n > 0 && (!states_u8 || !q_out)) || !aligned16(states_u8)) return GORILA_EINVAL;
     if (n == 0) return GORILA_OK;
-    const Plan p = make_plan(n, 0, params->n_actions);
+    const Plan p = make_plan(n, 0, params->n_actions, 1, params->dtype == GORILA_BF16);
     if (p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
-    const float* theta = (const float*)params->data;
+    const float* theta = nullptr;
     int splits = 0;
-    if ((rc = forward_one(ctx, p, theta, states_u8, n, &splits))) return rc;
+    if ((rc = forward_one(ctx, p, params, states_u8, n, &theta, &splits))) return rc;
     {
         StageTimer t(ctx, ST_HEAD);
         launch_q_head(at<float>(ctx, p.fc1part), splits, theta, n, params->n_actions, q_out,
@@ -351,15 +382,15 @@ int gorila_act(const gorila_params* params, const uint8_t* states_u8, int32_t n,
                uint64_t seed, int32_t* actions_out, float* q_out, gorila_ctx* ctx) {
     int rc = check_ctx(ctx);
     if (rc) return rc;
-    if ((rc = check_params(params))) return rc;
+    if ((rc = check_params(params, true))) return rc;
     if (n < 0 || (n > 0 && (!states_u8 || !actions_out)) || !aligned16(states_u8)) return GORILA_EINVAL;
     if (!(eps >= 0.0f && eps <= 1.0f)) return GORILA_EINVAL;
     if (n == 0) return GORILA_OK;
-    const Plan p = make_plan(n, 0, params->n_actions);
+    const Plan p = make_plan(n, 0, params->n_actions, 1, params->dtype == GORILA_BF16);
     if (p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
-    const float* theta = (const float*)params->data;
+    const float* theta = nullptr;
     int splits = 0;
-    if ((rc = forward_one(ctx, p, theta, states_u8, n, &splits))) return rc;
+    if ((rc = forward_one(ctx, p, params, states_u8, n, &theta, &splits))) return rc;
     {
         StageTimer t(ctx, ST_HEAD);
         launch_act_head(at<float>(ctx, p.fc1part), splits, theta, n, params->n_actions, eps, seed,
@@ -368,24 +399,40 @@ int gorila_act(const gorila_params* params, const uint8_t* states_u8, int32_t n,
     return check_launch();
 }
 
-int gorila_learner_step(const gorila_params* params, const gorila_params* target_params,
-                        const gorila_replay* replay, const int64_t* idx, int32_t batch,
-                        float gamma, float clip_delta, float* grads_out, float* loss_out,
-                        gorila_ctx* ctx) {
+}  // extern "C"
+
+namespace {
+
+// Shared launch sequence of the learner calls: G learner groups of b
+// transitions each, group g on parameter set params[g] and minibatch
+// idx[g*b .. g*b+b-1], all against one target set.
+int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G,
+                  const gorila_params* target_params, const gorila_replay* replay,
+                  const int64_t* idx, int b, float gamma, float clip_delta, float* grads_out,
+                  float* loss_out) {
     int rc = check_ctx(ctx);
     if (rc) return rc;
-    if ((rc = check_params(params)) || (rc = check_params(target_params))) return rc;
-    if (params->n_actions != target_params->n_actions) return GORILA_EINVAL;
+    if (G < 1 || G > MAX_LEARNER_GROUPS || !params) return GORILA_EINVAL;
+    if ((rc = check_params(target_params, G > 1))) return rc;
+    const int A = target_params->n_actions;
+    int n_bf16 = target_params->dtype == GORILA_BF16;
+    for (int g = 0; g < G; ++g) {
+        if ((rc = check_params(&params[g], G > 1))) return rc;
+        if (params[g].n_actions != A) return GORILA_EINVAL;
+        n_bf16 += params[g].dtype == GORILA_BF16;
+    }
     if ((rc = check_replay(replay))) return rc;
-    if (batch < 1 || !idx || !grads_out || !loss_out) return GORILA_EINVAL;
+    if (b < 1 || !idx || !grads_out || !loss_out) return GORILA_EINVAL;
+    if ((int64_t)b * G > (int64_t)1 << 30) return GORILA_EINVAL;
     if (!(gamma >= 0.0f && gamma <= 1.0f) || !(clip_delta > 0.0f)) return GORILA_EINVAL;
-    const int A = params->n_actions, B = batch;
-    const Plan p = make_plan(2 * (int64_t)B, B, A);
+    const int B = b * G;  // all learner rows
+    const Plan p = make_plan(2 * (int64_t)B, B, A, G, n_bf16);
     if (p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
     hipStream_t st = ctx->stream;
-    const float* theta = (const float*)params->data;
-    const float* theta_t = (const float*)target_params->data;
+    const int64_t P = param_count(A);
 
+    // ftab [2][B][4]: rows g*b .. g*b+b-1 of the s half are group g's states,
+    // the same rows of the s' half its next states
     const uint8_t** ftab = at<const uint8_t*>(ctx, p.ftab);
     int32_t* a = at<int32_t>(ctx, p.a);
     float* r = at<float>(ctx, p.r);
@@ -395,30 +442,42 @@ int gorila_learner_step(const gorila_params* params, const gorila_params* target
         launch_resolve(view_of(replay), idx, B, A, ftab, a, r, term, nullptr, at<unsigned>(ctx, p.err), st);
     }
 
-    WeightViews wv[2] = {
-        {theta, at<float>(ctx, p.w2t[0]), at<float>(ctx, p.w3t[0]), at<float>(ctx, p.w3d),
-         at<float>(ctx, p.w2p)},
-        {theta_t, at<float>(ctx, p.w2t[1]), at<float>(ctx, p.w3t[1]), nullptr, nullptr}};
-    { StageTimer t(ctx, ST_PREP); launch_prep_weights(wv, 2, st); }
+    WidenSet widen{};
+    int n_widen = 0;
+    const float* theta[MAX_LEARNER_GROUPS];
+    for (int g = 0; g < G; ++g) theta[g] = fp32_params(ctx, p, &params[g], widen, n_widen);
+    const float* theta_t = fp32_params(ctx, p, target_params, widen, n_widen);
+    WeightViews wv[MAX_NETS];
+    for (int g = 0; g <= G; ++g) {
+        wv[g].theta = g < G ? theta[g] : theta_t;
+        wv[g].w2t = at<float>(ctx, p.w2t + (size_t)g * W2T_BYTES);
+        wv[g].w3t = at<float>(ctx, p.w3t + (size_t)g * W3T_BYTES);
+        wv[g].w3d = g < G ? at<float>(ctx, p.w3d + (size_t)g * W3T_BYTES) : nullptr;
+        wv[g].w2p = g < G ? at<float>(ctx, p.w2p + (size_t)g * W2T_BYTES) : nullptr;
+    }
+    {
+        StageTimer t(ctx, ST_PREP);
+        if (n_widen) launch_widen_bf16(widen, n_widen, P, st);
+        launch_prep_weights(wv, G + 1, st);
+    }
+    // forward groups 0 .. G-1: online nets on s; G .. 2G-1: the target on s'
     GroupPtrs th{}, w2t{}, w3t{};
-    for (int g = 0; g < 2; ++g) {
-        th.p[g] = g ? theta_t : theta;
-        w2t.p[g] = wv[g].w2t;
-        w3t.p[g] = wv[g].w3t;
+    for (int g = 0; g < 2 * G; ++g) {
+        const int net = g < G ? g : G;
+        th.p[g] = wv[net].theta;
+        w2t.p[g] = wv[net].w2t;
+        w3t.p[g] = wv[net].w3t;
     }
     float* h1 = at<float>(ctx, p.h1);
     float* h2 = at<float>(ctx, p.h2);
     float* h3 = at<float>(ctx, p.h3);
     float* h4 = at<float>(ctx, p.h4);
-    // online (group 0, on s) and target (group 1, on s') forward passes
-    { StageTimer t(ctx, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 2, B, h1, st); }
-    { StageTimer t(ctx, ST_CONV2_FWD); launch_conv2_fwd(h1, w2t, th, 2, B, h2, st); }
-    { StageTimer t(ctx, ST_CONV3_FWD); launch_conv3_fwd(h2, w3t, th, 2, B, h3, st); }
-    int fc1_splits = 0;
-    {
-        StageTimer t(ctx, ST_FC1_FWD);
-        fc1_splits = launch_fc1_fwd(h3, th, 2, B, at<float>(ctx, p.fc1part), st);
-    }
+    float* fc1part = at<float>(ctx, p.fc1part);
+    { StageTimer t(ctx, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 2 * G, b, h1, st); }
+    { StageTimer t(ctx, ST_CONV2_FWD); launch_conv2_fwd(h1, w2t, th, 2 * G, b, h2, st); }
+    { StageTimer t(ctx, ST_CONV3_FWD); launch_conv3_fwd(h2, w3t, th, 2 * G, b, h3, st); }
+    int S = 0;
+    { StageTimer t(ctx, ST_FC1_FWD); S = launch_fc1_fwd(h3, th, 2 * G, b, fc1part, st); }
 
     float* dz4 = at<float>(ctx, p.dz4);
     float* dz3 = at<float>(ctx, p.dz3);
@@ -426,49 +485,71 @@ int gorila_learner_step(const gorila_params* params, const gorila_params* target
     float* dz1 = at<float>(ctx, p.dz1);
     float* ell = at<float>(ctx, p.ell);
     float* coef = at<float>(ctx, p.coef);
-    {
-        StageTimer t(ctx, ST_HEAD);
-        launch_td_head(at<float>(ctx, p.fc1part), fc1_splits, theta, theta_t, B, A, a, r, term,
-                       gamma, clip_delta, h4, at<float>(ctx, p.q), ell, coef, dz4, st);
-    }
-    int head_blocks = 0, s1 = 0, s2 = 0, s3 = 0;
+    float* q = at<float>(ctx, p.q);
     float* bpart = at<float>(ctx, p.bpart);
-    {
-        StageTimer t(ctx, ST_FC1_BWD);
-        head_blocks = launch_fc1_backward(dz4, theta, h3, h4, a, coef, ell, B, A, dz3, grads_out,
-                                          at<float>(ctx, p.hpart), st);
-    }
-    {
-        StageTimer t(ctx, ST_CONV3_BWD);
-        s3 = launch_conv3_backward(dz3, wv[0].w3d, h2, B, dz2, at<float>(ctx, p.part3),
-                                   bpart + 2 * BIAS_PART_STRIDE, st);
-    }
-    {
-        StageTimer t(ctx, ST_CONV2_BWD);
-        s2 = launch_conv2_backward(dz2, wv[0].w2p, h1, B, dz1, at<float>(ctx, p.part2),
-                                   bpart + BIAS_PART_STRIDE, st);
-    }
-    {
-        StageTimer t(ctx, ST_CONV1_WGRAD);
-        launch_conv1_wgrad(dz1, ftab, B, at<float>(ctx, p.part1), bpart, CONV1_WG_MAX_SPLITS, &s1, st);
-    }
-    {
-        StageTimer t(ctx, ST_GRAD_REDUCE);
-        ReduceArgs ra{at<float>(ctx, p.part1), at<float>(ctx, p.part2), at<float>(ctx, p.part3),
-                      bpart, at<float>(ctx, p.hpart), s1, s2, s3, head_blocks, B, A, grads_out,
-                      loss_out};
-        launch_grad_reduce(ra, st);
+    for (int g = 0; g < G; ++g) {
+        const int64_t r0 = (int64_t)g * b;  // first learner row of the group
+        const float* th_g = theta[g];
+        const float* on_part = fc1part + (int64_t)g * S * b * HID;
+        const float* tg_part = fc1part + (int64_t)(G + g) * S * b * HID;
+        {
+            StageTimer t(ctx, ST_HEAD);
+            launch_td_head(on_part, tg_part, S, th_g, theta_t, b, A, a + r0, r + r0, term + r0,
+                           gamma, clip_delta, h4 + r0 * HID, q + 2 * r0 * A, ell + r0, coef + r0,
+                           dz4 + r0 * HID, st);
+        }
+        float* grads = grads_out + (int64_t)g * P;
+        int head_blocks = 0, s1 = 0, s2 = 0, s3 = 0;
+        {
+            StageTimer t(ctx, ST_FC1_BWD);
+            head_blocks = launch_fc1_backward(dz4 + r0 * HID, th_g, h3 + r0 * FLAT, h4 + r0 * HID,
+                                              a + r0, coef + r0, ell + r0, b, A, dz3, grads,
+                                              at<float>(ctx, p.hpart), st);
+        }
+        {
+            StageTimer t(ctx, ST_CONV3_BWD);
+            s3 = launch_conv3_backward(dz3, wv[g].w3d, h2 + r0 * P2 * C2, b, dz2,
+                                       at<float>(ctx, p.part3), bpart + 2 * BIAS_PART_STRIDE, st);
+        }
+        {
+            StageTimer t(ctx, ST_CONV2_BWD);
+            s2 = launch_conv2_backward(dz2, wv[g].w2p, h1 + r0 * P1 * C1, b, dz1,
+                                       at<float>(ctx, p.part2), bpart + BIAS_PART_STRIDE, st);
+        }
+        {
+            StageTimer t(ctx, ST_CONV1_WGRAD);
+            launch_conv1_wgrad(dz1, ftab + r0 * 4, b, at<float>(ctx, p.part1), bpart,
+                               CONV1_WG_MAX_SPLITS, &s1, st);
+        }
+        {
+            StageTimer t(ctx, ST_GRAD_REDUCE);
+            ReduceArgs ra{at<float>(ctx, p.part1), at<float>(ctx, p.part2), at<float>(ctx, p.part3),
+                          bpart, at<float>(ctx, p.hpart), s1, s2, s3, head_blocks, b, A, grads,
+                          loss_out + g};
+            launch_grad_reduce(ra, st);
+        }
     }
     return check_launch();
+}
+
+}  // namespace
+
+extern "C" {
+
+int gorila_learner_step(const gorila_params* params, const gorila_params* target_params,
+                        const gorila_replay* replay, const int64_t* idx, int32_t batch,
+                        float gamma, float clip_delta, float* grads_out, float* loss_out,
+                        gorila_ctx* ctx) {
+    return learner_steps(ctx, params, 1, target_params, replay, idx, batch, gamma, clip_delta,
+                         grads_out, loss_out);
 }
 
 int gorila_learner_step_grouped(const gorila_params* params, int32_t groups,
                                 const gorila_params* target_params, const gorila_replay* replay,
                                 const int64_t* idx, int32_t batch, float gamma, float clip_delta,
                                 float* grads_out, float* loss_out, gorila_ctx* ctx) {
-    (void)params; (void)groups; (void)target_params; (void)replay; (void)idx; (void)batch;
-    (void)gamma; (void)clip_delta; (void)grads_out; (void)loss_out; (void)ctx;
-    return GORILA_EUNSUPPORTED;
+    return learner_steps(ctx, params, groups, target_params, replay, idx, batch, gamma,
+                         clip_delta, grads_out, loss_out);
 }
 
 }  // extern "C"

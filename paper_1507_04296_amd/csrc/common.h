@@ -40,6 +40,9 @@ __host__ __device__ constexpr int64_t param_count(int A) { return off_b5(A) + A;
 
 // Up to MAX_GROUPS parameter sets per launch, passed by value.
 constexpr int MAX_GROUPS = 32;
+// Learner groups per grouped step: their online and target forward passes
+// (2 per group) share the forward launches.
+constexpr int MAX_LEARNER_GROUPS = MAX_GROUPS / 2;
 struct GroupPtrs {
     const float* p[MAX_GROUPS];
 };

@@ -94,9 +94,11 @@ void launch_act_head(const float* fc1part, int splits, const float* theta, int n
                                                seed);
 }
 
-// fc1part holds [2][splits][n][512]: group 0 (online, on s), group 1 (target, on s').
+// fc1part_online / fc1part_target: [splits][n][512] for the online (on s) and
+// the target (on s') network.
 __global__ __launch_bounds__(256) void td_head_kernel(
-    const float* __restrict__ fc1part, int splits, const float* __restrict__ theta,
+    const float* __restrict__ fc1part, const float* __restrict__ fc1part_t, int splits,
+    const float* __restrict__ theta,
     const float* __restrict__ theta_t, int n, int A, const int32_t* __restrict__ a,
     const float* __restrict__ r, const uint8_t* __restrict__ term, float gamma, float clip,
     float* __restrict__ h4, float* __restrict__ q, float* __restrict__ ell,
@@ -106,7 +108,7 @@ __global__ __launch_bounds__(256) void td_head_kernel(
     const int64_t ss = (int64_t)n * HID;
     float h[8], ht[8];
     finish_h4(fc1part + (int64_t)b * HID, splits, ss, theta + OFF_B4, lane, h);
-    finish_h4(fc1part + splits * ss + (int64_t)b * HID, splits, ss, theta_t + OFF_B4, lane, ht);
+    finish_h4(fc1part_t + (int64_t)b * HID, splits, ss, theta_t + OFF_B4, lane, ht);
     float* h4row = h4 + (int64_t)b * HID + lane * 8;
     *(f32x4*)h4row = f32x4{h[0], h[1], h[2], h[3]};
     *(f32x4*)(h4row + 4) = f32x4{h[4], h[5], h[6], h[7]};
@@ -146,13 +148,14 @@ __global__ __launch_bounds__(256) void td_head_kernel(
     *(f32x4*)(out + 4) = o1;
 }
 
-void launch_td_head(const float* fc1part, int splits, const float* theta, const float* theta_target,
-                    int n, int A, const int32_t* a, const float* r, const uint8_t* term, float gamma,
-                    float clip, float* h4, float* q, float* ell, float* coef, float* dz4,
-                    hipStream_t st) {
+void launch_td_head(const float* fc1part_online, const float* fc1part_target, int splits,
+                    const float* theta, const float* theta_target, int n, int A, const int32_t* a,
+                    const float* r, const uint8_t* term, float gamma, float clip, float* h4,
+                    float* q, float* ell, float* coef, float* dz4, hipStream_t st) {
     if (n <= 0) return;
-    td_head_kernel<<<(n + 3) / 4, 256, 0, st>>>(fc1part, splits, theta, theta_target, n, A, a, r,
-                                                term, gamma, clip, h4, q, ell, coef, dz4);
+    td_head_kernel<<<(n + 3) / 4, 256, 0, st>>>(fc1part_online, fc1part_target, splits, theta,
+                                                theta_target, n, A, a, r, term, gamma, clip, h4, q,
+                                                ell, coef, dz4);
 }
 
 }  // namespace gorila

@@ -45,7 +45,18 @@ struct WeightViews {
     float* w3d;           // may be null (forward only)
     float* w2p;           // may be null
 };
+constexpr int MAX_NETS = MAX_LEARNER_GROUPS + 1;  // learner replicas + their shared target
+struct WeightViewSet {
+    WeightViews v[MAX_NETS];
+};
 void launch_prep_weights(const WeightViews* nets, int n_nets, hipStream_t st);
+
+// Widen bf16 parameter vectors (bit patterns) to fp32 exactly: dst[i][k] = src[i][k].
+struct WidenSet {
+    const uint16_t* src[MAX_NETS];
+    float* dst[MAX_NETS];
+};
+void launch_widen_bf16(const WidenSet& set, int n_nets, int64_t count, hipStream_t st);
 
 // Forward layers.  `groups` parameter sets; group g owns rows [g*n, (g+1)*n)
 // of every activation buffer.
@@ -67,10 +78,11 @@ void launch_q_head(const float* fc1part, int splits, const float* theta, int n, 
 void launch_act_head(const float* fc1part, int splits, const float* theta, int n, int A, float eps,
                      uint64_t seed, int32_t* actions, float* q_out, hipStream_t st);
 // Writes h4 (online rows), q [2n][A], ell, coef = dLoss/dQ(s,a) and dz4.
-void launch_td_head(const float* fc1part, int splits, const float* theta, const float* theta_target,
-                    int n, int A, const int32_t* a, const float* r, const uint8_t* term, float gamma,
-                    float clip, float* h4, float* q, float* ell, float* coef, float* dz4,
-                    hipStream_t st);
+// fc1part_online / fc1part_target each hold [splits][n][512].
+void launch_td_head(const float* fc1part_online, const float* fc1part_target, int splits,
+                    const float* theta, const float* theta_target, int n, int A, const int32_t* a,
+                    const float* r, const uint8_t* term, float gamma, float clip, float* h4,
+                    float* q, float* ell, float* coef, float* dz4, hipStream_t st);
 
 // Backward, three launches of independent jobs each:
 //  fc1: dz3 = [h3 > 0] W4^T dz4 (stored [b][p][o]), dW4 and db4 into grads,

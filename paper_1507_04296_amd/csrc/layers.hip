@@ -15,10 +15,9 @@ namespace gorila {
 // ---------------------------------------------------------------------------
 // Weight transposes (run once per call, small: < 0.3 MB)
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void prep_weights_kernel(WeightViews v0, WeightViews v1,
-                                                           int n_nets) {
-    const WeightViews v = blockIdx.y == 0 ? v0 : v1;
+__global__ __launch_bounds__(256) void prep_weights_kernel(WeightViewSet set, int n_nets) {
     if ((int)blockIdx.y >= n_nets) return;
+    const WeightViews v = set.v[blockIdx.y];
     const float* W2 = v.theta + OFF_W2;
     const float* W3 = v.theta + OFF_W3;
     for (int e = blockIdx.x * 256 + threadIdx.x; e < 16 * 64 * 32; e += gridDim.x * 256) {
@@ -42,8 +41,22 @@ __global__ __launch_bounds__(256) void prep_weights_kernel(WeightViews v0, Weigh
 }
 
 void launch_prep_weights(const WeightViews* nets, int n_nets, hipStream_t st) {
-    prep_weights_kernel<<<dim3(64, n_nets), 256, 0, st>>>(nets[0], n_nets > 1 ? nets[1] : nets[0],
-                                                          n_nets);
+    WeightViewSet set{};
+    for (int i = 0; i < n_nets && i < MAX_NETS; ++i) set.v[i] = nets[i];
+    prep_weights_kernel<<<dim3(64, n_nets), 256, 0, st>>>(set, n_nets);
+}
+
+// bf16 -> fp32 is exact: the 16 bits become the high half of the float.
+__global__ __launch_bounds__(256) void widen_bf16_kernel(WidenSet set, int64_t count) {
+    const uint16_t* src = set.src[blockIdx.y];
+    float* dst = set.dst[blockIdx.y];
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < count;
+         e += (int64_t)gridDim.x * 256)
+        dst[e] = __uint_as_float((uint32_t)src[e] << 16);
+}
+
+void launch_widen_bf16(const WidenSet& set, int n_nets, int64_t count, hipStream_t st) {
+    widen_bf16_kernel<<<dim3(512, n_nets), 256, 0, st>>>(set, count);
 }
 
 // ---------------------------------------------------------------------------

@@ -1,0 +1,192 @@
+"""GPU parity of the grouped learner step (Section 4: many learners, each on its
+own possibly stale copy of theta, one shared target theta-) and of bf16
+parameter sets, against the fp64 oracle run once per group.
+
+bf16 parameters are bit patterns; the oracle takes their exact fp64 values.
+The HIP path widens them exactly to fp32 and computes in fp32, so the fp32
+bars apply (Q and loss 1e-4 relative, every gradient tensor 1e-3 relative L2),
+well inside the 2e-2 bar stated for bf16 parameters with fp32 accumulation.
+Gradient parity runs on kink-certified rows of each group, picked out of a
+larger pool per group, so every group still runs at the batch under test.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import parity
+from paper_1507_04296_amd import datagen
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a ROCm device")
+    return torch
+
+
+@pytest.fixture(scope="module")
+def g(torch_cuda):
+    import paper_1507_04296_amd as gmod
+    gmod.lib()
+    return gmod
+
+
+def _dev(torch, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _pick_certified(oracle_mod, net, thetas64, target64, inp, pool, batch):
+    """idx [G*batch]: for group g, `batch` certified rows out of its `pool` rows."""
+    idx = []
+    for gi, th in enumerate(thetas64):
+        rows = slice(gi * pool, (gi + 1) * pool)
+        m = oracle_mod.learner_step(net, th, target64, inp.s[rows], inp.s2[rows], inp.a[rows],
+                                    inp.r[rows], inp.term[rows], inp.gamma, 1.0)["margin"]
+        idx.append(gi * pool + parity.kink_certified(m, batch))
+    return np.concatenate(idx).astype(np.int64)
+
+
+def _oracle_groups(oracle_mod, net, thetas64, target64, inp, idx, batch, clip=1.0):
+    out = []
+    for gi, th in enumerate(thetas64):
+        ix = idx[gi * batch:(gi + 1) * batch]
+        out.append(oracle_mod.learner_step(net, th, target64, inp.s[ix], inp.s2[ix], inp.a[ix],
+                                           inp.r[ix], inp.term[ix], inp.gamma, clip))
+    return out
+
+
+def _replay(torch, g, inp):
+    return g.Replay.stacked(_dev(torch, inp.s), _dev(torch, inp.s2), _dev(torch, inp.a),
+                            _dev(torch, inp.r), _dev(torch, inp.term))
+
+
+def test_grouped_16x64_bf16_a18(torch_cuda, g, oracle_mod):
+    """The stale-replica workload: 16 bf16 replicas x 64 transitions, 18 actions."""
+    torch = torch_cuda
+    w = datagen.WORKLOADS["grouped_g16_b64_a18_bf16"]
+    G, b, A, pool = w["groups"], w["batch"], w["n_actions"], 96
+    _say(f"grouped G={G} b={b} A={A} bf16 seed={w['seed']}")
+    inp = datagen.grouped_inputs(w["seed"], G, pool, A)
+    net = oracle_mod.Net(n_actions=A)
+    th64 = [datagen.bf16_bits_to_f64(t) for t in inp.theta_bf16]
+    tg64 = datagen.bf16_bits_to_f64(inp.target_bf16)
+    idx = _pick_certified(oracle_mod, net, th64, tg64, inp, pool, b)
+    ctx = g.Context(max_batch=b, n_actions=A, groups=G, dtype=g.GORILA_BF16)
+    thetas = _dev(torch, inp.theta_bf16.view(np.int16))
+    target = _dev(torch, inp.target_bf16.view(np.int16))
+    grads, loss = g.learner_step_grouped(ctx, thetas, target, A, _replay(torch, g, inp),
+                                         _dev(torch, idx), inp.gamma, 1.0)
+    ctx.check()
+    got_g, got_l = grads.cpu().numpy(), loss.cpu().numpy()
+    ref = _oracle_groups(oracle_mod, net, th64, tg64, inp, idx, b)
+    worst = {}
+    for gi in range(G):
+        errs = parity.assert_grads_close(got_g[gi], ref[gi]["grads"], A)
+        assert abs(got_l[gi] - ref[gi]["loss"]) <= parity.LOSS_TOL * abs(ref[gi]["loss"]), gi
+        for k, v in errs.items():
+            worst[k] = max(worst.get(k, 0.0), v)
+    _say(f"worst grad rel-L2 over groups {worst}")
+    # replicas differ, so their gradients must too
+    assert not np.array_equal(got_g[0], got_g[1])
+    ctx.close()
+
+
+def test_grouped_ragged_mixed_dtypes(torch_cuda, g, oracle_mod):
+    """3 groups of 37 rows, 7 actions; replicas fp32, bf16, fp32; bf16 target."""
+    torch = torch_cuda
+    G, b, A, pool = 3, 37, 7, 60
+    _say(f"grouped ragged G={G} b={b} A={A} mixed dtypes")
+    inp = datagen.grouped_inputs(8100, G, pool, A)
+    net = oracle_mod.Net(n_actions=A)
+    th64 = [datagen.bf16_bits_to_f64(t) for t in inp.theta_bf16]
+    # replica 0 and 2 in fp32: perturb so they are not bf16-representable
+    rng = np.random.default_rng(8101)
+    th64[0] = (th64[0] + 1e-4 * rng.standard_normal(th64[0].shape[0])).astype(np.float32)
+    th64[2] = (th64[2] - 1e-4 * rng.standard_normal(th64[2].shape[0])).astype(np.float32)
+    th64 = [np.asarray(t, np.float64) for t in th64]
+    tg64 = datagen.bf16_bits_to_f64(inp.target_bf16)
+    idx = _pick_certified(oracle_mod, net, th64, tg64, inp, pool, b)
+    ctx = g.Context(max_batch=b, n_actions=A, groups=G, dtype=g.GORILA_BF16)
+    thetas = [_dev(torch, th64[0].astype(np.float32)),
+              _dev(torch, inp.theta_bf16[1].view(np.int16)),
+              _dev(torch, th64[2].astype(np.float32))]
+    target = _dev(torch, inp.target_bf16.view(np.int16))
+    grads, loss = g.learner_step_grouped(ctx, thetas, target, A, _replay(torch, g, inp),
+                                         _dev(torch, idx), inp.gamma, 0.5)
+    ctx.check()
+    ref = _oracle_groups(oracle_mod, net, th64, tg64, inp, idx, b, clip=0.5)
+    for gi in range(G):
+        parity.assert_grads_close(grads[gi].cpu().numpy(), ref[gi]["grads"], A)
+        l = float(loss[gi].cpu())
+        assert abs(l - ref[gi]["loss"]) <= parity.LOSS_TOL * abs(ref[gi]["loss"]), gi
+    ctx.close()
+
+
+def test_grouped_one_group_matches_single_step(torch_cuda, g):
+    """G = 1 runs the single learner step's launches: results are bitwise equal."""
+    torch = torch_cuda
+    _say("grouped G=1 == learner_step")
+    inp = datagen.learner_inputs(8200, 48, 18)
+    ctx = g.Context(max_batch=48, n_actions=18)
+    theta, tgt = _dev(torch, inp.theta), _dev(torch, inp.theta_target)
+    rep = g.Replay.stacked(_dev(torch, inp.s), _dev(torch, inp.s2), _dev(torch, inp.a),
+                           _dev(torch, inp.r), _dev(torch, inp.term))
+    idx = _dev(torch, inp.idx)
+    g1, l1 = g.learner_step(ctx, theta, tgt, 18, rep, idx)
+    g2, l2 = g.learner_step_grouped(ctx, [theta], tgt, 18, rep, idx)
+    ctx.check()
+    assert torch.equal(g1, g2[0]) and torch.equal(l1, l2)
+    ctx.close()
+
+
+def test_grouped_argument_errors(torch_cuda, g):
+    torch = torch_cuda
+    inp = datagen.learner_inputs(8300, 4, 18)
+    ctx = g.Context(max_batch=4, n_actions=18, groups=2)
+    theta, tgt = _dev(torch, inp.theta), _dev(torch, inp.theta_target)
+    rep = g.Replay.stacked(_dev(torch, inp.s), _dev(torch, inp.s2), _dev(torch, inp.a),
+                           _dev(torch, inp.r), _dev(torch, inp.term))
+    idx = _dev(torch, np.tile(inp.idx, 2))
+    grads = torch.empty((17, g.param_count(18)), device="cuda")
+    loss = torch.empty(17, device="cuda")
+    with pytest.raises(g.GorilaError) as e:  # 17 groups: over the limit
+        g.gorila_learner_step_grouped(ctx, [theta] * 17, tgt, 18, rep, idx, 4, 0.99, 1.0,
+                                      grads, loss)
+    assert e.value.code == -1
+    with pytest.raises(g.GorilaError) as e:  # 3 groups need more workspace
+        g.gorila_learner_step_grouped(ctx, [theta] * 3, tgt, 18, rep, _dev(torch, np.tile(inp.idx, 3)),
+                                      4, 0.99, 1.0, grads, loss)
+    assert e.value.code == -3
+    # bf16 parameters are not accepted by the single learner step
+    bf = _dev(torch, datagen.to_bf16_bits(inp.theta.astype(np.float64)).view(np.int16))
+    with pytest.raises(g.GorilaError) as e:
+        g.learner_step(ctx, bf, tgt, 18, rep, _dev(torch, inp.idx))
+    assert e.value.code == -5
+    ctx.close()
+
+
+@pytest.mark.parametrize("n", [5, 300])
+def test_q_forward_bf16_params(torch_cuda, g, oracle_mod, n):
+    torch = torch_cuda
+    _say(f"q_forward bf16 n={n}")
+    inp = datagen.learner_inputs(8400 + n, n, 18)
+    bits = datagen.to_bf16_bits(inp.theta.astype(np.float64))
+    ctx = g.Context(max_batch=n, n_actions=18, dtype=g.GORILA_BF16)
+    q = g.q_forward(ctx, _dev(torch, bits.view(np.int16)), 18, _dev(torch, inp.s))
+    acts = g.act(ctx, _dev(torch, bits.view(np.int16)), 18, _dev(torch, inp.s), 0.0, 5)
+    ctx.check()
+    net = oracle_mod.Net(n_actions=18)
+    th64 = datagen.bf16_bits_to_f64(bits)
+    ref_a, ref_q = oracle_mod.act(net, th64, inp.s, 0.0, 5)
+    assert parity.q_rel_err(q.cpu().numpy(), ref_q) <= parity.Q_TOL
+    parity.assert_actions_match(acts.cpu().numpy(), ref_q, ref_a, np.zeros(n, bool))
+    ctx.close()
