@@ -128,6 +128,47 @@ def run_learner(torch, g, datagen, B, A, seed, steps, warmup, timed_stage=None):
                 dominant_ms=dom[0] / max(dom[1], 1), dominant_launches=dom[1])
 
 
+def run_grouped(torch, g, datagen, steps, warmup):
+    """The stale-replica workload: 16 bf16 replicas x 64 transitions, 18 actions."""
+    w = datagen.WORKLOADS["grouped_g16_b64_a18_bf16"]
+    G, b, A = w["groups"], w["batch"], w["n_actions"]
+    inp = datagen.grouped_inputs(w["seed"], G, b, A)
+    dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    thetas, tgt = t(inp.theta_bf16.view(np.int16)), t(inp.target_bf16.view(np.int16))
+    idx = torch.arange(G * b, dtype=torch.int64, device=dev)
+    rep = g.Replay.stacked(t(inp.s), t(inp.s2), t(inp.a), t(inp.r), t(inp.term))
+    ctx = g.Context(b, A, groups=G, device=dev, dtype=g.GORILA_BF16)
+    grads = torch.empty((G, g.param_count(A)), dtype=torch.float32, device=dev)
+    loss = torch.empty(G, dtype=torch.float32, device=dev)
+    step = lambda: g.gorila_learner_step_grouped(ctx, thetas, tgt, A, rep, idx, b, inp.gamma, 1.0,
+                                                 grads, loss)
+    for _ in range(warmup):
+        step()
+    ctx.check()
+    names = g.stage_names()
+    ctx.timing_begin(names, max_records=len(names) * G * max(steps, 1))
+    for _ in range(max(steps // 2, 1)):
+        step()
+    prof = ctx.timing_end()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        step()
+    stop.record()
+    torch.cuda.synchronize()
+    ctx.check()
+    ms = start.elapsed_time(stop) / steps
+    ctx.close()
+    n = max(steps // 2, 1)
+    tflops = G * b * step_flops_per_transition(A) / (ms * 1e-3) / 1e12
+    return {"workload": "grouped_g16_b64_a18_bf16", "value": round(G * b / (ms * 1e-3), 1),
+            "unit": "transitions/s", "ms_per_step": round(ms, 4), "tflops": round(tflops, 2),
+            "pct_mfma_peak": round(100 * tflops / FP32_MFMA_PEAK_TFLOPS, 2),
+            "stage_ms": {k: round(v[0] / n, 4) for k, v in prof.items()}}
+
+
 def cpu_baseline(datagen, B, A, seed, seconds):
     """The fp64 oracle (as it stands) running whole learner steps of the same
     batch-B workload on the host cores until `seconds` have passed."""
@@ -158,6 +199,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-b32", action="store_true", help="skip the batch-32 companion line")
+    ap.add_argument("--no-grouped", action="store_true",
+                    help="skip the 16-replica bf16 grouped-step companion line")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes three times "
                          "(calibrates the HBM traffic counters)")
@@ -224,6 +267,8 @@ def main():
                           "value": round(32 / (r32["ms_per_step"] * 1e-3), 1),
                           "ms_per_step": round(r32["ms_per_step"], 4), "tflops": round(t32, 3),
                           "pct_mfma_peak": round(100 * t32 / FP32_MFMA_PEAK_TFLOPS, 2)}
+    if not args.no_grouped:
+        out["grouped"] = run_grouped(torch, g, datagen, max(args.steps // 2, 5), args.warmup)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(datagen, B, A, seed, args.cpu_seconds)
     print(json.dumps(out), flush=True)

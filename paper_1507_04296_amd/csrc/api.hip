@@ -105,7 +105,7 @@ Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online = 1, int wi
     p.part2 = B ? take(4 * (size_t)WG_MAX_SPLITS * C2 * 16 * C1) : o;
     p.part3 = B ? take(4 * (size_t)WG_MAX_SPLITS * C3 * 9 * C2) : o;
     p.bpart = B ? take(4 * (size_t)3 * BIAS_PART_STRIDE) : o;
-    p.hpart = B ? take(4 * (size_t)HEAD_MAX_BLOCKS * HP_STRIDE) : o;
+    p.hpart = B ? take(4 * (size_t)online * HEAD_MAX_BLOCKS * HP_STRIDE) : o;
     p.total = o;
     return p;
 }
@@ -487,47 +487,45 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G,
     float* coef = at<float>(ctx, p.coef);
     float* q = at<float>(ctx, p.q);
     float* bpart = at<float>(ctx, p.bpart);
+    GroupPtrs on{}, w3d{}, w2p{};
     for (int g = 0; g < G; ++g) {
-        const int64_t r0 = (int64_t)g * b;  // first learner row of the group
-        const float* th_g = theta[g];
-        const float* on_part = fc1part + (int64_t)g * S * b * HID;
-        const float* tg_part = fc1part + (int64_t)(G + g) * S * b * HID;
-        {
-            StageTimer t(ctx, ST_HEAD);
-            launch_td_head(on_part, tg_part, S, th_g, theta_t, b, A, a + r0, r + r0, term + r0,
-                           gamma, clip_delta, h4 + r0 * HID, q + 2 * r0 * A, ell + r0, coef + r0,
-                           dz4 + r0 * HID, st);
-        }
-        float* grads = grads_out + (int64_t)g * P;
-        int head_blocks = 0, s1 = 0, s2 = 0, s3 = 0;
-        {
-            StageTimer t(ctx, ST_FC1_BWD);
-            head_blocks = launch_fc1_backward(dz4 + r0 * HID, th_g, h3 + r0 * FLAT, h4 + r0 * HID,
-                                              a + r0, coef + r0, ell + r0, b, A, dz3, grads,
-                                              at<float>(ctx, p.hpart), st);
-        }
-        {
-            StageTimer t(ctx, ST_CONV3_BWD);
-            s3 = launch_conv3_backward(dz3, wv[g].w3d, h2 + r0 * P2 * C2, b, dz2,
-                                       at<float>(ctx, p.part3), bpart + 2 * BIAS_PART_STRIDE, st);
-        }
-        {
-            StageTimer t(ctx, ST_CONV2_BWD);
-            s2 = launch_conv2_backward(dz2, wv[g].w2p, h1 + r0 * P1 * C1, b, dz1,
-                                       at<float>(ctx, p.part2), bpart + BIAS_PART_STRIDE, st);
-        }
-        {
-            StageTimer t(ctx, ST_CONV1_WGRAD);
-            launch_conv1_wgrad(dz1, ftab + r0 * 4, b, at<float>(ctx, p.part1), bpart,
-                               CONV1_WG_MAX_SPLITS, &s1, st);
-        }
-        {
-            StageTimer t(ctx, ST_GRAD_REDUCE);
-            ReduceArgs ra{at<float>(ctx, p.part1), at<float>(ctx, p.part2), at<float>(ctx, p.part3),
-                          bpart, at<float>(ctx, p.hpart), s1, s2, s3, head_blocks, b, A, grads,
-                          loss_out + g};
-            launch_grad_reduce(ra, st);
-        }
+        on.p[g] = theta[g];
+        w3d.p[g] = wv[g].w3d;
+        w2p.p[g] = wv[g].w2p;
+    }
+    const int64_t part_stride = (int64_t)S * b * HID;  // fc1 partials of one forward group
+    {
+        StageTimer t(ctx, ST_HEAD);
+        launch_td_head(fc1part, fc1part + G * part_stride, part_stride, S, on, G, theta_t, b, A, a,
+                       r, term, gamma, clip_delta, h4, q, ell, coef, dz4, st);
+    }
+    int head_blocks = 0, s1 = 0, s2 = 0, s3 = 0;
+    {
+        StageTimer t(ctx, ST_FC1_BWD);
+        head_blocks = launch_fc1_backward(dz4, on, G, h3, h4, a, coef, ell, b, A, dz3, grads_out, P,
+                                          at<float>(ctx, p.hpart), st);
+    }
+    {
+        StageTimer t(ctx, ST_CONV3_BWD);
+        s3 = launch_conv3_backward(dz3, w3d, G, h2, b, dz2, at<float>(ctx, p.part3),
+                                   bpart + 2 * BIAS_PART_STRIDE, st);
+    }
+    {
+        StageTimer t(ctx, ST_CONV2_BWD);
+        s2 = launch_conv2_backward(dz2, w2p, G, h1, b, dz1, at<float>(ctx, p.part2),
+                                   bpart + BIAS_PART_STRIDE, st);
+    }
+    {
+        StageTimer t(ctx, ST_CONV1_WGRAD);
+        launch_conv1_wgrad(dz1, ftab, G, b, at<float>(ctx, p.part1), bpart, CONV1_WG_MAX_SPLITS,
+                           &s1, st);
+    }
+    {
+        StageTimer t(ctx, ST_GRAD_REDUCE);
+        ReduceArgs ra{at<float>(ctx, p.part1), at<float>(ctx, p.part2), at<float>(ctx, p.part3),
+                      bpart, at<float>(ctx, p.hpart), s1, s2, s3, head_blocks, b, A, G, P,
+                      grads_out, loss_out};
+        launch_grad_reduce(ra, st);
     }
     return check_launch();
 }

@@ -123,35 +123,39 @@ struct Conv1WgradJob {
     const uint8_t* const* ftab;
     float* partial;
     float* bias_part;
-    int n, splits, cps;
+    int n, splits, cps, groups;
     using SH = GemmShape<32, C1W_BN, RMAJ, RMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     static constexpr int NCT = 256 / C1W_BN;
-    __host__ __device__ int blocks() const { return pad_xcd(NCT * splits); }
+    __host__ __device__ int blocks() const { return pad_xcd(NCT * splits * groups); }
     __device__ void run(int bid, float* smem) const {
         const int t = xcd_tile(bid, blocks());
-        if (t >= NCT * splits) return;
-        const int col0 = (t % NCT) * C1W_BN, split = t / NCT;  // column tiles of a split adjacent
+        if (t >= NCT * splits * groups) return;
+        // column tiles of a split adjacent; split runs over (group, split)
+        const int col0 = (t % NCT) * C1W_BN, split = t / NCT, g = split / splits;
         const int npix = n * P1;
         const int nchunks = (npix + BK - 1) / BK;
-        const int kc0 = split * cps, kc1 = min(nchunks, kc0 + cps);
-        Conv1WgradA la{dz1, npix};
-        Conv1WgradB lb{ftab, (const uint8_t*)dz1, npix, col0};
+        const int ks = split - g * splits;
+        const int kc0 = ks * cps, kc1 = min(nchunks, kc0 + cps);
+        const int64_t rows = (int64_t)g * n;
+        Conv1WgradA la{dz1 + rows * P1 * C1, npix};
+        Conv1WgradB lb{ftab + rows * 4, (const uint8_t*)dz1, npix, col0};
         PartialEpi epi{partial + (int64_t)split * C1 * 256, 256, col0, 1.0f / 255.0f};
         float* rs = col0 == 0 ? bias_part + (int64_t)split * 64 : nullptr;
         mfma_gemm<32, C1W_BN, 1, RMAJ, RMAJ>(smem, kc0, kc1, la, lb, epi, rs);
     }
 };
 
-void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int n, float* partial,
-                        float* bias_part, int max_splits, int* splits_out, hipStream_t st) {
+void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int groups, int n,
+                        float* partial, float* bias_part, int max_splits, int* splits_out,
+                        hipStream_t st) {
     const int nchunks = (n * P1 + BK - 1) / BK;
-    int splits = min(max_splits, max(1, TARGET_WGS / (256 / C1W_BN)));
+    int splits = max(1, min(max_splits, TARGET_WGS / (256 / C1W_BN)) / groups);
     splits = min(splits, nchunks);
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
     *splits_out = splits;
-    launch_jobs(st, Conv1WgradJob{dz1, ftab, partial, bias_part, n, splits, cps});
+    launch_jobs(st, Conv1WgradJob{dz1, ftab, partial, bias_part, n, splits, cps, groups});
 }
 
 }  // namespace gorila

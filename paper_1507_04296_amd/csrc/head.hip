@@ -94,22 +94,28 @@ void launch_act_head(const float* fc1part, int splits, const float* theta, int n
                                                seed);
 }
 
-// fc1part_online / fc1part_target: [splits][n][512] for the online (on s) and
-// the target (on s') network.
+// Learner group g (blockIdx.y) owns rows g*n .. g*n+n-1 of a, r, term, h4,
+// ell, coef and dz4, and rows 2gn .. 2gn+2n-1 of q (online, then target).
+// fc1part_online / fc1part_target + g * part_stride: [splits][n][512] for the
+// group's online network (on s) and the target network (on s').
 __global__ __launch_bounds__(256) void td_head_kernel(
-    const float* __restrict__ fc1part, const float* __restrict__ fc1part_t, int splits,
-    const float* __restrict__ theta,
-    const float* __restrict__ theta_t, int n, int A, const int32_t* __restrict__ a,
-    const float* __restrict__ r, const uint8_t* __restrict__ term, float gamma, float clip,
-    float* __restrict__ h4, float* __restrict__ q, float* __restrict__ ell,
-    float* __restrict__ coef, float* __restrict__ dz4) {
-    const int lane = threadIdx.x & 63, b = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (b >= n) return;
+    const float* __restrict__ fc1part, const float* __restrict__ fc1part_t, int64_t part_stride,
+    int splits, GroupPtrs thetas, const float* __restrict__ theta_t, int n, int A,
+    const int32_t* __restrict__ a, const float* __restrict__ r, const uint8_t* __restrict__ term,
+    float gamma, float clip, float* __restrict__ h4, float* __restrict__ q,
+    float* __restrict__ ell, float* __restrict__ coef, float* __restrict__ dz4) {
+    const int lane = threadIdx.x & 63, bl = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (bl >= n) return;
+    const int grp = blockIdx.y;
+    const float* theta = thetas.p[grp];
     const int64_t ss = (int64_t)n * HID;
     float h[8], ht[8];
-    finish_h4(fc1part + (int64_t)b * HID, splits, ss, theta + OFF_B4, lane, h);
-    finish_h4(fc1part_t + (int64_t)b * HID, splits, ss, theta_t + OFF_B4, lane, ht);
-    float* h4row = h4 + (int64_t)b * HID + lane * 8;
+    finish_h4(fc1part + grp * part_stride + (int64_t)bl * HID, splits, ss, theta + OFF_B4, lane, h);
+    finish_h4(fc1part_t + grp * part_stride + (int64_t)bl * HID, splits, ss, theta_t + OFF_B4, lane,
+              ht);
+    const int64_t b = (int64_t)grp * n + bl;  // learner row
+    q += (int64_t)grp * 2 * n * A;
+    float* h4row = h4 + b * HID + lane * 8;
     *(f32x4*)h4row = f32x4{h[0], h[1], h[2], h[3]};
     *(f32x4*)(h4row + 4) = f32x4{h[4], h[5], h[6], h[7]};
     const float* W5 = theta + OFF_W5;
@@ -122,8 +128,8 @@ __global__ __launch_bounds__(256) void td_head_kernel(
         const float s = wave_sum(dot8(h, W5 + k * HID + lane * 8)) + b5[k];
         const float st = wave_sum(dot8(ht, W5t + k * HID + lane * 8)) + b5t[k];
         if (lane == 0) {
-            q[(int64_t)b * A + k] = s;
-            q[(int64_t)(n + b) * A + k] = st;
+            q[(int64_t)bl * A + k] = s;
+            q[(int64_t)(n + bl) * A + k] = st;
         }
         if (k == ab) q_sa = s;
         m = k == 0 ? st : fmaxf(m, st);  // max_a' Q(s', a'; theta-)
@@ -138,7 +144,7 @@ __global__ __launch_bounds__(256) void td_head_kernel(
         coef[b] = cf;
     }
     const float* w = W5 + ab * HID + lane * 8;
-    float* out = dz4 + (int64_t)b * HID + lane * 8;
+    float* out = dz4 + b * HID + lane * 8;
     const f32x4 w0 = ld4(w), w1 = ld4(w + 4);
     const f32x4 o0 = {h[0] > 0.f ? cf * w0[0] : 0.f, h[1] > 0.f ? cf * w0[1] : 0.f,
                       h[2] > 0.f ? cf * w0[2] : 0.f, h[3] > 0.f ? cf * w0[3] : 0.f};
@@ -148,14 +154,15 @@ __global__ __launch_bounds__(256) void td_head_kernel(
     *(f32x4*)(out + 4) = o1;
 }
 
-void launch_td_head(const float* fc1part_online, const float* fc1part_target, int splits,
-                    const float* theta, const float* theta_target, int n, int A, const int32_t* a,
-                    const float* r, const uint8_t* term, float gamma, float clip, float* h4,
-                    float* q, float* ell, float* coef, float* dz4, hipStream_t st) {
+void launch_td_head(const float* fc1part_online, const float* fc1part_target, int64_t part_stride,
+                    int splits, const GroupPtrs& thetas, int groups, const float* theta_target,
+                    int n, int A, const int32_t* a, const float* r, const uint8_t* term,
+                    float gamma, float clip, float* h4, float* q, float* ell, float* coef,
+                    float* dz4, hipStream_t st) {
     if (n <= 0) return;
-    td_head_kernel<<<(n + 3) / 4, 256, 0, st>>>(fc1part_online, fc1part_target, splits, theta,
-                                                theta_target, n, A, a, r, term, gamma, clip, h4, q,
-                                                ell, coef, dz4);
+    td_head_kernel<<<dim3((n + 3) / 4, groups), 256, 0, st>>>(
+        fc1part_online, fc1part_target, part_stride, splits, thetas, theta_target, n, A, a, r, term,
+        gamma, clip, h4, q, ell, coef, dz4);
 }
 
 }  // namespace gorila

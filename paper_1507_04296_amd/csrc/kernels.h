@@ -78,37 +78,48 @@ void launch_q_head(const float* fc1part, int splits, const float* theta, int n, 
 void launch_act_head(const float* fc1part, int splits, const float* theta, int n, int A, float eps,
                      uint64_t seed, int32_t* actions, float* q_out, hipStream_t st);
 // Writes h4 (online rows), q [2n][A], ell, coef = dLoss/dQ(s,a) and dz4.
-// fc1part_online / fc1part_target each hold [splits][n][512].
-void launch_td_head(const float* fc1part_online, const float* fc1part_target, int splits,
-                    const float* theta, const float* theta_target, int n, int A, const int32_t* a,
-                    const float* r, const uint8_t* term, float gamma, float clip, float* h4,
-                    float* q, float* ell, float* coef, float* dz4, hipStream_t st);
+// `groups` learner groups of n rows each (group g: rows g*n .. g*n+n-1, online
+// parameters thetas.p[g]); fc1part_online / fc1part_target + g * part_stride
+// each hold [splits][n][512] for group g.
+void launch_td_head(const float* fc1part_online, const float* fc1part_target, int64_t part_stride,
+                    int splits, const GroupPtrs& thetas, int groups, const float* theta_target,
+                    int n, int A, const int32_t* a, const float* r, const uint8_t* term,
+                    float gamma, float clip, float* h4, float* q, float* ell, float* coef,
+                    float* dz4, hipStream_t st);
 
-// Backward, three launches of independent jobs each:
-//  fc1: dz3 = [h3 > 0] W4^T dz4 (stored [b][p][o]), dW4 and db4 into grads,
-//       and row-block partials of dW5, db5 and the loss (returns #row blocks);
-//  conv3: dz2 and split partials of dW3 / db3 (returns #splits);
-//  conv2: dz1 and split partials of dW2 / db2 (returns #splits).
-int launch_fc1_backward(const float* dz4, const float* theta, const float* h3, const float* h4,
-                        const int32_t* a, const float* coef, const float* ell, int n, int A,
-                        float* dz3, float* grads, float* hpart, hipStream_t st);
-int launch_conv3_backward(const float* dz3, const float* w3d, const float* h2, int n, float* dz2,
-                          float* partial, float* bias_part, hipStream_t st);
-int launch_conv2_backward(const float* dz2, const float* w2p, const float* h1, int n, float* dz1,
-                          float* partial, float* bias_part, hipStream_t st);
-void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int n, float* partial,
-                        float* bias_part, int max_splits, int* splits_out, hipStream_t st);
-// Conv weight-gradient partials [split][o][(tap, c)], bias partials
-// bias_part[layer][split][64] (one row per split, written by the weight-gradient
-// workgroups of column tile 0) and the head partials hpart[block][HP_STRIDE],
-// each summed in split / block order into grads and loss_out.
+// Backward of `groups` learner groups of n rows each (group g: rows
+// g*n .. g*n+n-1 of every per-sample tensor, parameters of set g), three
+// launches of independent jobs each:
+//  fc1: dz3 = [h3 > 0] W4^T dz4 (stored [b][p][o]), dW4 and db4 into
+//       grads + g * grads_stride, and row-block partials of dW5, db5 and the
+//       loss (returns row blocks per group);
+//  conv3: dz2 and split partials of dW3 / db3 (returns splits per group);
+//  conv2: dz1 and split partials of dW2 / db2 (returns splits per group).
+int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, int groups, const float* h3,
+                        const float* h4, const int32_t* a, const float* coef, const float* ell,
+                        int n, int A, float* dz3, float* grads, int64_t grads_stride,
+                        float* hpart, hipStream_t st);
+int launch_conv3_backward(const float* dz3, const GroupPtrs& w3d, int groups, const float* h2,
+                          int n, float* dz2, float* partial, float* bias_part, hipStream_t st);
+int launch_conv2_backward(const float* dz2, const GroupPtrs& w2p, int groups, const float* h1,
+                          int n, float* dz1, float* partial, float* bias_part, hipStream_t st);
+// ftab: [groups * n][4] frame pointers of the online states.
+void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int groups, int n,
+                        float* partial, float* bias_part, int max_splits, int* splits_out,
+                        hipStream_t st);
+// Conv weight-gradient partials [group][split][o][(tap, c)], bias partials
+// bias_part[layer][group][split][64] (one row per split, written by the
+// weight-gradient workgroups of column tile 0) and the head partials
+// hpart[group][block][HP_STRIDE], each summed in split / block order into
+// grads + g * grads_stride and loss_out[g].
 struct ReduceArgs {
     const float* part1;
     const float* part2;
     const float* part3;
     const float* bias_part;
     const float* hpart;
-    int s1, s2, s3, head_blocks, n, A;
+    int s1, s2, s3, head_blocks, n, A, groups;
+    int64_t grads_stride;
     float* grads;
     float* loss_out;
 };
@@ -122,7 +133,7 @@ constexpr int CONV3_WG_SPLITS = 114;         // 9 column tiles x 114 splits ~ 10
 constexpr int CONV2_WG_SPLITS = 64;          // 8 column tiles x 64 splits
 constexpr int CONV1_WG_MAX_SPLITS = 512;
 constexpr int BIAS_PART_STRIDE = 512 * 64;  // floats per layer in bias_part
-constexpr int HEAD_MAX_BLOCKS = 16;          // row blocks of the head partials
+constexpr int HEAD_MAX_BLOCKS = 16;          // row blocks of the head partials, per group
 constexpr int HP_DB5 = MAX_ACTIONS * HID;    // offsets inside one head partial
 constexpr int HP_LOSS = HP_DB5 + MAX_ACTIONS;
 constexpr int HP_STRIDE = HP_LOSS + 32;

@@ -294,22 +294,25 @@ struct Dz3NhwcStore {
 
 struct Fc1DgradJob {
     const float* dz4;
-    const float* W4;
+    GroupPtrs theta;
     const float* h3;
     float* dz3;
-    int n;
+    int n, groups;
     using SH = GemmShape<64, 64, KMAJ, RMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return ((n + 63) / 64) * (FLAT / 64); }
-    __host__ __device__ int blocks() const { return pad_xcd(tiles()); }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
     __device__ void run(int bid, float* smem) const {
-        const int t = xcd_tile(bid, blocks());
-        if (t >= tiles()) return;
+        int t = xcd_tile(bid, blocks());
+        if (t >= tiles() * groups) return;
+        const int g = t / tiles();
+        t -= g * tiles();
         const int mt = (n + 63) / 64;
         const int r0 = (t % mt) * 64, c0 = (t / mt) * 64;  // row tiles of one W4 column block adjacent
-        RowMajorK la{dz4, n, r0, HID};
-        RowMajorR lb{W4, c0, FLAT, HID};
-        Dz3NhwcStore epi{dz3, h3, n, r0, c0};
+        const int64_t rows = (int64_t)g * n;
+        RowMajorK la{dz4 + rows * HID, n, r0, HID};
+        RowMajorR lb{theta.p[g] + OFF_W4, c0, FLAT, HID};
+        Dz3NhwcStore epi{dz3 + rows * FLAT, h3 + rows * FLAT, n, r0, c0};
         mfma_gemm<64, 64, 2, KMAJ, RMAJ>(smem, 0, HID / BK, la, lb, epi);
     }
 };
@@ -321,22 +324,26 @@ struct Fc1DgradJob {
 struct Fc1WgradJob {
     const float* dz4;
     const float* h3;
-    float* gW4;
-    float* gb4;
-    int n;
+    float* grads;
+    int64_t grads_stride;
+    int n, groups;
     using SH = GemmShape<64, 64, RMAJ, RMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return (HID / 64) * (FLAT / 64); }
-    __host__ __device__ int blocks() const { return pad_xcd(tiles()); }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
     __device__ void run(int bid, float* smem) const {
-        const int t = xcd_tile(bid, blocks());
-        if (t >= tiles()) return;
+        int t = xcd_tile(bid, blocks());
+        if (t >= tiles() * groups) return;
+        const int g = t / tiles();
+        t -= g * tiles();
         const int r0 = (t % (HID / 64)) * 64, c0 = (t / (HID / 64)) * 64;
-        RowMajorR la{dz4, r0, HID, n};
-        RowMajorR lb{h3, c0, FLAT, n};
-        PlainStore epi{gW4, HID, r0, c0, FLAT};
+        const int64_t rows = (int64_t)g * n;
+        float* gr = grads + g * grads_stride;
+        RowMajorR la{dz4 + rows * HID, r0, HID, n};
+        RowMajorR lb{h3 + rows * FLAT, c0, FLAT, n};
+        PlainStore epi{gr + OFF_W4, HID, r0, c0, FLAT};
         // db4[o] = sum_b dz4[b][o]: the row sums of this GEMM's A operand
-        float* rs = c0 == 0 ? gb4 + r0 : nullptr;
+        float* rs = c0 == 0 ? gr + OFF_B4 + r0 : nullptr;
         mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, 0, (n + BK - 1) / BK, la, lb, epi, rs);
     }
 };
@@ -355,17 +362,19 @@ struct HeadPartialJob {
     const float* coef;
     const float* ell;
     float* hpart;
-    int n, A, rows_per_block, row_blocks;
+    int n, A, rows_per_block, row_blocks, groups;
     static constexpr int SMEM = 4 * MAX_ACTIONS * 64;
-    __host__ __device__ int blocks() const { return pad_xcd((HID / 64) * row_blocks); }
+    __host__ __device__ int blocks() const { return pad_xcd((HID / 64) * row_blocks * groups); }
     __device__ void run(int bid, float* smem) const {
-        if (bid >= (HID / 64) * row_blocks) return;
+        if (bid >= (HID / 64) * row_blocks * groups) return;
         float (*sacc)[MAX_ACTIONS][64] = (float (*)[MAX_ACTIONS][64])smem;
         const int tid = threadIdx.x, kl = tid & 63, bq = tid >> 6;
-        const int kt = bid % (HID / 64), bb = bid / (HID / 64);
+        const int kt = bid % (HID / 64), gbb = bid / (HID / 64);
+        const int g = gbb / row_blocks, bb = gbb - g * row_blocks;
         const int k = kt * 64 + kl;
-        const int b0 = bb * rows_per_block, b1 = min(n, b0 + rows_per_block);
-        float* out = hpart + (int64_t)bb * HP_STRIDE;
+        // rows of group g, block bb (learner rows g*n + b0 .. g*n + b1 - 1)
+        const int b0 = g * n + bb * rows_per_block, b1 = g * n + min(n, (bb + 1) * rows_per_block);
+        float* out = hpart + (int64_t)gbb * HP_STRIDE;
         for (int j = 0; j < A; ++j) sacc[bq][j][kl] = 0.0f;
         for (int b = b0 + bq; b < b1; b += 4) {
             const int ab = a[b];
@@ -397,15 +406,16 @@ struct HeadPartialJob {
     }
 };
 
-int launch_fc1_backward(const float* dz4, const float* theta, const float* h3, const float* h4,
-                        const int32_t* a, const float* coef, const float* ell, int n, int A,
-                        float* dz3, float* grads, float* hpart, hipStream_t st) {
+int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, int groups, const float* h3,
+                        const float* h4, const int32_t* a, const float* coef, const float* ell,
+                        int n, int A, float* dz3, float* grads, int64_t grads_stride,
+                        float* hpart, hipStream_t st) {
     if (n <= 0) return 0;
     const int rows = max(32, (n + HEAD_MAX_BLOCKS - 1) / HEAD_MAX_BLOCKS);
     const int row_blocks = (n + rows - 1) / rows;
-    launch_jobs(st, Fc1DgradJob{dz4, theta + OFF_W4, h3, dz3, n},
-                Fc1WgradJob{dz4, h3, grads + OFF_W4, grads + OFF_B4, n},
-                HeadPartialJob{h4, a, coef, ell, hpart, n, A, rows, row_blocks});
+    launch_jobs(st, Fc1DgradJob{dz4, theta, h3, dz3, n, groups},
+                Fc1WgradJob{dz4, h3, grads, grads_stride, n, groups},
+                HeadPartialJob{h4, a, coef, ell, hpart, n, A, rows, row_blocks, groups});
     return row_blocks;
 }
 
@@ -459,24 +469,27 @@ struct Conv3DgradStore {
 
 struct Conv3DgradJob {
     const float* dz3;
-    const float* w3d;
+    GroupPtrs w3d;
     const float* h2;
     float* dz2;
-    int n;
+    int n, groups;
     using SH = GemmShape<64, 64, KMAJ, KMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return P2 * ((n + 63) / 64); }
-    __host__ __device__ int blocks() const { return pad_xcd(tiles()); }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
     __device__ void run(int bid, float* smem) const {
-        const int t = xcd_tile(bid, blocks());
-        if (t >= tiles()) return;
+        int t = xcd_tile(bid, blocks());
+        if (t >= tiles() * groups) return;
+        const int g = t / tiles();
+        t -= g * tiles();
+        const int64_t rows = (int64_t)g * n;
         const int pos = t % P2, y = pos / H2, x = pos - y * H2, b0 = (t / P2) * 64;
         const int u0 = max(0, y - (H3 - 1)), u1 = min(K3 - 1, y);
         const int v0 = max(0, x - (H3 - 1)), v1 = min(K3 - 1, x);
         const int nv = v1 - v0 + 1, taps = (u1 - u0 + 1) * nv;
-        Conv3DgradA la{dz3, n, b0, y, x, u0, v0, nv};
-        Conv3DgradB lb{w3d, u0, v0, nv};
-        Conv3DgradStore epi{dz2, h2, n, b0, pos};
+        Conv3DgradA la{dz3 + rows * FLAT, n, b0, y, x, u0, v0, nv};
+        Conv3DgradB lb{w3d.p[g], u0, v0, nv};
+        Conv3DgradStore epi{dz2 + rows * P2 * C2, h2 + rows * P2 * C2, n, b0, pos};
         mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, 0, 2 * taps, la, lb, epi);
     }
 };
@@ -516,32 +529,37 @@ struct Conv3WgradJob {
     const float* h2;
     float* partial;
     float* bias_part;
-    int n, splits, cps;
+    int n, splits, cps, groups;
     using SH = GemmShape<64, 64, RMAJ, RMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
-    __host__ __device__ int blocks() const { return pad_xcd(9 * splits); }
+    __host__ __device__ int blocks() const { return pad_xcd(9 * splits * groups); }
     __device__ void run(int bid, float* smem) const {
         const int t = xcd_tile(bid, blocks());
-        if (t >= 9 * splits) return;
-        const int tap = t % 9, s = t / 9;  // the nine taps of one split share dz3 rows
+        if (t >= 9 * splits * groups) return;
+        // the nine taps of one split share dz3 rows; s runs over (group, split)
+        const int tap = t % 9, s = t / 9, g = s / splits;
         const int npix = n * P3, nchunks = (npix + BK - 1) / BK;
-        Conv3WgradA la{dz3, npix};
-        Conv3WgradB lb{h2, npix, tap};
+        const int64_t rows = (int64_t)g * n;
+        const int ks = s - g * splits;
+        Conv3WgradA la{dz3 + rows * FLAT, npix};
+        Conv3WgradB lb{h2 + rows * P2 * C2, npix, tap};
         PartialEpi epi{partial + (int64_t)s * C3 * 9 * C2, 9 * C2, tap * C2, 1.0f};
         float* rs = tap == 0 ? bias_part + (int64_t)s * 64 : nullptr;
-        mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, s * cps, min(nchunks, (s + 1) * cps), la, lb, epi, rs);
+        mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, ks * cps, min(nchunks, (ks + 1) * cps), la, lb, epi, rs);
     }
 };
 
-int launch_conv3_backward(const float* dz3, const float* w3d, const float* h2, int n, float* dz2,
-                          float* partial, float* bias_part, hipStream_t st) {
+// Splits per group shrink with the group count so one launch stays near the
+// same number of workgroups; groups * splits stays within WG_MAX_SPLITS.
+int launch_conv3_backward(const float* dz3, const GroupPtrs& w3d, int groups, const float* h2,
+                          int n, float* dz2, float* partial, float* bias_part, hipStream_t st) {
     if (n <= 0) return 0;
     const int nchunks = (n * P3 + BK - 1) / BK;
-    int splits = min(min(WG_MAX_SPLITS, nchunks), CONV3_WG_SPLITS);
+    int splits = min(min(WG_MAX_SPLITS / groups, nchunks), max(1, CONV3_WG_SPLITS / groups));
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
-    launch_jobs(st, Conv3DgradJob{dz3, w3d, h2, dz2, n},
-                Conv3WgradJob{dz3, h2, partial, bias_part, n, splits, cps});
+    launch_jobs(st, Conv3DgradJob{dz3, w3d, h2, dz2, n, groups},
+                Conv3WgradJob{dz3, h2, partial, bias_part, n, splits, cps, groups});
     return splits;
 }
 
@@ -602,25 +620,28 @@ struct Conv2DgradStore {
 
 struct Conv2DgradJob {
     const float* dz2;
-    const float* w2p;
+    GroupPtrs w2p;
     const float* h1;
     float* dz1;
-    int n;
+    int n, groups;
     using SH = GemmShape<64, 128, KMAJ, KMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return 100 * ((n + 63) / 64); }
-    __host__ __device__ int blocks() const { return pad_xcd(tiles()); }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
     __device__ void run(int bid, float* smem) const {
-        const int t = xcd_tile(bid, blocks());
-        if (t >= tiles()) return;
+        int t = xcd_tile(bid, blocks());
+        if (t >= tiles() * groups) return;
+        const int g = t / tiles();
+        t -= g * tiles();
+        const int64_t rows = (int64_t)g * n;
         const int pos = t % 100, b0 = (t / 100) * 64;  // neighbouring positions adjacent
         const int yy = pos / 10, xx = pos % 10;
         const int du0 = max(0, yy - (H2 - 1)), du1 = min(1, yy);
         const int dv0 = max(0, xx - (H2 - 1)), dv1 = min(1, xx);
         const int ndv = dv1 - dv0 + 1, taps = (du1 - du0 + 1) * ndv;
-        Conv2DgradA la{dz2, n, b0, yy, xx, du0, dv0, ndv};
-        Conv2DgradB lb{w2p, du0, dv0, ndv};
-        Conv2DgradStore epi{dz1, h1, n, b0, yy, xx};
+        Conv2DgradA la{dz2 + rows * P2 * C2, n, b0, yy, xx, du0, dv0, ndv};
+        Conv2DgradB lb{w2p.p[g], du0, dv0, ndv};
+        Conv2DgradStore epi{dz1 + rows * P1 * C1, h1 + rows * P1 * C1, n, b0, yy, xx};
         mfma_gemm<64, 128, 2, KMAJ, KMAJ>(smem, 0, 2 * taps, la, lb, epi);
     }
 };
@@ -662,32 +683,35 @@ struct Conv2WgradJob {
     const float* h1;
     float* partial;
     float* bias_part;
-    int n, splits, cps;
+    int n, splits, cps, groups;
     using SH = GemmShape<64, 64, RMAJ, RMAJ>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
-    __host__ __device__ int blocks() const { return pad_xcd(8 * splits); }
+    __host__ __device__ int blocks() const { return pad_xcd(8 * splits * groups); }
     __device__ void run(int bid, float* smem) const {
         const int t = xcd_tile(bid, blocks());
-        if (t >= 8 * splits) return;
-        const int tap0 = (t % 8) * 2, s = t / 8;  // the column tiles of one split share dz2 rows
+        if (t >= 8 * splits * groups) return;
+        // the column tiles of one split share dz2 rows; s runs over (group, split)
+        const int tap0 = (t % 8) * 2, s = t / 8, g = s / splits;
         const int npix = n * P2, nchunks = (npix + BK - 1) / BK;
-        Conv2WgradA la{dz2, npix};
-        Conv2WgradB lb{h1, npix, tap0};
+        const int64_t rows = (int64_t)g * n;
+        const int ks = s - g * splits;
+        Conv2WgradA la{dz2 + rows * P2 * C2, npix};
+        Conv2WgradB lb{h1 + rows * P1 * C1, npix, tap0};
         PartialEpi epi{partial + (int64_t)s * C2 * 16 * C1, 16 * C1, tap0 * C1, 1.0f};
         float* rs = tap0 == 0 ? bias_part + (int64_t)s * 64 : nullptr;
-        mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, s * cps, min(nchunks, (s + 1) * cps), la, lb, epi, rs);
+        mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, ks * cps, min(nchunks, (ks + 1) * cps), la, lb, epi, rs);
     }
 };
 
-int launch_conv2_backward(const float* dz2, const float* w2p, const float* h1, int n, float* dz1,
-                          float* partial, float* bias_part, hipStream_t st) {
+int launch_conv2_backward(const float* dz2, const GroupPtrs& w2p, int groups, const float* h1,
+                          int n, float* dz1, float* partial, float* bias_part, hipStream_t st) {
     if (n <= 0) return 0;
     const int nchunks = (n * P2 + BK - 1) / BK;
-    int splits = min(min(WG_MAX_SPLITS, nchunks), CONV2_WG_SPLITS);
+    int splits = min(min(WG_MAX_SPLITS / groups, nchunks), max(1, CONV2_WG_SPLITS / groups));
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
-    launch_jobs(st, Conv2DgradJob{dz2, w2p, h1, dz1, n},
-                Conv2WgradJob{dz2, h1, partial, bias_part, n, splits, cps});
+    launch_jobs(st, Conv2DgradJob{dz2, w2p, h1, dz1, n, groups},
+                Conv2WgradJob{dz2, h1, partial, bias_part, n, splits, cps, groups});
     return splits;
 }
 
@@ -712,6 +736,14 @@ __global__ __launch_bounds__(256) void grad_reduce_kernel(ReduceArgs ra) {
     __shared__ float red[4][64];
     const int el = threadIdx.x & 63, sq = threadIdx.x >> 6;
     const int e = blockIdx.x * 64 + el;
+    // learner group blockIdx.y: its own partial blocks, gradient and loss
+    const int g = blockIdx.y;
+    ra.part1 += (int64_t)g * ra.s1 * N1;
+    ra.part2 += (int64_t)g * ra.s2 * N2;
+    ra.part3 += (int64_t)g * ra.s3 * N3;
+    ra.hpart += (int64_t)g * ra.head_blocks * HP_STRIDE;
+    ra.grads += g * ra.grads_stride;
+    ra.loss_out += g;
     const float* src = nullptr;
     int nsplit = 0, stride = 0;
     float* dst = nullptr;
@@ -733,8 +765,8 @@ __global__ __launch_bounds__(256) void grad_reduce_kernel(ReduceArgs ra) {
         int layer = 2, o = q - C1 - C2;
         if (q < C1) { layer = 0; o = q; }
         else if (q < C1 + C2) { layer = 1; o = q - C1; }
-        src = ra.bias_part + (int64_t)layer * BIAS_PART_STRIDE + o;
         nsplit = layer == 0 ? ra.s1 : layer == 1 ? ra.s2 : ra.s3;
+        src = ra.bias_part + (int64_t)layer * BIAS_PART_STRIDE + (int64_t)g * nsplit * 64 + o;
         stride = 64;
         dst = ra.grads + (layer == 0 ? OFF_B1 : layer == 1 ? OFF_B2 : OFF_B3) + o;
     } else if (e < E2) {
@@ -762,7 +794,7 @@ __global__ __launch_bounds__(256) void grad_reduce_kernel(ReduceArgs ra) {
 
 void launch_grad_reduce(const ReduceArgs& ra, hipStream_t st) {
     const int total = C1 * 256 + C2 * 16 * C1 + C3 * 9 * C2 + C1 + C2 + C3 + ra.A * HID + ra.A + 1;
-    grad_reduce_kernel<<<(total + 63) / 64, 256, 0, st>>>(ra);
+    grad_reduce_kernel<<<dim3((total + 63) / 64, ra.groups), 256, 0, st>>>(ra);
 }
 
 }  // namespace gorila
