@@ -87,7 +87,32 @@ def stored_traffic(stage: str, B: int, A: int):
             k["write_kib"] / prof["copy_write_factor"]) * 1024.0
 
 
-def run_learner(torch, g, datagen, B, A, seed, steps, warmup, timed_stage=None):
+def step_percentiles(torch, fn, steps):
+    """p10 / p50 / p90 of per-call times (ms): one event between consecutive
+    calls on the current stream (a separate pass from the headline timing)."""
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    evs[0].record()
+    for i in range(steps):
+        fn()
+        evs[i + 1].record()
+    torch.cuda.synchronize()
+    per = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(steps)])
+    return [round(float(x), 4) for x in np.percentile(per, [10, 50, 90])]
+
+
+def time_region(torch, fn, steps):
+    """Mean ms per call over `steps` calls bracketed by two events."""
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        fn()
+    stop.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(stop) / steps
+
+
+def run_learner(torch, g, datagen, B, A, seed, steps, warmup, timed_stage=None, graph=False):
     inp = datagen.learner_inputs(seed, B, A)
     dev = torch.device("cuda:0")
     t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
@@ -123,9 +148,22 @@ def run_learner(torch, g, datagen, B, A, seed, steps, warmup, timed_stage=None):
     dom = ctx.timing_end()[dominant]
     ctx.check()
     ms_total = start.elapsed_time(stop)
+    pct = step_percentiles(torch, step, steps)
+    graph_ms = None
+    if graph:
+        # the same step captured once into a HIP graph and replayed
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            step()
+        for _ in range(warmup):
+            gr.replay()
+        graph_ms = time_region(torch, gr.replay, steps)
+        ctx.bind_stream()
+        ctx.check()
     ctx.close()
     return dict(inp=inp, ms_per_step=ms_total / steps, wall_s=wall, prof=prof, dominant=dominant,
-                dominant_ms=dom[0] / max(dom[1], 1), dominant_launches=dom[1])
+                dominant_ms=dom[0] / max(dom[1], 1), dominant_launches=dom[1], pct=pct,
+                graph_ms=graph_ms)
 
 
 def run_grouped(torch, g, datagen, steps, warmup):
@@ -169,6 +207,80 @@ def run_grouped(torch, g, datagen, steps, warmup):
             "stage_ms": {k: round(v[0] / n, 4) for k, v in prof.items()}}
 
 
+def run_actor(torch, g, datagen, steps, warmup):
+    """Actor inference: Q forward + epsilon-greedy for 1024 environments, 18 actions."""
+    w = datagen.WORKLOADS["actor_n1024_a18_f32"]
+    n, A = w["n"], w["n_actions"]
+    inp = datagen.actor_inputs(w["seed"], n, A, w["eps"])
+    dev = torch.device("cuda:0")
+    theta = torch.from_numpy(inp.theta).to(dev)
+    states = torch.from_numpy(np.ascontiguousarray(inp.states)).to(dev)
+    ctx = g.Context((n + 1) // 2, A, device=dev)
+    acts = torch.empty(n, dtype=torch.int32, device=dev)
+    q = torch.empty((n, A), dtype=torch.float32, device=dev)
+    call = lambda: g.gorila_act(ctx, theta, A, states, inp.eps, inp.seed, acts, q)
+    for _ in range(warmup):
+        call()
+    ctx.check()
+    ms = time_region(torch, call, steps)
+    ctx.check()
+    ctx.close()
+    flops = n * 2 * (MAC_CONV1 + MAC_CONV2 + MAC_CONV3 + MAC_FC1 + 512 * A)
+    tf = flops / (ms * 1e-3) / 1e12
+    return {"workload": "actor_n1024_a18_f32", "value": round(n / (ms * 1e-3), 1),
+            "unit": "envs/s", "ms_per_call": round(ms, 4), "tflops": round(tf, 2),
+            "pct_mfma_peak": round(100 * tf / FP32_MFMA_PEAK_TFLOPS, 2)}
+
+
+def run_ring(torch, g, datagen, steps, warmup):
+    """One-million-frame replay ring: the 256-index gather alone (bytes moved
+    against HBM peak) and the batch-256 learner step reading the ring."""
+    w = datagen.WORKLOADS["ring1m_gather_learner_b256_a18_f32"]
+    B, A, cap = w["batch"], w["n_actions"], w["capacity"]
+    rng = np.random.default_rng(w["seed"])
+    r = datagen.ring_inputs(rng, cap, A)
+    dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    rep = g.Replay.ring(t(r.frames), t(r.ep_start), t(r.action), t(r.reward), r.head)
+    del r
+    idx = t(rng.integers(0, cap - 1, B).astype(np.int64))
+    ctx = g.Context(B, A, device=dev)
+    s = torch.empty((B, 4, 84, 84), dtype=torch.uint8, device=dev)
+    s2, fmap = torch.empty_like(s), torch.empty((B, 2, 4), dtype=torch.int64, device=dev)
+    a = torch.empty(B, dtype=torch.int32, device=dev)
+    rr = torch.empty(B, dtype=torch.float32, device=dev)
+    term = torch.empty(B, dtype=torch.uint8, device=dev)
+    gather = lambda: g.gorila_gather(ctx, rep, idx, s, s2, fmap, a, rr, term)
+    for _ in range(warmup):
+        gather()
+    ctx.check()
+    gms = time_region(torch, gather, steps)
+    # algorithmic bytes: each distinct non-zero frame of s and s' read once
+    # (they share up to three), both stacks written
+    fm = fmap.cpu().numpy().reshape(B, 8)
+    read = sum(len(set(row.tolist()) - {-1}) for row in fm) * 7056
+    written = 2 * B * 28224
+    gbs = (read + written) / (gms * 1e-3) / 1e9
+    rng2 = np.random.default_rng(w["seed"] + 100)
+    theta = t(datagen.he_normal_params(rng2, A).astype(np.float32))
+    tgt = theta + 0.01 * torch.randn(theta.shape[0], device=dev, generator=torch.Generator(dev).manual_seed(5))
+    grads = torch.empty(g.param_count(A), dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    step = lambda: g.gorila_learner_step(ctx, theta, tgt, A, rep, idx, 0.99, 1.0, grads, loss)
+    for _ in range(warmup):
+        step()
+    ctx.check()
+    lms = time_region(torch, step, steps)
+    ctx.check()
+    ctx.close()
+    return {"workload": "ring1m_gather_learner_b256_a18_f32",
+            "gather": {"ms_per_call": round(gms, 4), "bytes": read + written,
+                       "gb_per_s": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)},
+            "learner": {"value": round(B / (lms * 1e-3), 1), "unit": "transitions/s",
+                        "ms_per_step": round(lms, 4),
+                        "note": "the step reads the ring in place (gather folded into conv1 staging)"}}
+
+
 def cpu_baseline(datagen, B, A, seed, seconds):
     """The fp64 oracle (as it stands) running whole learner steps of the same
     batch-B workload on the host cores until `seconds` have passed."""
@@ -183,10 +295,30 @@ def cpu_baseline(datagen, B, A, seed, seconds):
         dt = time.perf_counter() - t0
         if dt >= seconds:
             break
-    return {"value": steps * B / dt, "unit": "transitions/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": f"{steps} fp64 learner steps of the batch-{B} workload "
-                      f"({steps * B} transitions, {dt:.1f} s)"}
+    out = {"value": steps * B / dt, "unit": "transitions/s", "cores": oracle.num_threads(),
+           "kind": "oracle",
+           "sample": f"{steps} fp64 learner steps of the batch-{B} workload "
+                     f"({steps * B} transitions, {dt:.1f} s)"}
+    # one host thread, on the first 64 rows of the same workload (per-transition
+    # cost does not depend on the batch size)
+    nt = oracle.num_threads()
+    oracle.set_num_threads(1)
+    try:
+        b1 = min(64, B)
+        steps1, t0 = 0, time.perf_counter()
+        while True:
+            oracle.learner_step(net, inp.theta, inp.theta_target, inp.s[:b1], inp.s2[:b1],
+                                inp.a[:b1], inp.r[:b1], inp.term[:b1], inp.gamma, 1.0)
+            steps1 += 1
+            dt1 = time.perf_counter() - t0
+            if dt1 >= seconds / 2:
+                break
+    finally:
+        oracle.set_num_threads(nt)
+    out["single_thread"] = {"value": steps1 * b1 / dt1, "unit": "transitions/s", "cores": 1,
+                            "sample": f"{steps1} fp64 learner steps on {b1} rows of the same "
+                                      f"workload ({steps1 * b1} transitions, {dt1:.1f} s)"}
+    return out
 
 
 def main():
@@ -201,6 +333,9 @@ def main():
     ap.add_argument("--no-b32", action="store_true", help="skip the batch-32 companion line")
     ap.add_argument("--no-grouped", action="store_true",
                     help="skip the 16-replica bf16 grouped-step companion line")
+    ap.add_argument("--no-actor", action="store_true", help="skip the actor-inference line")
+    ap.add_argument("--no-ring", action="store_true",
+                    help="skip the one-million-frame ring gather / learner line")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes three times "
                          "(calibrates the HBM traffic counters)")
@@ -257,18 +392,26 @@ def main():
                      "traffic": stored_traffic(r["dominant"], B, A),
                      "avg_launch_ms": round(r["dominant_ms"], 4),
                      "flops_per_launch": dom_flops},
+        "step_ms_p10_p50_p90": r["pct"],
         "stages": stages,
     }
     if not args.no_b32:
         r32 = run_learner(torch, g, datagen, 32, 18, datagen.SEED_BASE + 0, max(args.steps, 50),
-                          args.warmup)
+                          args.warmup, graph=True)
         t32 = 32 * step_flops_per_transition(18) / (r32["ms_per_step"] * 1e-3) / 1e12
         out["batch32"] = {"workload": "learner_b32_a18_f32",
                           "value": round(32 / (r32["ms_per_step"] * 1e-3), 1),
                           "ms_per_step": round(r32["ms_per_step"], 4), "tflops": round(t32, 3),
-                          "pct_mfma_peak": round(100 * t32 / FP32_MFMA_PEAK_TFLOPS, 2)}
+                          "pct_mfma_peak": round(100 * t32 / FP32_MFMA_PEAK_TFLOPS, 2),
+                          "step_ms_p10_p50_p90": r32["pct"],
+                          "hip_graph": {"ms_per_step": round(r32["graph_ms"], 4),
+                                        "value": round(32 / (r32["graph_ms"] * 1e-3), 1)}}
     if not args.no_grouped:
         out["grouped"] = run_grouped(torch, g, datagen, max(args.steps // 2, 5), args.warmup)
+    if not args.no_actor:
+        out["actor"] = run_actor(torch, g, datagen, max(args.steps, 20), args.warmup)
+    if not args.no_ring:
+        out["ring"] = run_ring(torch, g, datagen, max(args.steps, 20), args.warmup)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(datagen, B, A, seed, args.cpu_seconds)
     print(json.dumps(out), flush=True)

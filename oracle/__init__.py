@@ -87,6 +87,7 @@ def lib() -> ctypes.CDLL:
         L.oracle_param_count.restype = ctypes.c_int64
         L.oracle_param_offsets.argtypes = [net_p, i64p]
         L.oracle_num_threads.restype = ctypes.c_int
+        L.oracle_set_num_threads.argtypes = [ctypes.c_int32]
         L.oracle_q_forward.argtypes = [net_p, dp, u8p, ctypes.c_int32, dp]
         L.oracle_act.argtypes = [net_p, dp, u8p, ctypes.c_int32, ctypes.c_double,
                                  ctypes.c_uint64, i32p, dp]
@@ -133,6 +134,10 @@ def param_offsets(net: Net) -> list[int]:
 
 def num_threads() -> int:
     return int(lib().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    _check(lib().oracle_set_num_threads(int(n)), "set_num_threads")
 
 
 def q_forward(net: Net, theta, states) -> np.ndarray:

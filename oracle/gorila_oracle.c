@@ -106,6 +106,14 @@ int oracle_num_threads(void) {
 #endif
 }
 
+int oracle_set_num_threads(int32_t n) {
+    if (n < 1) return -1;
+#ifdef _OPENMP
+    omp_set_num_threads(n);
+#endif
+    return 0;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Layers, written as their definitions                                      */
 /* ------------------------------------------------------------------------ */

@@ -55,8 +55,9 @@ int64_t oracle_param_count(const oracle_net* net);
  * (the 11th is the total). */
 int oracle_param_offsets(const oracle_net* net, int64_t* off);
 
-/* Threads the OpenMP loops use. */
+/* Threads the OpenMP loops use, and a way to change it (n >= 1). */
 int oracle_num_threads(void);
+int oracle_set_num_threads(int32_t n);
 
 /* Q(s, .; theta) for n states [n, in_c, in_h, in_w] -> q_out [n, A]. */
 int oracle_q_forward(const oracle_net* net, const double* theta,
