@@ -349,12 +349,8 @@ int gorila_gather(const gorila_replay* replay, const int64_t* idx, int32_t n, ui
         return GORILA_EINVAL;
     if (!aligned16(s_out) || !aligned16(s2_out)) return GORILA_EINVAL;
     if (n == 0) return GORILA_OK;
-    const Plan p = make_plan(n, 0, 1);
-    if (p.ftab + sizeof(void*) * 8 * (size_t)n > ctx->ws_bytes) return GORILA_EWORKSPACE;
-    const uint8_t** ftab = at<const uint8_t*>(ctx, p.ftab);
-    launch_resolve(view_of(replay), idx, n, 0x7fffffff, ftab, a_out, r_out, term_out, frame_map_out,
-                   at<unsigned>(ctx, p.err), ctx->stream);
-    launch_materialize(ftab, n, s_out, s2_out, ctx->stream);
+    launch_gather(view_of(replay), idx, n, 0x7fffffff, s_out, s2_out, frame_map_out, a_out, r_out,
+                  term_out, at<unsigned>(ctx, make_plan(1, 0, 1).err), ctx->stream);
     return check_launch();
 }
 
@@ -439,7 +435,7 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G,
     uint8_t* term = at<uint8_t>(ctx, p.term);
     {
         StageTimer t(ctx, ST_RESOLVE);
-        launch_resolve(view_of(replay), idx, B, A, ftab, a, r, term, nullptr, at<unsigned>(ctx, p.err), st);
+        launch_resolve(view_of(replay), idx, B, A, ftab, a, r, term, at<unsigned>(ctx, p.err), st);
     }
 
     WidenSet widen{};

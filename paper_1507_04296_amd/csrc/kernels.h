@@ -26,12 +26,14 @@ struct ReplayView {
 // Resolve minibatch indices: frame pointers ftab[2][n][4] (s then s'; null =
 // zero-filled channel), a/r/term per row, optional frame map [n][2][4].
 void launch_resolve(const ReplayView& rv, const int64_t* idx, int n, int n_actions,
-                    const uint8_t** ftab, int32_t* a, float* r, uint8_t* term,
-                    int64_t* frame_map, unsigned* err, hipStream_t st);
+                    const uint8_t** ftab, int32_t* a, float* r, uint8_t* term, unsigned* err,
+                    hipStream_t st);
 
-// Copy the stacks named by ftab into s_out / s2_out [n][4][84][84].
-void launch_materialize(const uint8_t* const* ftab, int n, uint8_t* s_out, uint8_t* s2_out,
-                        hipStream_t st);
+// Materialising gather: s_out / s2_out [n][4][84][84], frame_map [n][2][4]
+// (may be null), a, r, term, in one launch (one workgroup per transition).
+void launch_gather(const ReplayView& rv, const int64_t* idx, int n, int n_actions,
+                   uint8_t* s_out, uint8_t* s2_out, int64_t* frame_map, int32_t* a, float* r,
+                   uint8_t* term, unsigned* err, hipStream_t st);
 
 // Transposed conv weights used as MFMA operands.
 //  w2t [16][64][32]: W2[o][c][u][v] at [(u,v)][o][c]   (conv2 forward)

@@ -10,106 +10,207 @@
 
 namespace gorila {
 
+// Frame pointers (null = zero frame) and physical slots (-1) of s = stack(k)
+// and s' = stack(k+1), plus the transition's action, reward and terminal flag.
+// An index or action out of range sets a bit of the sticky error word (when
+// err is not null) and yields zero stacks / action 0, never an out-of-bounds
+// access.
+// Slot of head + l for 0 <= head < cap and 0 <= l < cap (no 64-bit division).
+__device__ inline int64_t wrap(int64_t x, int64_t cap) { return x >= cap ? x - cap : x; }
+
+struct Resolved {
+    const uint8_t* ptr[2][4];
+    int64_t slot[2][4];
+    int32_t act;
+    float rew;
+    uint8_t term;
+};
+
+__device__ Resolved resolve_one(const ReplayView& rv, int64_t k, int n_actions,
+                                unsigned* __restrict__ err) {
+    Resolved o;
+#pragma unroll
+    for (int w = 0; w < 2; ++w)
+    #pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            o.ptr[w][c] = nullptr;
+            o.slot[w][c] = -1;
+        }
+    o.act = 0;
+    o.rew = 0.f;
+    o.term = 1;
+    if (rv.kind == GORILA_REPLAY_STACKED) {
+        if (k < 0 || k >= rv.rows) {
+            if (err) atomicOr(err, ERR_IDX_RANGE);
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                o.ptr[0][c] = rv.s + k * STATE_BYTES + (int64_t)c * FRAME_BYTES;
+                o.ptr[1][c] = rv.s2 + k * STATE_BYTES + (int64_t)c * FRAME_BYTES;
+                o.slot[0][c] = o.slot[1][c] = k * 4 + c;
+            }
+            o.act = rv.action[k];
+            o.rew = rv.reward[k];
+            o.term = rv.term[k] ? 1 : 0;
+        }
+    } else {
+        const int64_t cap = rv.capacity;
+        if (k < 0 || k > cap - 2) {
+            if (err) atomicOr(err, ERR_IDX_RANGE);
+        } else {
+#pragma unroll
+            for (int w = 0; w < 2; ++w) {
+                const int64_t kn = k + w;  // newest frame of the stack
+                // start[d] = frame kn-d begins an episode (d = 0, 1, 2)
+                bool start[3];
+    #pragma unroll
+                for (int d = 0; d < 3; ++d) {
+                    const int64_t l = kn - d;
+                    start[d] = l >= 0 && rv.ep_start[wrap(rv.head + l, cap)] != 0;
+                }
+    #pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int64_t l = kn - 3 + j;
+                    bool zero = l < 0;
+                    // any start in (l, kn]: frames kn-d for d = 0 .. 2-j
+        #pragma unroll
+                    for (int d = 0; d <= 2 - j; ++d) zero = zero || start[d];
+                    if (!zero) {
+                        const int64_t p = wrap(rv.head + l, cap);
+                        o.ptr[w][j] = rv.frames + p * FRAME_BYTES;
+                        o.slot[w][j] = p;
+                    }
+                }
+            }
+            const int64_t p = wrap(rv.head + k, cap);
+            o.act = rv.action[p];
+            o.rew = rv.reward[p];
+            o.term = rv.ep_start[wrap(rv.head + k + 1, cap)] ? 1 : 0;
+        }
+    }
+    if (o.act < 0 || o.act >= n_actions) {
+        if (err) atomicOr(err, ERR_ACTION_RANGE);
+        o.act = 0;
+    }
+    return o;
+}
+
 __global__ __launch_bounds__(256) void resolve_kernel(ReplayView rv, const int64_t* __restrict__ idx,
                                                       int n, int n_actions,
                                                       const uint8_t** __restrict__ ftab,
                                                       int32_t* __restrict__ a_out,
                                                       float* __restrict__ r_out,
                                                       uint8_t* __restrict__ term_out,
-                                                      int64_t* __restrict__ fmap,
                                                       unsigned* __restrict__ err) {
     const int b = blockIdx.x * blockDim.x + threadIdx.x;
     if (b >= n) return;
-    const int64_t k = idx[b];
-    const uint8_t* ptr[2][4] = {};
-    int64_t slot[2][4] = {{-1, -1, -1, -1}, {-1, -1, -1, -1}};
-    int32_t act = 0;
-    float rew = 0.f;
-    uint8_t term = 1;
-    if (rv.kind == GORILA_REPLAY_STACKED) {
-        if (k < 0 || k >= rv.rows) {
-            atomicOr(err, ERR_IDX_RANGE);
-        } else {
-            for (int c = 0; c < 4; ++c) {
-                ptr[0][c] = rv.s + k * STATE_BYTES + (int64_t)c * FRAME_BYTES;
-                ptr[1][c] = rv.s2 + k * STATE_BYTES + (int64_t)c * FRAME_BYTES;
-                slot[0][c] = slot[1][c] = k * 4 + c;
-            }
-            act = rv.action[k];
-            rew = rv.reward[k];
-            term = rv.term[k] ? 1 : 0;
-        }
-    } else {
-        const int64_t cap = rv.capacity;
-        if (k < 0 || k > cap - 2) {
-            atomicOr(err, ERR_IDX_RANGE);
-        } else {
-            for (int w = 0; w < 2; ++w) {
-                const int64_t kn = k + w;  // newest frame of the stack
-                // start[d] = frame kn-d begins an episode (d = 0, 1, 2)
-                bool start[3];
-                for (int d = 0; d < 3; ++d) {
-                    const int64_t l = kn - d;
-                    start[d] = l >= 0 && rv.ep_start[(rv.head + l) % cap] != 0;
-                }
-                for (int j = 0; j < 4; ++j) {
-                    const int64_t l = kn - 3 + j;
-                    bool zero = l < 0;
-                    // any start in (l, kn]: frames kn-d for d = 0 .. 2-j
-                    for (int d = 0; d <= 2 - j; ++d) zero = zero || start[d];
-                    if (!zero) {
-                        const int64_t p = (rv.head + l) % cap;
-                        ptr[w][j] = rv.frames + p * FRAME_BYTES;
-                        slot[w][j] = p;
-                    }
-                }
-            }
-            const int64_t p = (rv.head + k) % cap;
-            act = rv.action[p];
-            rew = rv.reward[p];
-            term = rv.ep_start[(rv.head + k + 1) % cap] ? 1 : 0;
-        }
-    }
-    if (act < 0 || act >= n_actions) {
-        atomicOr(err, ERR_ACTION_RANGE);
-        act = 0;
-    }
+    const Resolved o = resolve_one(rv, idx[b], n_actions, err);
     for (int w = 0; w < 2; ++w)
-        for (int c = 0; c < 4; ++c) {
-            ftab[((int64_t)w * n + b) * 4 + c] = ptr[w][c];
-            if (fmap) fmap[((int64_t)b * 2 + w) * 4 + c] = slot[w][c];
-        }
-    a_out[b] = act;
-    r_out[b] = rew;
-    term_out[b] = term;
+        for (int c = 0; c < 4; ++c) ftab[((int64_t)w * n + b) * 4 + c] = o.ptr[w][c];
+    a_out[b] = o.act;
+    r_out[b] = o.rew;
+    term_out[b] = o.term;
 }
 
 void launch_resolve(const ReplayView& rv, const int64_t* idx, int n, int n_actions,
-                    const uint8_t** ftab, int32_t* a, float* r, uint8_t* term,
-                    int64_t* frame_map, unsigned* err, hipStream_t st) {
+                    const uint8_t** ftab, int32_t* a, float* r, uint8_t* term, unsigned* err,
+                    hipStream_t st) {
     if (n <= 0) return;
-    resolve_kernel<<<(n + 255) / 256, 256, 0, st>>>(rv, idx, n, n_actions, ftab, a, r, term,
-                                                    frame_map, err);
+    resolve_kernel<<<(n + 255) / 256, 256, 0, st>>>(rv, idx, n, n_actions, ftab, a, r, term, err);
 }
 
-// One workgroup per (transition, s|s'): four frames of 441 16-byte vectors.
-__global__ __launch_bounds__(256) void materialize_kernel(const uint8_t* const* __restrict__ ftab,
-                                                          int n, uint8_t* __restrict__ s_out,
-                                                          uint8_t* __restrict__ s2_out) {
-    const int b = blockIdx.x, w = blockIdx.y;
-    uint4* dst = (uint4*)((w ? s2_out : s_out) + (int64_t)b * STATE_BYTES);
+// The materialising gather: workgroup (b, f) resolves transition b (every
+// thread reads the same few flags) and copies one frame of its stacks, so a
+// launch has 5n (ring) or 8n (stacked) workgroups in flight.  From a ring,
+// logical frame k-3+f (f = 0 .. 4) is read once and written to s (channel f)
+// and s' (channel f-1), or zeros where a stack zero-fills it; stacked rows
+// copy s (f < 4) and s' (f >= 4) separately.  Workgroup (b, 0) writes the
+// frame map, action, reward and terminal flag.
+__global__ __launch_bounds__(256) void gather_kernel(ReplayView rv, const int64_t* __restrict__ idx,
+                                                     int n, int n_actions, uint8_t* __restrict__ s_out,
+                                                     uint8_t* __restrict__ s2_out,
+                                                     int64_t* __restrict__ fmap,
+                                                     int32_t* __restrict__ a_out,
+                                                     float* __restrict__ r_out,
+                                                     uint8_t* __restrict__ term_out,
+                                                     unsigned* __restrict__ err) {
+    const int b = blockIdx.x, f = blockIdx.y, tid = threadIdx.x;
+    const bool lead = f == 0 && tid == 0;
+    const Resolved o = resolve_one(rv, idx[b], n_actions, lead ? err : nullptr);
+    if (lead) {
+        a_out[b] = o.act;
+        r_out[b] = o.rew;
+        term_out[b] = o.term;
+        if (fmap)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) fmap[(int64_t)b * 8 + j] = o.slot[j >> 2][j & 3];
+    }
     constexpr int VEC = FRAME_BYTES / 16;  // 441
-    for (int e = threadIdx.x; e < 4 * VEC; e += 256) {
-        const int c = e / VEC, q = e - c * VEC;
-        const uint4* src = (const uint4*)ftab[((int64_t)w * n + b) * 4 + c];
-        dst[e] = src ? src[q] : make_uint4(0, 0, 0, 0);
+    uint4* ds = (uint4*)(s_out + (int64_t)b * STATE_BYTES);
+    uint4* ds2 = (uint4*)(s2_out + (int64_t)b * STATE_BYTES);
+    // Source and destinations of this workgroup's frame, chosen with constant
+    // indices (the pointers are uniform over the workgroup).
+    const uint8_t* in_s = nullptr;   // frame as channel cs of s (null: zeros)
+    const uint8_t* in_s2 = nullptr;  // frame as channel cs2 of s'
+    uint4* out_s = nullptr;
+    uint4* out_s2 = nullptr;
+    if (rv.kind == GORILA_REPLAY_RING) {
+        switch (f) {
+            case 0: in_s = o.ptr[0][0]; break;
+            case 1: in_s = o.ptr[0][1]; in_s2 = o.ptr[1][0]; break;
+            case 2: in_s = o.ptr[0][2]; in_s2 = o.ptr[1][1]; break;
+            case 3: in_s = o.ptr[0][3]; in_s2 = o.ptr[1][2]; break;
+            default: in_s2 = o.ptr[1][3]; break;
+        }
+        if (f < 4) out_s = ds + f * VEC;
+        if (f > 0) out_s2 = ds2 + (f - 1) * VEC;
+    } else {
+        switch (f) {
+            case 0: in_s = o.ptr[0][0]; break;
+            case 1: in_s = o.ptr[0][1]; break;
+            case 2: in_s = o.ptr[0][2]; break;
+            case 3: in_s = o.ptr[0][3]; break;
+            case 4: in_s2 = o.ptr[1][0]; break;
+            case 5: in_s2 = o.ptr[1][1]; break;
+            case 6: in_s2 = o.ptr[1][2]; break;
+            default: in_s2 = o.ptr[1][3]; break;
+        }
+        if (f < 4) out_s = ds + f * VEC;
+        else out_s2 = ds2 + (f - 4) * VEC;
+    }
+    // masks rather than selects between vectors, which the compiler would
+    // route through private memory
+    const uint4* src = (const uint4*)(in_s ? in_s : in_s2);  // one slot when both are set
+    const uint32_t ms = in_s ? ~0u : 0u, ms2 = in_s2 ? ~0u : 0u;
+    const uint4 z = make_uint4(0, 0, 0, 0);
+    if (src) {
+        uint4 v[2];
+        const int q0 = tid, q1 = tid + 256;
+        v[0] = src[q0];
+        if (q1 < VEC) v[1] = src[q1];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            const int q = tid + 256 * u;
+            if (q >= VEC) break;
+            if (out_s) out_s[q] = make_uint4(v[u].x & ms, v[u].y & ms, v[u].z & ms, v[u].w & ms);
+            if (out_s2)
+                out_s2[q] = make_uint4(v[u].x & ms2, v[u].y & ms2, v[u].z & ms2, v[u].w & ms2);
+        }
+    } else {
+        for (int q = tid; q < VEC; q += 256) {
+            if (out_s) out_s[q] = z;
+            if (out_s2) out_s2[q] = z;
+        }
     }
 }
 
-void launch_materialize(const uint8_t* const* ftab, int n, uint8_t* s_out, uint8_t* s2_out,
-                        hipStream_t st) {
+void launch_gather(const ReplayView& rv, const int64_t* idx, int n, int n_actions,
+                   uint8_t* s_out, uint8_t* s2_out, int64_t* frame_map, int32_t* a, float* r,
+                   uint8_t* term, unsigned* err, hipStream_t st) {
     if (n <= 0) return;
-    materialize_kernel<<<dim3(n, 2), 256, 0, st>>>(ftab, n, s_out, s2_out);
+    const int frames = rv.kind == GORILA_REPLAY_RING ? 5 : 8;
+    gather_kernel<<<dim3(n, frames), 256, 0, st>>>(rv, idx, n, n_actions, s_out, s2_out, frame_map,
+                                                   a, r, term, err);
 }
 
 }  // namespace gorila
