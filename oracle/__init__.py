@@ -6,7 +6,9 @@ TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 oracle shares no code with it.
 
 The arithmetic lives in ``gorila_oracle.c`` (plain C, fp64, OpenMP over
-samples); this module only marshals numpy arrays through ctypes.  Each function
+samples) and ``ps_oracle.c`` (the parameter-server apply and the loss-statistics
+filter, Section 4 and 4.2); this module only marshals numpy arrays through
+ctypes.  Each function
 cites the passage of Nair et al. 2015 it follows; the readings used where the
 paper is silent are listed at the top of the C source.
 
@@ -27,17 +29,18 @@ from dataclasses import dataclass
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "gorila_oracle.c")
+_SRCS = [os.path.join(_HERE, "gorila_oracle.c"), os.path.join(_HERE, "ps_oracle.c")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 
 def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (-O2, OpenMP, no BLAS)."""
+    """Compile the oracle with gcc (-O2, OpenMP, no BLAS; no contraction of
+    a*b+c into fused multiply-adds, so every fp64 operation rounds once)."""
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp%d" % os.getpid()
         subprocess.check_call(
-            ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared",
-             "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"])
+            ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-ffp-contract=off",
+             "-Wall", "-Wextra", "-o", tmp] + _SRCS + ["-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -97,8 +100,14 @@ def lib() -> ctypes.CDLL:
         L.oracle_gather.argtypes = [
             u8p, u8p, i32p, f32p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
             ctypes.c_int64, i64p, ctypes.c_int32, u8p, u8p, i64p, i32p, f32p, u8p]
+        L.oracle_loss_filter.argtypes = [dp, dp, ctypes.c_int32, ctypes.c_double,
+                                         ctypes.c_double, ctypes.c_int64, u8p]
+        L.oracle_ps_apply.argtypes = [dp, dp, ctypes.c_int64, dp, ctypes.c_int32, u8p, i64p,
+                                      i64p, ctypes.c_int64, ctypes.c_double, ctypes.c_double,
+                                      u8p]
         for f in ("oracle_param_offsets", "oracle_q_forward", "oracle_act",
-                  "oracle_learner_step", "oracle_gather"):
+                  "oracle_learner_step", "oracle_gather", "oracle_loss_filter",
+                  "oracle_ps_apply"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -221,3 +230,40 @@ def gather(frames, ep_start, action, reward, head: int, idx, hist: int = 4):
                                cap, head, hist, fbytes, _ptr(idx), n, _ptr(s), _ptr(s2),
                                _ptr(fmap), _ptr(a), _ptr(r), _ptr(t)), "gather")
     return dict(s=s, s2=s2, frame_map=fmap, a=a, r=r, term=t)
+
+
+def loss_filter(stats, loss, alpha: float, k: float, warmup: int):
+    """Section 4.2 loss-statistics filter for G learners.
+
+    stats [G, 3] = (n, mean, var) of each learner's absolute loss (fp64; a new
+    array is returned, the input is not modified); loss [G] (float32 values
+    promoted exactly).  Returns (keep [G] uint8, new stats)."""
+    st = _c(stats, np.float64).copy()
+    x = _c(np.asarray(loss, np.float32), np.float64)
+    G = x.shape[0]
+    assert st.shape == (G, 3)
+    keep = np.zeros(G, np.uint8)
+    _check(lib().oracle_loss_filter(_ptr(st), _ptr(x), G, float(alpha), float(k), int(warmup),
+                                    _ptr(keep)), "loss_filter")
+    return keep, st
+
+
+def ps_apply(theta, accum, grads, version, ps_version: int, max_delay: int, lr: float,
+             eps: float, keep=None):
+    """Section 4 / 4.2 parameter-server apply: AdaGrad updates of theta+ by the
+    gradients grads [G, n] taken in index order, skipping those not kept and
+    those older than max_delay server updates at their turn.  lr and eps are
+    float32 values promoted exactly.  Returns dict(theta, accum (fp64 [n]),
+    applied [G] uint8, ps_version)."""
+    th = _c(theta, np.float64).copy()
+    acc = _c(accum, np.float64).copy()
+    gr = _c(grads, np.float64)
+    G, n = gr.shape
+    ver = _c(version, np.int64)
+    kp = None if keep is None else _c(keep, np.uint8)
+    psv = np.array([ps_version], np.int64)
+    applied = np.zeros(G, np.uint8)
+    _check(lib().oracle_ps_apply(_ptr(th), _ptr(acc), n, _ptr(gr), G, _ptr(kp), _ptr(ver),
+                                 _ptr(psv), int(max_delay), float(np.float32(lr)),
+                                 float(np.float32(eps)), _ptr(applied)), "ps_apply")
+    return dict(theta=th, accum=acc, applied=applied, ps_version=int(psv[0]))

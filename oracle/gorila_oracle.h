@@ -93,6 +93,25 @@ int oracle_gather(const uint8_t* frames, const uint8_t* ep_start,
                   uint8_t* s_out, uint8_t* s2_out, int64_t* frame_map_out,
                   int32_t* a_out, float* r_out, uint8_t* term_out);
 
+/* ---- Parameter-server side (ps_oracle.c; Section 4 and Section 4.2) ---- */
+
+/* Loss-statistics gradient filter for `groups` learners: stats [groups][3]
+ * = (n, mean, var) of each learner's absolute loss, updated in place with
+ * loss[g]; keep_out[g] = 0 iff the gradient of that loss is discarded
+ * (n >= max(warmup, 1) and |loss| > mean + k sd before the update).  alpha > 0:
+ * exponentially weighted statistics; alpha = 0: cumulative. */
+int oracle_loss_filter(double* stats, const double* loss, int32_t groups, double alpha,
+                       double k, int64_t warmup, uint8_t* keep_out);
+
+/* Apply `groups` gradients grads [groups][n] to theta [n] with AdaGrad
+ * (accumulator accum [n]) in index order; gradient g is applied iff keep[g]
+ * (keep may be NULL) and *ps_version - version[g] <= max_delay at its turn;
+ * every applied gradient increments *ps_version.  applied_out [groups]. */
+int oracle_ps_apply(double* theta, double* accum, int64_t n, const double* grads,
+                    int32_t groups, const uint8_t* keep, const int64_t* version,
+                    int64_t* ps_version, int64_t max_delay, double lr, double eps,
+                    uint8_t* applied_out);
+
 #ifdef __cplusplus
 }
 #endif
