@@ -292,6 +292,43 @@ def run_ring(torch, g, datagen, steps, warmup):
                         "note": "the step reads the ring in place (gather folded into conv1 staging)"}}
 
 
+def run_ps(torch, g, datagen, steps, warmup):
+    """Parameter-server apply of 16 learner gradients of the 18-action network
+    (every gradient fresh and kept, so all 16 are applied), and the
+    loss-statistics filter of 16 learners."""
+    w = datagen.WORKLOADS["ps_apply_g16_a18_f32"]
+    G, P = w["groups"], datagen.param_count(w["n_actions"])
+    inp = datagen.ps_inputs(w["seed"], G, P)
+    dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    theta, accum, grads = t(inp.theta), t(inp.accum), t(inp.grads)
+    ver = torch.zeros(G, dtype=torch.int64, device=dev)
+    psv = torch.zeros(1, dtype=torch.int64, device=dev)
+    applied = torch.empty(G, dtype=torch.uint8, device=dev)
+    ctx = g.Context(1, w["n_actions"], device=dev)
+    big = 1 << 62
+    call = lambda: g.gorila_ps_apply(ctx, theta, accum, grads, ver, psv, big, 1e-4, 1e-3, applied)
+    for _ in range(warmup):
+        call()
+    ctx.check()
+    ms = time_region(torch, call, steps)
+    assert int(applied.sum().item()) == G
+    nbytes = P * 4 * (2 + G) + P * 4 * 2  # theta, accum and G gradients read; theta, accum written
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    stats = torch.zeros((G, 3), dtype=torch.float64, device=dev)
+    loss = t(datagen.loss_sequences(w["seed"], 1, G)[0])
+    keep = torch.empty(G, dtype=torch.uint8, device=dev)
+    filt = lambda: g.gorila_loss_filter(ctx, stats, loss, 0.05, 3.0, 10, keep)
+    for _ in range(warmup):
+        filt()
+    fms = time_region(torch, filt, steps)
+    ctx.check()
+    ctx.close()
+    return {"workload": "ps_apply_g16_a18_f32", "ms_per_call": round(ms, 4), "bytes": nbytes,
+            "gb_per_s": round(gbs, 1), "frac_hbm_peak": round(gbs / HBM_PEAK_GBS, 4),
+            "loss_filter_ms_per_call": round(fms, 4)}
+
+
 def cpu_baseline(datagen, B, A, seed, seconds):
     """The fp64 oracle (as it stands) running whole learner steps of the same
     batch-B workload on the host cores until `seconds` have passed."""
@@ -347,6 +384,8 @@ def main():
     ap.add_argument("--no-actor", action="store_true", help="skip the actor-inference line")
     ap.add_argument("--no-ring", action="store_true",
                     help="skip the one-million-frame ring gather / learner line")
+    ap.add_argument("--no-ps", action="store_true",
+                    help="skip the parameter-server apply / loss-filter line")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes three times "
                          "(calibrates the HBM traffic counters)")
@@ -423,6 +462,8 @@ def main():
         out["actor"] = run_actor(torch, g, datagen, max(args.steps, 20), args.warmup)
     if not args.no_ring:
         out["ring"] = run_ring(torch, g, datagen, max(args.steps, 20), args.warmup)
+    if not args.no_ps:
+        out["ps"] = run_ps(torch, g, datagen, max(args.steps, 20), args.warmup)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(datagen, B, A, seed, args.cpu_seconds)
     print(json.dumps(out), flush=True)

@@ -190,6 +190,49 @@ int gorila_learner_step_grouped(const gorila_params* params, int32_t groups,
                                 const int64_t* idx, int32_t batch, float gamma, float clip_delta,
                                 float* grads_out, float* loss_out, gorila_ctx* ctx);
 
+/* ---- Parameter-server side (Section 4, parameter server; Section 4.2) ---- */
+
+/* Most gradients one gorila_ps_apply call takes. */
+#define GORILA_PS_MAX_GROUPS 4096
+
+/* Loss-statistics gradient filter (Section 4.2: each learner keeps a running
+ * mean and standard deviation of its absolute DQN loss and discards a
+ * gradient whose absolute loss exceeds the mean by more than k standard
+ * deviations).  For learner g (0 <= g < groups): x = |loss[g]| (loss [groups]
+ * fp32, e.g. the loss_out of gorila_learner_step_grouped) is compared with
+ * its statistics stats[g] = (n, mean, var) (fp64 [groups][3], device, 8-byte
+ * aligned, caller-owned, zero-initialised before a learner's first loss):
+ * keep_out[g] = 0 iff n >= max(warmup, 1), x > mean and (x - mean)^2 > k^2
+ * var; then x joins the statistics (kept or not): the first x sets
+ * (1, x, 0); after that, alpha > 0 gives exponentially weighted statistics
+ * d = x - mean, mean += alpha d, var = (1 - alpha)(var + alpha d^2), and
+ * alpha = 0 cumulative ones, mean' = mean + d/(n+1),
+ * var' = (n var + d (x - mean')) / (n+1); n += 1.  Every step is one fp64
+ * operation rounded once.  EINVAL for alpha outside [0, 1] or k < 0. */
+int gorila_loss_filter(double* stats, const float* loss, int32_t groups, double alpha, double k,
+                       int64_t warmup, uint8_t* keep_out, gorila_ctx* ctx);
+
+/* Parameter-server apply (Section 4: the server applies learner gradients to
+ * theta+; Section 4.2: gradients computed from parameters older than a
+ * threshold are discarded, and the update rule is AdaGrad, Duchi, Hazan and
+ * Singer 2011).  grads [groups][n] fp32 (e.g. grads_out of the grouped learner
+ * step, n = P) are taken in index order; gradient g was computed from theta+
+ * at server version grad_version[g] (int64 [groups]); at its turn the server
+ * is at version V (*ps_version, int64 device scalar, earlier applied gradients
+ * of this call included) and it is applied iff keep[g] (u8 [groups], NULL =
+ * all kept, e.g. the keep_out of gorila_loss_filter) and V - grad_version[g]
+ * <= max_delay; each applied gradient advances *ps_version by one and updates
+ * every element i of theta_plus / accum [n] (fp32, in place):
+ *     accum[i] += g_i^2;  theta_plus[i] -= lr * g_i / (eps + sqrt(accum[i])).
+ * applied_out [groups] u8 receives the decisions.  All pointers are device
+ * pointers; fp32 arrays 4-byte aligned, int64 ones 8-byte aligned.  The
+ * decisions and the version stay on the device (no host round trip).
+ * EINVAL for eps <= 0, lr < 0, n > 2^31 - 1 or groups outside
+ * 0 .. GORILA_PS_MAX_GROUPS.  Uses no workspace. */
+int gorila_ps_apply(float* theta_plus, float* accum, int64_t n, const float* grads, int32_t groups,
+                    const uint8_t* keep, const int64_t* grad_version, int64_t* ps_version,
+                    int64_t max_delay, float lr, float eps, uint8_t* applied_out, gorila_ctx* ctx);
+
 #ifdef __cplusplus
 }
 #endif

@@ -31,6 +31,7 @@ EXPORTS = (
     "gorila_ctx_set_stream", "gorila_ctx_check", "gorila_strerror", "gorila_gather",
     "gorila_q_forward", "gorila_act", "gorila_learner_step", "gorila_learner_step_grouped",
     "gorila_ctx_timing_begin", "gorila_ctx_timing_end", "gorila_stage_name",
+    "gorila_loss_filter", "gorila_ps_apply",
 )
 
 
@@ -84,6 +85,10 @@ def lib() -> ctypes.CDLL:
         "gorila_ctx_timing_begin": (ctypes.c_int, [vp, ctypes.c_uint32, i32]),
         "gorila_ctx_timing_end": (ctypes.c_int, [vp, vp, vp, i32]),
         "gorila_stage_name": (ctypes.c_char_p, [i32]),
+        "gorila_loss_filter": (ctypes.c_int, [vp, vp, i32, ctypes.c_double, ctypes.c_double, i64,
+                                              vp, vp]),
+        "gorila_ps_apply": (ctypes.c_int, [vp, vp, i64, vp, i32, vp, vp, vp, i64, f32, f32, vp,
+                                           vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -269,6 +274,24 @@ def gorila_learner_step_grouped(ctx: Context, thetas, theta_target, n_actions: i
                                              _ptr(idx), batch, gamma, clip_delta, _ptr(grads_out),
                                              _ptr(loss_out), ctx.bind_stream()),
            "gorila_learner_step_grouped")
+
+
+def gorila_loss_filter(ctx: Context, stats, loss, alpha: float, k: float, warmup: int,
+                       keep_out) -> None:
+    """stats: float64 [G, 3] device tensor (updated in place); loss [G] fp32."""
+    _check(lib().gorila_loss_filter(_ptr(stats), _ptr(loss), loss.shape[0], alpha, k, warmup,
+                                    _ptr(keep_out), ctx.bind_stream()), "gorila_loss_filter")
+
+
+def gorila_ps_apply(ctx: Context, theta_plus, accum, grads, grad_version, ps_version,
+                    max_delay: int, lr: float, eps: float, applied_out, keep=None) -> None:
+    """theta_plus / accum fp32 [n] (updated in place); grads [G, n]; grad_version
+    int64 [G]; ps_version int64 [1] (advanced in place); applied_out uint8 [G]."""
+    G = grads.shape[0] if grads.dim() == 2 else 0
+    _check(lib().gorila_ps_apply(_ptr(theta_plus), _ptr(accum), theta_plus.numel(), _ptr(grads),
+                                 G, _ptr(keep), _ptr(grad_version), _ptr(ps_version), max_delay,
+                                 lr, eps, _ptr(applied_out), ctx.bind_stream()),
+           "gorila_ps_apply")
 
 
 # Convenience wrappers that allocate the outputs (torch) and return them.

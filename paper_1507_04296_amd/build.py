@@ -11,7 +11,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libgorila.so")
 BUILD_DIR = os.path.join(HERE, "_build")
-SOURCES = ["replay.hip", "conv1.hip", "layers.hip", "head.hip", "api.hip"]
+SOURCES = ["replay.hip", "conv1.hip", "layers.hip", "head.hip", "ps.hip", "api.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -546,4 +546,31 @@ int gorila_learner_step_grouped(const gorila_params* params, int32_t groups,
                          clip_delta, grads_out, loss_out);
 }
 
+int gorila_loss_filter(double* stats, const float* loss, int32_t groups, double alpha, double k,
+                       int64_t warmup, uint8_t* keep_out, gorila_ctx* ctx) {
+    int rc = check_ctx(ctx);
+    if (rc) return rc;
+    if (groups < 0 || (groups > 0 && (!stats || !loss || !keep_out))) return GORILA_EINVAL;
+    if (((uintptr_t)stats & 7u) != 0) return GORILA_EINVAL;
+    if (!(alpha >= 0.0 && alpha <= 1.0) || !(k >= 0.0)) return GORILA_EINVAL;
+    launch_loss_filter(stats, loss, groups, alpha, k, warmup, keep_out, ctx->stream);
+    return check_launch();
+}
+
+int gorila_ps_apply(float* theta_plus, float* accum, int64_t n, const float* grads, int32_t groups,
+                    const uint8_t* keep, const int64_t* grad_version, int64_t* ps_version,
+                    int64_t max_delay, float lr, float eps, uint8_t* applied_out, gorila_ctx* ctx) {
+    int rc = check_ctx(ctx);
+    if (rc) return rc;
+    if (n < 0 || n > INT32_MAX || groups < 0 || groups > GORILA_PS_MAX_GROUPS) return GORILA_EINVAL;
+    if (!ps_version || (groups > 0 && (!grad_version || !applied_out))) return GORILA_EINVAL;
+    if (n > 0 && (!theta_plus || !accum || (groups > 0 && !grads))) return GORILA_EINVAL;
+    if (((uintptr_t)theta_plus | (uintptr_t)accum | (uintptr_t)grads) & 3u) return GORILA_EINVAL;
+    if (((uintptr_t)grad_version | (uintptr_t)ps_version) & 7u) return GORILA_EINVAL;
+    if (!(eps > 0.0f) || !(lr >= 0.0f) || !(lr < INFINITY)) return GORILA_EINVAL;
+    launch_ps_apply(theta_plus, accum, n, grads, groups, keep, grad_version, ps_version, max_delay,
+                    lr, eps, applied_out, ctx->stream);
+    return check_launch();
+}
+
 }  // extern "C"

@@ -127,6 +127,17 @@ struct ReduceArgs {
 };
 void launch_grad_reduce(const ReduceArgs& ra, hipStream_t st);
 
+// Parameter-server side (ps.hip).  Loss-statistics filter: stats [groups][3]
+// (n, mean, var of |loss|, fp64) updated in place, keep [groups].  Apply:
+// decides which of grads [groups][n] to apply (applied [groups], *ps_version
+// advanced on the device; one workgroup), then AdaGrad-updates theta / accum
+// [n] with them.
+void launch_loss_filter(double* stats, const float* loss, int groups, double alpha, double k,
+                        int64_t warmup, uint8_t* keep, hipStream_t st);
+void launch_ps_apply(float* theta, float* accum, int64_t n, const float* grads, int groups,
+                     const uint8_t* keep, const int64_t* version, int64_t* ps_version,
+                     int64_t max_delay, float lr, float eps, uint8_t* applied, hipStream_t st);
+
 // Sizes of the split-K / partial buffers the launchers above may use.
 constexpr int TARGET_WGS = 1024;             // split-K launches aim at ~4 workgroups per CU
 constexpr int FC1_MAX_SPLITS = 14;

@@ -250,6 +250,45 @@ def grouped_inputs(seed: int, groups: int, batch: int, n_actions: int,
     return GroupedInputs(n_actions, groups, batch, theta, target, s, s2, a, r, term, gamma)
 
 
+@dataclass
+class PsInputs:
+    """Parameter-server apply inputs: theta+ and AdaGrad accumulator [n],
+    G learner gradients [G, n] with the server versions they were computed at."""
+    theta: np.ndarray      # f32 [n]
+    accum: np.ndarray      # f32 [n], >= 0
+    grads: np.ndarray      # f32 [G, n]
+    version: np.ndarray    # i64 [G]
+    ps_version: int
+    keep: np.ndarray       # u8 [G]
+
+
+def ps_inputs(seed: int, groups: int, n: int, max_lag: int = 6, keep_p: float = 0.9,
+              ps_version: int = 1000) -> PsInputs:
+    """theta ~ N(0, 0.05^2), accum ~ U[0, 0.01), gradients ~ N(0, 1e-3^2),
+    version = ps_version - U{0..max_lag-1}, keep ~ Bernoulli(keep_p); drawn in
+    that order."""
+    rng = np.random.default_rng(seed)
+    theta = (0.05 * rng.standard_normal(n)).astype(np.float32)
+    accum = (0.01 * rng.random(n)).astype(np.float32)
+    grads = (1e-3 * rng.standard_normal((groups, n))).astype(np.float32)
+    version = (ps_version - rng.integers(0, max_lag, groups)).astype(np.int64)
+    keep = (rng.random(groups) < keep_p).astype(np.uint8)
+    return PsInputs(theta, accum, grads, version, ps_version, keep)
+
+
+def loss_sequences(seed: int, steps: int, groups: int, outlier_p: float = 0.02) -> np.ndarray:
+    """f32 [steps, groups] learner losses: lognormal around 0.05 with a slow
+    drift, and outliers 5-50x the typical value with probability outlier_p;
+    some values negative, to exercise the absolute value."""
+    rng = np.random.default_rng(seed)
+    t = np.arange(steps)[:, None]
+    base = 0.05 * np.exp(0.3 * rng.standard_normal((steps, groups))) * (1.0 + 0.002 * t)
+    out = rng.random((steps, groups)) < outlier_p
+    base = np.where(out, base * rng.uniform(5, 50, (steps, groups)), base)
+    sign = np.where(rng.random((steps, groups)) < 0.1, -1.0, 1.0)
+    return (sign * base).astype(np.float32)
+
+
 # Named workloads (sizes of the paper's setting: 4x84x84 uint8 stacks, 18 or 6
 # actions, replay of one million frames, gamma 0.99).
 WORKLOADS = {
@@ -260,4 +299,7 @@ WORKLOADS = {
                                                 capacity=1_000_000, seed=SEED_BASE + 3),
     "grouped_g16_b64_a18_bf16": dict(kind="grouped", groups=16, batch=64, n_actions=18,
                                      seed=SEED_BASE + 4),
+    # the server side of the stale-replica workload: 16 gradients of the
+    # 18-action network applied to theta+
+    "ps_apply_g16_a18_f32": dict(kind="ps_apply", groups=16, n_actions=18, seed=SEED_BASE + 5),
 }
