@@ -6,9 +6,10 @@ TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
 oracle shares no code with it.
 
 The arithmetic lives in ``gorila_oracle.c`` (plain C, fp64, OpenMP over
-samples) and ``ps_oracle.c`` (the parameter-server apply and the loss-statistics
-filter, Section 4 and 4.2); this module only marshals numpy arrays through
-ctypes.  Each function
+samples), ``ps_oracle.c`` (the parameter-server apply and the loss-statistics
+filter, Section 4 and 4.2) and ``actor_oracle.c`` (replay insert and the
+epsilon schedule, Algorithm 1 and Section 5.1); this module only marshals
+numpy arrays through ctypes.  Each function
 cites the passage of Nair et al. 2015 it follows; the readings used where the
 paper is silent are listed at the top of the C source.
 
@@ -29,7 +30,7 @@ from dataclasses import dataclass
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRCS = [os.path.join(_HERE, "gorila_oracle.c"), os.path.join(_HERE, "ps_oracle.c")]
+_SRCS = [os.path.join(_HERE, f) for f in ("gorila_oracle.c", "ps_oracle.c", "actor_oracle.c")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 
@@ -105,9 +106,14 @@ def lib() -> ctypes.CDLL:
         L.oracle_ps_apply.argtypes = [dp, dp, ctypes.c_int64, dp, ctypes.c_int32, u8p, i64p,
                                       i64p, ctypes.c_int64, ctypes.c_double, ctypes.c_double,
                                       u8p]
+        L.oracle_replay_insert.argtypes = [u8p, u8p, i32p, f32p, ctypes.c_int64, ctypes.c_int64,
+                                           i64p, i64p, u8p, u8p, i32p, f32p, ctypes.c_int32]
+        L.oracle_epsilon.argtypes = [ctypes.c_int64, ctypes.c_double, ctypes.c_double,
+                                     ctypes.c_int64]
+        L.oracle_epsilon.restype = ctypes.c_double
         for f in ("oracle_param_offsets", "oracle_q_forward", "oracle_act",
                   "oracle_learner_step", "oracle_gather", "oracle_loss_filter",
-                  "oracle_ps_apply"):
+                  "oracle_ps_apply", "oracle_replay_insert"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -267,3 +273,31 @@ def ps_apply(theta, accum, grads, version, ps_version: int, max_delay: int, lr: 
                                  _ptr(psv), int(max_delay), float(np.float32(lr)),
                                  float(np.float32(eps)), _ptr(applied)), "ps_apply")
     return dict(theta=th, accum=acc, applied=applied, ps_version=int(psv[0]))
+
+
+def replay_insert(frames, ep_start, action, reward, head: int, size: int, frames_in, ep_in,
+                  act_in, rew_in):
+    """Algorithm 1 / Section 4: append m records to a replay ring in place
+    (frames [capacity, ...] u8, ep_start u8, action i32, reward f32, all
+    modified); returns the new (head, size)."""
+    for a, dt in ((frames, np.uint8), (ep_start, np.uint8), (action, np.int32),
+                  (reward, np.float32)):
+        assert a.dtype == dt and a.flags["C_CONTIGUOUS"]
+    cap = frames.shape[0]
+    fb = int(np.prod(frames.shape[1:]))
+    fi = _c(frames_in, np.uint8)
+    m = fi.shape[0]
+    h = np.array([head], np.int64)
+    sz = np.array([size], np.int64)
+    _check(lib().oracle_replay_insert(_ptr(frames), _ptr(ep_start), _ptr(action), _ptr(reward),
+                                      cap, fb, _ptr(h), _ptr(sz), _ptr(fi),
+                                      _ptr(_c(ep_in, np.uint8)), _ptr(_c(act_in, np.int32)),
+                                      _ptr(_c(rew_in, np.float32)), m), "replay_insert")
+    return int(h[0]), int(sz[0])
+
+
+def epsilon(update: int, eps_start: float = 1.0, eps_end: float = 0.1,
+            anneal_updates: int = 1_000_000) -> float:
+    """Section 5.1 behaviour-policy epsilon after `update` global updates."""
+    return float(lib().oracle_epsilon(int(update), float(eps_start), float(eps_end),
+                                      int(anneal_updates)))

@@ -93,6 +93,24 @@ int oracle_gather(const uint8_t* frames, const uint8_t* ep_start,
                   uint8_t* s_out, uint8_t* s2_out, int64_t* frame_map_out,
                   int32_t* a_out, float* r_out, uint8_t* term_out);
 
+/* ---- Actor side (actor_oracle.c; Algorithm 1, Section 4, Section 5.1) ---- */
+
+/* Store m experience records into a replay ring (Algorithm 1 "store the
+ * transition in D"; Section 4 replay memory): record j (frame of frame_bytes
+ * bytes, episode-start flag, the action taken at that frame and the reward
+ * that followed) goes to logical position size + j, i.e. physical slot
+ * (head + size + j) mod capacity; when the ring is full the oldest record is
+ * overwritten and head advances.  *head and *size are updated.  m <= capacity. */
+int oracle_replay_insert(uint8_t* frames, uint8_t* ep_start, int32_t* action, float* reward,
+                         int64_t capacity, int64_t frame_bytes, int64_t* head, int64_t* size,
+                         const uint8_t* frames_in, const uint8_t* ep_start_in,
+                         const int32_t* action_in, const float* reward_in, int32_t m);
+
+/* epsilon of the behaviour policy after `update` global updates (Section 5.1:
+ * annealed linearly from eps_start to eps_end over the first anneal_updates
+ * updates, constant after). */
+double oracle_epsilon(int64_t update, double eps_start, double eps_end, int64_t anneal_updates);
+
 /* ---- Parameter-server side (ps_oracle.c; Section 4 and Section 4.2) ---- */
 
 /* Loss-statistics gradient filter for `groups` learners: stats [groups][3]

@@ -1,0 +1,87 @@
+"""Pins of the oracle's actor side: replay insert (Algorithm 1 "store the
+transition in D", Section 4 replay memory) against a bounded-deque model of the
+same memory, and the epsilon schedule of Section 5.1 (1 -> 0.1 over the first
+million updates) against its closed form."""
+import collections
+
+import numpy as np
+
+
+def _ring(cap, fshape=(3, 5)):
+    return (np.zeros((cap,) + fshape, np.uint8), np.zeros(cap, np.uint8),
+            np.zeros(cap, np.int32), np.zeros(cap, np.float32))
+
+
+def test_insert_matches_bounded_deque(oracle_mod):
+    rng = np.random.default_rng(21)
+    cap = 11
+    frames, ep, act, rew = _ring(cap)
+    model = collections.deque(maxlen=cap)  # logical order, oldest first
+    head, size = 0, 0
+    for call in range(40):
+        m = int(rng.integers(0, 6))
+        fi = rng.integers(0, 256, (m, 3, 5)).astype(np.uint8)
+        ei = (rng.random(m) < 0.3).astype(np.uint8)
+        ai = rng.integers(0, 18, m).astype(np.int32)
+        ri = rng.standard_normal(m).astype(np.float32)
+        head, size = oracle_mod.replay_insert(frames, ep, act, rew, head, size, fi, ei, ai, ri)
+        for j in range(m):
+            model.append((fi[j].copy(), int(ei[j]), int(ai[j]), float(ri[j])))
+        assert size == len(model)
+        for k, (f, e, a, r) in enumerate(model):
+            slot = (head + k) % cap
+            np.testing.assert_array_equal(frames[slot], f)
+            assert (ep[slot], act[slot], rew[slot]) == (e, a, np.float32(r)), (call, k)
+
+
+def test_insert_then_gather_stacks_a_trajectory(oracle_mod):
+    """Frames stored by insert come back as four-frame stacks with zero-fill
+    at the episode starts the actor flagged (checked by brute force)."""
+    rng = np.random.default_rng(22)
+    cap, T = 9, 23  # the ring wraps twice
+    frames, ep, act, rew = _ring(cap, (2, 2))
+    traj_f = rng.integers(1, 256, (T, 2, 2)).astype(np.uint8)
+    traj_e = np.zeros(T, np.uint8)
+    traj_e[[0, 5, 6, 14, 20]] = 1
+    traj_a = np.arange(T, dtype=np.int32) % 18
+    traj_r = np.linspace(-1, 1, T).astype(np.float32)
+    head, size = 0, 0
+    for t in range(T):  # one record per environment step
+        head, size = oracle_mod.replay_insert(frames, ep, act, rew, head, size, traj_f[t:t + 1],
+                                              traj_e[t:t + 1], traj_a[t:t + 1], traj_r[t:t + 1])
+    assert size == cap and head == T % cap
+    first = T - cap  # trajectory index of logical 0
+    idx = np.arange(0, cap - 1, dtype=np.int64)
+    out = oracle_mod.gather(frames, ep, act, rew, head, idx)
+    for k in idx:
+        for w, key in ((0, "s"), (1, "s2")):
+            kn = k + w
+            # latest episode start at or before kn, logical 0 counting as one
+            e = max([0] + [j for j in range(1, kn + 1) if traj_e[first + j]])
+            for c in range(4):
+                l = kn - 3 + c
+                want = traj_f[first + l] if l >= e else np.zeros((2, 2), np.uint8)
+                np.testing.assert_array_equal(out[key][k, c], want, err_msg=f"k={k} {key} c={c}")
+        assert out["a"][k] == traj_a[first + k] and out["r"][k] == traj_r[first + k]
+        assert out["term"][k] == traj_e[first + k + 1]
+
+
+def test_insert_rejects_more_than_capacity(oracle_mod):
+    frames, ep, act, rew = _ring(4)
+    import pytest
+    with pytest.raises(ValueError):
+        oracle_mod.replay_insert(frames, ep, act, rew, 0, 0, np.zeros((5, 3, 5), np.uint8),
+                                 np.zeros(5), np.zeros(5), np.zeros(5))
+
+
+def test_epsilon_schedule_closed_form(oracle_mod):
+    assert oracle_mod.epsilon(0) == 1.0
+    assert oracle_mod.epsilon(-5) == 1.0
+    assert abs(oracle_mod.epsilon(500_000) - 0.55) < 1e-15
+    assert abs(oracle_mod.epsilon(250_000) - 0.775) < 1e-15
+    assert oracle_mod.epsilon(1_000_000) == 0.1 and oracle_mod.epsilon(5_000_000) == 0.1
+    e = [oracle_mod.epsilon(u) for u in range(0, 1_000_001, 50_000)]
+    assert all(a > b for a, b in zip(e, e[1:]))
+    # linear: equal steps per update
+    d = np.diff(e)
+    np.testing.assert_allclose(d, -0.9 / 20, rtol=1e-12)
