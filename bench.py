@@ -224,12 +224,31 @@ def run_actor(torch, g, datagen, steps, warmup):
     ctx.check()
     ms = time_region(torch, call, steps)
     ctx.check()
+    # storing the step: one record into each of the 1024 actors' rings (64 slots each)
+    rs = g.RingSet(n, 64, device=dev)
+    rng = np.random.default_rng(w["seed"])
+    fi = t_(torch, dev, datagen.random_frames(rng, n * 7056).reshape(1, n, 84, 84))
+    ei = torch.zeros((1, n), dtype=torch.uint8, device=dev)
+    ai = torch.zeros((1, n), dtype=torch.int32, device=dev)
+    ri = torch.zeros((1, n), dtype=torch.float32, device=dev)
+    ins = lambda: g.gorila_replay_insert(ctx, rs, fi, ei, ai, ri)
+    for _ in range(warmup):
+        ins()
+    ims = time_region(torch, ins, steps)
+    ctx.check()
     ctx.close()
+    ibytes = 2 * n * 7056 + n * (1 + 4 + 4) * 2
     flops = n * 2 * (MAC_CONV1 + MAC_CONV2 + MAC_CONV3 + MAC_FC1 + 512 * A)
     tf = flops / (ms * 1e-3) / 1e12
     return {"workload": "actor_n1024_a18_f32", "value": round(n / (ms * 1e-3), 1),
             "unit": "envs/s", "ms_per_call": round(ms, 4), "tflops": round(tf, 2),
-            "pct_mfma_peak": round(100 * tf / FP32_MFMA_PEAK_TFLOPS, 2)}
+            "pct_mfma_peak": round(100 * tf / FP32_MFMA_PEAK_TFLOPS, 2),
+            "replay_insert": {"ms_per_call": round(ims, 4), "bytes": ibytes,
+                              "gb_per_s": round(ibytes / (ims * 1e-3) / 1e9, 1)}}
+
+
+def t_(torch, dev, a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
 
 
 def run_ring(torch, g, datagen, steps, warmup):

@@ -69,7 +69,12 @@ typedef struct {
  *   term[k] (nonzero = s' is terminal).
  * RING: a ring of `capacity` single uint8 84x84 frames; `head` is the slot of
  *   the oldest frame and logical position k lives in slot
- *   (head + k) mod capacity.  ep_start[slot] != 0 marks the first frame of an
+ *   (head + k) mod capacity.  With rows = R > 1 the arrays hold R rings of
+ *   `capacity` slots each ([R][capacity] layout, one ring per actor of
+ *   Section 4's bundled mode, filled in lockstep so they share `head`), and a
+ *   minibatch index r * capacity + k names logical position k of ring r;
+ *   rows 0 or 1 is a single ring.  Frame maps then report global slots
+ *   r * capacity + slot.  ep_start[slot] != 0 marks the first frame of an
  *   episode; logical 0 also counts as one.  A minibatch index is a logical
  *   position k in [0, capacity-2]: s is the stack of frames k-3 .. k and s'
  *   of frames k-2 .. k+1 (oldest first), where any frame before the latest
@@ -189,6 +194,34 @@ int gorila_learner_step_grouped(const gorila_params* params, int32_t groups,
                                 const gorila_params* target_params, const gorila_replay* replay,
                                 const int64_t* idx, int32_t batch, float gamma, float clip_delta,
                                 float* grads_out, float* loss_out, gorila_ctx* ctx);
+
+/* ---- Actor side (Algorithm 1, Section 4 actors and replay memory, Section 5.1) ---- */
+
+/* Store experience in replay rings (Algorithm 1: the actor stores each step's
+ * transition in D; Section 4: one replay memory per actor in bundled mode).
+ * frames [rings][capacity][84][84] u8, ep_start / action / reward
+ * [rings][capacity] (device; the arrays of a gorila_replay RING with
+ * rows = rings); all rings share *head and *size (host values, updated at
+ * enqueue time: the rings are filled in lockstep).  m records per ring,
+ * inputs [m][rings][...] (frames_in [m][rings][84][84], ep_start_in,
+ * action_in, reward_in [m][rings], device): record j of ring r is the frame,
+ * its episode-start flag, the action taken at it and the reward that
+ * followed, and lands in slot (head + size + j) mod capacity of ring r, so
+ * once a ring is full each record overwrites the oldest and head advances.
+ * Then size = min(size + m, capacity) and head moves by the overflow.
+ * EINVAL for m outside 0 .. capacity or capacity < 2; frames and frames_in
+ * 16-byte aligned. */
+int gorila_replay_insert(uint8_t* frames, uint8_t* ep_start, int32_t* action, float* reward,
+                         int64_t capacity, int32_t rings, int64_t* head, int64_t* size,
+                         const uint8_t* frames_in, const uint8_t* ep_start_in,
+                         const int32_t* action_in, const float* reward_in, int32_t m,
+                         gorila_ctx* ctx);
+
+/* Behaviour-policy epsilon after `update` global updates (Section 5.1:
+ * annealed from 1 to 0.1 over the first million updates): eps_start for
+ * update <= 0, eps_end from anneal_updates on, linear in between.  Host
+ * arithmetic only; pass it to gorila_act. */
+double gorila_epsilon(int64_t update, double eps_start, double eps_end, int64_t anneal_updates);
 
 /* ---- Parameter-server side (Section 4, parameter server; Section 4.2) ---- */
 

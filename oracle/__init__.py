@@ -285,14 +285,17 @@ def replay_insert(frames, ep_start, action, reward, head: int, size: int, frames
         assert a.dtype == dt and a.flags["C_CONTIGUOUS"]
     cap = frames.shape[0]
     fb = int(np.prod(frames.shape[1:]))
+    # every array handed to C is held by a name until the call returns
     fi = _c(frames_in, np.uint8)
+    ei = _c(ep_in, np.uint8)
+    ai = _c(act_in, np.int32)
+    ri = _c(rew_in, np.float32)
     m = fi.shape[0]
     h = np.array([head], np.int64)
     sz = np.array([size], np.int64)
     _check(lib().oracle_replay_insert(_ptr(frames), _ptr(ep_start), _ptr(action), _ptr(reward),
-                                      cap, fb, _ptr(h), _ptr(sz), _ptr(fi),
-                                      _ptr(_c(ep_in, np.uint8)), _ptr(_c(act_in, np.int32)),
-                                      _ptr(_c(rew_in, np.float32)), m), "replay_insert")
+                                      cap, fb, _ptr(h), _ptr(sz), _ptr(fi), _ptr(ei), _ptr(ai),
+                                      _ptr(ri), m), "replay_insert")
     return int(h[0]), int(sz[0])
 
 

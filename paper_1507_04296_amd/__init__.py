@@ -31,7 +31,7 @@ EXPORTS = (
     "gorila_ctx_set_stream", "gorila_ctx_check", "gorila_strerror", "gorila_gather",
     "gorila_q_forward", "gorila_act", "gorila_learner_step", "gorila_learner_step_grouped",
     "gorila_ctx_timing_begin", "gorila_ctx_timing_end", "gorila_stage_name",
-    "gorila_loss_filter", "gorila_ps_apply",
+    "gorila_loss_filter", "gorila_ps_apply", "gorila_replay_insert", "gorila_epsilon",
 )
 
 
@@ -87,6 +87,9 @@ def lib() -> ctypes.CDLL:
         "gorila_stage_name": (ctypes.c_char_p, [i32]),
         "gorila_loss_filter": (ctypes.c_int, [vp, vp, i32, ctypes.c_double, ctypes.c_double, i64,
                                               vp, vp]),
+        "gorila_replay_insert": (ctypes.c_int, [vp, vp, vp, vp, i64, i32, ctypes.POINTER(i64),
+                                                ctypes.POINTER(i64), vp, vp, vp, vp, i32, vp]),
+        "gorila_epsilon": (ctypes.c_double, [i64, ctypes.c_double, ctypes.c_double, i64]),
         "gorila_ps_apply": (ctypes.c_int, [vp, vp, i64, vp, i32, vp, vp, vp, i64, f32, f32, vp,
                                            vp]),
     }
@@ -216,6 +219,7 @@ class Replay:
     frames: object = None
     ep_start: object = None
     head: int = 0
+    rings: int = 1
 
     @staticmethod
     def stacked(s, s2, action, reward, term) -> "Replay":
@@ -223,11 +227,23 @@ class Replay:
 
     @staticmethod
     def ring(frames, ep_start, action, reward, head: int) -> "Replay":
+        """One ring: frames [capacity, 84, 84]."""
         return Replay(REPLAY_RING, action, reward, frames=frames, ep_start=ep_start, head=head)
 
+    @staticmethod
+    def rings_of(frames, ep_start, action, reward, head: int) -> "Replay":
+        """R rings filled in lockstep: frames [R, capacity, 84, 84], the others [R, capacity];
+        minibatch index r * capacity + k is logical position k of ring r."""
+        return Replay(REPLAY_RING, action, reward, frames=frames, ep_start=ep_start, head=head,
+                      rings=frames.shape[0])
+
     def c(self) -> _Replay:
-        rows = self.s.shape[0] if self.s is not None else 0
-        cap = self.frames.shape[0] if self.frames is not None else 0
+        if self.kind == REPLAY_RING:
+            rows = self.rings if self.rings > 1 else 0
+            cap = self.frames.shape[1] if self.rings > 1 else self.frames.shape[0]
+        else:
+            rows = self.s.shape[0] if self.s is not None else 0
+            cap = 0
         return _Replay(self.kind, 0, _ptr(self.s), _ptr(self.s2), _ptr(self.term), rows,
                        _ptr(self.frames), _ptr(self.ep_start), cap, int(self.head),
                        _ptr(self.action), _ptr(self.reward))
@@ -292,6 +308,44 @@ def gorila_ps_apply(ctx: Context, theta_plus, accum, grads, grad_version, ps_ver
                                  G, _ptr(keep), _ptr(grad_version), _ptr(ps_version), max_delay,
                                  lr, eps, _ptr(applied_out), ctx.bind_stream()),
            "gorila_ps_apply")
+
+
+class RingSet:
+    """Replay rings of one or more actors on the device (Section 4 bundled mode:
+    one ring per actor, filled in lockstep), with the host-side head / size."""
+
+    def __init__(self, rings: int, capacity: int, device=None):
+        import torch
+        dev = torch.device(device if device is not None else "cuda")
+        self.rings, self.capacity = rings, capacity
+        self.frames = torch.zeros((rings, capacity, 84, 84), dtype=torch.uint8, device=dev)
+        self.ep_start = torch.zeros((rings, capacity), dtype=torch.uint8, device=dev)
+        self.action = torch.zeros((rings, capacity), dtype=torch.int32, device=dev)
+        self.reward = torch.zeros((rings, capacity), dtype=torch.float32, device=dev)
+        self.head, self.size = 0, 0
+
+    def replay(self) -> Replay:
+        if self.rings == 1:
+            return Replay.ring(self.frames[0], self.ep_start[0], self.action[0], self.reward[0],
+                               self.head)
+        return Replay.rings_of(self.frames, self.ep_start, self.action, self.reward, self.head)
+
+
+def gorila_replay_insert(ctx: Context, rs: RingSet, frames_in, ep_in, act_in, rew_in) -> None:
+    """Append m records to every ring: frames_in [m, rings, 84, 84] u8, the others [m, rings]."""
+    m = frames_in.shape[0]
+    h, sz = ctypes.c_int64(rs.head), ctypes.c_int64(rs.size)
+    _check(lib().gorila_replay_insert(_ptr(rs.frames), _ptr(rs.ep_start), _ptr(rs.action),
+                                      _ptr(rs.reward), rs.capacity, rs.rings, ctypes.byref(h),
+                                      ctypes.byref(sz), _ptr(frames_in), _ptr(ep_in), _ptr(act_in),
+                                      _ptr(rew_in), m, ctx.bind_stream()), "gorila_replay_insert")
+    rs.head, rs.size = h.value, sz.value
+
+
+def epsilon(update: int, eps_start: float = 1.0, eps_end: float = 0.1,
+            anneal_updates: int = 1_000_000) -> float:
+    """Section 5.1 schedule (gorila_epsilon)."""
+    return float(lib().gorila_epsilon(update, eps_start, eps_end, anneal_updates))
 
 
 # Convenience wrappers that allocate the outputs (torch) and return them.

@@ -158,7 +158,7 @@ int check_replay(const gorila_replay* rv) {
         return GORILA_OK;
     }
     if (rv->kind == GORILA_REPLAY_RING) {
-        if (!rv->frames || !rv->ep_start || rv->capacity < 2) return GORILA_EINVAL;
+        if (!rv->frames || !rv->ep_start || rv->capacity < 2 || rv->rows < 0) return GORILA_EINVAL;
         if (rv->head < 0 || rv->head >= rv->capacity || !aligned16(rv->frames)) return GORILA_EINVAL;
         return GORILA_OK;
     }
@@ -544,6 +544,41 @@ int gorila_learner_step_grouped(const gorila_params* params, int32_t groups,
                                 float* grads_out, float* loss_out, gorila_ctx* ctx) {
     return learner_steps(ctx, params, groups, target_params, replay, idx, batch, gamma,
                          clip_delta, grads_out, loss_out);
+}
+
+int gorila_replay_insert(uint8_t* frames, uint8_t* ep_start, int32_t* action, float* reward,
+                         int64_t capacity, int32_t rings, int64_t* head, int64_t* size,
+                         const uint8_t* frames_in, const uint8_t* ep_start_in,
+                         const int32_t* action_in, const float* reward_in, int32_t m,
+                         gorila_ctx* ctx) {
+    int rc = check_ctx(ctx);
+    if (rc) return rc;
+    if (!head || !size || capacity < 2 || rings < 1 || m < 0 || m > capacity) return GORILA_EINVAL;
+    if (*head < 0 || *head >= capacity || *size < 0 || *size > capacity) return GORILA_EINVAL;
+    if ((int64_t)m * rings > INT32_MAX) return GORILA_EINVAL;
+    if (m == 0) return GORILA_OK;
+    if (!frames || !ep_start || !action || !reward || !frames_in || !ep_start_in || !action_in ||
+        !reward_in)
+        return GORILA_EINVAL;
+    if (!aligned16(frames) || !aligned16(frames_in)) return GORILA_EINVAL;
+    const int64_t base = (*head + *size) % capacity;
+    launch_insert(frames, ep_start, action, reward, capacity, rings, base, frames_in, ep_start_in,
+                  action_in, reward_in, m * rings, ctx->stream);
+    if ((rc = check_launch())) return rc;
+    const int64_t total = *size + m;
+    if (total <= capacity) {
+        *size = total;
+    } else {
+        *head = (*head + (total - capacity)) % capacity;
+        *size = capacity;
+    }
+    return GORILA_OK;
+}
+
+double gorila_epsilon(int64_t update, double eps_start, double eps_end, int64_t anneal_updates) {
+    if (update <= 0) return eps_start;
+    if (anneal_updates <= 0 || update >= anneal_updates) return eps_end;
+    return eps_start + (eps_end - eps_start) * ((double)update / (double)anneal_updates);
 }
 
 int gorila_loss_filter(double* stats, const float* loss, int32_t groups, double alpha, double k,

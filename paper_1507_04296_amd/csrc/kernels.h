@@ -35,6 +35,14 @@ void launch_gather(const ReplayView& rv, const int64_t* idx, int n, int n_action
                    uint8_t* s_out, uint8_t* s2_out, int64_t* frame_map, int32_t* a, float* r,
                    uint8_t* term, unsigned* err, hipStream_t st);
 
+// Replay insert into `rings` rings of `capacity` slots ([rings][capacity]
+// layout): record j of ring r (inputs [records / rings][rings]) goes to slot
+// (base + j) mod capacity of its ring; base + j never exceeds 2 capacity.
+void launch_insert(uint8_t* frames, uint8_t* ep_start, int32_t* action, float* reward,
+                   int64_t capacity, int rings, int64_t base, const uint8_t* frames_in,
+                   const uint8_t* ep_in, const int32_t* act_in, const float* rew_in, int records,
+                   hipStream_t st);
+
 // Transposed conv weights used as MFMA operands.
 //  w2t [16][64][32]: W2[o][c][u][v] at [(u,v)][o][c]   (conv2 forward)
 //  w3t [9][64][64]:  W3[o][c][u][v] at [(u,v)][o][c]   (conv3 forward)

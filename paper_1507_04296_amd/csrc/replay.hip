@@ -1,4 +1,4 @@
-// Replay minibatch resolution and the materialising gather.
+// Replay minibatch resolution, the materialising gather and the replay insert.
 //
 // Frame stacking (Section 5.1): a state is the four most recent frames,
 // oldest in channel 0.  Out of a ring of single frames, channel j of the
@@ -55,7 +55,13 @@ __device__ Resolved resolve_one(const ReplayView& rv, int64_t k, int n_actions,
         }
     } else {
         const int64_t cap = rv.capacity;
-        if (k < 0 || k > cap - 2) {
+        // rows > 1: that many rings of `capacity` slots sharing `head`, and
+        // index r * capacity + k names logical position k of ring r
+        const int64_t rings = rv.rows > 1 ? rv.rows : 1;
+        const int64_t r = rings > 1 && k >= 0 ? k / cap : 0;
+        if (rings > 1) k -= r * cap;
+        const int64_t ring0 = r * cap;  // first slot of ring r
+        if (k < 0 || k > cap - 2 || r >= rings) {
             if (err) atomicOr(err, ERR_IDX_RANGE);
         } else {
 #pragma unroll
@@ -66,7 +72,7 @@ __device__ Resolved resolve_one(const ReplayView& rv, int64_t k, int n_actions,
     #pragma unroll
                 for (int d = 0; d < 3; ++d) {
                     const int64_t l = kn - d;
-                    start[d] = l >= 0 && rv.ep_start[wrap(rv.head + l, cap)] != 0;
+                    start[d] = l >= 0 && rv.ep_start[ring0 + wrap(rv.head + l, cap)] != 0;
                 }
     #pragma unroll
                 for (int j = 0; j < 4; ++j) {
@@ -76,16 +82,16 @@ __device__ Resolved resolve_one(const ReplayView& rv, int64_t k, int n_actions,
         #pragma unroll
                     for (int d = 0; d <= 2 - j; ++d) zero = zero || start[d];
                     if (!zero) {
-                        const int64_t p = wrap(rv.head + l, cap);
+                        const int64_t p = ring0 + wrap(rv.head + l, cap);
                         o.ptr[w][j] = rv.frames + p * FRAME_BYTES;
                         o.slot[w][j] = p;
                     }
                 }
             }
-            const int64_t p = wrap(rv.head + k, cap);
+            const int64_t p = ring0 + wrap(rv.head + k, cap);
             o.act = rv.action[p];
             o.rew = rv.reward[p];
-            o.term = rv.ep_start[wrap(rv.head + k + 1, cap)] ? 1 : 0;
+            o.term = rv.ep_start[ring0 + wrap(rv.head + k + 1, cap)] ? 1 : 0;
         }
     }
     if (o.act < 0 || o.act >= n_actions) {
@@ -211,6 +217,40 @@ void launch_gather(const ReplayView& rv, const int64_t* idx, int n, int n_action
     const int frames = rv.kind == GORILA_REPLAY_RING ? 5 : 8;
     gather_kernel<<<dim3(n, frames), 256, 0, st>>>(rv, idx, n, n_actions, s_out, s2_out, frame_map,
                                                    a, r, term, err);
+}
+
+// Replay insert: record j of ring r (frames_in [m][rings][84*84] etc.) goes to
+// slot (base + j) mod capacity of ring r; one workgroup per record.
+__global__ __launch_bounds__(256) void insert_kernel(uint8_t* __restrict__ frames,
+                                                     uint8_t* __restrict__ ep_start,
+                                                     int32_t* __restrict__ action,
+                                                     float* __restrict__ reward, int64_t capacity,
+                                                     int rings, int64_t base,
+                                                     const uint8_t* __restrict__ frames_in,
+                                                     const uint8_t* __restrict__ ep_in,
+                                                     const int32_t* __restrict__ act_in,
+                                                     const float* __restrict__ rew_in) {
+    const int rec = blockIdx.x;  // = j * rings + r
+    const int j = rec / rings, r = rec - j * rings;
+    const int64_t slot = (int64_t)r * capacity + wrap(base + j, capacity);
+    constexpr int VEC = FRAME_BYTES / 16;
+    const uint4* src = (const uint4*)(frames_in + (int64_t)rec * FRAME_BYTES);
+    uint4* dst = (uint4*)(frames + slot * FRAME_BYTES);
+    for (int q = threadIdx.x; q < VEC; q += 256) dst[q] = src[q];
+    if (threadIdx.x == 0) {
+        ep_start[slot] = ep_in[rec] ? 1 : 0;
+        action[slot] = act_in[rec];
+        reward[slot] = rew_in[rec];
+    }
+}
+
+void launch_insert(uint8_t* frames, uint8_t* ep_start, int32_t* action, float* reward,
+                   int64_t capacity, int rings, int64_t base, const uint8_t* frames_in,
+                   const uint8_t* ep_in, const int32_t* act_in, const float* rew_in, int records,
+                   hipStream_t st) {
+    if (records <= 0) return;
+    insert_kernel<<<records, 256, 0, st>>>(frames, ep_start, action, reward, capacity, rings, base,
+                                           frames_in, ep_in, act_in, rew_in);
 }
 
 }  // namespace gorila

@@ -250,6 +250,57 @@ def grouped_inputs(seed: int, groups: int, batch: int, n_actions: int,
     return GroupedInputs(n_actions, groups, batch, theta, target, s, s2, a, r, term, gamma)
 
 
+class SpriteEnv:
+    """A synthetic stand-in for the Atari environments (none are available):
+    n independent games on a dark 84x84 screen with one 8x8 sprite the agent
+    moves and one fixed target.  Action a in [0, A) moves the sprite by
+    (dy, dx) = ((a % 9) // 3 - 1, (a % 9) % 3 - 1) * 4 px (the 9 joystick
+    directions; higher actions repeat them); reaching the target gives +1 and
+    ends the episode, every other step gives 0, and an episode also ends after
+    `max_steps` steps.  A new episode draws fresh positions from the env's
+    seeded generator.  Pure host numpy: shared by both sides of a test as an
+    input generator."""
+
+    def __init__(self, seed: int, n: int, max_steps: int = 25):
+        self.rng = np.random.default_rng(seed)
+        self.n, self.max_steps = n, max_steps
+        self.bg = self.rng.integers(0, 25, (n, FRAME_H, FRAME_W), dtype=np.uint8)
+        self.pos = np.zeros((n, 2), np.int64)
+        self.goal = np.zeros((n, 2), np.int64)
+        self.t = np.zeros(n, np.int64)
+        for e in range(n):
+            self._reset(e)
+
+    def _reset(self, e: int):
+        self.pos[e] = self.rng.integers(0, 77, 2)
+        self.goal[e] = self.rng.integers(0, 77, 2)
+        self.t[e] = 0
+
+    def frames(self) -> np.ndarray:
+        """Current screens, u8 [n, 84, 84]."""
+        out = self.bg.copy()
+        for e in range(self.n):
+            gy, gx = self.goal[e]
+            out[e, gy:gy + 8, gx:gx + 8] = np.maximum(out[e, gy:gy + 8, gx:gx + 8], 120)
+            y, x = self.pos[e]
+            out[e, y:y + 8, x:x + 8] = 255
+        return out
+
+    def step(self, actions: np.ndarray):
+        """Apply one action per game: returns (reward f32 [n], done u8 [n]); a
+        finished game has already been reset to its next episode's start."""
+        a = np.asarray(actions, np.int64) % 9
+        d = np.stack([a // 3 - 1, a % 3 - 1], axis=1) * 4
+        self.pos = np.clip(self.pos + d, 0, 76)
+        self.t += 1
+        hit = np.all(np.abs(self.pos - self.goal) < 8, axis=1)
+        reward = hit.astype(np.float32)
+        done = (hit | (self.t >= self.max_steps)).astype(np.uint8)
+        for e in np.nonzero(done)[0]:
+            self._reset(int(e))
+        return reward, done
+
+
 @dataclass
 class PsInputs:
     """Parameter-server apply inputs: theta+ and AdaGrad accumulator [n],

@@ -86,3 +86,17 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(g, "LIB_PATH", str(tmp_path / "libgorila.so"))
     with pytest.raises(RuntimeError, match="missing"):
         g.lib()
+
+
+def test_epsilon_schedule_matches_oracle(oracle_mod):
+    """gorila_epsilon is host arithmetic: equal to the oracle's schedule."""
+    import paper_1507_04296_amd as g
+    for u in (-3, 0, 1, 17, 250_000, 999_999, 1_000_000, 10**7):
+        assert g.epsilon(u) == oracle_mod.epsilon(u)
+    assert g.epsilon(5, 1.0, 0.3, 20) == oracle_mod.epsilon(5, 1.0, 0.3, 20)
+
+
+def test_workspace_rejects_too_many_groups():
+    import paper_1507_04296_amd as g
+    assert g.workspace_bytes(64, 18, g.GORILA_BF16, 16) > 0
+    assert g.workspace_bytes(64, 18, g.GORILA_BF16, 17) == 0

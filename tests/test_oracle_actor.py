@@ -85,3 +85,23 @@ def test_epsilon_schedule_closed_form(oracle_mod):
     # linear: equal steps per update
     d = np.diff(e)
     np.testing.assert_allclose(d, -0.9 / 20, rtol=1e-12)
+
+
+def test_insert_accepts_strided_inputs(oracle_mod):
+    """Column views of [m, rings] record arrays (copied by the wrapper) store
+    the same records as contiguous inputs."""
+    rng = np.random.default_rng(23)
+    m, rings, cap = 6, 3, 10
+    fi = rng.integers(0, 256, (m, rings, 3, 5)).astype(np.uint8)
+    ei = (rng.random((m, rings)) < 0.5).astype(np.uint8)
+    ai = rng.integers(0, 18, (m, rings)).astype(np.int32)
+    ri = rng.standard_normal((m, rings)).astype(np.float32)
+    a = _ring(cap)
+    b = _ring(cap)
+    oracle_mod.replay_insert(*a, 0, 0, fi[:, 1], ei[:, 1], ai[:, 1], ri[:, 1])
+    oracle_mod.replay_insert(*b, 0, 0, fi[:, 1].copy(), ei[:, 1].copy(), ai[:, 1].copy(),
+                             ri[:, 1].copy())
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)
+    np.testing.assert_array_equal(a[2][:m], ai[:, 1])
+    np.testing.assert_array_equal(a[3][:m], ri[:, 1])
