@@ -111,9 +111,13 @@ def lib() -> ctypes.CDLL:
         L.oracle_epsilon.argtypes = [ctypes.c_int64, ctypes.c_double, ctypes.c_double,
                                      ctypes.c_int64]
         L.oracle_epsilon.restype = ctypes.c_double
+        L.oracle_params_sync.argtypes = [f32p, dp, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.c_int64, i64p, ctypes.c_int64, u8p]
+        L.oracle_f32_to_bf16.argtypes = [ctypes.c_float]
+        L.oracle_f32_to_bf16.restype = ctypes.c_uint16
         for f in ("oracle_param_offsets", "oracle_q_forward", "oracle_act",
                   "oracle_learner_step", "oracle_gather", "oracle_loss_filter",
-                  "oracle_ps_apply", "oracle_replay_insert"):
+                  "oracle_ps_apply", "oracle_replay_insert", "oracle_params_sync"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -304,3 +308,25 @@ def epsilon(update: int, eps_start: float = 1.0, eps_end: float = 0.1,
     """Section 5.1 behaviour-policy epsilon after `update` global updates."""
     return float(lib().oracle_epsilon(int(update), float(eps_start), float(eps_end),
                                       int(anneal_updates)))
+
+
+def params_sync(src, dst_versions, ps_version: int, period: int, copies: int, to_bf16: bool,
+                dst=None):
+    """Algorithm 1 parameter pull / periodic target sync.  src fp32 [n];
+    dst [copies, n] (fp32, or uint16 bf16 bits; zeros if None) and
+    dst_versions [copies] are copied, updated and returned as
+    (dst, versions, synced)."""
+    s = _c(src, np.float32)
+    n = s.shape[0]
+    dt = np.uint16 if to_bf16 else np.float32
+    d = np.zeros((copies, n), dt) if dst is None else _c(dst, dt).copy()
+    v = _c(dst_versions, np.int64).copy()
+    synced = np.zeros(copies, np.uint8)
+    _check(lib().oracle_params_sync(_ptr(s), _ptr(d), n, copies, int(bool(to_bf16)),
+                                    int(ps_version), _ptr(v), int(period), _ptr(synced)),
+           "params_sync")
+    return d, v, synced
+
+
+def f32_to_bf16(x: float) -> int:
+    return int(lib().oracle_f32_to_bf16(float(x)))

@@ -106,6 +106,22 @@ int oracle_replay_insert(uint8_t* frames, uint8_t* ep_start, int32_t* action, fl
                          const uint8_t* frames_in, const uint8_t* ep_start_in,
                          const int32_t* action_in, const float* reward_in, int32_t m);
 
+/* Parameter pull / target sync (Algorithm 1: learners and actors update theta
+ * from theta+, and every N global updates the learner syncs theta- with
+ * theta+; Section 5.1: N = 60K).  For each of `copies` destinations
+ * dst[c] ([copies][n], fp32 when to_bf16 == 0, else bf16 bit patterns
+ * rounded to nearest even from the fp32 value) with version dst_version[c]:
+ * when period == 0, or ps_version / period > dst_version[c] / period
+ * (integer division: a multiple of period was crossed), dst[c] = src and
+ * dst_version[c] = ps_version; otherwise both are left alone.
+ * synced_out[c] = 1 iff copied. */
+int oracle_params_sync(const float* src, void* dst, int64_t n, int32_t copies, int32_t to_bf16,
+                       int64_t ps_version, int64_t* dst_version, int64_t period,
+                       uint8_t* synced_out);
+
+/* bf16 bit pattern of an fp32 value, round to nearest even (NaN stays NaN). */
+uint16_t oracle_f32_to_bf16(float x);
+
 /* epsilon of the behaviour policy after `update` global updates (Section 5.1:
  * annealed linearly from eps_start to eps_end over the first anneal_updates
  * updates, constant after). */

@@ -105,3 +105,56 @@ def test_insert_accepts_strided_inputs(oracle_mod):
         np.testing.assert_array_equal(x, y)
     np.testing.assert_array_equal(a[2][:m], ai[:, 1])
     np.testing.assert_array_equal(a[3][:m], ri[:, 1])
+
+
+# ---------------------------------------------------------------------------
+# Parameter pull / target sync (Algorithm 1; Section 5.1 N = 60K)
+# ---------------------------------------------------------------------------
+def test_bf16_rounding_hand_values(oracle_mod):
+    assert oracle_mod.f32_to_bf16(1.0) == 0x3F80
+    assert oracle_mod.f32_to_bf16(1 + 2 ** -8) == 0x3F80          # tie, even stays
+    assert oracle_mod.f32_to_bf16(1 + 3 * 2 ** -8) == 0x3F82      # tie, rounds up to even
+    assert oracle_mod.f32_to_bf16(1 + 2 ** -8 + 2 ** -20) == 0x3F81  # above the tie
+    assert oracle_mod.f32_to_bf16(1.9921875 + 2 ** -8) == 0x4000   # tie carrying into the exponent
+    assert oracle_mod.f32_to_bf16(-2.5) == 0xC020
+    assert oracle_mod.f32_to_bf16(0.0) == 0 and oracle_mod.f32_to_bf16(-0.0) == 0x8000
+
+
+def test_bf16_rounding_matches_torch():
+    """torch's float32 -> bfloat16 conversion (round to nearest even) is a
+    library special case of the oracle's rounding."""
+    import torch
+
+    import oracle
+    rng = np.random.default_rng(24)
+    x = np.concatenate([rng.standard_normal(20000), rng.standard_normal(20000) * 1e-39,
+                        rng.standard_normal(20000) * 1e30]).astype(np.float32)
+    want = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    d, _, _ = oracle.params_sync(x, [0], 1, 0, 1, True)
+    np.testing.assert_array_equal(d[0], want)
+
+
+def test_sync_period_crossing(oracle_mod):
+    """Copied iff some multiple of the period lies in (held version, current]."""
+    rng = np.random.default_rng(25)
+    src = rng.standard_normal(5).astype(np.float32)
+    for trial in range(300):
+        period = int(rng.integers(1, 12))
+        held = rng.integers(0, 60, 4)
+        now = int(held.max() + rng.integers(0, 30))
+        d, v, synced = oracle_mod.params_sync(src, held, now, period, 4, False)
+        for c in range(4):
+            want = any(m % period == 0 for m in range(int(held[c]) + 1, now + 1))
+            assert synced[c] == want, (trial, period, held[c], now)
+            if want:
+                np.testing.assert_array_equal(d[c], src)
+                assert v[c] == now
+            else:
+                assert not d[c].any() and v[c] == held[c]
+
+
+def test_pull_without_period_always_copies(oracle_mod):
+    src = np.arange(7, dtype=np.float32) - 3.5
+    d, v, synced = oracle_mod.params_sync(src, [5, 9], 9, 0, 2, False)
+    assert list(synced) == [1, 1] and list(v) == [9, 9]
+    np.testing.assert_array_equal(d, np.stack([src, src]))
