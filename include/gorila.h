@@ -217,6 +217,23 @@ int gorila_replay_insert(uint8_t* frames, uint8_t* ep_start, int32_t* action, fl
                          const int32_t* action_in, const float* reward_in, int32_t m,
                          gorila_ctx* ctx);
 
+/* Parameter pull and periodic target sync (Algorithm 1: actors and learners
+ * update theta from theta+ of the parameter server; every N global updates
+ * the learner syncs theta- with theta+; Section 5.1: N = 60K).  src [n] fp32
+ * (theta+, device); dst [copies][n] (device, fp32 or, with dst_dtype
+ * GORILA_BF16, bf16 bit patterns rounded to nearest even; copies 0 .. 64);
+ * dst_version [copies] (int64, device) is the server version each copy
+ * holds.  With *ps_version (int64 device scalar) the current version, copy c
+ * is due when period == 0 (a pull) or a multiple of period lies in
+ * (dst_version[c], *ps_version] (period > 0, versions >= 0: a sync); a due
+ * copy receives src and dst_version[c] = *ps_version; synced_out [copies]
+ * (u8, may be NULL) reports which were copied.  Everything stays on the
+ * device.  EINVAL for a bad dtype, period < 0, copies > 64 or misalignment
+ * (fp32 4-byte, bf16 2-byte, int64 8-byte). */
+int gorila_params_sync(const float* src, void* dst, int64_t n, int32_t copies, int32_t dst_dtype,
+                       const int64_t* ps_version, int64_t* dst_version, int64_t period,
+                       uint8_t* synced_out, gorila_ctx* ctx);
+
 /* Behaviour-policy epsilon after `update` global updates (Section 5.1:
  * annealed from 1 to 0.1 over the first million updates): eps_start for
  * update <= 0, eps_end from anneal_updates on, linear in between.  Host

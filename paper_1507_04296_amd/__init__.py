@@ -32,6 +32,7 @@ EXPORTS = (
     "gorila_q_forward", "gorila_act", "gorila_learner_step", "gorila_learner_step_grouped",
     "gorila_ctx_timing_begin", "gorila_ctx_timing_end", "gorila_stage_name",
     "gorila_loss_filter", "gorila_ps_apply", "gorila_replay_insert", "gorila_epsilon",
+    "gorila_params_sync",
 )
 
 
@@ -90,6 +91,7 @@ def lib() -> ctypes.CDLL:
         "gorila_replay_insert": (ctypes.c_int, [vp, vp, vp, vp, i64, i32, ctypes.POINTER(i64),
                                                 ctypes.POINTER(i64), vp, vp, vp, vp, i32, vp]),
         "gorila_epsilon": (ctypes.c_double, [i64, ctypes.c_double, ctypes.c_double, i64]),
+        "gorila_params_sync": (ctypes.c_int, [vp, vp, i64, i32, i32, vp, vp, i64, vp, vp]),
         "gorila_ps_apply": (ctypes.c_int, [vp, vp, i64, vp, i32, vp, vp, vp, i64, f32, f32, vp,
                                            vp]),
     }
@@ -340,6 +342,16 @@ def gorila_replay_insert(ctx: Context, rs: RingSet, frames_in, ep_in, act_in, re
                                       ctypes.byref(sz), _ptr(frames_in), _ptr(ep_in), _ptr(act_in),
                                       _ptr(rew_in), m, ctx.bind_stream()), "gorila_replay_insert")
     rs.head, rs.size = h.value, sz.value
+
+
+def gorila_params_sync(ctx: Context, src, dst, dst_version, ps_version, period: int,
+                       synced_out=None) -> None:
+    """Pull (period 0) or periodic target sync of theta+ (src fp32 [n]) into
+    dst [copies, n] (fp32, or bf16 bits as int16 / uint16 / bfloat16)."""
+    copies = dst.shape[0]
+    _check(lib().gorila_params_sync(_ptr(src), _ptr(dst), src.numel(), copies, dtype_of(dst),
+                                    _ptr(ps_version), _ptr(dst_version), period,
+                                    _ptr(synced_out), ctx.bind_stream()), "gorila_params_sync")
 
 
 def epsilon(update: int, eps_start: float = 1.0, eps_end: float = 0.1,

@@ -575,6 +575,23 @@ int gorila_replay_insert(uint8_t* frames, uint8_t* ep_start, int32_t* action, fl
     return GORILA_OK;
 }
 
+int gorila_params_sync(const float* src, void* dst, int64_t n, int32_t copies, int32_t dst_dtype,
+                       const int64_t* ps_version, int64_t* dst_version, int64_t period,
+                       uint8_t* synced_out, gorila_ctx* ctx) {
+    int rc = check_ctx(ctx);
+    if (rc) return rc;
+    if (n < 0 || copies < 0 || copies > 64 || period < 0) return GORILA_EINVAL;
+    if (dst_dtype != GORILA_F32 && dst_dtype != GORILA_BF16) return GORILA_EINVAL;
+    if (copies == 0) return GORILA_OK;
+    if (!ps_version || !dst_version || (n > 0 && (!src || !dst))) return GORILA_EINVAL;
+    if (((uintptr_t)src & 3u) || ((uintptr_t)dst & (dst_dtype == GORILA_BF16 ? 1u : 3u)))
+        return GORILA_EINVAL;
+    if (((uintptr_t)ps_version | (uintptr_t)dst_version) & 7u) return GORILA_EINVAL;
+    launch_params_sync(src, dst, n, copies, dst_dtype == GORILA_BF16, ps_version, dst_version,
+                       period, synced_out, ctx->stream);
+    return check_launch();
+}
+
 double gorila_epsilon(int64_t update, double eps_start, double eps_end, int64_t anneal_updates) {
     if (update <= 0) return eps_start;
     if (anneal_updates <= 0 || update >= anneal_updates) return eps_end;

@@ -146,6 +146,13 @@ void launch_ps_apply(float* theta, float* accum, int64_t n, const float* grads, 
                      const uint8_t* keep, const int64_t* version, int64_t* ps_version,
                      int64_t max_delay, float lr, float eps, uint8_t* applied, hipStream_t st);
 
+// Parameter pull / periodic target sync (ps.hip): copies <= 64 destinations
+// dst [copies][n] (fp32 or bf16), each copied when due, versions recorded by
+// a second launch.
+void launch_params_sync(const float* src, void* dst, int64_t n, int copies, bool to_bf16,
+                        const int64_t* ps_version, int64_t* dst_version, int64_t period,
+                        uint8_t* synced, hipStream_t st);
+
 // Sizes of the split-K / partial buffers the launchers above may use.
 constexpr int TARGET_WGS = 1024;             // split-K launches aim at ~4 workgroups per CU
 constexpr int FC1_MAX_SPLITS = 14;

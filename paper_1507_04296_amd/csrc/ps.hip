@@ -228,4 +228,95 @@ void launch_ps_apply(float* theta, float* accum, int64_t n, const float* grads, 
                                                          eps);
 }
 
+// ---------------------------------------------------------------------------
+// Parameter pull / periodic target sync (Algorithm 1: replicas update theta
+// from theta+; every N global updates theta- is synced with theta+).  A copy
+// is due when period == 0 or a multiple of period lies in (held version,
+// current version].  The copy kernel reads src once per element and writes
+// every due destination (fp32, or bf16 rounded to nearest even); a second,
+// one-workgroup launch then records the versions, so no workgroup can see a
+// version updated by another.
+// ---------------------------------------------------------------------------
+constexpr int SYNC_MAX_COPIES = 64;
+
+__device__ inline bool sync_due(int64_t now, int64_t held, int64_t period) {
+    return period == 0 || now / period > held / period;
+}
+
+__device__ inline uint16_t f32_to_bf16_rne(float x) {
+    const uint32_t u = __float_as_uint(x);
+    if ((u & 0x7f800000u) == 0x7f800000u && (u & 0x007fffffu) != 0)
+        return (uint16_t)((u >> 16) | 0x0040u);  // NaN stays a quiet NaN
+    return (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void sync_copy_kernel(const float* __restrict__ src,
+                                                        void* __restrict__ dst, int64_t n,
+                                                        int copies,
+                                                        const int64_t* __restrict__ ps_version,
+                                                        const int64_t* __restrict__ dst_version,
+                                                        int64_t period) {
+    __shared__ uint64_t sdue;  // bit c: destination c is due (copies <= 64)
+    if (threadIdx.x == 0) {
+        const int64_t now = *ps_version;
+        uint64_t m = 0;
+        for (int c = 0; c < copies; ++c)
+            if (sync_due(now, dst_version[c], period)) m |= 1ull << c;
+        sdue = m;
+    }
+    __syncthreads();
+    const uint64_t due = sdue;
+    if (!due) return;
+    constexpr int ILP = 4;
+    const int64_t stride = (int64_t)gridDim.x * 256 * ILP;
+    for (int64_t base = (int64_t)blockIdx.x * 256 * ILP + threadIdx.x; base < n; base += stride) {
+        float v[ILP];
+#pragma unroll
+        for (int u = 0; u < ILP; ++u) {
+            const int64_t i = base + u * 256;
+            v[u] = src[i < n ? i : 0];
+        }
+        for (int c = 0; c < copies; ++c) {
+            if (!((due >> c) & 1ull)) continue;
+#pragma unroll
+            for (int u = 0; u < ILP; ++u) {
+                const int64_t i = base + u * 256;
+                if (i >= n) continue;
+                if (BF16) ((uint16_t*)dst)[(int64_t)c * n + i] = f32_to_bf16_rne(v[u]);
+                else ((float*)dst)[(int64_t)c * n + i] = v[u];
+            }
+        }
+    }
+}
+
+__global__ void sync_finalize_kernel(int copies, const int64_t* __restrict__ ps_version,
+                                     int64_t* __restrict__ dst_version, int64_t period,
+                                     uint8_t* __restrict__ synced) {
+    const int c = threadIdx.x;
+    if (c >= copies) return;
+    const int64_t now = *ps_version;
+    const bool d = sync_due(now, dst_version[c], period);
+    if (d) dst_version[c] = now;
+    if (synced) synced[c] = d ? 1 : 0;
+}
+
+void launch_params_sync(const float* src, void* dst, int64_t n, int copies, bool to_bf16,
+                        const int64_t* ps_version, int64_t* dst_version, int64_t period,
+                        uint8_t* synced, hipStream_t st) {
+    if (copies <= 0) return;
+    if (n > 0) {
+        int64_t blocks = (n + 256 * 4 - 1) / (256 * 4);
+        if (blocks > 4096) blocks = 4096;
+        if (to_bf16)
+            sync_copy_kernel<true><<<(int)blocks, 256, 0, st>>>(src, dst, n, copies, ps_version,
+                                                                 dst_version, period);
+        else
+            sync_copy_kernel<false><<<(int)blocks, 256, 0, st>>>(src, dst, n, copies, ps_version,
+                                                                  dst_version, period);
+    }
+    sync_finalize_kernel<<<1, SYNC_MAX_COPIES, 0, st>>>(copies, ps_version, dst_version, period,
+                                                        synced);
+}
+
 }  // namespace gorila

@@ -157,3 +157,50 @@ def test_loss_filter_argument_errors(torch_cuda, g, ctx):
         with pytest.raises(g.GorilaError) as e:
             g.gorila_loss_filter(ctx, st, loss, alpha, k, 5, keep)
         assert e.value.code == -1
+
+
+# ---------------------------------------------------------------------------
+# Parameter pull / periodic target sync (Algorithm 1; Section 5.1)
+# ---------------------------------------------------------------------------
+def test_pull_16_bf16_replicas_full_network(torch_cuda, g, ctx, oracle_mod):
+    """theta+ of the 18-action network rounded into 16 bf16 replicas: bit-exact."""
+    torch = torch_cuda
+    P = datagen.param_count(18)
+    _say(f"params_sync pull 16 bf16 replicas n={P}")
+    rng = np.random.default_rng(9300)
+    src = (0.05 * rng.standard_normal(P)).astype(np.float32)
+    held = np.arange(16, dtype=np.int64)
+    dst = torch.zeros((16, P), dtype=torch.int16, device="cuda")
+    ver = _dev(torch, held)
+    psv = _dev(torch, np.array([40], np.int64))
+    synced = torch.empty(16, dtype=torch.uint8, device="cuda")
+    g.gorila_params_sync(ctx, _dev(torch, src), dst, ver, psv, 0, synced)
+    ctx.check()
+    want, wver, wsync = oracle_mod.params_sync(src, held, 40, 0, 16, True)
+    np.testing.assert_array_equal(dst.cpu().numpy().view(np.uint16), want)
+    np.testing.assert_array_equal(ver.cpu().numpy(), wver)
+    np.testing.assert_array_equal(synced.cpu().numpy(), wsync)
+
+
+@pytest.mark.parametrize("bf16", [False, True])
+def test_periodic_target_sync(torch_cuda, g, ctx, oracle_mod, bf16):
+    torch = torch_cuda
+    _say(f"params_sync period 60 bf16={bf16}")
+    rng = np.random.default_rng(9400 + bf16)
+    n, copies, period, now = 10007, 6, 60, 245
+    src = rng.standard_normal(n).astype(np.float32)
+    held = np.array([0, 180, 239, 240, 241, 245], np.int64)  # due: 0, 180, 239
+    prev_np = (rng.integers(0, 2 ** 15, (copies, n)).astype(np.uint16) if bf16 else
+               rng.standard_normal((copies, n)).astype(np.float32))
+    dst = _dev(torch, prev_np.view(np.int16) if bf16 else prev_np)
+    ver = _dev(torch, held)
+    psv = _dev(torch, np.array([now], np.int64))
+    synced = torch.empty(copies, dtype=torch.uint8, device="cuda")
+    g.gorila_params_sync(ctx, _dev(torch, src), dst, ver, psv, period, synced)
+    ctx.check()
+    want, wver, wsync = oracle_mod.params_sync(src, held, now, period, copies, bf16, dst=prev_np)
+    got = dst.cpu().numpy()
+    np.testing.assert_array_equal(got.view(np.uint16) if bf16 else got, want)
+    np.testing.assert_array_equal(ver.cpu().numpy(), wver)
+    np.testing.assert_array_equal(synced.cpu().numpy(), wsync)
+    assert list(wsync) == [1, 1, 1, 0, 0, 0]
