@@ -115,8 +115,10 @@ struct GemmShape {
 // Loaders: `la.init(j, row, k)` is called once per quad slot j of this thread
 // with the quad's tile coordinates; `la.load(kc, j)` returns the quad for
 // reduction chunk kc (zeros where the operand is zero-padded).
-// If rowsum_out is not null, thread t < BM also writes sum_k A[t][k] over this
-// workgroup's reduction range (in chunk order) to rowsum_out[t].
+// If rowsum_out is not null, rowsum_out[t] (t < BM) receives sum_k A[t][k]
+// over this workgroup's reduction range: wave w adds the k of every chunk in
+// [8w, 8w + 8) for rows lane < BM (so the four waves carry equal extra work),
+// and the four wave sums are added in wave order at the end (BM <= 64 only).
 //
 // Epilogue protocol: epi.pre(row, col) returns a value the epilogue needs for
 // that output element (a ReLU mask, a bias, or 0 when it needs none); it is
@@ -186,7 +188,7 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
         for (int j = 0; j < LB::NQ; ++j) LB::put(buf + LA::SIZE, qb_row[j], qb_k[j], rb[j]);
     };
 
-    const bool do_rowsum = rowsum_out != nullptr && tid < BM;
+    const bool do_rowsum = rowsum_out != nullptr;  // uniform over the workgroup
     float rowsum = 0.0f;
     auto compute = [&](const float* buf) {
         const float* sa = buf;
@@ -207,12 +209,9 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
                     for (int j = 0; j < TN; ++j)
                         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i][q], bv[j][q], acc[i][j], 0, 0, 0);
         }
-        if (do_rowsum) {
-#pragma unroll
-            for (int k = 0; k < BK; k += 4) {
-                const f32x4 v = LA::get(sa, tid, k);
-                rowsum += ((v[0] + v[1]) + v[2]) + v[3];
-            }
+        if (BM <= 64 && do_rowsum && lane < BM) {
+            const f32x4 v0 = LA::get(sa, lane, 8 * wave), v1 = LA::get(sa, lane, 8 * wave + 4);
+            rowsum += (((v0[0] + v0[1]) + (v0[2] + v0[3])) + ((v1[0] + v1[1]) + (v1[2] + v1[3])));
         }
     };
 
@@ -235,7 +234,12 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
         if (kc + 2 < kc_end) sstore(smem, ra0, rb0);
         __syncthreads();
     }
-    if (do_rowsum) rowsum_out[tid] = rowsum;
+    if (BM <= 64 && do_rowsum) {
+        // the LDS buffers are free after the loop's last barrier
+        if (lane < BM) smem[wave * 64 + lane] = rowsum;
+        __syncthreads();
+        if (tid < BM) rowsum_out[tid] = ((smem[tid] + smem[64 + tid]) + smem[128 + tid]) + smem[192 + tid];
+    }
 
 #pragma unroll
     for (int i = 0; i < TM; ++i)
@@ -310,5 +314,18 @@ __device__ inline f32x4 sel4(bool ok, f32x4 v) {
     return f32x4{ok ? v[0] : 0.f, ok ? v[1] : 0.f, ok ? v[2] : 0.f, ok ? v[3] : 0.f};
 }
 __device__ inline f32x4 ld4(const float* p) { return *(const f32x4*)p; }
+
+// Loads through a pointer that was itself read from memory (the replay frame
+// tables) would otherwise use the flat address space, whose loads also count
+// against the LDS wait counter, so every wait for LDS data would wait for them
+// too; these state that the data lives in global memory.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const uint32_t global_u32;
+typedef __attribute__((address_space(1))) const u32x4 global_u32x4;
+__device__ inline uint32_t ldg_u32(const uint8_t* p) { return *(global_u32*)p; }
+__device__ inline uint4 ldg_u4(const uint4* p) {
+    const u32x4 v = *(global_u32x4*)p;
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
 
 }  // namespace gorila

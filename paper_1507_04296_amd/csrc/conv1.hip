@@ -26,7 +26,7 @@ __global__ __launch_bounds__(256, 2) void conv1_fwd_kernel(const uint8_t* const*
         const int sc = e / VEC, q = e - sc * VEC;  // sc = sample * 4 + channel
         const int s = sc >> 2, c = sc & 3;
         const uint4* src = s < ns ? (const uint4*)ftab[((int64_t)g * n + b0 + s) * 4 + c] : nullptr;
-        ((uint4*)xs)[e] = src ? src[q] : make_uint4(0, 0, 0, 0);
+        ((uint4*)xs)[e] = src ? ldg_u4(src + q) : make_uint4(0, 0, 0, 0);
     }
 
     const float* W1 = theta.p[g];
@@ -110,13 +110,17 @@ struct Conv1WgradB {  // input bytes rows (c,u,v), RMAJ quads along v at one pix
         const int b = mm / P1, p = mm - b * P1, i = p / H1, jj = p - i * H1;
         const uint8_t* f = ftab[(int64_t)b * 4 + chan[j]];
         const bool ok = m < npix && f != nullptr;
-        const uint32_t d = *(const uint32_t*)((ok ? f : safe) + (S1 * i) * IN_W + S1 * jj + off[j]);
+        const uint32_t d = ldg_u32((ok ? f : safe) + (S1 * i) * IN_W + S1 * jj + off[j]);
         return sel4(ok, f32x4{(float)(d & 255u), (float)((d >> 8) & 255u),
                               (float)((d >> 16) & 255u), (float)(d >> 24)});
     }
 };
 
 constexpr int C1W_BN = 128;
+// The launch aims at one round of three workgroups per CU (the job's register
+// budget allows three): 754 workgroups of 17 chunks measured 58 us against
+// 65 us for 986 of 13 chunks (1.3 rounds) at batch 512.
+constexpr int C1W_TARGET_WGS = 768;
 
 struct Conv1WgradJob {
     const float* dz1;
@@ -150,7 +154,7 @@ void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int groups
                         float* partial, float* bias_part, int max_splits, int* splits_out,
                         hipStream_t st) {
     const int nchunks = (n * P1 + BK - 1) / BK;
-    int splits = max(1, min(max_splits, TARGET_WGS / (256 / C1W_BN)) / groups);
+    int splits = max(1, min(max_splits, C1W_TARGET_WGS / (256 / C1W_BN)) / groups);
     splits = min(splits, nchunks);
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
