@@ -21,12 +21,30 @@ __global__ __launch_bounds__(256, 2) void conv1_fwd_kernel(const uint8_t* const*
     const int ns = min(2, n - b0);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
+    // Stage the 8 frames (2 samples x 4 channels): the frame pointers are read
+    // once (uniform loads), then every thread issues all of its 16-byte loads
+    // before its first LDS store, so the copy costs one memory latency rather
+    // than one per vector.
     constexpr int VEC = FRAME_BYTES / 16;  // 441 16-byte vectors per frame
-    for (int e = tid; e < 8 * VEC; e += 256) {
-        const int sc = e / VEC, q = e - sc * VEC;  // sc = sample * 4 + channel
-        const int s = sc >> 2, c = sc & 3;
-        const uint4* src = s < ns ? (const uint4*)ftab[((int64_t)g * n + b0 + s) * 4 + c] : nullptr;
-        ((uint4*)xs)[e] = src ? ldg_u4(src + q) : make_uint4(0, 0, 0, 0);
+    const uint4* fp[8];
+#pragma unroll
+    for (int f = 0; f < 8; ++f)
+        fp[f] = (f >> 2) < ns ? (const uint4*)ftab[((int64_t)g * n + b0 + (f >> 2)) * 4 + (f & 3)]
+                              : nullptr;
+    {
+        const bool second = tid + 256 < VEC;  // lanes that copy a second vector per frame
+        uint4 v0[8], v1[8];
+        const uint4 z = make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int f = 0; f < 8; ++f) {
+            v0[f] = fp[f] ? ldg_u4(fp[f] + tid) : z;
+            v1[f] = fp[f] && second ? ldg_u4(fp[f] + tid + 256) : z;
+        }
+#pragma unroll
+        for (int f = 0; f < 8; ++f) {
+            ((uint4*)xs)[f * VEC + tid] = v0[f];
+            if (second) ((uint4*)xs)[f * VEC + tid + 256] = v1[f];
+        }
     }
 
     const float* W1 = theta.p[g];
