@@ -31,12 +31,23 @@ __device__ inline float dot8(const float* h, const float* w) {
 // h[0..7] = relu(b4[8l..] + sum_s part[s][b][8l..]) for one row b.
 __device__ inline void finish_h4(const float* part, int splits, int64_t split_stride,
                                  const float* b4, int lane, float* h) {
-    f32x4 a = ld4(part + lane * 8), c = ld4(part + lane * 8 + 4);
-    for (int s = 1; s < splits; ++s) {
-        const float* p = part + s * split_stride + lane * 8;
-        a += ld4(p);
-        c += ld4(p + 4);
-    }
+    // every split's partial is loaded before the first addition, so the loads
+    // overlap instead of waiting for one another
+    f32x4 pa[FC1_MAX_SPLITS], pc[FC1_MAX_SPLITS];
+#pragma unroll
+    for (int s = 0; s < FC1_MAX_SPLITS; ++s)
+        if (s < splits) {
+            const float* p = part + s * split_stride + lane * 8;
+            pa[s] = ld4(p);
+            pc[s] = ld4(p + 4);
+        }
+    f32x4 a = pa[0], c = pc[0];
+#pragma unroll
+    for (int s = 1; s < FC1_MAX_SPLITS; ++s)
+        if (s < splits) {
+            a += pa[s];
+            c += pc[s];
+        }
     const f32x4 ba = ld4(b4 + lane * 8), bc = ld4(b4 + lane * 8 + 4);
     h[0] = fmaxf(a[0] + ba[0], 0.f); h[1] = fmaxf(a[1] + ba[1], 0.f);
     h[2] = fmaxf(a[2] + ba[2], 0.f); h[3] = fmaxf(a[3] + ba[3], 0.f);

@@ -782,10 +782,21 @@ __global__ __launch_bounds__(256) void grad_reduce_kernel(ReduceArgs ra) {
         dst = ra.loss_out;
         scale = 1.0f / (float)ra.n;
     }
+    // partials s = sq, sq + 4, ... added in that order; sixteen of them are
+    // loaded before the first is added, so the loads overlap
     float acc = 0.0f;
     if (dst) {
-#pragma unroll 4
-        for (int s = sq; s < nsplit; s += 4) acc += src[(int64_t)s * stride];
+        for (int s0 = sq; s0 < nsplit; s0 += 4 * 16) {
+            float v[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                const int s = s0 + 4 * u;
+                v[u] = s < nsplit ? src[(int64_t)s * stride] : 0.0f;
+            }
+#pragma unroll
+            for (int u = 0; u < 16; ++u)
+                if (s0 + 4 * u < nsplit) acc += v[u];
+        }
     }
     red[sq][el] = acc;
     __syncthreads();
