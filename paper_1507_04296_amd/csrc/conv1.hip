@@ -64,7 +64,10 @@ __global__ __launch_bounds__(256, 2) void conv1_fwd_kernel(const uint8_t* const*
     const int rows = ns * P1;
     const int ntiles = (rows + 31) / 32;
     float* out = h1 + ((int64_t)g * n + b0) * P1 * C1;
-    for (int t = wave; t < ntiles; t += 4) {
+    // workgroup z of gridDim.z takes tiles z, z + zs, ... (small batches
+    // spread one sample pair's 25 tiles over several workgroups)
+    const int z = blockIdx.z, zs = gridDim.z;
+    for (int t = z + zs * wave; t < ntiles; t += 4 * zs) {
         int m = t * 32 + (lane & 31);
         if (m >= rows) m = 0;  // padding rows compute on a valid pixel, never stored
         const int s = m / P1, p = m - s * P1, i = p / H1, j = p - i * H1;
@@ -92,7 +95,11 @@ __global__ __launch_bounds__(256, 2) void conv1_fwd_kernel(const uint8_t* const*
 void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int groups, int n,
                       float* h1, hipStream_t st) {
     if (n <= 0) return;
-    conv1_fwd_kernel<<<dim3((n + 1) / 2, groups), 256, 0, st>>>(ftab, theta, n, h1);
+    // Aim at >= 512 workgroups (two per CU): below that, split each pair's
+    // tiles over up to 8 workgroups, each staging the pair's frames.
+    const int blocks = (n + 1) / 2 * groups;
+    const int split = blocks >= 512 ? 1 : min(8, (512 + blocks - 1) / blocks);
+    conv1_fwd_kernel<<<dim3((n + 1) / 2, groups, split), 256, 0, st>>>(ftab, theta, n, h1);
 }
 
 // Weight gradient: dW1[o][(c,u,v)] = (1/255) sum_pixels dz1[pixel][o] * x[c][4i+u][4j+v]
