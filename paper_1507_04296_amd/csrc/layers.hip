@@ -47,12 +47,27 @@ void launch_prep_weights(const WeightViews* nets, int n_nets, hipStream_t st) {
 }
 
 // bf16 -> fp32 is exact: the 16 bits become the high half of the float.
+// Each lane reads four bf16 values as one 8-byte load: the elements before
+// the first 8-byte boundary of the (2-byte aligned) source, and those after
+// the last whole group of four, are widened one by one.
 __global__ __launch_bounds__(256) void widen_bf16_kernel(WidenSet set, int64_t count) {
     const uint16_t* src = set.src[blockIdx.y];
     float* dst = set.dst[blockIdx.y];
-    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < count;
-         e += (int64_t)gridDim.x * 256)
-        dst[e] = __uint_as_float((uint32_t)src[e] << 16);
+    const int64_t head = min<int64_t>(count, ((8 - ((uintptr_t)src & 7)) & 7) >> 1);
+    const int64_t quads = (count - head) >> 2;
+    const int64_t tid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    if (tid < head) dst[tid] = __uint_as_float((uint32_t)src[tid] << 16);
+    for (int64_t q = tid; q < quads; q += stride) {
+        const int64_t e = head + 4 * q;
+        const uint2 v = *(const uint2*)(src + e);
+        dst[e] = __uint_as_float(v.x << 16);
+        dst[e + 1] = __uint_as_float(v.x & 0xffff0000u);
+        dst[e + 2] = __uint_as_float(v.y << 16);
+        dst[e + 3] = __uint_as_float(v.y & 0xffff0000u);
+    }
+    const int64_t tail = head + 4 * quads;
+    if (tail + tid < count) dst[tail + tid] = __uint_as_float((uint32_t)src[tail + tid] << 16);
 }
 
 void launch_widen_bf16(const WidenSet& set, int n_nets, int64_t count, hipStream_t st) {
