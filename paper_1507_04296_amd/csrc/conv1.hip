@@ -133,8 +133,10 @@ struct Conv1WgradB {  // input bytes rows (c,u,v), RMAJ quads along v at one pix
         const int m = kc * BK + kk[j];
         const int mm = m < npix ? m : 0;
         const int b = mm / P1, p = mm - b * P1, i = p / H1, jj = p - i * H1;
+        // pixels past the end read pixel 0 (the A operand is zero there); a
+        // zero-filled frame (null pointer) is zeros
         const uint8_t* f = ftab[(int64_t)b * 4 + chan[j]];
-        const bool ok = m < npix && f != nullptr;
+        const bool ok = f != nullptr;
         const uint32_t d = ldg_u32((ok ? f : safe) + (S1 * i) * IN_W + S1 * jj + off[j]);
         return sel4(ok, f32x4{(float)(d & 255u), (float)((d >> 8) & 255u),
                               (float)((d >> 16) & 255u), (float)(d >> 24)});

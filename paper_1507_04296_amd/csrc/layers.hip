@@ -82,17 +82,16 @@ struct Conv2FwdA {
     const float* h1;
     int rows, m0;
     const float* base[MAXQ];
-    bool ok[MAXQ];
     __device__ void init(int j, int row, int k) {
         const int m = m0 + row;
         const int mm = m < rows ? m : 0;
         const int b = mm / P2, p = mm - b * P2, i = p / H2, jj = p - i * H2;
         base[j] = h1 + (((int64_t)b * H1 + S2 * i) * H1 + S2 * jj) * C1 + k;
-        ok[j] = m < rows;
     }
+    // rows past the end read row 0 (finite values) and are never stored
     __device__ f32x4 load(int kc, int j) const {
         const int u = kc >> 2, v = kc & 3;
-        return sel4(ok[j], ld4(base[j] + (u * H1 + v) * C1));
+        return ld4(base[j] + (u * H1 + v) * C1);
     }
 };
 struct WtapB {  // transposed weights w[tap][row][k]; per_tap chunks of 32 k per tap
@@ -154,17 +153,16 @@ struct Conv3FwdB {
     const float* h2;
     int rows, m0;
     const float* base[MAXQ];
-    bool ok[MAXQ];
     __device__ void init(int j, int row, int k) {
         const int m = m0 + row;
         const int mm = m < rows ? m : 0;
         const int b = mm / P3, p = mm - b * P3, i = p / H3, jj = p - i * H3;
         base[j] = h2 + (((int64_t)b * H2 + i) * H2 + jj) * C2 + k;
-        ok[j] = m < rows;
     }
+    // columns past the end read pixel 0 (finite values) and are never stored
     __device__ f32x4 load(int kc, int j) const {
         const int t = kc >> 1, u = t / 3, v = t - u * 3;
-        return sel4(ok[j], ld4(base[j] + (u * H2 + v) * C2 + (kc & 1) * BK));
+        return ld4(base[j] + (u * H2 + v) * C2 + (kc & 1) * BK);
     }
 };
 struct Conv3FwdStore {  // row = o, col = pixel index within the tile
@@ -215,12 +213,12 @@ struct RowMajorK {  // rows of a row-major [rows][ld] matrix, quads along k
     const float* a;
     int rows, r0, ld;
     const float* base[MAXQ];
-    bool ok[MAXQ];
+    // rows past the end read row 0 (finite values); they are output rows or
+    // columns that are never stored
     __device__ void init(int j, int row, int k) {
-        ok[j] = r0 + row < rows;
-        base[j] = a + (int64_t)(ok[j] ? r0 + row : 0) * ld + k;
+        base[j] = a + (int64_t)(r0 + row < rows ? r0 + row : 0) * ld + k;
     }
-    __device__ f32x4 load(int kc, int j) const { return sel4(ok[j], ld4(base[j] + kc * BK)); }
+    __device__ f32x4 load(int kc, int j) const { return ld4(base[j] + kc * BK); }
 };
 struct PlainStore {
     float* out;
@@ -446,15 +444,13 @@ struct Conv3DgradA {  // KMAJ quads dz3[b][p][o..o+3] at p = (y-u)*7 + (x-v)
     const float* dz3;
     int n, b0, y, x, u0, v0, nv;
     const float* base[MAXQ];
-    bool ok[MAXQ];
     __device__ void init(int j, int row, int k) {
         const int b = b0 + row;
-        ok[j] = b < n;
-        base[j] = dz3 + (int64_t)(ok[j] ? b : 0) * FLAT + k;
+        base[j] = dz3 + (int64_t)(b < n ? b : 0) * FLAT + k;  // rows past n: never stored
     }
     __device__ f32x4 load(int kc, int j) const {
         const int t = kc >> 1, u = u0 + t / nv, v = v0 + t % nv;
-        return sel4(ok[j], ld4(base[j] + ((y - u) * H3 + (x - v)) * C3 + (kc & 1) * BK));
+        return ld4(base[j] + ((y - u) * H3 + (x - v)) * C3 + (kc & 1) * BK);
     }
 };
 struct Conv3DgradB {  // w3d[(u,v)][c][o], rows c, quads along o
@@ -535,7 +531,8 @@ struct Conv3WgradB {  // RMAJ quads: 4 channels of h2 at one (pixel, tap)
         const int mm = m < npix ? m : 0;
         const int b = mm / P3, p = mm - b * P3, i = p / H3, jj = p - i * H3;
         const int u = tap / 3, v = tap - u * 3;
-        return sel4(m < npix, ld4(h2 + (((int64_t)b * H2 + i + u) * H2 + jj + v) * C2 + c0[j]));
+        // pixels past the end read pixel 0; the A operand is zero there
+        return ld4(h2 + (((int64_t)b * H2 + i + u) * H2 + jj + v) * C2 + c0[j]);
     }
 };
 
@@ -592,15 +589,13 @@ struct Conv2DgradA {  // KMAJ quads dz2[b][i][j][o..o+3]
     const float* dz2;
     int n, b0, yy, xx, du0, dv0, ndv;
     const float* base[MAXQ];
-    bool ok[MAXQ];
     __device__ void init(int j, int row, int k) {
         const int b = b0 + row;
-        ok[j] = b < n;
-        base[j] = dz2 + (int64_t)(ok[j] ? b : 0) * P2 * C2 + k;
+        base[j] = dz2 + (int64_t)(b < n ? b : 0) * P2 * C2 + k;  // rows past n: never stored
     }
     __device__ f32x4 load(int kc, int j) const {
         const int t = kc >> 1, du = du0 + t / ndv, dv = dv0 + t % ndv;
-        return sel4(ok[j], ld4(base[j] + ((yy - du) * H2 + (xx - dv)) * C2 + (kc & 1) * BK));
+        return ld4(base[j] + ((yy - du) * H2 + (xx - dv)) * C2 + (kc & 1) * BK);
     }
 };
 struct Conv2DgradB {  // w2p[(du,dv)][phase][c][o], rows (phase, c), quads along o
@@ -689,7 +684,8 @@ struct Conv2WgradB {  // h1 quads along c at one (pixel, tap)
         const int m = kc * BK + kk[j];
         const int mm = m < npix ? m : 0;
         const int b = mm / P2, p = mm - b * P2, i = p / H2, jj = p - i * H2;
-        return sel4(m < npix, ld4(h1 + (((int64_t)b * H1 + S2 * i) * H1 + S2 * jj) * C1 + off[j]));
+        // pixels past the end read pixel 0; the A operand is zero there
+        return ld4(h1 + (((int64_t)b * H1 + S2 * i) * H1 + S2 * jj) * C1 + off[j]);
     }
 };
 
