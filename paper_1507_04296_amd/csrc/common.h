@@ -17,6 +17,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 namespace gorila {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -81,10 +84,20 @@ struct LdsTile {
     static constexpr int QUADS = ROWS * BK / 4;
     static constexpr int NQ = (QUADS + 255) / 256;   // quads per thread
 
-    // Tile coordinates (row, k) of the first element of quad e.
-    __device__ static inline void quad_coord(int e, int& row, int& k) {
-        if (MODE == KMAJ) { row = e / (BK / 4); k = (e % (BK / 4)) * 4; }
-        else              { k = e / (ROWS / 4); row = (e % (ROWS / 4)) * 4; }
+    // Tile coordinates (row, k) of the first element of quad j of thread t.
+    // RMAJ: all NQ quads of a thread share one k (rows 4s, 4(s + S), ... with
+    // S = ROWS / (4 NQ) threads per k), so a loader can decompose the
+    // reduction index once per chunk for all of them.
+    __device__ static inline void quad_coord(int t, int j, int& row, int& k) {
+        if (MODE == KMAJ) {
+            const int e = t + 256 * j;
+            row = e / (BK / 4);
+            k = (e % (BK / 4)) * 4;
+        } else {
+            constexpr int S = ROWS / 4 / NQ;  // threads per k
+            k = t / S;
+            row = ((t % S) + S * j) * 4;
+        }
     }
     __device__ static inline void put(float* s, int row, int k, f32x4 v) {
         if (MODE == KMAJ) *(f32x4*)(s + row * LD + k) = v;
@@ -102,8 +115,13 @@ struct LdsTile {
     }
 };
 
-// Loaders keep per-quad state in arrays of MAXQ entries.
+// Loaders keep per-quad state in arrays of MAXQ entries.  A loader may also
+// have prep(kc), called once per chunk before its load(kc, j) calls (an RMAJ
+// loader's quads share one k, so per-k work can be done there once).
 constexpr int MAXQ = 4;
+template <class T, class = void> struct HasPrep : std::false_type {};
+template <class T>
+struct HasPrep<T, std::void_t<decltype(std::declval<T&>().prep(0))>> : std::true_type {};
 
 template <int BM, int BN, int AMODE, int BMODE>
 struct GemmShape {
@@ -144,6 +162,8 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
     static_assert(TM * 32 == WM && TN * 32 == WN, "wave tile must be a multiple of 32");
     static_assert(LA::NQ <= MAXQ && LB::NQ <= MAXQ, "loader state arrays hold MAXQ quads");
     static_assert(LA::QUADS % 256 == 0 && LB::QUADS % 256 == 0, "every thread owns whole quads");
+    static_assert((AMODE == KMAJ || (BM / 4) % LA::NQ == 0) && (BMODE == KMAJ || (BN / 4) % LB::NQ == 0),
+                  "RMAJ tiles split each k's quads evenly over a thread's quads");
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave % WAVES_M, wn = wave / WAVES_M;
@@ -151,12 +171,12 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
     int qa_row[LA::NQ], qa_k[LA::NQ], qb_row[LB::NQ], qb_k[LB::NQ];
 #pragma unroll
     for (int j = 0; j < LA::NQ; ++j) {
-        LA::quad_coord(tid + 256 * j, qa_row[j], qa_k[j]);
+        LA::quad_coord(tid, j, qa_row[j], qa_k[j]);
         la.init(j, qa_row[j], qa_k[j]);
     }
 #pragma unroll
     for (int j = 0; j < LB::NQ; ++j) {
-        LB::quad_coord(tid + 256 * j, qb_row[j], qb_k[j]);
+        LB::quad_coord(tid, j, qb_row[j], qb_k[j]);
         lb.init(j, qb_row[j], qb_k[j]);
     }
 
@@ -176,6 +196,8 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
     // with (kc - kc_begin) % 2 == s.
     f32x4 ra0[LA::NQ], rb0[LB::NQ], ra1[LA::NQ], rb1[LB::NQ];
     auto gload = [&](int kc, f32x4* ra, f32x4* rb) {
+        if constexpr (HasPrep<LoadA>::value) la.prep(kc);
+        if constexpr (HasPrep<LoadB>::value) lb.prep(kc);
 #pragma unroll
         for (int j = 0; j < LA::NQ; ++j) ra[j] = la.load(kc, j);
 #pragma unroll

@@ -129,15 +129,20 @@ struct Conv1WgradB {  // input bytes rows (c,u,v), RMAJ quads along v at one pix
         off[j] = ((kr >> 3) & 7) * IN_W + (kr & 7);
         kk[j] = k;
     }
-    __device__ f32x4 load(int kc, int j) const {
-        const int m = kc * BK + kk[j];
-        const int mm = m < npix ? m : 0;
+    const uint8_t* const* fsample = nullptr;  // this chunk's sample's frame pointers
+    int poff = 0;                              // this chunk's pixel within a frame
+    __device__ void prep(int kc) {  // the thread's quads share one pixel
+        const int m = kc * BK + kk[0];
+        const int mm = m < npix ? m : 0;  // past the end: pixel 0 (A is zero there)
         const int b = mm / P1, p = mm - b * P1, i = p / H1, jj = p - i * H1;
-        // pixels past the end read pixel 0 (the A operand is zero there); a
-        // zero-filled frame (null pointer) is zeros
-        const uint8_t* f = ftab[(int64_t)b * 4 + chan[j]];
+        fsample = ftab + (int64_t)b * 4;
+        poff = (S1 * i) * IN_W + S1 * jj;
+    }
+    __device__ f32x4 load(int, int j) const {
+        // a zero-filled frame (null pointer) is zeros
+        const uint8_t* f = fsample[chan[j]];
         const bool ok = f != nullptr;
-        const uint32_t d = ldg_u32((ok ? f : safe) + (S1 * i) * IN_W + S1 * jj + off[j]);
+        const uint32_t d = ldg_u32((ok ? f : safe) + poff + off[j]);
         return sel4(ok, f32x4{(float)(d & 255u), (float)((d >> 8) & 255u),
                               (float)((d >> 16) & 255u), (float)(d >> 24)});
     }

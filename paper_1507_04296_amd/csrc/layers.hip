@@ -274,7 +274,11 @@ int launch_fc1_fwd(const float* h3, const GroupPtrs& theta, int groups, int n, f
 // fc1 data gradient: dz3 = [h3 > 0] * (W4^T dz4), rows b, cols k (3136 = 49
 // tiles), reduction o (16 chunks); dz3 is written as [b][p][o].
 // ---------------------------------------------------------------------------
-struct RowMajorR {  // B[col][k] = M[k][c0 + col] of a row-major [k][ld] matrix (RMAJ quads)
+// B[col][k] = M[k][c0 + col] of a row-major [k][ld] matrix (RMAJ quads).
+// Reduction indices k >= kmax read row 0; ZERO makes them zeros (one operand
+// of a padded reduction must be zero there, the other only finite).
+template <bool ZERO>
+struct RowMajorR {
     const float* a;
     int c0, ld, kmax;
     const float* base[MAXQ];
@@ -282,7 +286,8 @@ struct RowMajorR {  // B[col][k] = M[k][c0 + col] of a row-major [k][ld] matrix 
     __device__ void init(int j, int row, int k) { base[j] = a + c0 + row; kk[j] = k; }
     __device__ f32x4 load(int kc, int j) const {
         const int k = kc * BK + kk[j];
-        return sel4(k < kmax, ld4(base[j] + (int64_t)(k < kmax ? k : 0) * ld));
+        const f32x4 v = ld4(base[j] + (int64_t)(k < kmax ? k : 0) * ld);
+        return ZERO ? sel4(k < kmax, v) : v;
     }
 };
 
@@ -324,7 +329,7 @@ struct Fc1DgradJob {
         const int r0 = (t % mt) * 64, c0 = (t / mt) * 64;  // row tiles of one W4 column block adjacent
         const int64_t rows = (int64_t)g * n;
         RowMajorK la{dz4 + rows * HID, n, r0, HID};
-        RowMajorR lb{theta.p[g] + OFF_W4, c0, FLAT, HID};
+        RowMajorR<false> lb{theta.p[g] + OFF_W4, c0, FLAT, HID};  // HID is a whole number of chunks
         Dz3NhwcStore epi{dz3 + rows * FLAT, h3 + rows * FLAT, n, r0, c0};
         mfma_gemm<64, 64, 2, KMAJ, RMAJ>(smem, 0, HID / BK, la, lb, epi);
     }
@@ -352,8 +357,8 @@ struct Fc1WgradJob {
         const int r0 = (t % (HID / 64)) * 64, c0 = (t / (HID / 64)) * 64;
         const int64_t rows = (int64_t)g * n;
         float* gr = grads + g * grads_stride;
-        RowMajorR la{dz4 + rows * HID, r0, HID, n};
-        RowMajorR lb{h3 + rows * FLAT, c0, FLAT, n};
+        RowMajorR<true> la{dz4 + rows * HID, r0, HID, n};
+        RowMajorR<false> lb{h3 + rows * FLAT, c0, FLAT, n};
         PlainStore epi{gr + OFF_W4, HID, r0, c0, FLAT};
         // db4[o] = sum_b dz4[b][o]: the row sums of this GEMM's A operand
         float* rs = c0 == 0 ? gr + OFF_B4 + r0 : nullptr;
@@ -525,15 +530,16 @@ struct Conv3WgradB {  // RMAJ quads: 4 channels of h2 at one (pixel, tap)
     const float* h2;
     int npix, tap;
     int c0[MAXQ], kk[MAXQ];
+    const float* pix = nullptr;  // h2 at this chunk's (pixel, tap), set by prep
     __device__ void init(int j, int row, int k) { c0[j] = row; kk[j] = k; }
-    __device__ f32x4 load(int kc, int j) const {
-        const int m = kc * BK + kk[j];
-        const int mm = m < npix ? m : 0;
+    __device__ void prep(int kc) {  // the thread's quads share one pixel
+        const int m = kc * BK + kk[0];
+        const int mm = m < npix ? m : 0;  // past the end: pixel 0 (A is zero there)
         const int b = mm / P3, p = mm - b * P3, i = p / H3, jj = p - i * H3;
         const int u = tap / 3, v = tap - u * 3;
-        // pixels past the end read pixel 0; the A operand is zero there
-        return ld4(h2 + (((int64_t)b * H2 + i + u) * H2 + jj + v) * C2 + c0[j]);
+        pix = h2 + (((int64_t)b * H2 + i + u) * H2 + jj + v) * C2;
     }
+    __device__ f32x4 load(int, int j) const { return ld4(pix + c0[j]); }
 };
 
 struct Conv3WgradJob {
@@ -680,13 +686,14 @@ struct Conv2WgradB {  // h1 quads along c at one (pixel, tap)
         off[j] = ((t >> 2) * H1 + (t & 3)) * C1 + c0;
         kk[j] = k;
     }
-    __device__ f32x4 load(int kc, int j) const {
-        const int m = kc * BK + kk[j];
-        const int mm = m < npix ? m : 0;
+    const float* pix = nullptr;  // h1 at this chunk's pixel, set by prep
+    __device__ void prep(int kc) {  // the thread's quads share one pixel
+        const int m = kc * BK + kk[0];
+        const int mm = m < npix ? m : 0;  // past the end: pixel 0 (A is zero there)
         const int b = mm / P2, p = mm - b * P2, i = p / H2, jj = p - i * H2;
-        // pixels past the end read pixel 0; the A operand is zero there
-        return ld4(h1 + (((int64_t)b * H1 + S2 * i) * H1 + S2 * jj) * C1 + off[j]);
+        pix = h1 + (((int64_t)b * H1 + S2 * i) * H1 + S2 * jj) * C1;
     }
+    __device__ f32x4 load(int, int j) const { return ld4(pix + off[j]); }
 };
 
 struct Conv2WgradJob {
