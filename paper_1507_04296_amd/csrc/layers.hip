@@ -94,16 +94,17 @@ struct Conv2FwdA {
         return ld4(base[j] + (u * H1 + v) * C1);
     }
 };
-struct WtapB {  // transposed weights w[tap][row][k]; per_tap chunks of 32 k per tap
+// Transposed weights w[tap][row][k] with LDK k per row (LDK / BK chunks per
+// tap) and ROWS rows per tap.
+template <int LDK, int ROWS>
+struct WtapB {
+    static constexpr int PER_TAP = LDK / BK;
     const float* w;
-    int ldk;      // k extent of one row
-    int per_tap;  // chunks per tap
-    int rows;     // rows per tap
     const float* base[MAXQ];
-    __device__ void init(int j, int row, int k) { base[j] = w + (int64_t)row * ldk + k; }
+    __device__ void init(int j, int row, int k) { base[j] = w + row * LDK + k; }
     __device__ f32x4 load(int kc, int j) const {
-        const int t = kc / per_tap, part = kc - t * per_tap;
-        return ld4(base[j] + (int64_t)t * rows * ldk + part * BK);
+        const int t = kc / PER_TAP, part = kc - t * PER_TAP;
+        return ld4(base[j] + t * (ROWS * LDK) + part * BK);
     }
 };
 struct BiasReluStore {
@@ -132,7 +133,7 @@ struct Conv2FwdJob {
         const int g = t / tiles(), m0 = (t % tiles()) * 64;
         const int rows = n * P2;
         Conv2FwdA la{h1 + (int64_t)g * n * P1 * C1, rows, m0};
-        WtapB lb{w2t.p[g], C1, 1, C2};
+        WtapB<C1, C2> lb{w2t.p[g]};
         BiasReluStore epi{h2 + (int64_t)g * n * P2 * C2, theta.p[g] + OFF_B2, rows, m0, C2};
         mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, 0, 16, la, lb, epi);
     }
@@ -192,7 +193,7 @@ struct Conv3FwdJob {
         if (t >= tiles() * groups) return;
         const int g = t / tiles(), m0 = (t % tiles()) * 64;
         const int rows = n * P3;
-        WtapB la{w3t.p[g], C2, 2, C3};
+        WtapB<C2, C3> la{w3t.p[g]};
         Conv3FwdB lb{h2 + (int64_t)g * n * P2 * C2, rows, m0};
         Conv3FwdStore epi{h3 + (int64_t)g * n * FLAT, theta.p[g] + OFF_B3, rows, m0};
         mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, 0, 18, la, lb, epi);
