@@ -60,7 +60,10 @@ constexpr unsigned ERR_IDX_RANGE = 1u, ERR_ACTION_RANGE = 2u;
 // C = sum_k A[row][k] * B[col][k] with v_mfma_f32_32x32x2_f32.  The reduction
 // runs in chunks of BK = 32 that are staged through LDS, double buffered, one
 // barrier per chunk.  Each operand tile lives in LDS in one of two layouts:
-//   KMAJ: [rows][BK + 4]   (reduction index contiguous; read as one b128)
+//   KMAJ: [rows][BK]       (reduction index contiguous; read as one b128;
+//                           the 8 quads of row r are stored XOR-permuted by
+//                           (r ^ r >> 3) & 7, so 16 consecutive rows read or
+//                           written at one quad cover every LDS bank once)
 //   RMAJ: [BK][rows + 4]   (row index contiguous; read as four b32)
 // and is filled from global memory in 16-byte quads that are contiguous in
 // the operand's natural global layout: along k for KMAJ, along rows for RMAJ.
@@ -79,7 +82,10 @@ enum { KMAJ = 0, RMAJ = 1 };
 
 template <int ROWS, int MODE>
 struct LdsTile {
-    static constexpr int LD = MODE == KMAJ ? BK + 4 : ROWS + 4;
+    static constexpr int LD = MODE == KMAJ ? BK : ROWS + 4;
+    __device__ static inline int swz(int row, int k) {  // KMAJ: k of quad (k / 4) in LDS
+        return (((k >> 2) ^ (row ^ (row >> 3))) & 7) << 2;
+    }
     static constexpr int SIZE = MODE == KMAJ ? ROWS * LD : BK * LD;  // floats
     static constexpr int QUADS = ROWS * BK / 4;
     static constexpr int NQ = (QUADS + 255) / 256;   // quads per thread
@@ -100,12 +106,12 @@ struct LdsTile {
         }
     }
     __device__ static inline void put(float* s, int row, int k, f32x4 v) {
-        if (MODE == KMAJ) *(f32x4*)(s + row * LD + k) = v;
+        if (MODE == KMAJ) *(f32x4*)(s + row * LD + swz(row, k)) = v;
         else              *(f32x4*)(s + k * LD + row) = v;
     }
     // Values (row r, k = kb .. kb+3).
     __device__ static inline f32x4 get(const float* s, int r, int kb) {
-        if (MODE == KMAJ) return *(const f32x4*)(s + r * LD + kb);
+        if (MODE == KMAJ) return *(const f32x4*)(s + r * LD + swz(r, kb));
         f32x4 v;
         v[0] = s[(kb + 0) * LD + r];
         v[1] = s[(kb + 1) * LD + r];
@@ -122,6 +128,10 @@ constexpr int MAXQ = 4;
 template <class T, class = void> struct HasPrep : std::false_type {};
 template <class T>
 struct HasPrep<T, std::void_t<decltype(std::declval<T&>().prep(0))>> : std::true_type {};
+// An epilogue with `static constexpr bool MASK = true` only tests pre > 0.
+template <class T, class = void> struct IsMaskEpi : std::false_type {};
+template <class T>
+struct IsMaskEpi<T, std::void_t<decltype(T::MASK)>> : std::bool_constant<T::MASK> {};
 
 template <int BM, int BN, int AMODE, int BMODE>
 struct GemmShape {
@@ -142,7 +152,9 @@ struct GemmShape {
 // that output element (a ReLU mask, a bias, or 0 when it needs none); it is
 // called for every accumulator element before the reduction loop, so its
 // loads overlap the loop instead of waiting behind the epilogue's own stores.
-// epi(row, col, value, pre) then writes the element.
+// epi(row, col, value, pre) then writes the element.  A mask epilogue's
+// values are kept as one bit per element (pre > 0), 16 bits per accumulator
+// tile instead of 16 registers, and handed back as 1 or 0.
 //
 // The chunk loop is unrolled by two so that the LDS buffer and the register
 // set of every access are compile-time constants: LDS is then addressed with
@@ -180,7 +192,9 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
         lb.init(j, qb_row[j], qb_k[j]);
     }
 
+    constexpr bool MASK = IsMaskEpi<Epi>::value;
     f32x16 acc[TM][TN], pre[TM][TN];
+    uint32_t bits[TM][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -191,6 +205,17 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
                 pre[i][j][r] = epi.pre(wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3),
                                        wn * WN + j * 32 + (lane & 31));
         }
+    auto pack_mask = [&]() {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                uint32_t b = 0;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) b |= (pre[i][j][r] > 0.0f ? 1u : 0u) << r;
+                bits[i][j] = b;
+            }
+    };
 
     // Register sets 0/1 hold chunks fetched ahead; set s always holds chunks
     // with (kc - kc_begin) % 2 == s.
@@ -242,18 +267,27 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
         if (kc_begin + 1 < kc_end) gload(kc_begin + 1, ra1, rb1);
         sstore(smem, ra0, rb0);
     }
+    // the mask loads were issued before the first chunk's, whose data is in
+    // LDS by now, so packing them here waits for nothing more
+    if constexpr (MASK) pack_mask();
     __syncthreads();
-    for (int kc = kc_begin; kc < kc_end; kc += 2) {
+    // One exit, so the accumulators stay in the same registers on every trip
+    // (an exit between the two halves makes the compiler copy them).
+    int kc = kc_begin;
+    for (; kc + 1 < kc_end; kc += 2) {
         // even chunk: LDS buffer 0, refill register set 0 with chunk kc+2
         if (kc + 2 < kc_end) gload(kc + 2, ra0, rb0);
         compute(smem);
-        if (kc + 1 < kc_end) sstore(smem + STAGE, ra1, rb1);
+        sstore(smem + STAGE, ra1, rb1);
         __syncthreads();
-        if (kc + 1 >= kc_end) break;
         // odd chunk: LDS buffer 1, refill register set 1 with chunk kc+3
         if (kc + 3 < kc_end) gload(kc + 3, ra1, rb1);
         compute(smem + STAGE);
         if (kc + 2 < kc_end) sstore(smem, ra0, rb0);
+        __syncthreads();
+    }
+    if (kc < kc_end) {  // an odd chunk count ends in buffer 0
+        compute(smem);
         __syncthreads();
     }
     if (BM <= 64 && do_rowsum) {
@@ -263,15 +297,23 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
         if (tid < BM) rowsum_out[tid] = ((smem[tid] + smem[64 + tid]) + smem[128 + tid]) + smem[192 + tid];
     }
 
+    // The epilogue's element coordinates come from an opaque copy of the
+    // lane index, so its address arithmetic is redone here instead of being
+    // shared with the prologue's pre() and held in registers across the loop.
+    int elane = lane;
+    asm volatile("" : "+v"(elane));
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                int row = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                int col = wn * WN + j * 32 + (lane & 31);
-                epi(row, col, acc[i][j][r], pre[i][j][r]);
+                int row = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (elane >> 5) + (r & 3);
+                int col = wn * WN + j * 32 + (elane & 31);
+                if constexpr (MASK)
+                    epi(row, col, acc[i][j][r], (bits[i][j] >> r) & 1u ? 1.0f : 0.0f);
+                else
+                    epi(row, col, acc[i][j][r], pre[i][j][r]);
             }
 }
 

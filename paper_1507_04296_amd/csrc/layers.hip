@@ -296,6 +296,7 @@ struct RowMajorR {
 // pixel-major ([b][p][o], like the other activation gradients) so that the
 // conv3 backward kernels read it in 16-byte quads.
 struct Dz3NhwcStore {
+    static constexpr bool MASK = true;
     float* dz3;
     const float* h3;
     int rows, r0, c0;
@@ -470,6 +471,7 @@ struct Conv3DgradB {  // w3d[(u,v)][c][o], rows c, quads along o
     }
 };
 struct Conv3DgradStore {
+    static constexpr bool MASK = true;
     float* dz2;
     const float* h2;
     int n, b0, pos;
@@ -616,6 +618,7 @@ struct Conv2DgradB {  // w2p[(du,dv)][phase][c][o], rows (phase, c), quads along
     }
 };
 struct Conv2DgradStore {
+    static constexpr bool MASK = true;
     float* dz1;
     const float* h1;
     int n, b0, yy, xx;
