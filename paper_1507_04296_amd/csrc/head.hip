@@ -15,8 +15,7 @@
 
 namespace gorila {
 
-__device__ inline float dot8(const float* h, const float* w) {
-    const f32x4 w0 = ld4(w), w1 = ld4(w + 4);
+__device__ inline float dot8(const float* h, f32x4 w0, f32x4 w1) {
     float s = h[0] * w0[0];
     s = fmaf(h[1], w0[1], s);
     s = fmaf(h[2], w0[2], s);
@@ -26,6 +25,26 @@ __device__ inline float dot8(const float* h, const float* w) {
     s = fmaf(h[6], w1[2], s);
     s = fmaf(h[7], w1[3], s);
     return s;
+}
+
+// out[j] = b5[k] + sum_i h4[i] W5[k][i] for k = k0 + j, j < HB (k < A
+// matter; later ones repeat row A - 1).  All HB rows are loaded before the
+// first dot product and the HB butterfly sums are independent, so a block of
+// actions costs one memory round trip instead of one per action.
+constexpr int HB = 6;
+__device__ inline void head_rows(const float* h, const float* W5, const float* b5, int k0, int A,
+                                 int lane, float* out) {
+    f32x4 w0[HB], w1[HB];
+#pragma unroll
+    for (int j = 0; j < HB; ++j) {
+        const float* w = W5 + min(k0 + j, A - 1) * HID + lane * 8;
+        w0[j] = ld4(w);
+        w1[j] = ld4(w + 4);
+    }
+#pragma unroll
+    for (int j = 0; j < HB; ++j) out[j] = dot8(h, w0[j], w1[j]);
+#pragma unroll
+    for (int j = 0; j < HB; ++j) out[j] = wave_sum(out[j]) + b5[min(k0 + j, A - 1)];
 }
 
 // h[0..7] = relu(b4[8l..] + sum_s part[s][b][8l..]) for one row b.
@@ -75,10 +94,17 @@ __global__ __launch_bounds__(256) void q_head_kernel(const float* __restrict__ f
     const float* b5 = theta + off_b5(A);
     float best = 0.0f;
     int best_a = 0;
-    for (int k = 0; k < A; ++k) {
-        const float s = wave_sum(dot8(h, W5 + k * HID + lane * 8)) + b5[k];
-        if (q && lane == 0) q[(int64_t)b * A + k] = s;
-        if (k == 0 || s > best) { best = s; best_a = k; }  // lowest index among the maxima
+    for (int k0 = 0; k0 < A; k0 += HB) {
+        float qs[HB];
+        head_rows(h, W5, b5, k0, A, lane, qs);
+#pragma unroll
+        for (int j = 0; j < HB; ++j) {
+            const int k = k0 + j;
+            if (k >= A) break;
+            const float s = qs[j];
+            if (q && lane == 0) q[(int64_t)b * A + k] = s;
+            if (k == 0 || s > best) { best = s; best_a = k; }  // lowest index among the maxima
+        }
     }
     if (actions && lane == 0) {
         const uint64_t G = 0x9E3779B97F4A7C15ull;
@@ -135,15 +161,22 @@ __global__ __launch_bounds__(256) void td_head_kernel(
     const float* b5t = theta_t + off_b5(A);
     const int ab = a[b];
     float q_sa = 0.0f, m = 0.0f;
-    for (int k = 0; k < A; ++k) {
-        const float s = wave_sum(dot8(h, W5 + k * HID + lane * 8)) + b5[k];
-        const float st = wave_sum(dot8(ht, W5t + k * HID + lane * 8)) + b5t[k];
-        if (lane == 0) {
-            q[(int64_t)bl * A + k] = s;
-            q[(int64_t)(n + bl) * A + k] = st;
+    for (int k0 = 0; k0 < A; k0 += HB) {
+        float qs[HB], qt[HB];
+        head_rows(h, W5, b5, k0, A, lane, qs);
+        head_rows(ht, W5t, b5t, k0, A, lane, qt);
+#pragma unroll
+        for (int j = 0; j < HB; ++j) {
+            const int k = k0 + j;
+            if (k >= A) break;
+            const float s = qs[j], st = qt[j];
+            if (lane == 0) {
+                q[(int64_t)bl * A + k] = s;
+                q[(int64_t)(n + bl) * A + k] = st;
+            }
+            if (k == ab) q_sa = s;
+            m = k == 0 ? st : fmaxf(m, st);  // max_a' Q(s', a'; theta-)
         }
-        if (k == ab) q_sa = s;
-        m = k == 0 ? st : fmaxf(m, st);  // max_a' Q(s', a'; theta-)
     }
     const float y = term[b] ? r[b] : r[b] + gamma * m;
     const float d = y - q_sa;

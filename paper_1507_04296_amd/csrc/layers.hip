@@ -396,7 +396,21 @@ struct HeadPartialJob {
         const int b0 = g * n + bb * rows_per_block, b1 = g * n + min(n, (bb + 1) * rows_per_block);
         float* out = hpart + (int64_t)gbb * HP_STRIDE;
         for (int j = 0; j < A; ++j) sacc[bq][j][kl] = 0.0f;
-        for (int b = b0 + bq; b < b1; b += 4) {
+        int b = b0 + bq;
+        for (; b + 12 < b1; b += 16) {  // four rows a trip, their loads issued together
+            int ab[4];
+            float cf[4], hv[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                ab[u] = a[b + 4 * u];
+                cf[u] = coef[b + 4 * u];
+                hv[u] = h4[(int64_t)(b + 4 * u) * HID + k];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                sacc[bq][ab[u]][kl] = fmaf(cf[u], hv[u], sacc[bq][ab[u]][kl]);
+        }
+        for (; b < b1; b += 4) {
             const int ab = a[b];
             sacc[bq][ab][kl] = fmaf(coef[b], h4[(int64_t)b * HID + k], sacc[bq][ab][kl]);
         }
