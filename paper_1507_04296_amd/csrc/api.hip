@@ -198,10 +198,11 @@ int forward_one(gorila_ctx* c, const Plan& p, const gorila_params* prm, const ui
     th.p[0] = theta;
     w2t.p[0] = wv.w2t;
     w3t.p[0] = wv.w3t;
-    { StageTimer t(c, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 1, n, at<float>(c, p.h1), st); }
-    { StageTimer t(c, ST_CONV2_FWD); launch_conv2_fwd(at<float>(c, p.h1), w2t, th, 1, n, at<float>(c, p.h2), st); }
-    { StageTimer t(c, ST_CONV3_FWD); launch_conv3_fwd(at<float>(c, p.h2), w3t, th, 1, n, at<float>(c, p.h3), st); }
-    { StageTimer t(c, ST_FC1_FWD); *fc1_splits = launch_fc1_fwd(at<float>(c, p.h3), th, 1, n, at<float>(c, p.fc1part), st); }
+    // forward-only calls compute in fp32 (bf16 parameters are widened exactly)
+    { StageTimer t(c, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 1, n, at<float>(c, p.h1), false, st); }
+    { StageTimer t(c, ST_CONV2_FWD); launch_conv2_fwd(at<float>(c, p.h1), w2t, th, 1, n, at<float>(c, p.h2), false, st); }
+    { StageTimer t(c, ST_CONV3_FWD); launch_conv3_fwd(at<float>(c, p.h2), w3t, th, 1, n, at<float>(c, p.h3), false, st); }
+    { StageTimer t(c, ST_FC1_FWD); *fc1_splits = launch_fc1_fwd(at<float>(c, p.h3), th, 1, n, at<float>(c, p.fc1part), false, st); }
     return check_launch();
 }
 
@@ -402,18 +403,18 @@ namespace {
 // Shared launch sequence of the learner calls: G learner groups of b
 // transitions each, group g on parameter set params[g] and minibatch
 // idx[g*b .. g*b+b-1], all against one target set.
-int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G,
+int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allow_bf16,
                   const gorila_params* target_params, const gorila_replay* replay,
                   const int64_t* idx, int b, float gamma, float clip_delta, float* grads_out,
                   float* loss_out) {
     int rc = check_ctx(ctx);
     if (rc) return rc;
     if (G < 1 || G > MAX_LEARNER_GROUPS || !params) return GORILA_EINVAL;
-    if ((rc = check_params(target_params, G > 1))) return rc;
+    if ((rc = check_params(target_params, allow_bf16))) return rc;
     const int A = target_params->n_actions;
     int n_bf16 = target_params->dtype == GORILA_BF16;
     for (int g = 0; g < G; ++g) {
-        if ((rc = check_params(&params[g], G > 1))) return rc;
+        if ((rc = check_params(&params[g], allow_bf16))) return rc;
         if (params[g].n_actions != A) return GORILA_EINVAL;
         n_bf16 += params[g].dtype == GORILA_BF16;
     }
@@ -422,6 +423,8 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G,
     if ((int64_t)b * G > (int64_t)1 << 30) return GORILA_EINVAL;
     if (!(gamma >= 0.0f && gamma <= 1.0f) || !(clip_delta > 0.0f)) return GORILA_EINVAL;
     const int B = b * G;  // all learner rows
+    // bf16 MFMA products when every parameter set is bf16, fp32 otherwise
+    const bool bf16 = n_bf16 == G + 1;
     const Plan p = make_plan(2 * (int64_t)B, B, A, G, n_bf16);
     if (p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
     hipStream_t st = ctx->stream;
@@ -469,11 +472,11 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G,
     float* h3 = at<float>(ctx, p.h3);
     float* h4 = at<float>(ctx, p.h4);
     float* fc1part = at<float>(ctx, p.fc1part);
-    { StageTimer t(ctx, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 2 * G, b, h1, st); }
-    { StageTimer t(ctx, ST_CONV2_FWD); launch_conv2_fwd(h1, w2t, th, 2 * G, b, h2, st); }
-    { StageTimer t(ctx, ST_CONV3_FWD); launch_conv3_fwd(h2, w3t, th, 2 * G, b, h3, st); }
+    { StageTimer t(ctx, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 2 * G, b, h1, bf16, st); }
+    { StageTimer t(ctx, ST_CONV2_FWD); launch_conv2_fwd(h1, w2t, th, 2 * G, b, h2, bf16, st); }
+    { StageTimer t(ctx, ST_CONV3_FWD); launch_conv3_fwd(h2, w3t, th, 2 * G, b, h3, bf16, st); }
     int S = 0;
-    { StageTimer t(ctx, ST_FC1_FWD); S = launch_fc1_fwd(h3, th, 2 * G, b, fc1part, st); }
+    { StageTimer t(ctx, ST_FC1_FWD); S = launch_fc1_fwd(h3, th, 2 * G, b, fc1part, bf16, st); }
 
     float* dz4 = at<float>(ctx, p.dz4);
     float* dz3 = at<float>(ctx, p.dz3);
@@ -499,22 +502,22 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G,
     {
         StageTimer t(ctx, ST_FC1_BWD);
         head_blocks = launch_fc1_backward(dz4, on, G, h3, h4, a, coef, ell, b, A, dz3, grads_out, P,
-                                          at<float>(ctx, p.hpart), st);
+                                          at<float>(ctx, p.hpart), bf16, st);
     }
     {
         StageTimer t(ctx, ST_CONV3_BWD);
         s3 = launch_conv3_backward(dz3, w3d, G, h2, b, dz2, at<float>(ctx, p.part3),
-                                   bpart + 2 * BIAS_PART_STRIDE, st);
+                                   bpart + 2 * BIAS_PART_STRIDE, bf16, st);
     }
     {
         StageTimer t(ctx, ST_CONV2_BWD);
         s2 = launch_conv2_backward(dz2, w2p, G, h1, b, dz1, at<float>(ctx, p.part2),
-                                   bpart + BIAS_PART_STRIDE, st);
+                                   bpart + BIAS_PART_STRIDE, bf16, st);
     }
     {
         StageTimer t(ctx, ST_CONV1_WGRAD);
         launch_conv1_wgrad(dz1, ftab, G, b, at<float>(ctx, p.part1), bpart, CONV1_WG_MAX_SPLITS,
-                           &s1, st);
+                           &s1, bf16, st);
     }
     {
         StageTimer t(ctx, ST_GRAD_REDUCE);
@@ -534,15 +537,15 @@ int gorila_learner_step(const gorila_params* params, const gorila_params* target
                         const gorila_replay* replay, const int64_t* idx, int32_t batch,
                         float gamma, float clip_delta, float* grads_out, float* loss_out,
                         gorila_ctx* ctx) {
-    return learner_steps(ctx, params, 1, target_params, replay, idx, batch, gamma, clip_delta,
-                         grads_out, loss_out);
+    return learner_steps(ctx, params, 1, false, target_params, replay, idx, batch, gamma,
+                         clip_delta, grads_out, loss_out);
 }
 
 int gorila_learner_step_grouped(const gorila_params* params, int32_t groups,
                                 const gorila_params* target_params, const gorila_replay* replay,
                                 const int64_t* idx, int32_t batch, float gamma, float clip_delta,
                                 float* grads_out, float* loss_out, gorila_ctx* ctx) {
-    return learner_steps(ctx, params, groups, target_params, replay, idx, batch, gamma,
+    return learner_steps(ctx, params, groups, true, target_params, replay, idx, batch, gamma,
                          clip_delta, grads_out, loss_out);
 }
 

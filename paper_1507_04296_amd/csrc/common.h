@@ -133,11 +133,77 @@ template <class T, class = void> struct IsMaskEpi : std::false_type {};
 template <class T>
 struct IsMaskEpi<T, std::void_t<decltype(T::MASK)>> : std::bool_constant<T::MASK> {};
 
-template <int BM, int BN, int AMODE, int BMODE>
+// ---------------------------------------------------------------------------
+// bf16 operands (v_mfma_f32_32x32x16_bf16, fp32 accumulation).
+//
+// With P > 0 the engine below keeps an operand in LDS as P planes of bf16
+// instead of fp32: plane 0 holds each value rounded to the nearest bf16, and
+// with P = 2 plane 1 holds the rounding residual, itself rounded to bf16, so
+// that hi + lo carries about 16 significant bits and the engine adds both
+// products hi*B and lo*B.  The loaders still deliver fp32 quads; they are
+// converted as they are stored to LDS.  A plane is [rows][BK] bf16 (64 bytes
+// a row) whose four 16-byte chunks are stored XOR-permuted by
+// ((r >> 1) ^ (r >> 3)) & 3, so that 16 consecutive rows reading one chunk
+// touch every LDS bank once.  Lane l of an MFMA supplies row l % 32 and the
+// eight reduction indices 8 (l / 32) .. +7 of its 16-wide step; the
+// accumulator layout is that of the fp32 instruction.
+// ---------------------------------------------------------------------------
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+template <int ROWS, int PL>
+struct Bf16Tile {
+    static constexpr int PLANE = ROWS * BK * 2;  // bytes
+    static constexpr int BYTES = PL * PLANE;
+    __device__ static inline int chunk(int row, int c) {
+        return row * (BK * 2) + (((c ^ (row >> 1) ^ (row >> 3)) & 3) << 4);
+    }
+    // Quad v of a MODE-laid operand at tile coordinates (row, k): KMAJ quads
+    // are 4 reduction indices of one row, RMAJ quads 4 rows at one index.
+    template <int MODE>
+    __device__ static inline void put(char* s, int row, int k, f32x4 v) {
+        bf16x4 hi, lo;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            hi[e] = (__bf16)v[e];
+            if (PL == 2) lo[e] = (__bf16)(v[e] - (float)hi[e]);  // the difference is exact
+        }
+        if (MODE == KMAJ) {
+            const int off = chunk(row, k >> 3) + ((k & 4) << 1);
+            *(bf16x4*)(s + off) = hi;
+            if (PL == 2) *(bf16x4*)(s + PLANE + off) = lo;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int off = chunk(row + e, k >> 3) + ((k & 7) << 1);
+                *(__bf16*)(s + off) = hi[e];
+                if (PL == 2) *(__bf16*)(s + PLANE + off) = lo[e];
+            }
+        }
+    }
+    __device__ static inline bf16x8 get(const char* s, int plane, int row, int c) {
+        return *(const bf16x8*)(s + plane * PLANE + chunk(row, c));
+    }
+};
+
+// Planes per operand role when a step runs on bf16 parameters.  Forward
+// activations are split: the TD error is a small difference of Q values, so
+// Q needs more than bf16's 8 bits (rounding every activation to bf16 leaves
+// gradients several percent off, split activations about 0.2 %).  Weights are
+// bf16 values already, exact in one plane; the backward gradients are
+// rounded, and the weight gradients read the split activations.
+constexpr int BF_ACT_FWD = 2, BF_WEIGHT = 1, BF_GRAD = 1, BF_ACT_WGRAD = 2;
+
+// PA, PB: bf16 planes of A and B (0 and 0: the fp32 engine).
+template <int BM, int BN, int AMODE, int BMODE, int PA = 0, int PB = 0>
 struct GemmShape {
+    static_assert((PA > 0) == (PB > 0) && PA <= 2 && PB <= 2, "both operands fp32, or both bf16");
     using LA = LdsTile<BM, AMODE>;
     using LB = LdsTile<BN, BMODE>;
-    static constexpr int SMEM_FLOATS = 2 * (LA::SIZE + LB::SIZE);
+    using TA = Bf16Tile<BM, PA ? PA : 1>;
+    using TB = Bf16Tile<BN, PB ? PB : 1>;
+    static constexpr int STAGE_FLOATS = PA ? (TA::BYTES + TB::BYTES) / 4 : LA::SIZE + LB::SIZE;
+    static constexpr int SMEM_FLOATS = 2 * STAGE_FLOATS;
 };
 
 // Loaders: `la.init(j, row, k)` is called once per quad slot j of this thread
@@ -160,17 +226,21 @@ struct GemmShape {
 // set of every access are compile-time constants: LDS is then addressed with
 // ds_read/ds_write, and each global load is waited for only where its data is
 // stored to LDS, one chunk later.
-template <int BM, int BN, int WAVES_M, int AMODE, int BMODE, class LoadA, class LoadB, class Epi>
+template <int BM, int BN, int WAVES_M, int AMODE, int BMODE, int PA = 0, int PB = 0, class LoadA,
+          class LoadB, class Epi>
 __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
                                           LoadA& la, LoadB& lb, Epi& epi,
                                           float* rowsum_out = nullptr) {
-    using SH = GemmShape<BM, BN, AMODE, BMODE>;
+    using SH = GemmShape<BM, BN, AMODE, BMODE, PA, PB>;
     using LA = typename SH::LA;
     using LB = typename SH::LB;
+    using TA = typename SH::TA;
+    using TB = typename SH::TB;
+    constexpr bool BF = PA > 0;
     constexpr int WAVES_N = 4 / WAVES_M;
     constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
     constexpr int TM = WM / 32, TN = WN / 32;
-    constexpr int STAGE = LA::SIZE + LB::SIZE;  // floats per LDS buffer
+    constexpr int STAGE = SH::STAGE_FLOATS;  // floats per LDS buffer
     static_assert(TM * 32 == WM && TN * 32 == WN, "wave tile must be a multiple of 32");
     static_assert(LA::NQ <= MAXQ && LB::NQ <= MAXQ, "loader state arrays hold MAXQ quads");
     static_assert(LA::QUADS % 256 == 0 && LB::QUADS % 256 == 0, "every thread owns whole quads");
@@ -229,15 +299,67 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
         for (int j = 0; j < LB::NQ; ++j) rb[j] = lb.load(kc, j);
     };
     auto sstore = [&](float* buf, const f32x4* ra, const f32x4* rb) {
+        if constexpr (BF) {
 #pragma unroll
-        for (int j = 0; j < LA::NQ; ++j) LA::put(buf, qa_row[j], qa_k[j], ra[j]);
+            for (int j = 0; j < LA::NQ; ++j)
+                TA::template put<AMODE>((char*)buf, qa_row[j], qa_k[j], ra[j]);
 #pragma unroll
-        for (int j = 0; j < LB::NQ; ++j) LB::put(buf + LA::SIZE, qb_row[j], qb_k[j], rb[j]);
+            for (int j = 0; j < LB::NQ; ++j)
+                TB::template put<BMODE>((char*)buf + TA::BYTES, qb_row[j], qb_k[j], rb[j]);
+        } else {
+#pragma unroll
+            for (int j = 0; j < LA::NQ; ++j) LA::put(buf, qa_row[j], qa_k[j], ra[j]);
+#pragma unroll
+            for (int j = 0; j < LB::NQ; ++j) LB::put(buf + LA::SIZE, qb_row[j], qb_k[j], rb[j]);
+        }
     };
 
     const bool do_rowsum = rowsum_out != nullptr;  // uniform over the workgroup
     float rowsum = 0.0f;
+    auto compute_bf16 = [&](const float* buf) {
+        const char* sa = (const char*)buf;
+        const char* sb = sa + TA::BYTES;
+#pragma unroll
+        for (int st = 0; st < BK / 16; ++st) {
+            const int c = 2 * st + (lane >> 5);
+            bf16x8 a0[TM], a1[TM], b0[TN], b1[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) {
+                a0[i] = TA::get(sa, 0, wm * WM + i * 32 + (lane & 31), c);
+                if (PA == 2) a1[i] = TA::get(sa, 1, wm * WM + i * 32 + (lane & 31), c);
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                b0[j] = TB::get(sb, 0, wn * WN + j * 32 + (lane & 31), c);
+                if (PB == 2) b1[j] = TB::get(sb, 1, wn * WN + j * 32 + (lane & 31), c);
+            }
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[i], b0[j], acc[i][j], 0, 0, 0);
+                    if (PA == 2)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[i], b0[j], acc[i][j], 0, 0, 0);
+                    if (PB == 2)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[i], b1[j], acc[i][j], 0, 0, 0);
+                }
+        }
+        if (BM <= 64 && do_rowsum && lane < BM) {  // chunk `wave` of row `lane`: k = 8w .. 8w+7
+            float t = 0.0f;
+#pragma unroll
+            for (int pl = 0; pl < PA; ++pl) {
+                const bf16x8 v = TA::get(sa, pl, lane, wave);
+                t += (((float)v[0] + (float)v[1]) + ((float)v[2] + (float)v[3])) +
+                     (((float)v[4] + (float)v[5]) + ((float)v[6] + (float)v[7]));
+            }
+            rowsum += t;
+        }
+    };
     auto compute = [&](const float* buf) {
+        if constexpr (BF) {
+            compute_bf16(buf);
+            return;
+        }
         const float* sa = buf;
         const float* sb = buf + LA::SIZE;
 #pragma unroll

@@ -13,6 +13,34 @@
 
 namespace gorila {
 
+// Stage the 8 frames (2 samples x 4 channels) of sample pair b0 of group g in
+// LDS: the frame pointers are read once (uniform loads), then every thread
+// issues all of its 16-byte loads before its first LDS store, so the copy
+// costs one memory latency rather than one per vector.  Null frames are zeros.
+__device__ inline void stage_pair(const uint8_t* const* ftab, int g, int n, int b0, int ns,
+                                  uint8_t* xs) {
+    const int tid = threadIdx.x;
+    constexpr int VEC = FRAME_BYTES / 16;  // 441 16-byte vectors per frame
+    const uint4* fp[8];
+#pragma unroll
+    for (int f = 0; f < 8; ++f)
+        fp[f] = (f >> 2) < ns ? (const uint4*)ftab[((int64_t)g * n + b0 + (f >> 2)) * 4 + (f & 3)]
+                              : nullptr;
+    const bool second = tid + 256 < VEC;  // lanes that copy a second vector per frame
+    uint4 v0[8], v1[8];
+    const uint4 z = make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+        v0[f] = fp[f] ? ldg_u4(fp[f] + tid) : z;
+        v1[f] = fp[f] && second ? ldg_u4(fp[f] + tid + 256) : z;
+    }
+#pragma unroll
+    for (int f = 0; f < 8; ++f) {
+        ((uint4*)xs)[f * VEC + tid] = v0[f];
+        if (second) ((uint4*)xs)[f * VEC + tid + 256] = v1[f];
+    }
+}
+
 __global__ __launch_bounds__(256, 2) void conv1_fwd_kernel(const uint8_t* const* __restrict__ ftab,
                                                            GroupPtrs theta, int n,
                                                            float* __restrict__ h1) {
@@ -21,31 +49,7 @@ __global__ __launch_bounds__(256, 2) void conv1_fwd_kernel(const uint8_t* const*
     const int ns = min(2, n - b0);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
-    // Stage the 8 frames (2 samples x 4 channels): the frame pointers are read
-    // once (uniform loads), then every thread issues all of its 16-byte loads
-    // before its first LDS store, so the copy costs one memory latency rather
-    // than one per vector.
-    constexpr int VEC = FRAME_BYTES / 16;  // 441 16-byte vectors per frame
-    const uint4* fp[8];
-#pragma unroll
-    for (int f = 0; f < 8; ++f)
-        fp[f] = (f >> 2) < ns ? (const uint4*)ftab[((int64_t)g * n + b0 + (f >> 2)) * 4 + (f & 3)]
-                              : nullptr;
-    {
-        const bool second = tid + 256 < VEC;  // lanes that copy a second vector per frame
-        uint4 v0[8], v1[8];
-        const uint4 z = make_uint4(0, 0, 0, 0);
-#pragma unroll
-        for (int f = 0; f < 8; ++f) {
-            v0[f] = fp[f] ? ldg_u4(fp[f] + tid) : z;
-            v1[f] = fp[f] && second ? ldg_u4(fp[f] + tid + 256) : z;
-        }
-#pragma unroll
-        for (int f = 0; f < 8; ++f) {
-            ((uint4*)xs)[f * VEC + tid] = v0[f];
-            if (second) ((uint4*)xs)[f * VEC + tid + 256] = v1[f];
-        }
-    }
+    stage_pair(ftab, g, n, b0, ns, xs);
 
     const float* W1 = theta.p[g];
     const int col = lane & 31, h = lane >> 5;
@@ -92,14 +96,81 @@ __global__ __launch_bounds__(256, 2) void conv1_fwd_kernel(const uint8_t* const*
     }
 }
 
+// The same layer for bf16 parameter sets on v_mfma_f32_32x32x16_bf16: bytes
+// (integers 0..255) and bf16 weights are exact bf16 operands, so every
+// product is exact and only the fp32 accumulation rounds.  One 16-wide step
+// covers two filter rows (c, u) of 8 columns v: lane half h takes row
+// 2 * step + h, so a lane's eight operands are eight consecutive input bytes.
+__device__ inline uint32_t bf16_pair_exact(float lo, float hi) {  // both bf16-representable
+    return (__float_as_uint(hi) & 0xffff0000u) | (__float_as_uint(lo) >> 16);
+}
+__device__ inline bf16x8 bytes_bf16x8(uint32_t d0, uint32_t d1) {
+    typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+    const u32x4v q = {bf16_pair_exact((float)(d0 & 255u), (float)((d0 >> 8) & 255u)),
+                      bf16_pair_exact((float)((d0 >> 16) & 255u), (float)(d0 >> 24)),
+                      bf16_pair_exact((float)(d1 & 255u), (float)((d1 >> 8) & 255u)),
+                      bf16_pair_exact((float)((d1 >> 16) & 255u), (float)(d1 >> 24))};
+    return __builtin_bit_cast(bf16x8, q);
+}
+
+__global__ __launch_bounds__(256, 2) void conv1_fwd_bf16_kernel(
+    const uint8_t* const* __restrict__ ftab, GroupPtrs theta, int n, float* __restrict__ h1) {
+    __shared__ __attribute__((aligned(16))) uint8_t xs[2 * STATE_BYTES];
+    const int g = blockIdx.y, b0 = blockIdx.x * 2;
+    const int ns = min(2, n - b0);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    stage_pair(ftab, g, n, b0, ns, xs);
+
+    const float* W1 = theta.p[g];
+    const int col = lane & 31, h = lane >> 5;
+    bf16x8 w[16];  // step st: W1[col][row 2 st + h][v = 0..7]
+#pragma unroll
+    for (int st = 0; st < 16; ++st) {
+        const f32x4 a = ld4(W1 + OFF_W1 + col * 256 + (2 * st + h) * 8);
+        const f32x4 b = ld4(W1 + OFF_W1 + col * 256 + (2 * st + h) * 8 + 4);
+        typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+        const u32x4v q = {bf16_pair_exact(a[0], a[1]), bf16_pair_exact(a[2], a[3]),
+                          bf16_pair_exact(b[0], b[1]), bf16_pair_exact(b[2], b[3])};
+        w[st] = __builtin_bit_cast(bf16x8, q);
+    }
+    const float bias = W1[OFF_B1 + col];
+    __syncthreads();
+
+    const int rows = ns * P1;
+    const int ntiles = (rows + 31) / 32;
+    float* out = h1 + ((int64_t)g * n + b0) * P1 * C1;
+    const int z = blockIdx.z, zs = gridDim.z;
+    for (int t = z + zs * wave; t < ntiles; t += 4 * zs) {
+        int m = t * 32 + (lane & 31);
+        if (m >= rows) m = 0;  // padding rows compute on a valid pixel, never stored
+        const int s = m / P1, p = m - s * P1, i = p / H1, j = p - i * H1;
+        const uint8_t* base = xs + s * STATE_BYTES + (S1 * i) * IN_W + S1 * j;
+        f32x16 acc = f32x16{};
+#pragma unroll
+        for (int st = 0; st < 16; ++st) {
+            const int cb = 2 * st + h, c = cb >> 3, u = cb & 7;
+            const uint8_t* px = base + c * FRAME_BYTES + u * IN_W;  // 4-byte aligned
+            const uint32_t d0 = *(const uint32_t*)px, d1 = *(const uint32_t*)(px + 4);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bytes_bf16x8(d0, d1), w[st], acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int row = t * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (row < rows) out[(int64_t)row * C1 + col] = fmaxf(acc[r] * (1.0f / 255.0f) + bias, 0.0f);
+        }
+    }
+}
+
 void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int groups, int n,
-                      float* h1, hipStream_t st) {
+                      float* h1, bool bf16, hipStream_t st) {
     if (n <= 0) return;
     // Aim at >= 512 workgroups (two per CU): below that, split each pair's
     // tiles over up to 8 workgroups, each staging the pair's frames.
     const int blocks = (n + 1) / 2 * groups;
     const int split = blocks >= 512 ? 1 : min(8, (512 + blocks - 1) / blocks);
-    conv1_fwd_kernel<<<dim3((n + 1) / 2, groups, split), 256, 0, st>>>(ftab, theta, n, h1);
+    const dim3 grid((n + 1) / 2, groups, split);
+    if (bf16) conv1_fwd_bf16_kernel<<<grid, 256, 0, st>>>(ftab, theta, n, h1);
+    else      conv1_fwd_kernel<<<grid, 256, 0, st>>>(ftab, theta, n, h1);
 }
 
 // Weight gradient: dW1[o][(c,u,v)] = (1/255) sum_pixels dz1[pixel][o] * x[c][4i+u][4j+v]
@@ -154,13 +225,16 @@ constexpr int C1W_BN = 128;
 // 65 us for 986 of 13 chunks (1.3 rounds) at batch 512.
 constexpr int C1W_TARGET_WGS = 768;
 
+template <int BF>
 struct Conv1WgradJob {
     const float* dz1;
     const uint8_t* const* ftab;
     float* partial;
     float* bias_part;
     int n, splits, cps, groups;
-    using SH = GemmShape<32, C1W_BN, RMAJ, RMAJ>;
+    // in bf16 the bytes are exact operands (one plane)
+    static constexpr int PA = BF ? BF_GRAD : 0, PB = BF ? 1 : 0;
+    using SH = GemmShape<32, C1W_BN, RMAJ, RMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     static constexpr int NCT = 256 / C1W_BN;
     __host__ __device__ int blocks() const { return pad_xcd(NCT * splits * groups); }
@@ -178,20 +252,21 @@ struct Conv1WgradJob {
         Conv1WgradB lb{ftab + rows * 4, (const uint8_t*)dz1, npix, col0};
         PartialEpi epi{partial + (int64_t)split * C1 * 256, 256, col0, 1.0f / 255.0f};
         float* rs = col0 == 0 ? bias_part + (int64_t)split * 64 : nullptr;
-        mfma_gemm<32, C1W_BN, 1, RMAJ, RMAJ>(smem, kc0, kc1, la, lb, epi, rs);
+        mfma_gemm<32, C1W_BN, 1, RMAJ, RMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi, rs);
     }
 };
 
 void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int groups, int n,
                         float* partial, float* bias_part, int max_splits, int* splits_out,
-                        hipStream_t st) {
+                        bool bf16, hipStream_t st) {
     const int nchunks = (n * P1 + BK - 1) / BK;
     int splits = max(1, min(max_splits, C1W_TARGET_WGS / (256 / C1W_BN)) / groups);
     splits = min(splits, nchunks);
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
     *splits_out = splits;
-    launch_jobs(st, Conv1WgradJob{dz1, ftab, partial, bias_part, n, splits, cps, groups});
+    if (bf16) launch_jobs(st, Conv1WgradJob<1>{dz1, ftab, partial, bias_part, n, splits, cps, groups});
+    else      launch_jobs(st, Conv1WgradJob<0>{dz1, ftab, partial, bias_part, n, splits, cps, groups});
 }
 
 }  // namespace gorila

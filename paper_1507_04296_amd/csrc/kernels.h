@@ -69,17 +69,18 @@ struct WidenSet {
 void launch_widen_bf16(const WidenSet& set, int n_nets, int64_t count, hipStream_t st);
 
 // Forward layers.  `groups` parameter sets; group g owns rows [g*n, (g+1)*n)
-// of every activation buffer.
+// of every activation buffer.  bf16: the parameter sets hold bf16 values
+// (widened to fp32) and the products run on bf16 MFMA operands (common.h).
 void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int groups, int n,
-                      float* h1, hipStream_t st);
+                      float* h1, bool bf16, hipStream_t st);
 void launch_conv2_fwd(const float* h1, const GroupPtrs& w2t, const GroupPtrs& theta, int groups,
-                      int n, float* h2, hipStream_t st);
+                      int n, float* h2, bool bf16, hipStream_t st);
 void launch_conv3_fwd(const float* h2, const GroupPtrs& w3t, const GroupPtrs& theta, int groups,
-                      int n, float* h3, hipStream_t st);
+                      int n, float* h3, bool bf16, hipStream_t st);
 // fc1 forward as split-K partial sums partial[g][s][b][512]; returns the
 // number of splits s (the head kernels finish the layer).
 int launch_fc1_fwd(const float* h3, const GroupPtrs& theta, int groups, int n, float* partial,
-                   hipStream_t st);
+                   bool bf16, hipStream_t st);
 
 // Head: Q values, epsilon-greedy actions, TD error / Huber loss / dLoss.
 // Each first finishes the FC-512 layer (splits in order, bias, ReLU).
@@ -108,15 +109,17 @@ void launch_td_head(const float* fc1part_online, const float* fc1part_target, in
 int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, int groups, const float* h3,
                         const float* h4, const int32_t* a, const float* coef, const float* ell,
                         int n, int A, float* dz3, float* grads, int64_t grads_stride,
-                        float* hpart, hipStream_t st);
+                        float* hpart, bool bf16, hipStream_t st);
 int launch_conv3_backward(const float* dz3, const GroupPtrs& w3d, int groups, const float* h2,
-                          int n, float* dz2, float* partial, float* bias_part, hipStream_t st);
+                          int n, float* dz2, float* partial, float* bias_part, bool bf16,
+                          hipStream_t st);
 int launch_conv2_backward(const float* dz2, const GroupPtrs& w2p, int groups, const float* h1,
-                          int n, float* dz1, float* partial, float* bias_part, hipStream_t st);
+                          int n, float* dz1, float* partial, float* bias_part, bool bf16,
+                          hipStream_t st);
 // ftab: [groups * n][4] frame pointers of the online states.
 void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int groups, int n,
                         float* partial, float* bias_part, int max_splits, int* splits_out,
-                        hipStream_t st);
+                        bool bf16, hipStream_t st);
 // Conv weight-gradient partials [group][split][o][(tap, c)], bias partials
 // bias_part[layer][group][split][64] (one row per split, written by the
 // weight-gradient workgroups of column tile 0) and the head partials

@@ -118,12 +118,14 @@ struct BiasReluStore {
     }
 };
 
+template <int BF>
 struct Conv2FwdJob {
     const float* h1;
     GroupPtrs w2t, theta;
     float* h2;
     int n, groups;
-    using SH = GemmShape<64, 64, KMAJ, KMAJ>;
+    static constexpr int PA = BF ? BF_ACT_FWD : 0, PB = BF ? BF_WEIGHT : 0;
+    using SH = GemmShape<64, 64, KMAJ, KMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return (n * P2 + 63) / 64; }
     __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
@@ -135,14 +137,15 @@ struct Conv2FwdJob {
         Conv2FwdA la{h1 + (int64_t)g * n * P1 * C1, rows, m0};
         WtapB<C1, C2> lb{w2t.p[g]};
         BiasReluStore epi{h2 + (int64_t)g * n * P2 * C2, theta.p[g] + OFF_B2, rows, m0, C2};
-        mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, 0, 16, la, lb, epi);
+        mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, 0, 16, la, lb, epi);
     }
 };
 
 void launch_conv2_fwd(const float* h1, const GroupPtrs& w2t, const GroupPtrs& theta, int groups,
-                      int n, float* h2, hipStream_t st) {
+                      int n, float* h2, bool bf16, hipStream_t st) {
     if (n <= 0) return;
-    launch_jobs(st, Conv2FwdJob{h1, w2t, theta, h2, n, groups});
+    if (bf16) launch_jobs(st, Conv2FwdJob<1>{h1, w2t, theta, h2, n, groups});
+    else      launch_jobs(st, Conv2FwdJob<0>{h1, w2t, theta, h2, n, groups});
 }
 
 // ---------------------------------------------------------------------------
@@ -179,12 +182,14 @@ struct Conv3FwdStore {  // row = o, col = pixel index within the tile
     }
 };
 
+template <int BF>
 struct Conv3FwdJob {
     const float* h2;
     GroupPtrs w3t, theta;
     float* h3;
     int n, groups;
-    using SH = GemmShape<64, 64, KMAJ, KMAJ>;
+    static constexpr int PA = BF ? BF_WEIGHT : 0, PB = BF ? BF_ACT_FWD : 0;
+    using SH = GemmShape<64, 64, KMAJ, KMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return (n * P3 + 63) / 64; }
     __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
@@ -196,14 +201,15 @@ struct Conv3FwdJob {
         WtapB<C2, C3> la{w3t.p[g]};
         Conv3FwdB lb{h2 + (int64_t)g * n * P2 * C2, rows, m0};
         Conv3FwdStore epi{h3 + (int64_t)g * n * FLAT, theta.p[g] + OFF_B3, rows, m0};
-        mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, 0, 18, la, lb, epi);
+        mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, 0, 18, la, lb, epi);
     }
 };
 
 void launch_conv3_fwd(const float* h2, const GroupPtrs& w3t, const GroupPtrs& theta, int groups,
-                      int n, float* h3, hipStream_t st) {
+                      int n, float* h3, bool bf16, hipStream_t st) {
     if (n <= 0) return;
-    launch_jobs(st, Conv3FwdJob{h2, w3t, theta, h3, n, groups});
+    if (bf16) launch_jobs(st, Conv3FwdJob<1>{h2, w3t, theta, h3, n, groups});
+    else      launch_jobs(st, Conv3FwdJob<0>{h2, w3t, theta, h3, n, groups});
 }
 
 // ---------------------------------------------------------------------------
@@ -234,12 +240,14 @@ constexpr int FC1_CHUNKS = FLAT / BK;  // 98
 
 // Logical tile order (group, split, column tile, row tile): the row tiles that
 // share a block of W4 are neighbours and so share an XCD's L2.
+template <int BF>
 struct Fc1FwdJob {
     const float* h3;
     GroupPtrs theta;
     float* partial;
     int n, groups, splits, cps;
-    using SH = GemmShape<64, 64, KMAJ, KMAJ>;
+    static constexpr int PA = BF ? BF_ACT_FWD : 0, PB = BF ? BF_WEIGHT : 0;
+    using SH = GemmShape<64, 64, KMAJ, KMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int mt() const { return (n + 63) / 64; }
     __host__ __device__ int tiles() const { return mt() * (HID / 64) * groups * splits; }
@@ -256,18 +264,19 @@ struct Fc1FwdJob {
         RowMajorK lb{theta.p[g] + OFF_W4, HID, c0, FLAT};
         PlainStore epi{partial + ((int64_t)g * splits + s) * n * HID, n, r0, c0, HID};
         const int kc0 = s * cps, kc1 = min(FC1_CHUNKS, kc0 + cps);
-        mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, kc0, kc1, la, lb, epi);
+        mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi);
     }
 };
 
 int launch_fc1_fwd(const float* h3, const GroupPtrs& theta, int groups, int n, float* partial,
-                   hipStream_t st) {
+                   bool bf16, hipStream_t st) {
     if (n <= 0) return 0;
     const int mt = (n + 63) / 64, tiles = mt * (HID / 64) * groups;
     int splits = min(FC1_MAX_SPLITS, max(1, (TARGET_WGS + tiles - 1) / tiles));
     const int cps = (FC1_CHUNKS + splits - 1) / splits;
     splits = (FC1_CHUNKS + cps - 1) / cps;
-    launch_jobs(st, Fc1FwdJob{h3, theta, partial, n, groups, splits, cps});
+    if (bf16) launch_jobs(st, Fc1FwdJob<1>{h3, theta, partial, n, groups, splits, cps});
+    else      launch_jobs(st, Fc1FwdJob<0>{h3, theta, partial, n, groups, splits, cps});
     return splits;
 }
 
@@ -312,13 +321,15 @@ struct Dz3NhwcStore {
     }
 };
 
+template <int BF>
 struct Fc1DgradJob {
     const float* dz4;
     GroupPtrs theta;
     const float* h3;
     float* dz3;
     int n, groups;
-    using SH = GemmShape<64, 64, KMAJ, RMAJ>;
+    static constexpr int PA = BF ? BF_GRAD : 0, PB = BF ? BF_WEIGHT : 0;
+    using SH = GemmShape<64, 64, KMAJ, RMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return ((n + 63) / 64) * (FLAT / 64); }
     __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
@@ -333,7 +344,7 @@ struct Fc1DgradJob {
         RowMajorK la{dz4 + rows * HID, n, r0, HID};
         RowMajorR<false> lb{theta.p[g] + OFF_W4, c0, FLAT, HID};  // HID is a whole number of chunks
         Dz3NhwcStore epi{dz3 + rows * FLAT, h3 + rows * FLAT, n, r0, c0};
-        mfma_gemm<64, 64, 2, KMAJ, RMAJ>(smem, 0, HID / BK, la, lb, epi);
+        mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, 0, HID / BK, la, lb, epi);
     }
 };
 
@@ -341,13 +352,15 @@ struct Fc1DgradJob {
 // fc1 weight gradient: dW4[o][k] = sum_b dz4[b][o] h3[b][k]  (written in place)
 // rows o (512), cols k (3136), reduction b.
 // ---------------------------------------------------------------------------
+template <int BF>
 struct Fc1WgradJob {
     const float* dz4;
     const float* h3;
     float* grads;
     int64_t grads_stride;
     int n, groups;
-    using SH = GemmShape<64, 64, RMAJ, RMAJ>;
+    static constexpr int PA = BF ? BF_GRAD : 0, PB = BF ? BF_ACT_WGRAD : 0;
+    using SH = GemmShape<64, 64, RMAJ, RMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return (HID / 64) * (FLAT / 64); }
     __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
@@ -364,7 +377,7 @@ struct Fc1WgradJob {
         PlainStore epi{gr + OFF_W4, HID, r0, c0, FLAT};
         // db4[o] = sum_b dz4[b][o]: the row sums of this GEMM's A operand
         float* rs = c0 == 0 ? gr + OFF_B4 + r0 : nullptr;
-        mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, 0, (n + BK - 1) / BK, la, lb, epi, rs);
+        mfma_gemm<64, 64, 2, RMAJ, RMAJ, PA, PB>(smem, 0, (n + BK - 1) / BK, la, lb, epi, rs);
     }
 };
 
@@ -443,13 +456,17 @@ struct HeadPartialJob {
 int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, int groups, const float* h3,
                         const float* h4, const int32_t* a, const float* coef, const float* ell,
                         int n, int A, float* dz3, float* grads, int64_t grads_stride,
-                        float* hpart, hipStream_t st) {
+                        float* hpart, bool bf16, hipStream_t st) {
     if (n <= 0) return 0;
     const int rows = max(32, (n + HEAD_MAX_BLOCKS - 1) / HEAD_MAX_BLOCKS);
     const int row_blocks = (n + rows - 1) / rows;
-    launch_jobs(st, Fc1DgradJob{dz4, theta, h3, dz3, n, groups},
-                Fc1WgradJob{dz4, h3, grads, grads_stride, n, groups},
-                HeadPartialJob{h4, a, coef, ell, hpart, n, A, rows, row_blocks, groups});
+    const HeadPartialJob hp{h4, a, coef, ell, hpart, n, A, rows, row_blocks, groups};
+    if (bf16)
+        launch_jobs(st, Fc1DgradJob<1>{dz4, theta, h3, dz3, n, groups},
+                    Fc1WgradJob<1>{dz4, h3, grads, grads_stride, n, groups}, hp);
+    else
+        launch_jobs(st, Fc1DgradJob<0>{dz4, theta, h3, dz3, n, groups},
+                    Fc1WgradJob<0>{dz4, h3, grads, grads_stride, n, groups}, hp);
     return row_blocks;
 }
 
@@ -500,13 +517,15 @@ struct Conv3DgradStore {
     }
 };
 
+template <int BF>
 struct Conv3DgradJob {
     const float* dz3;
     GroupPtrs w3d;
     const float* h2;
     float* dz2;
     int n, groups;
-    using SH = GemmShape<64, 64, KMAJ, KMAJ>;
+    static constexpr int PA = BF ? BF_GRAD : 0, PB = BF ? BF_WEIGHT : 0;
+    using SH = GemmShape<64, 64, KMAJ, KMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return P2 * ((n + 63) / 64); }
     __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
@@ -523,7 +542,7 @@ struct Conv3DgradJob {
         Conv3DgradA la{dz3 + rows * FLAT, n, b0, y, x, u0, v0, nv};
         Conv3DgradB lb{w3d.p[g], u0, v0, nv};
         Conv3DgradStore epi{dz2 + rows * P2 * C2, h2 + rows * P2 * C2, n, b0, pos};
-        mfma_gemm<64, 64, 2, KMAJ, KMAJ>(smem, 0, 2 * taps, la, lb, epi);
+        mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, 0, 2 * taps, la, lb, epi);
     }
 };
 
@@ -559,13 +578,15 @@ struct Conv3WgradB {  // RMAJ quads: 4 channels of h2 at one (pixel, tap)
     __device__ f32x4 load(int, int j) const { return ld4(pix + c0[j]); }
 };
 
+template <int BF>
 struct Conv3WgradJob {
     const float* dz3;
     const float* h2;
     float* partial;
     float* bias_part;
     int n, splits, cps, groups;
-    using SH = GemmShape<64, 64, RMAJ, RMAJ>;
+    static constexpr int PA = BF ? BF_GRAD : 0, PB = BF ? BF_ACT_WGRAD : 0;
+    using SH = GemmShape<64, 64, RMAJ, RMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int blocks() const { return pad_xcd(9 * splits * groups); }
     __device__ void run(int bid, float* smem) const {
@@ -580,21 +601,26 @@ struct Conv3WgradJob {
         Conv3WgradB lb{h2 + rows * P2 * C2, npix, tap};
         PartialEpi epi{partial + (int64_t)s * C3 * 9 * C2, 9 * C2, tap * C2, 1.0f};
         float* rs = tap == 0 ? bias_part + (int64_t)s * 64 : nullptr;
-        mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, ks * cps, min(nchunks, (ks + 1) * cps), la, lb, epi, rs);
+        mfma_gemm<64, 64, 2, RMAJ, RMAJ, PA, PB>(smem, ks * cps, min(nchunks, (ks + 1) * cps), la, lb, epi, rs);
     }
 };
 
 // Splits per group shrink with the group count so one launch stays near the
 // same number of workgroups; groups * splits stays within WG_MAX_SPLITS.
 int launch_conv3_backward(const float* dz3, const GroupPtrs& w3d, int groups, const float* h2,
-                          int n, float* dz2, float* partial, float* bias_part, hipStream_t st) {
+                          int n, float* dz2, float* partial, float* bias_part, bool bf16,
+                          hipStream_t st) {
     if (n <= 0) return 0;
     const int nchunks = (n * P3 + BK - 1) / BK;
     int splits = min(min(WG_MAX_SPLITS / groups, nchunks), max(1, CONV3_WG_SPLITS / groups));
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
-    launch_jobs(st, Conv3DgradJob{dz3, w3d, h2, dz2, n, groups},
-                Conv3WgradJob{dz3, h2, partial, bias_part, n, splits, cps, groups});
+    if (bf16)
+        launch_jobs(st, Conv3DgradJob<1>{dz3, w3d, h2, dz2, n, groups},
+                    Conv3WgradJob<1>{dz3, h2, partial, bias_part, n, splits, cps, groups});
+    else
+        launch_jobs(st, Conv3DgradJob<0>{dz3, w3d, h2, dz2, n, groups},
+                    Conv3WgradJob<0>{dz3, h2, partial, bias_part, n, splits, cps, groups});
     return splits;
 }
 
@@ -652,13 +678,15 @@ struct Conv2DgradStore {
     }
 };
 
+template <int BF>
 struct Conv2DgradJob {
     const float* dz2;
     GroupPtrs w2p;
     const float* h1;
     float* dz1;
     int n, groups;
-    using SH = GemmShape<64, 128, KMAJ, KMAJ>;
+    static constexpr int PA = BF ? BF_GRAD : 0, PB = BF ? BF_WEIGHT : 0;
+    using SH = GemmShape<64, 128, KMAJ, KMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return 100 * ((n + 63) / 64); }
     __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
@@ -676,7 +704,7 @@ struct Conv2DgradJob {
         Conv2DgradA la{dz2 + rows * P2 * C2, n, b0, yy, xx, du0, dv0, ndv};
         Conv2DgradB lb{w2p.p[g], du0, dv0, ndv};
         Conv2DgradStore epi{dz1 + rows * P1 * C1, h1 + rows * P1 * C1, n, b0, yy, xx};
-        mfma_gemm<64, 128, 2, KMAJ, KMAJ>(smem, 0, 2 * taps, la, lb, epi);
+        mfma_gemm<64, 128, 2, KMAJ, KMAJ, PA, PB>(smem, 0, 2 * taps, la, lb, epi);
     }
 };
 
@@ -714,13 +742,15 @@ struct Conv2WgradB {  // h1 quads along c at one (pixel, tap)
     __device__ f32x4 load(int, int j) const { return ld4(pix + off[j]); }
 };
 
+template <int BF>
 struct Conv2WgradJob {
     const float* dz2;
     const float* h1;
     float* partial;
     float* bias_part;
     int n, splits, cps, groups;
-    using SH = GemmShape<64, 64, RMAJ, RMAJ>;
+    static constexpr int PA = BF ? BF_GRAD : 0, PB = BF ? BF_ACT_WGRAD : 0;
+    using SH = GemmShape<64, 64, RMAJ, RMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int blocks() const { return pad_xcd(8 * splits * groups); }
     __device__ void run(int bid, float* smem) const {
@@ -735,19 +765,24 @@ struct Conv2WgradJob {
         Conv2WgradB lb{h1 + rows * P1 * C1, npix, tap0};
         PartialEpi epi{partial + (int64_t)s * C2 * 16 * C1, 16 * C1, tap0 * C1, 1.0f};
         float* rs = tap0 == 0 ? bias_part + (int64_t)s * 64 : nullptr;
-        mfma_gemm<64, 64, 2, RMAJ, RMAJ>(smem, ks * cps, min(nchunks, (ks + 1) * cps), la, lb, epi, rs);
+        mfma_gemm<64, 64, 2, RMAJ, RMAJ, PA, PB>(smem, ks * cps, min(nchunks, (ks + 1) * cps), la, lb, epi, rs);
     }
 };
 
 int launch_conv2_backward(const float* dz2, const GroupPtrs& w2p, int groups, const float* h1,
-                          int n, float* dz1, float* partial, float* bias_part, hipStream_t st) {
+                          int n, float* dz1, float* partial, float* bias_part, bool bf16,
+                          hipStream_t st) {
     if (n <= 0) return 0;
     const int nchunks = (n * P2 + BK - 1) / BK;
     int splits = min(min(WG_MAX_SPLITS / groups, nchunks), max(1, CONV2_WG_SPLITS / groups));
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
-    launch_jobs(st, Conv2DgradJob{dz2, w2p, h1, dz1, n, groups},
-                Conv2WgradJob{dz2, h1, partial, bias_part, n, splits, cps, groups});
+    if (bf16)
+        launch_jobs(st, Conv2DgradJob<1>{dz2, w2p, h1, dz1, n, groups},
+                    Conv2WgradJob<1>{dz2, h1, partial, bias_part, n, splits, cps, groups});
+    else
+        launch_jobs(st, Conv2DgradJob<0>{dz2, w2p, h1, dz1, n, groups},
+                    Conv2WgradJob<0>{dz2, h1, partial, bias_part, n, splits, cps, groups});
     return splits;
 }
 

@@ -3,9 +3,12 @@ own possibly stale copy of theta, one shared target theta-) and of bf16
 parameter sets, against the fp64 oracle run once per group.
 
 bf16 parameters are bit patterns; the oracle takes their exact fp64 values.
-The HIP path widens them exactly to fp32 and computes in fp32, so the fp32
-bars apply (Q and loss 1e-4 relative, every gradient tensor 1e-3 relative L2),
-well inside the 2e-2 bar stated for bf16 parameters with fp32 accumulation.
+When every parameter set of a step is bf16 the HIP path multiplies bf16 MFMA
+operands with fp32 accumulation (forward activations as two bf16 terms,
+backward gradients rounded to bf16): every gradient tensor within 2e-2
+relative L2 and the loss within 1e-4 relative.  Mixed fp32 / bf16 steps and
+the forward-only calls compute in fp32 from the exactly widened values and
+meet the fp32 bars (Q and loss 1e-4 relative, gradients 1e-3 relative L2).
 Gradient parity runs on kink-certified rows of each group, picked out of a
 larger pool per group, so every group still runs at the batch under test.
 """
@@ -90,7 +93,7 @@ def test_grouped_16x64_bf16_a18(torch_cuda, g, oracle_mod):
     ref = _oracle_groups(oracle_mod, net, th64, tg64, inp, idx, b)
     worst = {}
     for gi in range(G):
-        errs = parity.assert_grads_close(got_g[gi], ref[gi]["grads"], A)
+        errs = parity.assert_grads_close(got_g[gi], ref[gi]["grads"], A, parity.GRAD_TOL_BF16)
         assert abs(got_l[gi] - ref[gi]["loss"]) <= parity.LOSS_TOL * abs(ref[gi]["loss"]), gi
         for k, v in errs.items():
             worst[k] = max(worst.get(k, 0.0), v)
@@ -128,6 +131,34 @@ def test_grouped_ragged_mixed_dtypes(torch_cuda, g, oracle_mod):
         parity.assert_grads_close(grads[gi].cpu().numpy(), ref[gi]["grads"], A)
         l = float(loss[gi].cpu())
         assert abs(l - ref[gi]["loss"]) <= parity.LOSS_TOL * abs(ref[gi]["loss"]), gi
+    ctx.close()
+
+
+@pytest.mark.parametrize("G,b,A,clip", [(3, 37, 7, 0.5), (1, 100, 4, 1.0)])
+def test_grouped_all_bf16_ragged(torch_cuda, g, oracle_mod, G, b, A, clip):
+    """All-bf16 steps (bf16 MFMA operands) at ragged batch sizes: partial
+    row tiles, one group on its own."""
+    torch = torch_cuda
+    pool = b + b // 2 + 8
+    _say(f"grouped all-bf16 G={G} b={b} A={A}")
+    inp = datagen.grouped_inputs(8300 + G, G, pool, A)
+    net = oracle_mod.Net(n_actions=A)
+    th64 = [datagen.bf16_bits_to_f64(t) for t in inp.theta_bf16]
+    tg64 = datagen.bf16_bits_to_f64(inp.target_bf16)
+    idx = _pick_certified(oracle_mod, net, th64, tg64, inp, pool, b)
+    ctx = g.Context(max_batch=b, n_actions=A, groups=G, dtype=g.GORILA_BF16)
+    thetas = _dev(torch, inp.theta_bf16.view(np.int16))
+    target = _dev(torch, inp.target_bf16.view(np.int16))
+    grads, loss = g.learner_step_grouped(ctx, thetas, target, A, _replay(torch, g, inp),
+                                         _dev(torch, idx), inp.gamma, clip)
+    ctx.check()
+    ref = _oracle_groups(oracle_mod, net, th64, tg64, inp, idx, b, clip=clip)
+    for gi in range(G):
+        errs = parity.assert_grads_close(grads[gi].cpu().numpy(), ref[gi]["grads"], A,
+                                         parity.GRAD_TOL_BF16)
+        l = float(loss[gi].cpu())
+        assert abs(l - ref[gi]["loss"]) <= parity.LOSS_TOL * abs(ref[gi]["loss"]), gi
+    _say(f"grad rel-L2 of the last group {errs}")
     ctx.close()
 
 
