@@ -202,7 +202,7 @@ int forward_one(gorila_ctx* c, const Plan& p, const gorila_params* prm, const ui
     { StageTimer t(c, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 1, n, at<float>(c, p.h1), false, st); }
     { StageTimer t(c, ST_CONV2_FWD); launch_conv2_fwd(at<float>(c, p.h1), w2t, th, 1, n, at<float>(c, p.h2), false, st); }
     { StageTimer t(c, ST_CONV3_FWD); launch_conv3_fwd(at<float>(c, p.h2), w3t, th, 1, n, at<float>(c, p.h3), false, st); }
-    { StageTimer t(c, ST_FC1_FWD); *fc1_splits = launch_fc1_fwd(at<float>(c, p.h3), th, 1, n, at<float>(c, p.fc1part), false, st); }
+    { StageTimer t(c, ST_FC1_FWD); *fc1_splits = launch_fc1_fwd(at<float>(c, p.h3), th, GroupPtrs16{}, 1, n, at<float>(c, p.fc1part), false, st); }
     return check_launch();
 }
 
@@ -454,18 +454,36 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
         wv[g].w3d = g < G ? at<float>(ctx, p.w3d + (size_t)g * W3T_BYTES) : nullptr;
         wv[g].w2p = g < G ? at<float>(ctx, p.w2p + (size_t)g * W2T_BYTES) : nullptr;
     }
+    // bf16 steps read W4 in place (the fc1 kernels widen it as they load), so
+    // only the other tensors are widened
+    GroupPtrs16 w4b{};
+    if (bf16)
+        for (int g = 0; g <= G; ++g)
+            w4b.p[g] = (const uint16_t*)(g < G ? params[g].data : target_params->data) + OFF_W4;
     {
         StageTimer t(ctx, ST_PREP);
-        if (n_widen) launch_widen_bf16(widen, n_widen, P, st);
+        if (n_widen && bf16) {
+            launch_widen_bf16(widen, n_widen, OFF_W4, st);
+            WidenSet tail = widen;
+            for (int i = 0; i < n_widen; ++i) {
+                tail.src[i] += OFF_B4;
+                tail.dst[i] += OFF_B4;
+            }
+            launch_widen_bf16(tail, n_widen, P - OFF_B4, st);
+        } else if (n_widen) {
+            launch_widen_bf16(widen, n_widen, P, st);
+        }
         launch_prep_weights(wv, G + 1, st);
     }
     // forward groups 0 .. G-1: online nets on s; G .. 2G-1: the target on s'
     GroupPtrs th{}, w2t{}, w3t{};
+    GroupPtrs16 w4f{};
     for (int g = 0; g < 2 * G; ++g) {
         const int net = g < G ? g : G;
         th.p[g] = wv[net].theta;
         w2t.p[g] = wv[net].w2t;
         w3t.p[g] = wv[net].w3t;
+        w4f.p[g] = w4b.p[net];
     }
     float* h1 = at<float>(ctx, p.h1);
     float* h2 = at<float>(ctx, p.h2);
@@ -476,7 +494,7 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
     { StageTimer t(ctx, ST_CONV2_FWD); launch_conv2_fwd(h1, w2t, th, 2 * G, b, h2, bf16, st); }
     { StageTimer t(ctx, ST_CONV3_FWD); launch_conv3_fwd(h2, w3t, th, 2 * G, b, h3, bf16, st); }
     int S = 0;
-    { StageTimer t(ctx, ST_FC1_FWD); S = launch_fc1_fwd(h3, th, 2 * G, b, fc1part, bf16, st); }
+    { StageTimer t(ctx, ST_FC1_FWD); S = launch_fc1_fwd(h3, th, w4f, 2 * G, b, fc1part, bf16, st); }
 
     float* dz4 = at<float>(ctx, p.dz4);
     float* dz3 = at<float>(ctx, p.dz3);
@@ -501,7 +519,7 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
     int head_blocks = 0, s1 = 0, s2 = 0, s3 = 0;
     {
         StageTimer t(ctx, ST_FC1_BWD);
-        head_blocks = launch_fc1_backward(dz4, on, G, h3, h4, a, coef, ell, b, A, dz3, grads_out, P,
+        head_blocks = launch_fc1_backward(dz4, on, w4b, G, h3, h4, a, coef, ell, b, A, dz3, grads_out, P,
                                           at<float>(ctx, p.hpart), bf16, st);
     }
     {

@@ -49,6 +49,9 @@ constexpr int MAX_LEARNER_GROUPS = MAX_GROUPS / 2;
 struct GroupPtrs {
     const float* p[MAX_GROUPS];
 };
+struct GroupPtrs16 {  // bf16 bit patterns
+    const uint16_t* p[MAX_GROUPS];
+};
 
 // Sticky device error bits (workspace word 0).
 constexpr unsigned ERR_IDX_RANGE = 1u, ERR_ACTION_RANGE = 2u;

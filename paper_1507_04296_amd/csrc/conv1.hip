@@ -98,66 +98,94 @@ __global__ __launch_bounds__(256, 2) void conv1_fwd_kernel(const uint8_t* const*
 
 // The same layer for bf16 parameter sets on v_mfma_f32_32x32x16_bf16: bytes
 // (integers 0..255) and bf16 weights are exact bf16 operands, so every
-// product is exact and only the fp32 accumulation rounds.  One 16-wide step
-// covers two filter rows (c, u) of 8 columns v: lane half h takes row
-// 2 * step + h, so a lane's eight operands are eight consecutive input bytes.
-__device__ inline uint32_t bf16_pair_exact(float lo, float hi) {  // both bf16-representable
-    return (__float_as_uint(hi) & 0xffff0000u) | (__float_as_uint(lo) >> 16);
-}
-__device__ inline bf16x8 bytes_bf16x8(uint32_t d0, uint32_t d1) {
-    typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
-    const u32x4v q = {bf16_pair_exact((float)(d0 & 255u), (float)((d0 >> 8) & 255u)),
-                      bf16_pair_exact((float)((d0 >> 16) & 255u), (float)(d0 >> 24)),
-                      bf16_pair_exact((float)(d1 & 255u), (float)((d1 >> 8) & 255u)),
-                      bf16_pair_exact((float)((d1 >> 16) & 255u), (float)(d1 >> 24))};
-    return __builtin_bit_cast(bf16x8, q);
-}
+// product is exact and only the fp32 accumulation rounds.  A workgroup of 13
+// waves keeps W1 (bf16) in LDS and walks samples b = blockIdx.x,
+// b + gridDim.x, ... of its parameter set: it converts a sample's 4 frames to
+// bf16 once, into LDS, fetches the next sample's frames into registers while
+// wave t computes pixel tile t (32 pixels x 32 filters; the 13th tile is half
+// full).  One 16-wide MFMA step covers two filter rows (c, u) of 8 columns v:
+// lane half h takes row 2 * step + h, so a lane's eight operands are eight
+// consecutive bf16 pixels of one input row.
+constexpr int C1F_WAVES = (P1 + 31) / 32;  // 13
+constexpr int C1F_THREADS = 64 * C1F_WAVES;
+constexpr int C1F_WLD = 256 + 8;           // W1 row stride in LDS (bf16): 528 bytes
+constexpr int C1F_XV = STATE_BYTES / 16;   // 1764 16-byte vectors per sample
+constexpr int C1F_XPT = (C1F_XV + C1F_THREADS - 1) / C1F_THREADS;
+constexpr int C1F_TARGET_WGS = 512;        // two workgroups per CU
 
-__global__ __launch_bounds__(256, 2) void conv1_fwd_bf16_kernel(
+__launch_bounds__(C1F_THREADS) __global__ void conv1_fwd_bf16_kernel(
     const uint8_t* const* __restrict__ ftab, GroupPtrs theta, int n, float* __restrict__ h1) {
-    __shared__ __attribute__((aligned(16))) uint8_t xs[2 * STATE_BYTES];
-    const int g = blockIdx.y, b0 = blockIdx.x * 2;
-    const int ns = min(2, n - b0);
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    stage_pair(ftab, g, n, b0, ns, xs);
-
+    __shared__ __attribute__((aligned(16))) __bf16 xs[STATE_BYTES];
+    __shared__ __attribute__((aligned(16))) __bf16 ws[C1 * C1F_WLD];
+    const int g = blockIdx.y;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const float* W1 = theta.p[g];
-    const int col = lane & 31, h = lane >> 5;
-    bf16x8 w[16];  // step st: W1[col][row 2 st + h][v = 0..7]
-#pragma unroll
-    for (int st = 0; st < 16; ++st) {
-        const f32x4 a = ld4(W1 + OFF_W1 + col * 256 + (2 * st + h) * 8);
-        const f32x4 b = ld4(W1 + OFF_W1 + col * 256 + (2 * st + h) * 8 + 4);
-        typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
-        const u32x4v q = {bf16_pair_exact(a[0], a[1]), bf16_pair_exact(a[2], a[3]),
-                          bf16_pair_exact(b[0], b[1]), bf16_pair_exact(b[2], b[3])};
-        w[st] = __builtin_bit_cast(bf16x8, q);
-    }
-    const float bias = W1[OFF_B1 + col];
-    __syncthreads();
 
-    const int rows = ns * P1;
-    const int ntiles = (rows + 31) / 32;
-    float* out = h1 + ((int64_t)g * n + b0) * P1 * C1;
-    const int z = blockIdx.z, zs = gridDim.z;
-    for (int t = z + zs * wave; t < ntiles; t += 4 * zs) {
-        int m = t * 32 + (lane & 31);
-        if (m >= rows) m = 0;  // padding rows compute on a valid pixel, never stored
-        const int s = m / P1, p = m - s * P1, i = p / H1, j = p - i * H1;
-        const uint8_t* base = xs + s * STATE_BYTES + (S1 * i) * IN_W + S1 * j;
+    uint4 xv[C1F_XPT];
+    auto fetch = [&](int b) {  // the sample's 16-byte vectors of this thread
+        const uint8_t* const* fr = ftab + ((int64_t)g * n + b) * 4;
+#pragma unroll
+        for (int k = 0; k < C1F_XPT; ++k) {
+            const int e = tid + k * C1F_THREADS;  // vector e: frame e / 441
+            const uint8_t* f = e < C1F_XV ? fr[e / (FRAME_BYTES / 16)] : nullptr;
+            xv[k] = f ? ldg_u4((const uint4*)f + e % (FRAME_BYTES / 16)) : make_uint4(0, 0, 0, 0);
+        }
+    };
+    fetch(blockIdx.x);
+
+    constexpr int WQ = C1 * 256 / 4;  // 2048 weight quads
+    for (int q = tid; q < WQ; q += C1F_THREADS) {
+        const f32x4 w = ld4(W1 + OFF_W1 + 4 * q);
+        bf16x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = (__bf16)w[i];  // exact: bf16 values
+        *(bf16x4*)(ws + (q >> 6) * C1F_WLD + 4 * (q & 63)) = v;
+    }
+    const int col = lane & 31, h = lane >> 5;
+    const float bias = W1[OFF_B1 + col];
+
+    int m = wave * 32 + (lane & 31);
+    if (m >= P1) m = 0;  // padding rows compute on a valid pixel, never stored
+    const int i = m / H1, j = m - i * H1;
+    const __bf16* xb = xs + (S1 * i) * IN_W + S1 * j;  // 8-byte aligned
+    const __bf16* wb = ws + col * C1F_WLD + 8 * h;      // 16-byte aligned
+
+    for (int b = blockIdx.x; b < n; b += gridDim.x) {
+#pragma unroll
+        for (int k = 0; k < C1F_XPT; ++k) {
+            const int e = tid + k * C1F_THREADS;
+            if (e < C1F_XV) {
+                const uint32_t d[4] = {xv[k].x, xv[k].y, xv[k].z, xv[k].w};
+                bf16x8 lo, hi;
+#pragma unroll
+                for (int t = 0; t < 8; ++t) {
+                    lo[t] = (__bf16)(float)((d[t >> 2] >> (8 * (t & 3))) & 255u);
+                    hi[t] = (__bf16)(float)((d[2 + (t >> 2)] >> (8 * (t & 3))) & 255u);
+                }
+                *(bf16x8*)(xs + 16 * e) = lo;
+                *(bf16x8*)(xs + 16 * e + 8) = hi;
+            }
+        }
+        __syncthreads();
+        if (b + (int)gridDim.x < n) fetch(b + gridDim.x);  // in flight during the products
+
         f32x16 acc = f32x16{};
 #pragma unroll
         for (int st = 0; st < 16; ++st) {
             const int cb = 2 * st + h, c = cb >> 3, u = cb & 7;
-            const uint8_t* px = base + c * FRAME_BYTES + u * IN_W;  // 4-byte aligned
-            const uint32_t d0 = *(const uint32_t*)px, d1 = *(const uint32_t*)(px + 4);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bytes_bf16x8(d0, d1), w[st], acc, 0, 0, 0);
+            const __bf16* px = xb + c * FRAME_BYTES + u * IN_W;
+            const bf16x4 x0 = *(const bf16x4*)px, x1 = *(const bf16x4*)(px + 4);
+            const bf16x8 x = __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7);
+            const bf16x8 w = *(const bf16x8*)(wb + 16 * st);
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, w, acc, 0, 0, 0);
         }
+        float* out = h1 + ((int64_t)g * n + b) * P1 * C1;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const int row = t * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-            if (row < rows) out[(int64_t)row * C1 + col] = fmaxf(acc[r] * (1.0f / 255.0f) + bias, 0.0f);
+            const int row = wave * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
+            if (row < P1) out[row * C1 + col] = fmaxf(acc[r] * (1.0f / 255.0f) + bias, 0.0f);
         }
+        __syncthreads();  // every wave is done with xs before the next sample lands
     }
 }
 
@@ -168,9 +196,12 @@ void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int gr
     // tiles over up to 8 workgroups, each staging the pair's frames.
     const int blocks = (n + 1) / 2 * groups;
     const int split = blocks >= 512 ? 1 : min(8, (512 + blocks - 1) / blocks);
-    const dim3 grid((n + 1) / 2, groups, split);
-    if (bf16) conv1_fwd_bf16_kernel<<<grid, 256, 0, st>>>(ftab, theta, n, h1);
-    else      conv1_fwd_kernel<<<grid, 256, 0, st>>>(ftab, theta, n, h1);
+    if (bf16) {
+        const int per_group = max(1, min(n, C1F_TARGET_WGS / groups));
+        conv1_fwd_bf16_kernel<<<dim3(per_group, groups), C1F_THREADS, 0, st>>>(ftab, theta, n, h1);
+    }
+    else
+        conv1_fwd_kernel<<<dim3((n + 1) / 2, groups, split), 256, 0, st>>>(ftab, theta, n, h1);
 }
 
 // Weight gradient: dW1[o][(c,u,v)] = (1/255) sum_pixels dz1[pixel][o] * x[c][4i+u][4j+v]

@@ -78,9 +78,10 @@ void launch_conv2_fwd(const float* h1, const GroupPtrs& w2t, const GroupPtrs& th
 void launch_conv3_fwd(const float* h2, const GroupPtrs& w3t, const GroupPtrs& theta, int groups,
                       int n, float* h3, bool bf16, hipStream_t st);
 // fc1 forward as split-K partial sums partial[g][s][b][512]; returns the
-// number of splits s (the head kernels finish the layer).
-int launch_fc1_fwd(const float* h3, const GroupPtrs& theta, int groups, int n, float* partial,
-                   bool bf16, hipStream_t st);
+// number of splits s (the head kernels finish the layer).  With bf16, W4 is
+// read from w4b (the sets' bf16 W4 blocks, 2-byte aligned at least), not theta.
+int launch_fc1_fwd(const float* h3, const GroupPtrs& theta, const GroupPtrs16& w4b, int groups,
+                   int n, float* partial, bool bf16, hipStream_t st);
 
 // Head: Q values, epsilon-greedy actions, TD error / Huber loss / dLoss.
 // Each first finishes the FC-512 layer (splits in order, bias, ReLU).
@@ -106,7 +107,8 @@ void launch_td_head(const float* fc1part_online, const float* fc1part_target, in
 //       loss (returns row blocks per group);
 //  conv3: dz2 and split partials of dW3 / db3 (returns splits per group);
 //  conv2: dz1 and split partials of dW2 / db2 (returns splits per group).
-int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, int groups, const float* h3,
+int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, const GroupPtrs16& w4b,
+                        int groups, const float* h3,
                         const float* h4, const int32_t* a, const float* coef, const float* ell,
                         int n, int A, float* dz3, float* grads, int64_t grads_stride,
                         float* hpart, bool bf16, hipStream_t st);

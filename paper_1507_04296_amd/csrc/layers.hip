@@ -227,6 +227,42 @@ struct RowMajorK {  // rows of a row-major [rows][ld] matrix, quads along k
     }
     __device__ f32x4 load(int kc, int j) const { return ld4(base[j] + kc * BK); }
 };
+// bf16 weights read in place and widened exactly: a quad is 4 values at a
+// multiple of 4 along a row of W4, so its alignment is that of the matrix,
+// which the parameter layout only guarantees to 2 bytes; `al` (8, 4 or 2)
+// picks one, two or four loads per quad.
+__device__ inline int align_of(const uint16_t* p) {
+    const uintptr_t a = (uintptr_t)p;
+    return (a & 7) == 0 ? 8 : (a & 3) == 0 ? 4 : 2;
+}
+__device__ inline f32x4 ld4_bf16(const uint16_t* p, int al) {
+    uint32_t a, b;
+    if (al == 8) {
+        const uint2 v = *(const uint2*)p;
+        a = v.x;
+        b = v.y;
+    } else if (al == 4) {
+        a = *(const uint32_t*)p;
+        b = *(const uint32_t*)(p + 2);
+    } else {
+        a = p[0] | ((uint32_t)p[1] << 16);
+        b = p[2] | ((uint32_t)p[3] << 16);
+    }
+    return f32x4{__uint_as_float(a << 16), __uint_as_float(a & 0xffff0000u),
+                 __uint_as_float(b << 16), __uint_as_float(b & 0xffff0000u)};
+}
+struct RowMajorK16 {  // RowMajorK over a bf16 matrix
+    const uint16_t* a;
+    int rows, r0, ld;
+    const uint16_t* base[MAXQ];
+    int al = 8;
+    __device__ void init(int j, int row, int k) {
+        base[j] = a + (int64_t)(r0 + row < rows ? r0 + row : 0) * ld + k;
+        al = align_of(a);
+    }
+    __device__ f32x4 load(int kc, int j) const { return ld4_bf16(base[j] + kc * BK, al); }
+};
+
 struct PlainStore {
     float* out;
     int rows, r0, c0, ld;
@@ -244,6 +280,7 @@ template <int BF>
 struct Fc1FwdJob {
     const float* h3;
     GroupPtrs theta;
+    GroupPtrs16 w4b;  // bf16 steps: W4 of each set, read in place
     float* partial;
     int n, groups, splits, cps;
     static constexpr int PA = BF ? BF_ACT_FWD : 0, PB = BF ? BF_WEIGHT : 0;
@@ -261,22 +298,27 @@ struct Fc1FwdJob {
         t /= HID / 64;
         const int s = t % splits, g = t / splits;
         RowMajorK la{h3 + (int64_t)g * n * FLAT, n, r0, FLAT};
-        RowMajorK lb{theta.p[g] + OFF_W4, HID, c0, FLAT};
         PlainStore epi{partial + ((int64_t)g * splits + s) * n * HID, n, r0, c0, HID};
         const int kc0 = s * cps, kc1 = min(FC1_CHUNKS, kc0 + cps);
-        mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi);
+        if constexpr (BF > 0) {
+            RowMajorK16 lb{w4b.p[g], HID, c0, FLAT};
+            mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi);
+        } else {
+            RowMajorK lb{theta.p[g] + OFF_W4, HID, c0, FLAT};
+            mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi);
+        }
     }
 };
 
-int launch_fc1_fwd(const float* h3, const GroupPtrs& theta, int groups, int n, float* partial,
-                   bool bf16, hipStream_t st) {
+int launch_fc1_fwd(const float* h3, const GroupPtrs& theta, const GroupPtrs16& w4b, int groups,
+                   int n, float* partial, bool bf16, hipStream_t st) {
     if (n <= 0) return 0;
     const int mt = (n + 63) / 64, tiles = mt * (HID / 64) * groups;
     int splits = min(FC1_MAX_SPLITS, max(1, (TARGET_WGS + tiles - 1) / tiles));
     const int cps = (FC1_CHUNKS + splits - 1) / splits;
     splits = (FC1_CHUNKS + cps - 1) / cps;
-    if (bf16) launch_jobs(st, Fc1FwdJob<1>{h3, theta, partial, n, groups, splits, cps});
-    else      launch_jobs(st, Fc1FwdJob<0>{h3, theta, partial, n, groups, splits, cps});
+    if (bf16) launch_jobs(st, Fc1FwdJob<1>{h3, theta, w4b, partial, n, groups, splits, cps});
+    else      launch_jobs(st, Fc1FwdJob<0>{h3, theta, w4b, partial, n, groups, splits, cps});
     return splits;
 }
 
@@ -298,6 +340,23 @@ struct RowMajorR {
         const int k = kc * BK + kk[j];
         const f32x4 v = ld4(base[j] + (int64_t)(k < kmax ? k : 0) * ld);
         return ZERO ? sel4(k < kmax, v) : v;
+    }
+};
+
+struct RowMajorR16 {  // RowMajorR<false> over a bf16 matrix
+    const uint16_t* a;
+    int c0, ld, kmax;
+    const uint16_t* base[MAXQ];
+    int kk[MAXQ];
+    int al = 8;
+    __device__ void init(int j, int row, int k) {
+        base[j] = a + c0 + row;
+        kk[j] = k;
+        al = align_of(a);
+    }
+    __device__ f32x4 load(int kc, int j) const {
+        const int k = kc * BK + kk[j];
+        return ld4_bf16(base[j] + (int64_t)(k < kmax ? k : 0) * ld, al);
     }
 };
 
@@ -325,6 +384,7 @@ template <int BF>
 struct Fc1DgradJob {
     const float* dz4;
     GroupPtrs theta;
+    GroupPtrs16 w4b;  // bf16 steps: W4 of each set, read in place
     const float* h3;
     float* dz3;
     int n, groups;
@@ -342,9 +402,15 @@ struct Fc1DgradJob {
         const int r0 = (t % mt) * 64, c0 = (t / mt) * 64;  // row tiles of one W4 column block adjacent
         const int64_t rows = (int64_t)g * n;
         RowMajorK la{dz4 + rows * HID, n, r0, HID};
-        RowMajorR<false> lb{theta.p[g] + OFF_W4, c0, FLAT, HID};  // HID is a whole number of chunks
         Dz3NhwcStore epi{dz3 + rows * FLAT, h3 + rows * FLAT, n, r0, c0};
-        mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, 0, HID / BK, la, lb, epi);
+        // HID is a whole number of chunks
+        if constexpr (BF > 0) {
+            RowMajorR16 lb{w4b.p[g], c0, FLAT, HID};
+            mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, 0, HID / BK, la, lb, epi);
+        } else {
+            RowMajorR<false> lb{theta.p[g] + OFF_W4, c0, FLAT, HID};
+            mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, 0, HID / BK, la, lb, epi);
+        }
     }
 };
 
@@ -453,7 +519,8 @@ struct HeadPartialJob {
     }
 };
 
-int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, int groups, const float* h3,
+int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, const GroupPtrs16& w4b,
+                        int groups, const float* h3,
                         const float* h4, const int32_t* a, const float* coef, const float* ell,
                         int n, int A, float* dz3, float* grads, int64_t grads_stride,
                         float* hpart, bool bf16, hipStream_t st) {
@@ -462,10 +529,10 @@ int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, int groups, co
     const int row_blocks = (n + rows - 1) / rows;
     const HeadPartialJob hp{h4, a, coef, ell, hpart, n, A, rows, row_blocks, groups};
     if (bf16)
-        launch_jobs(st, Fc1DgradJob<1>{dz4, theta, h3, dz3, n, groups},
+        launch_jobs(st, Fc1DgradJob<1>{dz4, theta, w4b, h3, dz3, n, groups},
                     Fc1WgradJob<1>{dz4, h3, grads, grads_stride, n, groups}, hp);
     else
-        launch_jobs(st, Fc1DgradJob<0>{dz4, theta, h3, dz3, n, groups},
+        launch_jobs(st, Fc1DgradJob<0>{dz4, theta, w4b, h3, dz3, n, groups},
                     Fc1WgradJob<0>{dz4, h3, grads, grads_stride, n, groups}, hp);
     return row_blocks;
 }
