@@ -145,9 +145,10 @@ struct IsMaskEpi<T, std::void_t<decltype(T::MASK)>> : std::bool_constant<T::MASK
 // that hi + lo carries about 16 significant bits and the engine adds both
 // products hi*B and lo*B.  The loaders still deliver fp32 quads; they are
 // converted as they are stored to LDS.  A plane is [rows][BK] bf16 (64 bytes
-// a row) whose four 16-byte chunks are stored XOR-permuted by
-// ((r >> 1) ^ (r >> 3)) & 3, so that 16 consecutive rows reading one chunk
-// touch every LDS bank once.  Lane l of an MFMA supplies row l % 32 and the
+// a row) whose four 16-byte chunks are stored XOR-permuted by (r >> 2) & 3:
+// rows r and r + 4k share LDS banks, and the permutation spreads them
+// (measured: no bank conflicts for k-contiguous operands, against 0.33-0.6
+// of LDS cycles for permutations by the low row bits or none).  Lane l of an MFMA supplies row l % 32 and the
 // eight reduction indices 8 (l / 32) .. +7 of its 16-wide step; the
 // accumulator layout is that of the fp32 instruction.
 // ---------------------------------------------------------------------------
@@ -159,7 +160,7 @@ struct Bf16Tile {
     static constexpr int PLANE = ROWS * BK * 2;  // bytes
     static constexpr int BYTES = PL * PLANE;
     __device__ static inline int chunk(int row, int c) {
-        return row * (BK * 2) + (((c ^ (row >> 1) ^ (row >> 3)) & 3) << 4);
+        return row * (BK * 2) + (((c ^ (row >> 2)) & 3) << 4);
     }
     // Quad v of a MODE-laid operand at tile coordinates (row, k): KMAJ quads
     // are 4 reduction indices of one row, RMAJ quads 4 rows at one index.

@@ -1,161 +1,97 @@
 // First convolution (Section 5.1: 32 filters of 4x8x8, stride 4, ReLU) on the
-// raw uint8 frames, forward and weight gradient.
-//
-// Forward: one workgroup takes two samples, stages their 2 x 28224 input bytes
-// in LDS (16-byte copies straight from the replay frames), keeps W1 in
-// registers and runs the 800 x 32 x 256 product as 25 M-tiles of 32 pixels.
-// The reduction index is ordered (c, u, v) with lane half h feeding v = 4h..4h+3
-// of one filter row, so one aligned 4-byte LDS read gives a lane the four
-// input bytes of four consecutive MFMAs.  Bytes enter the MFMA as exact
-// integers; the 1/255 input scale is applied once in the epilogue.
+// raw uint8 frames, forward and weight gradient.  Bytes enter the products as
+// exact integers; the 1/255 input scale is applied once in each epilogue.
 #include "common.h"
 #include "kernels.h"
 
 namespace gorila {
 
-// Stage the 8 frames (2 samples x 4 channels) of sample pair b0 of group g in
-// LDS: the frame pointers are read once (uniform loads), then every thread
-// issues all of its 16-byte loads before its first LDS store, so the copy
-// costs one memory latency rather than one per vector.  Null frames are zeros.
-__device__ inline void stage_pair(const uint8_t* const* ftab, int g, int n, int b0, int ns,
-                                  uint8_t* xs) {
-    const int tid = threadIdx.x;
-    constexpr int VEC = FRAME_BYTES / 16;  // 441 16-byte vectors per frame
-    const uint4* fp[8];
-#pragma unroll
-    for (int f = 0; f < 8; ++f)
-        fp[f] = (f >> 2) < ns ? (const uint4*)ftab[((int64_t)g * n + b0 + (f >> 2)) * 4 + (f & 3)]
-                              : nullptr;
-    const bool second = tid + 256 < VEC;  // lanes that copy a second vector per frame
-    uint4 v0[8], v1[8];
-    const uint4 z = make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int f = 0; f < 8; ++f) {
-        v0[f] = fp[f] ? ldg_u4(fp[f] + tid) : z;
-        v1[f] = fp[f] && second ? ldg_u4(fp[f] + tid + 256) : z;
-    }
-#pragma unroll
-    for (int f = 0; f < 8; ++f) {
-        ((uint4*)xs)[f * VEC + tid] = v0[f];
-        if (second) ((uint4*)xs)[f * VEC + tid + 256] = v1[f];
-    }
-}
-
-__global__ __launch_bounds__(256, 2) void conv1_fwd_kernel(const uint8_t* const* __restrict__ ftab,
-                                                           GroupPtrs theta, int n,
-                                                           float* __restrict__ h1) {
-    __shared__ __attribute__((aligned(16))) uint8_t xs[2 * STATE_BYTES];
-    const int g = blockIdx.y, b0 = blockIdx.x * 2;
-    const int ns = min(2, n - b0);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-
-    stage_pair(ftab, g, n, b0, ns, xs);
-
-    const float* W1 = theta.p[g];
-    const int col = lane & 31, h = lane >> 5;
-    float w[128];  // w[4*(c*8+u) + q] = W1[col][c][u][4h+q]
-#pragma unroll
-    for (int cb = 0; cb < 32; ++cb) {
-        f32x4 v = ld4(W1 + OFF_W1 + col * 256 + cb * 8 + 4 * h);
-        w[4 * cb + 0] = v[0];
-        w[4 * cb + 1] = v[1];
-        w[4 * cb + 2] = v[2];
-        w[4 * cb + 3] = v[3];
-    }
-    const float bias = W1[OFF_B1 + col];
-    __syncthreads();
-
-    const int rows = ns * P1;
-    const int ntiles = (rows + 31) / 32;
-    float* out = h1 + ((int64_t)g * n + b0) * P1 * C1;
-    // workgroup z of gridDim.z takes tiles z, z + zs, ... (small batches
-    // spread one sample pair's 25 tiles over several workgroups)
-    const int z = blockIdx.z, zs = gridDim.z;
-    for (int t = z + zs * wave; t < ntiles; t += 4 * zs) {
-        int m = t * 32 + (lane & 31);
-        if (m >= rows) m = 0;  // padding rows compute on a valid pixel, never stored
-        const int s = m / P1, p = m - s * P1, i = p / H1, j = p - i * H1;
-        const uint8_t* base = xs + s * STATE_BYTES + (S1 * i) * IN_W + S1 * j + 4 * h;
-        f32x16 acc = f32x16{};
-#pragma unroll
-        for (int c = 0; c < 4; ++c)
-#pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const uint32_t d = *(const uint32_t*)(base + c * FRAME_BYTES + u * IN_W);
-                const int cb = c * 8 + u;
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32((float)(d & 255u), w[4 * cb + 0], acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32((float)((d >> 8) & 255u), w[4 * cb + 1], acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32((float)((d >> 16) & 255u), w[4 * cb + 2], acc, 0, 0, 0);
-                acc = __builtin_amdgcn_mfma_f32_32x32x2f32((float)(d >> 24), w[4 * cb + 3], acc, 0, 0, 0);
-            }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int row = t * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-            if (row < rows) out[(int64_t)row * C1 + col] = fmaxf(acc[r] * (1.0f / 255.0f) + bias, 0.0f);
-        }
-    }
-}
-
-// The same layer for bf16 parameter sets on v_mfma_f32_32x32x16_bf16: bytes
-// (integers 0..255) and bf16 weights are exact bf16 operands, so every
-// product is exact and only the fp32 accumulation rounds.  A workgroup of 13
-// waves keeps W1 (bf16) in LDS and walks samples b = blockIdx.x,
-// b + gridDim.x, ... of its parameter set: it converts a sample's 4 frames to
-// bf16 once, into LDS, fetches the next sample's frames into registers while
-// wave t computes pixel tile t (32 pixels x 32 filters; the 13th tile is half
-// full).  One 16-wide MFMA step covers two filter rows (c, u) of 8 columns v:
-// lane half h takes row 2 * step + h, so a lane's eight operands are eight
-// consecutive bf16 pixels of one input row.
+// The layer on v_mfma_f32_32x32x16_bf16 with exact products: the bytes
+// (integers 0..255) are exact bf16 values, and W1 enters as WP bf16 planes
+// whose sum is W1 exactly -- one plane for bf16 parameter sets; for fp32 sets
+// three (w = hi + mid + lo, each the rounded remainder of the previous: 8 + 8
+// + 8 significant bits cover fp32's 24), so every product is exact and only
+// the fp32 accumulation rounds, as in an fp32 GEMM.  A workgroup of 13 waves
+// keeps the planes in LDS and walks samples b = blockIdx.x, b + gridDim.x,
+// ... of its parameter set: it converts a sample's 4 frames to bf16 once, into
+// LDS, fetches the next sample's frames into registers while wave t computes
+// pixel tile t (32 pixels x 32 filters; the 13th tile is half full).  One
+// 16-wide MFMA step covers two filter rows (c, u) of 8 columns v: lane half h
+// takes row 2 * step + h, so a lane's eight operands are eight consecutive
+// bf16 pixels of one input row.
 constexpr int C1F_WAVES = (P1 + 31) / 32;  // 13
 constexpr int C1F_THREADS = 64 * C1F_WAVES;
 constexpr int C1F_WLD = 256 + 8;           // W1 row stride in LDS (bf16): 528 bytes
 constexpr int C1F_XV = STATE_BYTES / 16;   // 1764 16-byte vectors per sample
 constexpr int C1F_XPT = (C1F_XV + C1F_THREADS - 1) / C1F_THREADS;
-constexpr int C1F_TARGET_WGS = 512;        // two workgroups per CU
+// resident workgroups: two per CU with one plane (73 KB of LDS), one with three
+__host__ __device__ constexpr int c1f_target_wgs(int wp) { return wp == 1 ? 512 : 256; }
 
-__launch_bounds__(C1F_THREADS) __global__ void conv1_fwd_bf16_kernel(
+template <int WP>
+__launch_bounds__(C1F_THREADS) __global__ void conv1_fwd_mfma16_kernel(
     const uint8_t* const* __restrict__ ftab, GroupPtrs theta, int n, float* __restrict__ h1) {
     __shared__ __attribute__((aligned(16))) __bf16 xs[STATE_BYTES];
-    __shared__ __attribute__((aligned(16))) __bf16 ws[C1 * C1F_WLD];
+    __shared__ __attribute__((aligned(16))) __bf16 ws[WP][C1 * C1F_WLD];
+    __shared__ float bs[C1];
     const int g = blockIdx.y;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const float* W1 = theta.p[g];
 
     uint4 xv[C1F_XPT];
-    auto fetch = [&](int b) {  // the sample's 16-byte vectors of this thread
+    unsigned okm = 0;  // bit k: xv[k] holds frame bytes (else zeros)
+    // The sample's 16-byte vectors of this thread.  Branch-free, so all of
+    // them are in flight together: the four frame pointers are read first (the
+    // same for every thread), a null frame reads W1 instead and is zeroed when
+    // converted (not here, which would wait for the loads).
+    auto fetch = [&](int b) {
         const uint8_t* const* fr = ftab + ((int64_t)g * n + b) * 4;
+        const uint8_t* f0 = fr[0];
+        const uint8_t* f1 = fr[1];
+        const uint8_t* f2 = fr[2];
+        const uint8_t* f3 = fr[3];
 #pragma unroll
         for (int k = 0; k < C1F_XPT; ++k) {
             const int e = tid + k * C1F_THREADS;  // vector e: frame e / 441
-            const uint8_t* f = e < C1F_XV ? fr[e / (FRAME_BYTES / 16)] : nullptr;
-            xv[k] = f ? ldg_u4((const uint4*)f + e % (FRAME_BYTES / 16)) : make_uint4(0, 0, 0, 0);
+            const int fi = e / (FRAME_BYTES / 16);
+            const uint8_t* f = fi == 0 ? f0 : fi == 1 ? f1 : fi == 2 ? f2 : f3;
+            const bool ok = e < C1F_XV && f != nullptr;
+            xv[k] = ldg_u4(ok ? (const uint4*)f + (e - fi * (FRAME_BYTES / 16))
+                              : (const uint4*)(W1 + OFF_W1));
+            okm = k == 0 ? (unsigned)ok : okm | ((unsigned)ok << k);
         }
     };
     fetch(blockIdx.x);
 
     constexpr int WQ = C1 * 256 / 4;  // 2048 weight quads
     for (int q = tid; q < WQ; q += C1F_THREADS) {
-        const f32x4 w = ld4(W1 + OFF_W1 + 4 * q);
-        bf16x4 v;
+        f32x4 w = ld4(W1 + OFF_W1 + 4 * q);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = (__bf16)w[i];  // exact: bf16 values
-        *(bf16x4*)(ws + (q >> 6) * C1F_WLD + 4 * (q & 63)) = v;
+        for (int pl = 0; pl < WP; ++pl) {
+            bf16x4 v;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                v[i] = (__bf16)w[i];
+                w[i] -= (float)v[i];  // exact: the remainder has at most 16 significant bits
+            }
+            *(bf16x4*)(ws[pl] + (q >> 6) * C1F_WLD + 4 * (q & 63)) = v;
+        }
     }
+    if (tid < C1) bs[tid] = W1[OFF_B1 + tid];
     const int col = lane & 31, h = lane >> 5;
-    const float bias = W1[OFF_B1 + col];
 
     int m = wave * 32 + (lane & 31);
     if (m >= P1) m = 0;  // padding rows compute on a valid pixel, never stored
     const int i = m / H1, j = m - i * H1;
     const __bf16* xb = xs + (S1 * i) * IN_W + S1 * j;  // 8-byte aligned
-    const __bf16* wb = ws + col * C1F_WLD + 8 * h;      // 16-byte aligned
+    const int wofs = col * C1F_WLD + 8 * h;             // 16-byte aligned
 
     for (int b = blockIdx.x; b < n; b += gridDim.x) {
 #pragma unroll
         for (int k = 0; k < C1F_XPT; ++k) {
             const int e = tid + k * C1F_THREADS;
             if (e < C1F_XV) {
-                const uint32_t d[4] = {xv[k].x, xv[k].y, xv[k].z, xv[k].w};
+                const uint4 v = (okm >> k) & 1u ? xv[k] : make_uint4(0, 0, 0, 0);
+                const uint32_t d[4] = {v.x, v.y, v.z, v.w};
                 bf16x8 lo, hi;
 #pragma unroll
                 for (int t = 0; t < 8; ++t) {
@@ -176,14 +112,23 @@ __launch_bounds__(C1F_THREADS) __global__ void conv1_fwd_bf16_kernel(
             const __bf16* px = xb + c * FRAME_BYTES + u * IN_W;
             const bf16x4 x0 = *(const bf16x4*)px, x1 = *(const bf16x4*)(px + 4);
             const bf16x8 x = __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7);
-            const bf16x8 w = *(const bf16x8*)(wb + 16 * st);
-            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, w, acc, 0, 0, 0);
-        }
-        float* out = h1 + ((int64_t)g * n + b) * P1 * C1;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int row = wave * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-            if (row < P1) out[row * C1 + col] = fmaxf(acc[r] * (1.0f / 255.0f) + bias, 0.0f);
+            for (int pl = 0; pl < WP; ++pl) {
+                const bf16x8 w = *(const bf16x8*)(ws[pl] + wofs + 16 * st);
+                acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(x, w, acc, 0, 0, 0);
+            }
+        }
+        float* out = h1 + ((int64_t)g * n + b) * P1 * C1 + (wave * 32 + 4 * h) * C1 + col;
+        const float bias = bs[col];
+        if (wave < C1F_WAVES - 1) {  // full tiles: no per-store conditions
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                out[(8 * (r >> 2) + (r & 3)) * C1] = fmaxf(acc[r] * (1.0f / 255.0f) + bias, 0.0f);
+        } else {
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                if (wave * 32 + 8 * (r >> 2) + 4 * h + (r & 3) < P1)
+                    out[(8 * (r >> 2) + (r & 3)) * C1] = fmaxf(acc[r] * (1.0f / 255.0f) + bias, 0.0f);
         }
         __syncthreads();  // every wave is done with xs before the next sample lands
     }
@@ -192,16 +137,14 @@ __launch_bounds__(C1F_THREADS) __global__ void conv1_fwd_bf16_kernel(
 void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int groups, int n,
                       float* h1, bool bf16, hipStream_t st) {
     if (n <= 0) return;
-    // Aim at >= 512 workgroups (two per CU): below that, split each pair's
-    // tiles over up to 8 workgroups, each staging the pair's frames.
-    const int blocks = (n + 1) / 2 * groups;
-    const int split = blocks >= 512 ? 1 : min(8, (512 + blocks - 1) / blocks);
+    // one round of resident workgroups, each walking its set's samples
     if (bf16) {
-        const int per_group = max(1, min(n, C1F_TARGET_WGS / groups));
-        conv1_fwd_bf16_kernel<<<dim3(per_group, groups), C1F_THREADS, 0, st>>>(ftab, theta, n, h1);
+        const int per_group = max(1, min(n, c1f_target_wgs(1) / groups));
+        conv1_fwd_mfma16_kernel<1><<<dim3(per_group, groups), C1F_THREADS, 0, st>>>(ftab, theta, n, h1);
+    } else {
+        const int per_group = max(1, min(n, c1f_target_wgs(3) / groups));
+        conv1_fwd_mfma16_kernel<3><<<dim3(per_group, groups), C1F_THREADS, 0, st>>>(ftab, theta, n, h1);
     }
-    else
-        conv1_fwd_kernel<<<dim3((n + 1) / 2, groups, split), 256, 0, st>>>(ftab, theta, n, h1);
 }
 
 // Weight gradient: dW1[o][(c,u,v)] = (1/255) sum_pixels dz1[pixel][o] * x[c][4i+u][4j+v]
