@@ -10,8 +10,8 @@ namespace gorila {
 // (integers 0..255) are exact bf16 values, and W1 enters as WP bf16 planes
 // whose sum is W1 exactly -- one plane for bf16 parameter sets; for fp32 sets
 // three (w = hi + mid + lo, each the rounded remainder of the previous: 8 + 8
-// + 8 significant bits cover fp32's 24), so every product is exact and only
-// the fp32 accumulation rounds, as in an fp32 GEMM.  A workgroup of 13 waves
+// + 8 significant bits cover fp32's 24; exact for |w| above ~2^-90), so every
+// product is exact and only the fp32 accumulation rounds, as in an fp32 GEMM.  A workgroup of 13 waves
 // keeps the planes in LDS and walks samples b = blockIdx.x, b + gridDim.x,
 // ... of its parameter set: it converts a sample's 4 frames to bf16 once, into
 // LDS, fetches the next sample's frames into registers while wave t computes
