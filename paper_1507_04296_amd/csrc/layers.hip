@@ -844,12 +844,14 @@ int launch_conv2_backward(const float* dz2, const GroupPtrs& w2p, int groups, co
     int splits = min(min(WG_MAX_SPLITS / groups, nchunks), max(1, CONV2_WG_SPLITS / groups));
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
+    // the weight-gradient workgroups are the longer ones (21 chunks against at
+    // most 8 at batch 512): dispatched first, they do not trail the launch
     if (bf16)
-        launch_jobs(st, Conv2DgradJob<1>{dz2, w2p, h1, dz1, n, groups},
-                    Conv2WgradJob<1>{dz2, h1, partial, bias_part, n, splits, cps, groups});
+        launch_jobs(st, Conv2WgradJob<1>{dz2, h1, partial, bias_part, n, splits, cps, groups},
+                    Conv2DgradJob<1>{dz2, w2p, h1, dz1, n, groups});
     else
-        launch_jobs(st, Conv2DgradJob<0>{dz2, w2p, h1, dz1, n, groups},
-                    Conv2WgradJob<0>{dz2, h1, partial, bias_part, n, splits, cps, groups});
+        launch_jobs(st, Conv2WgradJob<0>{dz2, h1, partial, bias_part, n, splits, cps, groups},
+                    Conv2DgradJob<0>{dz2, w2p, h1, dz1, n, groups});
     return splits;
 }
 
