@@ -103,6 +103,7 @@ def test_learner_step_batch512_a6(torch_cuda, g, ctx, oracle_mod):
 
 @pytest.mark.parametrize("B,A,clip,term_p", [
     (1, 18, 1.0, 0.5), (37, 18, math.inf, 0.5), (97, 4, 1.0, 0.0), (65, 32, 0.5, 1.0),
+    (33, 1, 1.0, 0.1),  # one action: max_a' is that action's Q
 ])
 def test_learner_step_ragged_and_degenerate(torch_cuda, g, ctx, oracle_mod, B, A, clip, term_p):
     _say(f"learner ragged B={B} A={A} clip={clip} term_p={term_p}")
@@ -164,6 +165,29 @@ def test_host_argument_errors(torch_cuda, g, ctx):
         g.gorila_learner_step(small, theta, tgt, 18, rep, idx, 0.99, 1.0, grads, loss)
     assert e.value.code == -3
     small.close()
+
+
+def test_empty_calls_and_empty_batch(torch_cuda, g, ctx):
+    """Zero states or transitions: forward, act and gather return at once with
+    nothing written; a learner step needs at least one transition (EINVAL)."""
+    _say("n = 0 calls")
+    torch = torch_cuda
+    inp = datagen.learner_inputs(7600, 4, 18)
+    theta, tgt = _dev(torch, inp.theta), _dev(torch, inp.theta_target)
+    none = torch.empty((0, 4, 84, 84), dtype=torch.uint8, device="cuda")
+    assert g.q_forward(ctx, theta, 18, none).shape == (0, 18)
+    acts, q = g.act(ctx, theta, 18, none, 0.05, 1, with_q=True)
+    assert acts.shape == (0,) and q.shape == (0, 18)
+    out = g.gather(ctx, _stacked(torch, g, inp), torch.empty(0, dtype=torch.int64, device="cuda"))
+    assert out["s"].shape[0] == 0
+    ctx.check()
+    grads = torch.empty(g.param_count(18), device="cuda")
+    loss = torch.empty(1, device="cuda")
+    with pytest.raises(g.GorilaError) as e:
+        g.gorila_learner_step(ctx, theta, tgt, 18, _stacked(torch, g, inp),
+                              torch.empty(0, dtype=torch.int64, device="cuda"), 0.99, 1.0,
+                              grads, loss)
+    assert e.value.code == -1
 
 
 # ---------------------------------------------------------------------------
