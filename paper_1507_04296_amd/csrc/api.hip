@@ -436,10 +436,6 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
     int32_t* a = at<int32_t>(ctx, p.a);
     float* r = at<float>(ctx, p.r);
     uint8_t* term = at<uint8_t>(ctx, p.term);
-    {
-        StageTimer t(ctx, ST_RESOLVE);
-        launch_resolve(view_of(replay), idx, B, A, ftab, a, r, term, at<unsigned>(ctx, p.err), st);
-    }
 
     WidenSet widen{};
     int n_widen = 0;
@@ -460,9 +456,20 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
     if (bf16)
         for (int g = 0; g <= G; ++g)
             w4b.p[g] = (const uint16_t*)(g < G ? params[g].data : target_params->data) + OFF_W4;
-    {
+    if (n_widen == 0) {
+        // fp32 sets: the minibatch resolution and the weight transposes are
+        // independent and share one launch
         StageTimer t(ctx, ST_PREP);
-        if (n_widen && bf16) {
+        launch_resolve_prep(view_of(replay), idx, B, A, ftab, a, r, term,
+                            at<unsigned>(ctx, p.err), wv, G + 1, st);
+    } else {
+        {
+            StageTimer t(ctx, ST_RESOLVE);
+            launch_resolve(view_of(replay), idx, B, A, ftab, a, r, term, at<unsigned>(ctx, p.err),
+                           st);
+        }
+        StageTimer t(ctx, ST_PREP);
+        if (bf16) {
             launch_widen_bf16(widen, n_widen, OFF_W4, st);
             WidenSet tail = widen;
             for (int i = 0; i < n_widen; ++i) {
@@ -470,7 +477,7 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
                 tail.dst[i] += OFF_B4;
             }
             launch_widen_bf16(tail, n_widen, P - OFF_B4, st);
-        } else if (n_widen) {
+        } else {
             launch_widen_bf16(widen, n_widen, P, st);
         }
         launch_prep_weights(wv, G + 1, st);

@@ -61,6 +61,43 @@ struct WeightViewSet {
 };
 void launch_prep_weights(const WeightViews* nets, int n_nets, hipStream_t st);
 
+// Block `blk` of `nblk` (256 threads each) of one net's transposes.  Every
+// destination is written in index order (coalesced); the scattered reads come
+// from the 128 KB of W2 and W3, which stay in L2.
+constexpr int PREP_BLOCKS = 64;  // blocks per net
+__device__ inline void prep_weights_part(const WeightViews& v, int blk, int nblk) {
+    const float* W2 = v.theta + OFF_W2;  // [o][c][u][v], 64 x 32 x 4 x 4
+    const float* W3 = v.theta + OFF_W3;  // [o][c][u][v], 64 x 64 x 3 x 3
+    const int stride = nblk * 256;
+    for (int d = blk * 256 + (int)threadIdx.x; d < 16 * 64 * 32; d += stride) {
+        {  // w2t[t][o][c], t = u*4 + v
+            const int c = d & 31, o = (d >> 5) & 63, t = d >> 11;
+            v.w2t[d] = W2[((o * 32 + c) * 4 + (t >> 2)) * 4 + (t & 3)];
+        }
+        if (v.w2p) {  // w2p[tp][phase][c][o]: tap pair (u/2, v/2), stride phase (u%2, v%2)
+            const int o = d & 63, c = (d >> 6) & 31, phase = (d >> 11) & 3, tp = d >> 13;
+            const int u = (tp >> 1) * 2 + (phase >> 1), vv = (tp & 1) * 2 + (phase & 1);
+            v.w2p[d] = W2[((o * 32 + c) * 4 + u) * 4 + vv];
+        }
+    }
+    for (int d = blk * 256 + (int)threadIdx.x; d < 9 * 64 * 64; d += stride) {
+        {  // w3t[t][o][c], t = u*3 + v
+            const int c = d & 63, o = (d >> 6) & 63, t = d >> 12;
+            v.w3t[d] = W3[(o * 64 + c) * 9 + t];
+        }
+        if (v.w3d) {  // w3d[t][c][o]
+            const int o = d & 63, c = (d >> 6) & 63, t = d >> 12;
+            v.w3d[d] = W3[(o * 64 + c) * 9 + t];
+        }
+    }
+}
+
+// launch_resolve and launch_prep_weights in one launch (they are independent):
+// the first blocks resolve the minibatch, the rest transpose the weights.
+void launch_resolve_prep(const ReplayView& rv, const int64_t* idx, int n, int n_actions,
+                         const uint8_t** ftab, int32_t* a, float* r, uint8_t* term,
+                         unsigned* err, const WeightViews* nets, int n_nets, hipStream_t st);
+
 // Widen bf16 parameter vectors (bit patterns) to fp32 exactly: dst[i][k] = src[i][k].
 struct WidenSet {
     const uint16_t* src[MAX_NETS];

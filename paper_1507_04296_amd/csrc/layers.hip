@@ -15,41 +15,15 @@ namespace gorila {
 // ---------------------------------------------------------------------------
 // Weight transposes (run once per call, small: < 0.3 MB)
 // ---------------------------------------------------------------------------
-// Every destination is written in index order (coalesced); the scattered
-// reads come from the 128 KB of W2 and W3, which stay in L2.
 __global__ __launch_bounds__(256) void prep_weights_kernel(WeightViewSet set, int n_nets) {
     if ((int)blockIdx.y >= n_nets) return;
-    const WeightViews v = set.v[blockIdx.y];
-    const float* W2 = v.theta + OFF_W2;  // [o][c][u][v], 64 x 32 x 4 x 4
-    const float* W3 = v.theta + OFF_W3;  // [o][c][u][v], 64 x 64 x 3 x 3
-    const int stride = gridDim.x * 256;
-    for (int d = blockIdx.x * 256 + threadIdx.x; d < 16 * 64 * 32; d += stride) {
-        {  // w2t[t][o][c], t = u*4 + v
-            const int c = d & 31, o = (d >> 5) & 63, t = d >> 11;
-            v.w2t[d] = W2[((o * 32 + c) * 4 + (t >> 2)) * 4 + (t & 3)];
-        }
-        if (v.w2p) {  // w2p[tp][phase][c][o]: tap pair (u/2, v/2), stride phase (u%2, v%2)
-            const int o = d & 63, c = (d >> 6) & 31, phase = (d >> 11) & 3, tp = d >> 13;
-            const int u = (tp >> 1) * 2 + (phase >> 1), vv = (tp & 1) * 2 + (phase & 1);
-            v.w2p[d] = W2[((o * 32 + c) * 4 + u) * 4 + vv];
-        }
-    }
-    for (int d = blockIdx.x * 256 + threadIdx.x; d < 9 * 64 * 64; d += stride) {
-        {  // w3t[t][o][c], t = u*3 + v
-            const int c = d & 63, o = (d >> 6) & 63, t = d >> 12;
-            v.w3t[d] = W3[(o * 64 + c) * 9 + t];
-        }
-        if (v.w3d) {  // w3d[t][c][o]
-            const int o = d & 63, c = (d >> 6) & 63, t = d >> 12;
-            v.w3d[d] = W3[(o * 64 + c) * 9 + t];
-        }
-    }
+    prep_weights_part(set.v[blockIdx.y], blockIdx.x, gridDim.x);
 }
 
 void launch_prep_weights(const WeightViews* nets, int n_nets, hipStream_t st) {
     WeightViewSet set{};
     for (int i = 0; i < n_nets && i < MAX_NETS; ++i) set.v[i] = nets[i];
-    prep_weights_kernel<<<dim3(64, n_nets), 256, 0, st>>>(set, n_nets);
+    prep_weights_kernel<<<dim3(PREP_BLOCKS, n_nets), 256, 0, st>>>(set, n_nets);
 }
 
 // bf16 -> fp32 is exact: the 16 bits become the high half of the float.

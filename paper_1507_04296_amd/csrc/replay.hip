@@ -125,6 +125,37 @@ void launch_resolve(const ReplayView& rv, const int64_t* idx, int n, int n_actio
     resolve_kernel<<<(n + 255) / 256, 256, 0, st>>>(rv, idx, n, n_actions, ftab, a, r, term, err);
 }
 
+__global__ __launch_bounds__(256) void resolve_prep_kernel(
+    ReplayView rv, const int64_t* __restrict__ idx, int n, int n_actions,
+    const uint8_t** __restrict__ ftab, int32_t* __restrict__ a_out, float* __restrict__ r_out,
+    uint8_t* __restrict__ term_out, unsigned* __restrict__ err, WeightViewSet set, int rblocks) {
+    if ((int)blockIdx.x >= rblocks) {
+        const int q = blockIdx.x - rblocks;
+        prep_weights_part(set.v[q / PREP_BLOCKS], q % PREP_BLOCKS, PREP_BLOCKS);
+        return;
+    }
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= n) return;
+    const Resolved o = resolve_one(rv, idx[b], n_actions, err);
+    for (int w = 0; w < 2; ++w)
+        for (int c = 0; c < 4; ++c) ftab[((int64_t)w * n + b) * 4 + c] = o.ptr[w][c];
+    a_out[b] = o.act;
+    r_out[b] = o.rew;
+    term_out[b] = o.term;
+}
+
+void launch_resolve_prep(const ReplayView& rv, const int64_t* idx, int n, int n_actions,
+                         const uint8_t** ftab, int32_t* a, float* r, uint8_t* term,
+                         unsigned* err, const WeightViews* nets, int n_nets, hipStream_t st) {
+    WeightViewSet set{};
+    for (int i = 0; i < n_nets && i < MAX_NETS; ++i) set.v[i] = nets[i];
+    const int rblocks = n > 0 ? (n + 255) / 256 : 0;
+    const int blocks = rblocks + PREP_BLOCKS * min(n_nets, MAX_NETS);
+    if (blocks > 0)
+        resolve_prep_kernel<<<blocks, 256, 0, st>>>(rv, idx, n, n_actions, ftab, a, r, term, err,
+                                                    set, rblocks);
+}
+
 // The materialising gather: workgroup (b, f) resolves transition b (every
 // thread reads the same few flags) and copies one frame of its stacks, so a
 // launch has 5n (ring) or 8n (stacked) workgroups in flight.  From a ring,
