@@ -189,7 +189,7 @@ int gorila_learner_step(const gorila_params* params, const gorila_params* target
  * loss_out[g] (fp32).  When every set (the target's included) is bf16, the
  * products run on bf16 MFMA operands with fp32 accumulation: forward
  * activations as two bf16 terms (value rounded to bf16, plus the rounded
- * residual), backward gradients rounded to bf16, weights exact; gradients
+ * residual), backward operands rounded to bf16, weights exact; gradients
  * then agree with the exact step to a few 1e-3 relative L2 (fp32: ~1e-6).
  * Otherwise bf16 sets are widened exactly to fp32 and the step runs in fp32.  The forward passes of all groups share launches.
  * Needs gorila_workspace_bytes(batch, A, GORILA_BF16 if any set is bf16 else

@@ -5,7 +5,7 @@ parameter sets, against the fp64 oracle run once per group.
 bf16 parameters are bit patterns; the oracle takes their exact fp64 values.
 When every parameter set of a step is bf16 the HIP path multiplies bf16 MFMA
 operands with fp32 accumulation (forward activations as two bf16 terms,
-backward gradients rounded to bf16): every gradient tensor within 2e-2
+backward operands rounded to bf16): every gradient tensor within 2e-2
 relative L2 and the loss within 1e-4 relative.  Mixed fp32 / bf16 steps and
 the forward-only calls compute in fp32 from the exactly widened values and
 meet the fp32 bars (Q and loss 1e-4 relative, gradients 1e-3 relative L2).
