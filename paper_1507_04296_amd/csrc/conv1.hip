@@ -147,100 +147,173 @@ void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int gr
     }
 }
 
-// Weight gradient: dW1[o][(c,u,v)] = (1/255) sum_pixels dz1[pixel][o] * x[c][4i+u][4j+v]
-// over every pixel of the n online samples.  Rows o (32), columns (c,u,v)
-// (256, two tiles of 128), reduction over pixels split across workgroups;
-// partial[split][o][k] is summed in a fixed order afterwards.
-struct Conv1WgradA {  // dz1 rows o, RMAJ quads along o at one pixel
-    const float* dz1;
-    int npix;
-    int o0[MAXQ];
-    int kk[MAXQ];
-    __device__ void init(int j, int row, int k) { o0[j] = row; kk[j] = k; }
-    __device__ f32x4 load(int kc, int j) const {
-        const int m = kc * BK + kk[j];
-        return sel4(m < npix, ld4(dz1 + (int64_t)(m < npix ? m : 0) * C1 + o0[j]));
-    }
+// The weight gradient on v_mfma_f32_32x32x16_bf16 with exact products:
+// dW1[o][n] for the 256 columns n = (c, u, v) is a sum over pixels of
+// dz1[pixel][o] * byte.  The bytes are exact bf16 values; dz1 enters as WP
+// bf16 planes whose sum is dz1 exactly (three for fp32 steps, as in the
+// forward kernel; one, rounded, for bf16 steps), so only the fp32
+// accumulation rounds.  The stride-4 columns are made contiguous by staging
+// each input row in LDS by phase: xs[c][r][m][s][q] = row r byte 4 (q + s) + m,
+// so the bytes of columns v = 4s + m at pixels j .. j+7 are eight consecutive
+// entries.  A unit is two output rows of one sample (40 pixels, padded to 2 x
+// 24 = 6 groups of 8, with zeros past j = 19); an MFMA step takes two groups
+// (lane half h: group 2 step + h), so a unit is three steps.  Each workgroup
+// (4 waves; wave w owns columns 64 w .. 64 w + 63) sums a contiguous range of
+// units of one parameter set into its partial [32][256]; db1 is summed from
+// the fp32 dz1 values as they are staged.  The LDS stage is double buffered
+// and the next unit's data is fetched into registers during the products.
+constexpr int C1W_UR = 2;                       // output rows per unit
+constexpr int C1W_UNITS = H1 / C1W_UR;          // 10 units per sample
+constexpr int C1W_JP = 24;                      // padded pixel columns per output row
+constexpr int C1W_XR = S1 * (C1W_UR - 1) + K1;  // 12 input rows per unit
+constexpr int C1W_DQ = C1W_UR * H1 * C1 / 4;    // 320 dz1 quads per unit
+constexpr int C1W_XW = IN_C * C1W_XR * IN_W / 4;  // 1008 input words per unit
+constexpr int C1W_TARGET = 512;                 // workgroups: two per CU
+
+template <int WP>
+struct C1wStage {
+    __bf16 d[WP][C1][C1W_UR * C1W_JP];          // dz1 planes [o][(row, j)]
+    __bf16 x[IN_C][C1W_XR][4][2][C1W_JP];      // [c][r][m][s][q]
 };
 
-struct Conv1WgradB {  // input bytes rows (c,u,v), RMAJ quads along v at one pixel
-    const uint8_t* const* ftab;
-    const uint8_t* safe;  // any readable 7056 bytes, read in place of a zero-filled frame
-    int npix, col0;
-    int chan[MAXQ], off[MAXQ], kk[MAXQ];
-    __device__ void init(int j, int row, int k) {
-        const int kr = col0 + row;  // (c, u, v0) with v0 in {0, 4}
-        chan[j] = kr >> 6;
-        off[j] = ((kr >> 3) & 7) * IN_W + (kr & 7);
-        kk[j] = k;
-    }
-    const uint8_t* const* fsample = nullptr;  // this chunk's sample's frame pointers
-    int poff = 0;                              // this chunk's pixel within a frame
-    __device__ void prep(int kc) {  // the thread's quads share one pixel
-        const int m = kc * BK + kk[0];
-        const int mm = m < npix ? m : 0;  // past the end: pixel 0 (A is zero there)
-        const int b = mm / P1, p = mm - b * P1, i = p / H1, jj = p - i * H1;
-        fsample = ftab + (int64_t)b * 4;
-        poff = (S1 * i) * IN_W + S1 * jj;
-    }
-    __device__ f32x4 load(int, int j) const {
-        // a zero-filled frame (null pointer) is zeros
-        const uint8_t* f = fsample[chan[j]];
-        const bool ok = f != nullptr;
-        const uint32_t d = ldg_u32((ok ? f : safe) + poff + off[j]);
-        return sel4(ok, f32x4{(float)(d & 255u), (float)((d >> 8) & 255u),
-                              (float)((d >> 16) & 255u), (float)(d >> 24)});
-    }
-};
+template <int WP>
+__global__ __launch_bounds__(256) void conv1_wgrad_mfma16_kernel(
+    const float* __restrict__ dz1, const uint8_t* const* __restrict__ ftab, int n,
+    float* __restrict__ partial, float* __restrict__ bias_part) {
+    __shared__ __attribute__((aligned(16))) C1wStage<WP> stg[2];
+    __shared__ float bred[256 / 8][C1];
+    const int g = blockIdx.y, S = gridDim.x, x = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int U = n * C1W_UNITS;
+    const int u0 = (int)((int64_t)x * U / S), u1 = (int)((int64_t)(x + 1) * U / S);
 
-constexpr int C1W_BN = 128;
-// The launch aims at one round of three workgroups per CU (the job's register
-// budget allows three): 754 workgroups of 17 chunks measured 58 us against
-// 65 us for 986 of 13 chunks (1.3 rounds) at batch 512.
-constexpr int C1W_TARGET_WGS = 768;
+    for (int e = tid; e < (int)(sizeof(stg) / 16); e += 256) ((uint4*)stg)[e] = make_uint4(0, 0, 0, 0);
 
-template <int BF>
-struct Conv1WgradJob {
-    const float* dz1;
-    const uint8_t* const* ftab;
-    float* partial;
-    float* bias_part;
-    int n, splits, cps, groups;
-    // in bf16 the bytes are exact operands (one plane)
-    static constexpr int PA = BF ? BF_GRAD : 0, PB = BF ? 1 : 0;
-    using SH = GemmShape<32, C1W_BN, RMAJ, RMAJ, PA, PB>;
-    static constexpr int SMEM = SH::SMEM_FLOATS;
-    static constexpr int NCT = 256 / C1W_BN;
-    __host__ __device__ int blocks() const { return pad_xcd(NCT * splits * groups); }
-    __device__ void run(int bid, float* smem) const {
-        const int t = xcd_tile(bid, blocks());
-        if (t >= NCT * splits * groups) return;
-        // column tiles of a split adjacent; split runs over (group, split)
-        const int col0 = (t % NCT) * C1W_BN, split = t / NCT, g = split / splits;
-        const int npix = n * P1;
-        const int nchunks = (npix + BK - 1) / BK;
-        const int ks = split - g * splits;
-        const int kc0 = ks * cps, kc1 = min(nchunks, kc0 + cps);
-        const int64_t rows = (int64_t)g * n;
-        Conv1WgradA la{dz1 + rows * P1 * C1, npix};
-        Conv1WgradB lb{ftab + rows * 4, (const uint8_t*)dz1, npix, col0};
-        PartialEpi epi{partial + (int64_t)split * C1 * 256, 256, col0, 1.0f / 255.0f};
-        float* rs = col0 == 0 ? bias_part + (int64_t)split * 64 : nullptr;
-        mfma_gemm<32, C1W_BN, 1, RMAJ, RMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi, rs);
+    // prefetch registers: two dz1 quads (pixels 2p and 2p + 1 of the unit,
+    // channels 4 (t % 8) .. +3; threads t < 160) and four input words
+    const bool dz_lane = tid < C1W_DQ / 2;
+    const int dq0 = (tid >> 3) * 16 + (tid & 7);  // quad of pixel 2p (8 quads a pixel)
+    f32x4 dq[2];
+    uint32_t xw[4];
+    auto fetch = [&](int u) {
+        const int b = u / C1W_UNITS, i0 = (u - b * C1W_UNITS) * C1W_UR;
+        const float* dsrc = dz1 + (((int64_t)g * n + b) * P1 + i0 * H1) * C1;
+#pragma unroll
+        for (int k = 0; k < 2; ++k) dq[k] = ld4(dsrc + 4 * (dz_lane ? dq0 + 8 * k : 0));
+        const uint8_t* const* fr = ftab + ((int64_t)g * n + b) * 4;
+        const uint8_t* f0 = fr[0];
+        const uint8_t* f1 = fr[1];
+        const uint8_t* f2 = fr[2];
+        const uint8_t* f3 = fr[3];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int w = tid + 256 * k;  // word w: channel w / 252
+            const int c = w / (C1W_XW / IN_C);
+            const uint8_t* f = c == 0 ? f0 : c == 1 ? f1 : c == 2 ? f2 : f3;
+            const bool ok = w < C1W_XW && f != nullptr;
+            const int wi = w - c * (C1W_XW / IN_C);
+            // branch-free: a null frame or a spare lane reads dz1 instead
+            const uint32_t v = ldg_u32(ok ? f + S1 * i0 * IN_W + 4 * wi : (const uint8_t*)dsrc);
+            xw[k] = ok ? v : 0u;
+        }
+    };
+    float bsum[4] = {0.f, 0.f, 0.f, 0.f};  // db1 of o = 4 (tid % 8) + e
+    auto stage = [&](C1wStage<WP>& sg) {
+        if (dz_lane) {  // two pixels, one packed pair of columns per channel and plane
+            const int pu = 2 * (tid >> 3), o0 = 4 * (tid & 7);
+            const int col = (pu / H1) * C1W_JP + pu % H1;  // even
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                float v0 = dq[0][e], v1 = dq[1][e];
+                bsum[e] += v0;
+                bsum[e] += v1;
+#pragma unroll
+                for (int pl = 0; pl < WP; ++pl) {
+                    const __bf16 h0 = (__bf16)v0, h1 = (__bf16)v1;
+                    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+                    *(bf16x2*)&sg.d[pl][o0 + e][col] = bf16x2{h0, h1};
+                    v0 -= (float)h0;  // exact remainders
+                    v1 -= (float)h1;
+                }
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int w = tid + 256 * k;
+            if (w < C1W_XW) {
+                const int c = w / (C1W_XW / IN_C), wi = w - c * (C1W_XW / IN_C);
+                const int r = (4 * wi) / IN_W, q0 = ((4 * wi) % IN_W) / 4;
+#pragma unroll
+                for (int m = 0; m < 4; ++m) {
+                    const __bf16 h = (__bf16)(float)((xw[k] >> (8 * m)) & 255u);
+                    sg.x[c][r][m][0][q0] = h;
+                    if (q0 > 0) sg.x[c][r][m][1][q0 - 1] = h;
+                }
+            }
+        }
+    };
+
+    f32x16 acc[2] = {f32x16{}, f32x16{}};
+    const int h = lane >> 5;
+    if (u0 < u1) fetch(u0);
+    __syncthreads();  // the zero fill is complete
+    for (int u = u0; u < u1; ++u) {
+        C1wStage<WP>& sg = stg[u & 1];
+        stage(sg);
+        __syncthreads();
+        if (u + 1 < u1) fetch(u + 1);
+#pragma unroll
+        for (int st = 0; st < 3; ++st) {
+            const int grp = 2 * st + h, ir = grp / 3, j0 = 8 * (grp % 3);
+            bf16x8 a[WP];
+#pragma unroll
+            for (int pl = 0; pl < WP; ++pl)
+                a[pl] = *(const bf16x8*)&sg.d[pl][lane & 31][ir * C1W_JP + j0];
+#pragma unroll
+            for (int tt = 0; tt < 2; ++tt) {
+                const int nc = 64 * wave + 32 * tt + (lane & 31);
+                const int c = nc >> 6, uu = (nc >> 3) & 7, v = nc & 7;
+                const bf16x8 bx = *(const bf16x8*)&sg.x[c][S1 * ir + uu][v & 3][v >> 2][j0];
+#pragma unroll
+                for (int pl = 0; pl < WP; ++pl)
+                    acc[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[pl], bx, acc[tt], 0, 0, 0);
+            }
+        }
     }
-};
+
+    const int split = g * S + x;
+    float* out = partial + (int64_t)split * C1 * 256;
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            out[(8 * (r >> 2) + 4 * h + (r & 3)) * 256 + 64 * wave + 32 * tt + (lane & 31)] =
+                acc[tt][r] * (1.0f / 255.0f);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) bred[tid >> 3][4 * (tid & 7) + e] = bsum[e];
+    __syncthreads();
+    if (tid < C1) {
+        float t = 0.0f;
+        for (int k = 0; k < 256 / 8; ++k) t += bred[k][tid];
+        bias_part[(int64_t)split * 64 + tid] = t;
+    }
+}
 
 void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int groups, int n,
                         float* partial, float* bias_part, int max_splits, int* splits_out,
                         bool bf16, hipStream_t st) {
-    const int nchunks = (n * P1 + BK - 1) / BK;
-    int splits = max(1, min(max_splits, C1W_TARGET_WGS / (256 / C1W_BN)) / groups);
-    splits = min(splits, nchunks);
-    const int cps = (nchunks + splits - 1) / splits;
-    splits = (nchunks + cps - 1) / cps;
+    if (n <= 0) {
+        *splits_out = 0;
+        return;
+    }
+    // splits per group: one round of two workgroups per CU, each over a
+    // contiguous range of units; groups * splits stays within max_splits
+    const int splits = max(1, min(n * C1W_UNITS, min(C1W_TARGET, max_splits) / groups));
     *splits_out = splits;
-    if (bf16) launch_jobs(st, Conv1WgradJob<1>{dz1, ftab, partial, bias_part, n, splits, cps, groups});
-    else      launch_jobs(st, Conv1WgradJob<0>{dz1, ftab, partial, bias_part, n, splits, cps, groups});
+    if (bf16)
+        conv1_wgrad_mfma16_kernel<1><<<dim3(splits, groups), 256, 0, st>>>(dz1, ftab, n, partial, bias_part);
+    else
+        conv1_wgrad_mfma16_kernel<3><<<dim3(splits, groups), 256, 0, st>>>(dz1, ftab, n, partial, bias_part);
 }
 
 }  // namespace gorila
