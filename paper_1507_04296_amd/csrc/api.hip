@@ -98,8 +98,8 @@ Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online = 1, int wi
     p.ell = take(4 * (size_t)B);
     p.coef = take(4 * (size_t)B);
     p.dz4 = take(4 * (size_t)B * HID);
-    p.dz3 = take(4 * (size_t)B * FLAT);
-    p.dz2 = take(4 * (size_t)B * P2 * C2);
+    p.dz3 = take(4 * (size_t)bwd_split_rows(B) * FLAT);  // dz3_parts(B) partial planes
+    p.dz2 = take(4 * (size_t)bwd_split_rows(B) * P2 * C2);
     p.dz1 = take(4 * (size_t)B * P1 * C1);
     p.part1 = B ? take(4 * (size_t)CONV1_WG_MAX_SPLITS * C1 * 256) : o;
     p.part2 = B ? take(4 * (size_t)WG_MAX_SPLITS * C2 * 16 * C1) : o;
@@ -524,20 +524,21 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
                        r, term, gamma, clip_delta, h4, q, ell, coef, dz4, st);
     }
     int head_blocks = 0, s1 = 0, s2 = 0, s3 = 0;
+    const int kp3 = dz3_parts(B), kp2 = dz2_parts(B);
     {
         StageTimer t(ctx, ST_FC1_BWD);
         head_blocks = launch_fc1_backward(dz4, on, w4b, G, h3, h4, a, coef, ell, b, A, dz3, grads_out, P,
-                                          at<float>(ctx, p.hpart), bf16, st);
+                                          at<float>(ctx, p.hpart), kp3, bf16, st);
     }
     {
         StageTimer t(ctx, ST_CONV3_BWD);
         s3 = launch_conv3_backward(dz3, w3d, G, h2, b, dz2, at<float>(ctx, p.part3),
-                                   bpart + 2 * BIAS_PART_STRIDE, bf16, st);
+                                   bpart + 2 * BIAS_PART_STRIDE, kp3, kp2, bf16, st);
     }
     {
         StageTimer t(ctx, ST_CONV2_BWD);
         s2 = launch_conv2_backward(dz2, w2p, G, h1, b, dz1, at<float>(ctx, p.part2),
-                                   bpart + BIAS_PART_STRIDE, bf16, st);
+                                   bpart + BIAS_PART_STRIDE, kp2, bf16, st);
     }
     {
         StageTimer t(ctx, ST_CONV1_WGRAD);

@@ -144,16 +144,19 @@ void launch_td_head(const float* fc1part_online, const float* fc1part_target, in
 //       loss (returns row blocks per group);
 //  conv3: dz2 and split partials of dW3 / db3 (returns splits per group);
 //  conv2: dz1 and split partials of dW2 / db2 (returns splits per group).
+// kp: dz3 / dz2 partial planes, each groups * n rows long; fc1 writes kp
+// planes of dz3, conv3 reads them and writes kp_out planes of dz2, conv2
+// reads those.
 int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, const GroupPtrs16& w4b,
                         int groups, const float* h3,
                         const float* h4, const int32_t* a, const float* coef, const float* ell,
                         int n, int A, float* dz3, float* grads, int64_t grads_stride,
-                        float* hpart, bool bf16, hipStream_t st);
+                        float* hpart, int kp, bool bf16, hipStream_t st);
 int launch_conv3_backward(const float* dz3, const GroupPtrs& w3d, int groups, const float* h2,
-                          int n, float* dz2, float* partial, float* bias_part, bool bf16,
-                          hipStream_t st);
+                          int n, float* dz2, float* partial, float* bias_part, int kp, int kp_out,
+                          bool bf16, hipStream_t st);
 int launch_conv2_backward(const float* dz2, const GroupPtrs& w2p, int groups, const float* h1,
-                          int n, float* dz1, float* partial, float* bias_part, bool bf16,
+                          int n, float* dz1, float* partial, float* bias_part, int kp, bool bf16,
                           hipStream_t st);
 // ftab: [groups * n][4] frame pointers of the online states.
 void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int groups, int n,
@@ -202,6 +205,17 @@ constexpr int WG_MAX_SPLITS = 256;
 constexpr int CONV3_WG_SPLITS = 114;         // 9 column tiles x 114 splits ~ 1024 workgroups
 constexpr int CONV2_WG_SPLITS = 64;          // 8 column tiles x 64 splits
 constexpr int CONV1_WG_MAX_SPLITS = 512;
+// Small batches split the fc1 and conv3 data gradients over the reduction:
+// with B learner rows, dz3 arrives as dz3_parts(B) and dz2 as dz2_parts(B)
+// partial planes (each already masked by the ReLU, which is linear in them)
+// that the conv3 and conv2 backward loaders add in plane order.
+// bwd_split_rows(B) >= parts * B rows are reserved per tensor; it never
+// decreases with B, so a workspace sized for a batch serves every smaller one.
+__host__ __device__ constexpr int dz3_parts(int64_t rows) { return rows <= 64 ? 4 : rows <= 128 ? 2 : 1; }
+__host__ __device__ constexpr int dz2_parts(int64_t rows) { return dz3_parts(rows); }
+__host__ __device__ constexpr int64_t bwd_split_rows(int64_t rows) {
+    return rows <= 64 ? 4 * rows : rows <= 256 ? 256 : rows;
+}
 constexpr int BIAS_PART_STRIDE = 512 * 64;  // floats per layer in bias_part
 constexpr int HEAD_MAX_BLOCKS = 16;          // row blocks of the head partials, per group
 constexpr int HP_DB5 = MAX_ACTIONS * HID;    // offsets inside one head partial

@@ -12,6 +12,15 @@
 
 namespace gorila {
 
+// Quad at p summed over the KP partial planes p, p + ps, ... in plane order.
+template <int KP>
+__device__ __forceinline__ f32x4 ld4_parts(const float* p, int64_t ps) {
+    f32x4 v = ld4(p);
+#pragma unroll
+    for (int s = 1; s < KP; ++s) v += ld4(p + s * ps);
+    return v;
+}
+
 // ---------------------------------------------------------------------------
 // Weight transposes (run once per call, small: < 0.3 MB)
 // ---------------------------------------------------------------------------
@@ -360,6 +369,8 @@ struct Dz3NhwcStore {
     }
 };
 
+// kp > 1 cuts the reduction over the 512 hidden units into kp parts, each
+// writing its masked dz3 plane (the ReLU mask is linear in the parts).
 template <int BF>
 struct Fc1DgradJob {
     const float* dz4;
@@ -367,29 +378,33 @@ struct Fc1DgradJob {
     GroupPtrs16 w4b;  // bf16 steps: W4 of each set, read in place
     const float* h3;
     float* dz3;
-    int n, groups;
+    int n, groups, kp;  // kp reduction parts, each writing its own dz3 plane
     static constexpr int PA = BF ? BF_GRAD : 0, PB = BF ? BF_WEIGHT : 0;
     using SH = GemmShape<64, 64, KMAJ, RMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return ((n + 63) / 64) * (FLAT / 64); }
-    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups * kp); }
     __device__ void run(int bid, float* smem) const {
         int t = xcd_tile(bid, blocks());
-        if (t >= tiles() * groups) return;
+        if (t >= tiles() * groups * kp) return;
+        const int part = t / (tiles() * groups);
+        t -= part * tiles() * groups;
         const int g = t / tiles();
         t -= g * tiles();
         const int mt = (n + 63) / 64;
         const int r0 = (t % mt) * 64, c0 = (t / mt) * 64;  // row tiles of one W4 column block adjacent
         const int64_t rows = (int64_t)g * n;
         RowMajorK la{dz4 + rows * HID, n, r0, HID};
-        Dz3NhwcStore epi{dz3 + rows * FLAT, h3 + rows * FLAT, n, r0, c0};
+        Dz3NhwcStore epi{dz3 + part * (int64_t)groups * n * FLAT + rows * FLAT, h3 + rows * FLAT, n,
+                         r0, c0};
+        const int kc0 = part * (HID / BK) / kp, kc1 = (part + 1) * (HID / BK) / kp;
         // HID is a whole number of chunks
         if constexpr (BF > 0) {
             RowMajorR16 lb{w4b.p[g], c0, FLAT, HID};
-            mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, 0, HID / BK, la, lb, epi);
+            mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi);
         } else {
             RowMajorR<false> lb{theta.p[g] + OFF_W4, c0, FLAT, HID};
-            mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, 0, HID / BK, la, lb, epi);
+            mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi);
         }
     }
 };
@@ -503,16 +518,16 @@ int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, const GroupPtr
                         int groups, const float* h3,
                         const float* h4, const int32_t* a, const float* coef, const float* ell,
                         int n, int A, float* dz3, float* grads, int64_t grads_stride,
-                        float* hpart, bool bf16, hipStream_t st) {
+                        float* hpart, int kp, bool bf16, hipStream_t st) {
     if (n <= 0) return 0;
     const int rows = max(32, (n + HEAD_MAX_BLOCKS - 1) / HEAD_MAX_BLOCKS);
     const int row_blocks = (n + rows - 1) / rows;
     const HeadPartialJob hp{h4, a, coef, ell, hpart, n, A, rows, row_blocks, groups};
     if (bf16)
-        launch_jobs(st, Fc1DgradJob<1>{dz4, theta, w4b, h3, dz3, n, groups},
+        launch_jobs(st, Fc1DgradJob<1>{dz4, theta, w4b, h3, dz3, n, groups, kp},
                     Fc1WgradJob<1>{dz4, h3, grads, grads_stride, n, groups}, hp);
     else
-        launch_jobs(st, Fc1DgradJob<0>{dz4, theta, w4b, h3, dz3, n, groups},
+        launch_jobs(st, Fc1DgradJob<0>{dz4, theta, w4b, h3, dz3, n, groups, kp},
                     Fc1WgradJob<0>{dz4, h3, grads, grads_stride, n, groups}, hp);
     return row_blocks;
 }
@@ -525,9 +540,11 @@ int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, const GroupPtr
 // the reduction: only the 1..9 valid taps x 64 channels are multiplied.
 // rows b, cols c (64), reduction (valid tap, o) in chunks of 32 o.
 // ---------------------------------------------------------------------------
+template <int KP>
 struct Conv3DgradA {  // KMAJ quads dz3[b][p][o..o+3] at p = (y-u)*7 + (x-v)
     const float* dz3;
     int n, b0, y, x, u0, v0, nv;
+    int64_t ps;  // KP planes of dz3, ps floats apart
     const float* base[MAXQ];
     __device__ void init(int j, int row, int k) {
         const int b = b0 + row;
@@ -535,7 +552,7 @@ struct Conv3DgradA {  // KMAJ quads dz3[b][p][o..o+3] at p = (y-u)*7 + (x-v)
     }
     __device__ f32x4 load(int kc, int j) const {
         const int t = kc >> 1, u = u0 + t / nv, v = v0 + t % nv;
-        return ld4(base[j] + ((y - u) * H3 + (x - v)) * C3 + (kc & 1) * BK);
+        return ld4_parts<KP>(base[j] + ((y - u) * H3 + (x - v)) * C3 + (kc & 1) * BK, ps);
     }
 };
 struct Conv3DgradB {  // w3d[(u,v)][c][o], rows c, quads along o
@@ -564,7 +581,9 @@ struct Conv3DgradStore {
     }
 };
 
-template <int BF>
+// dz3 arrives as KP partial planes; KPO > 1 cuts the reduction over (tap, o)
+// into KPO parts, each writing its own masked dz2 plane.
+template <int BF, int KP, int KPO>
 struct Conv3DgradJob {
     const float* dz3;
     GroupPtrs w3d;
@@ -575,21 +594,24 @@ struct Conv3DgradJob {
     using SH = GemmShape<64, 64, KMAJ, KMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return P2 * ((n + 63) / 64); }
-    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups * KPO); }
     __device__ void run(int bid, float* smem) const {
         int t = xcd_tile(bid, blocks());
-        if (t >= tiles() * groups) return;
+        if (t >= tiles() * groups * KPO) return;
+        const int part = t / (tiles() * groups);
+        t -= part * tiles() * groups;
         const int g = t / tiles();
         t -= g * tiles();
-        const int64_t rows = (int64_t)g * n;
+        const int64_t rows = (int64_t)g * n, plane = (int64_t)groups * n;
         const int pos = t % P2, y = pos / H2, x = pos - y * H2, b0 = (t / P2) * 64;
         const int u0 = max(0, y - (H3 - 1)), u1 = min(K3 - 1, y);
         const int v0 = max(0, x - (H3 - 1)), v1 = min(K3 - 1, x);
         const int nv = v1 - v0 + 1, taps = (u1 - u0 + 1) * nv;
-        Conv3DgradA la{dz3 + rows * FLAT, n, b0, y, x, u0, v0, nv};
+        Conv3DgradA<KP> la{dz3 + rows * FLAT, n, b0, y, x, u0, v0, nv, plane * FLAT};
         Conv3DgradB lb{w3d.p[g], u0, v0, nv};
-        Conv3DgradStore epi{dz2 + rows * P2 * C2, h2 + rows * P2 * C2, n, b0, pos};
-        mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, 0, 2 * taps, la, lb, epi);
+        Conv3DgradStore epi{dz2 + (part * plane + rows) * P2 * C2, h2 + rows * P2 * C2, n, b0, pos};
+        mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, part * 2 * taps / KPO,
+                                                 (part + 1) * 2 * taps / KPO, la, lb, epi);
     }
 };
 
@@ -599,14 +621,16 @@ struct Conv3DgradJob {
 // reduction over the n*49 output pixels, split across workgroups.
 // partial[s][o][tap*64 + c].
 // ---------------------------------------------------------------------------
+template <int KP>
 struct Conv3WgradA {  // RMAJ quads dz3[b][p][o0..o0+3] at one output pixel m = (b, p)
     const float* dz3;
     int npix;
+    int64_t ps;  // KP planes of dz3, ps floats apart
     int o0[MAXQ], kk[MAXQ];
     __device__ void init(int j, int row, int k) { o0[j] = row; kk[j] = k; }
     __device__ f32x4 load(int kc, int j) const {
         const int m = kc * BK + kk[j];
-        return sel4(m < npix, ld4(dz3 + (int64_t)(m < npix ? m : 0) * C3 + o0[j]));
+        return sel4(m < npix, ld4_parts<KP>(dz3 + (int64_t)(m < npix ? m : 0) * C3 + o0[j], ps));
     }
 };
 struct Conv3WgradB {  // RMAJ quads: 4 channels of h2 at one (pixel, tap)
@@ -625,7 +649,7 @@ struct Conv3WgradB {  // RMAJ quads: 4 channels of h2 at one (pixel, tap)
     __device__ f32x4 load(int, int j) const { return ld4(pix + c0[j]); }
 };
 
-template <int BF>
+template <int BF, int KP>
 struct Conv3WgradJob {
     const float* dz3;
     const float* h2;
@@ -644,7 +668,7 @@ struct Conv3WgradJob {
         const int npix = n * P3, nchunks = (npix + BK - 1) / BK;
         const int64_t rows = (int64_t)g * n;
         const int ks = s - g * splits;
-        Conv3WgradA la{dz3 + rows * FLAT, npix};
+        Conv3WgradA<KP> la{dz3 + rows * FLAT, npix, (int64_t)groups * n * FLAT};
         Conv3WgradB lb{h2 + rows * P2 * C2, npix, tap};
         PartialEpi epi{partial + (int64_t)s * C3 * 9 * C2, 9 * C2, tap * C2, 1.0f};
         float* rs = tap == 0 ? bias_part + (int64_t)s * 64 : nullptr;
@@ -654,20 +678,40 @@ struct Conv3WgradJob {
 
 // Splits per group shrink with the group count so one launch stays near the
 // same number of workgroups; groups * splits stays within WG_MAX_SPLITS.
+template <int BF, int KP, int KPO>
+static void conv3_backward_jobs(const float* dz3, const GroupPtrs& w3d, int groups, const float* h2,
+                                int n, float* dz2, float* partial, float* bias_part, int splits,
+                                int cps, hipStream_t st) {
+    launch_jobs(st, Conv3DgradJob<BF, KP, KPO>{dz3, w3d, h2, dz2, n, groups},
+                Conv3WgradJob<BF, KP>{dz3, h2, partial, bias_part, n, splits, cps, groups});
+}
+
+// f(integral_constant<int, k>) for the plane count k in {1, 2, 4}
+template <class F>
+static void with_parts(int k, F&& f) {
+    if (k == 4) f(std::integral_constant<int, 4>{});
+    else if (k == 2) f(std::integral_constant<int, 2>{});
+    else f(std::integral_constant<int, 1>{});
+}
+
 int launch_conv3_backward(const float* dz3, const GroupPtrs& w3d, int groups, const float* h2,
-                          int n, float* dz2, float* partial, float* bias_part, bool bf16,
-                          hipStream_t st) {
+                          int n, float* dz2, float* partial, float* bias_part, int kp, int kp_out,
+                          bool bf16, hipStream_t st) {
     if (n <= 0) return 0;
     const int nchunks = (n * P3 + BK - 1) / BK;
     int splits = min(min(WG_MAX_SPLITS / groups, nchunks), max(1, CONV3_WG_SPLITS / groups));
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
-    if (bf16)
-        launch_jobs(st, Conv3DgradJob<1>{dz3, w3d, h2, dz2, n, groups},
-                    Conv3WgradJob<1>{dz3, h2, partial, bias_part, n, splits, cps, groups});
-    else
-        launch_jobs(st, Conv3DgradJob<0>{dz3, w3d, h2, dz2, n, groups},
-                    Conv3WgradJob<0>{dz3, h2, partial, bias_part, n, splits, cps, groups});
+    with_parts(kp, [&](auto ki) {
+        with_parts(kp_out, [&](auto ko) {
+            if (bf16)
+                conv3_backward_jobs<1, ki.value, ko.value>(dz3, w3d, groups, h2, n, dz2, partial,
+                                                           bias_part, splits, cps, st);
+            else
+                conv3_backward_jobs<0, ki.value, ko.value>(dz3, w3d, groups, h2, n, dz2, partial,
+                                                           bias_part, splits, cps, st);
+        });
+    });
     return splits;
 }
 
@@ -681,9 +725,11 @@ int launch_conv3_backward(const float* dz3, const GroupPtrs& w3d, int groups, co
 // for every row and column and are skipped.  Reduction (valid tap, o) in
 // chunks of 32 o; dz1 = dh1 * [h1 > 0].
 // ---------------------------------------------------------------------------
+template <int KP>
 struct Conv2DgradA {  // KMAJ quads dz2[b][i][j][o..o+3]
     const float* dz2;
     int n, b0, yy, xx, du0, dv0, ndv;
+    int64_t ps;  // KP planes of dz2, ps floats apart
     const float* base[MAXQ];
     __device__ void init(int j, int row, int k) {
         const int b = b0 + row;
@@ -691,7 +737,7 @@ struct Conv2DgradA {  // KMAJ quads dz2[b][i][j][o..o+3]
     }
     __device__ f32x4 load(int kc, int j) const {
         const int t = kc >> 1, du = du0 + t / ndv, dv = dv0 + t % ndv;
-        return ld4(base[j] + ((yy - du) * H2 + (xx - dv)) * C2 + (kc & 1) * BK);
+        return ld4_parts<KP>(base[j] + ((yy - du) * H2 + (xx - dv)) * C2 + (kc & 1) * BK, ps);
     }
 };
 struct Conv2DgradB {  // w2p[(du,dv)][phase][c][o], rows (phase, c), quads along o
@@ -725,7 +771,7 @@ struct Conv2DgradStore {
     }
 };
 
-template <int BF>
+template <int BF, int KP>
 struct Conv2DgradJob {
     const float* dz2;
     GroupPtrs w2p;
@@ -752,7 +798,8 @@ struct Conv2DgradJob {
         const int du0 = max(0, yy - (H2 - 1)), du1 = min(1, yy);
         const int dv0 = max(0, xx - (H2 - 1)), dv1 = min(1, xx);
         const int ndv = dv1 - dv0 + 1, taps = (du1 - du0 + 1) * ndv;
-        Conv2DgradA la{dz2 + rows * P2 * C2, n, b0, yy, xx, du0, dv0, ndv};
+        Conv2DgradA<KP> la{dz2 + rows * P2 * C2, n, b0, yy, xx, du0, dv0, ndv,
+                           (int64_t)groups * n * P2 * C2};
         Conv2DgradB lb{w2p.p[g] + ct * BN * C2, du0, dv0, ndv};
         Conv2DgradStore epi{dz1 + rows * P1 * C1, h1 + rows * P1 * C1, n, b0, yy, xx, ct * BN};
         mfma_gemm<64, BN, 2, KMAJ, KMAJ, PA, PB>(smem, 0, 2 * taps, la, lb, epi);
@@ -764,14 +811,16 @@ struct Conv2DgradJob {
 // rows o (64), cols (tap, c) with two taps per 64-column tile, reduction over
 // the n*81 output pixels split across workgroups.  partial[s][o][tap*32 + c].
 // ---------------------------------------------------------------------------
+template <int KP>
 struct Conv2WgradA {  // dz2 quads along o at one pixel
     const float* dz2;
     int npix;
+    int64_t ps;  // KP planes of dz2, ps floats apart
     int o0[MAXQ], kk[MAXQ];
     __device__ void init(int j, int row, int k) { o0[j] = row; kk[j] = k; }
     __device__ f32x4 load(int kc, int j) const {
         const int m = kc * BK + kk[j];
-        return sel4(m < npix, ld4(dz2 + (int64_t)(m < npix ? m : 0) * C2 + o0[j]));
+        return sel4(m < npix, ld4_parts<KP>(dz2 + (int64_t)(m < npix ? m : 0) * C2 + o0[j], ps));
     }
 };
 struct Conv2WgradB {  // h1 quads along c at one (pixel, tap)
@@ -793,7 +842,7 @@ struct Conv2WgradB {  // h1 quads along c at one (pixel, tap)
     __device__ f32x4 load(int, int j) const { return ld4(pix + off[j]); }
 };
 
-template <int BF>
+template <int BF, int KP>
 struct Conv2WgradJob {
     const float* dz2;
     const float* h1;
@@ -812,7 +861,7 @@ struct Conv2WgradJob {
         const int npix = n * P2, nchunks = (npix + BK - 1) / BK;
         const int64_t rows = (int64_t)g * n;
         const int ks = s - g * splits;
-        Conv2WgradA la{dz2 + rows * P2 * C2, npix};
+        Conv2WgradA<KP> la{dz2 + rows * P2 * C2, npix, (int64_t)groups * n * P2 * C2};
         Conv2WgradB lb{h1 + rows * P1 * C1, npix, tap0};
         PartialEpi epi{partial + (int64_t)s * C2 * 16 * C1, 16 * C1, tap0 * C1, 1.0f};
         float* rs = tap0 == 0 ? bias_part + (int64_t)s * 64 : nullptr;
@@ -820,22 +869,32 @@ struct Conv2WgradJob {
     }
 };
 
+// the weight-gradient workgroups are the longer ones (21 chunks against at
+// most 8 at batch 512): dispatched first, they do not trail the launch
+template <int BF, int KP>
+static void conv2_backward_jobs(const float* dz2, const GroupPtrs& w2p, int groups, const float* h1,
+                                int n, float* dz1, float* partial, float* bias_part, int splits,
+                                int cps, hipStream_t st) {
+    launch_jobs(st, Conv2WgradJob<BF, KP>{dz2, h1, partial, bias_part, n, splits, cps, groups},
+                Conv2DgradJob<BF, KP>{dz2, w2p, h1, dz1, n, groups});
+}
+
 int launch_conv2_backward(const float* dz2, const GroupPtrs& w2p, int groups, const float* h1,
-                          int n, float* dz1, float* partial, float* bias_part, bool bf16,
+                          int n, float* dz1, float* partial, float* bias_part, int kp, bool bf16,
                           hipStream_t st) {
     if (n <= 0) return 0;
     const int nchunks = (n * P2 + BK - 1) / BK;
     int splits = min(min(WG_MAX_SPLITS / groups, nchunks), max(1, CONV2_WG_SPLITS / groups));
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
-    // the weight-gradient workgroups are the longer ones (21 chunks against at
-    // most 8 at batch 512): dispatched first, they do not trail the launch
-    if (bf16)
-        launch_jobs(st, Conv2WgradJob<1>{dz2, h1, partial, bias_part, n, splits, cps, groups},
-                    Conv2DgradJob<1>{dz2, w2p, h1, dz1, n, groups});
-    else
-        launch_jobs(st, Conv2WgradJob<0>{dz2, h1, partial, bias_part, n, splits, cps, groups},
-                    Conv2DgradJob<0>{dz2, w2p, h1, dz1, n, groups});
+    with_parts(kp, [&](auto k) {
+        if (bf16)
+            conv2_backward_jobs<1, k.value>(dz2, w2p, groups, h1, n, dz1, partial, bias_part, splits,
+                                            cps, st);
+        else
+            conv2_backward_jobs<0, k.value>(dz2, w2p, groups, h1, n, dz1, partial, bias_part, splits,
+                                            cps, st);
+    });
     return splits;
 }
 

@@ -55,6 +55,12 @@ def test_workspace_sizing_is_monotone():
     assert g.workspace_bytes(0, 18) == 0
     assert g.workspace_bytes(8, 40) == 0
     assert g.workspace_bytes(8, 18, groups=16) > g.workspace_bytes(8, 18)
+    # a context sized for a batch serves every smaller batch: small batches keep
+    # several partial planes of the data gradients, so check every size across
+    # the thresholds where the plane count changes
+    for A in (6, 18):
+        sizes = [g.workspace_bytes(b, A) for b in range(1, 300)]
+        assert all(x <= y for x, y in zip(sizes, sizes[1:])), A
 
 
 def test_strerror_names_every_code():
