@@ -31,6 +31,7 @@ struct gorila_ctx {
     char* ws;
     size_t ws_bytes;
     int device;
+    int cus = 0;  // compute units of the device
     uint32_t timing_mask = 0;
     std::vector<TimingRecord> records;  // events created by timing_begin
     size_t used = 0;
@@ -70,8 +71,14 @@ struct Plan {
     size_t h1, h2, h3, h4, q, ell, coef;
     size_t dz4, dz3, dz2, dz1;
     size_t fc1part, part1, part2, part3, bpart, hpart;
+    size_t split;  // TailSplit partial tiles, or SIZE_MAX when the batch is too small to use them
     size_t total;
 };
+
+// The zeroed head of the workspace: the sticky error word, then the TailSplit
+// counters at SPLIT_CNT_OFFSET (zero between launches).
+constexpr size_t SPLIT_CNT_OFFSET = 128;
+static_assert(SPLIT_CNT_OFFSET + 4 * SPLIT_MAX_TILES <= ALIGN, "counters fit the zeroed head");
 
 Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online = 1, int widened = 0) {
     Plan p{};
@@ -98,7 +105,7 @@ Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online = 1, int wi
     p.ell = take(4 * (size_t)B);
     p.coef = take(4 * (size_t)B);
     p.dz4 = take(4 * (size_t)B * HID);
-    p.dz3 = take(4 * (size_t)bwd_split_rows(B) * FLAT);  // dz3_parts(B) partial planes
+    p.dz3 = take(4 * (size_t)bwd_split_rows(B) * FLAT);  // bwd_parts(B) partial planes
     p.dz2 = take(4 * (size_t)bwd_split_rows(B) * P2 * C2);
     p.dz1 = take(4 * (size_t)B * P1 * C1);
     p.part1 = B ? take(4 * (size_t)CONV1_WG_MAX_SPLITS * C1 * 256) : o;
@@ -106,12 +113,26 @@ Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online = 1, int wi
     p.part3 = B ? take(4 * (size_t)WG_MAX_SPLITS * C3 * 9 * C2) : o;
     p.bpart = B ? take(4 * (size_t)3 * BIAS_PART_STRIDE) : o;
     p.hpart = B ? take(4 * (size_t)online * HEAD_MAX_BLOCKS * HP_STRIDE) : o;
+    // a launch needs at least one tile per compute unit before its tail is
+    // split; smaller batches never split, and leave the region out
+    p.split = F >= 128 ? take(4 * (size_t)SPLIT_MAX_TILES * SPLIT_MAX_PIECES * SPLIT_TILE_FLOATS)
+                       : SIZE_MAX;
     p.total = o;
     return p;
 }
 
 template <class T>
 T* at(gorila_ctx* c, size_t off) { return (T*)(c->ws + off); }
+
+SplitWs split_ws(gorila_ctx* c, const Plan& p) {
+    SplitWs sw;
+    sw.cus = c->cus;
+    if (p.split != SIZE_MAX) {
+        sw.ws = at<float>(c, p.split);
+        sw.cnt = at<int>(c, p.err + SPLIT_CNT_OFFSET);
+    }
+    return sw;
+}
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -200,8 +221,9 @@ int forward_one(gorila_ctx* c, const Plan& p, const gorila_params* prm, const ui
     w3t.p[0] = wv.w3t;
     // forward-only calls compute in fp32 (bf16 parameters are widened exactly)
     { StageTimer t(c, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 1, n, at<float>(c, p.h1), false, st); }
+    const SplitWs sw = split_ws(c, p);
     { StageTimer t(c, ST_CONV2_FWD); launch_conv2_fwd(at<float>(c, p.h1), w2t, th, 1, n, at<float>(c, p.h2), false, st); }
-    { StageTimer t(c, ST_CONV3_FWD); launch_conv3_fwd(at<float>(c, p.h2), w3t, th, 1, n, at<float>(c, p.h3), false, st); }
+    { StageTimer t(c, ST_CONV3_FWD); launch_conv3_fwd(at<float>(c, p.h2), w3t, th, 1, n, at<float>(c, p.h3), sw, false, st); }
     { StageTimer t(c, ST_FC1_FWD); *fc1_splits = launch_fc1_fwd(at<float>(c, p.h3), th, GroupPtrs16{}, 1, n, at<float>(c, p.fc1part), false, st); }
     return check_launch();
 }
@@ -227,14 +249,17 @@ size_t gorila_workspace_bytes(int32_t max_batch, int32_t n_actions, int32_t dtyp
 int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_t ws_bytes) {
     if (!out || !workspace || !aligned16(workspace)) return GORILA_EINVAL;
     if (ws_bytes < make_plan(1, 1, 1).err + ALIGN) return GORILA_EWORKSPACE;
-    int dev = -1;
+    int dev = -1, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) return GORILA_EHIP;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return GORILA_EHIP;
     gorila_ctx* c = new (std::nothrow) gorila_ctx;
     if (c) {
         c->stream = (hipStream_t)hip_stream;
         c->ws = (char*)workspace;
         c->ws_bytes = ws_bytes;
         c->device = dev;
+        c->cus = cus;
     }
     if (!c) return GORILA_EINVAL;
     if (hipMemsetAsync(c->ws, 0, ALIGN, c->stream) != hipSuccess) {
@@ -498,8 +523,9 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
     float* h4 = at<float>(ctx, p.h4);
     float* fc1part = at<float>(ctx, p.fc1part);
     { StageTimer t(ctx, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 2 * G, b, h1, bf16, st); }
+    const SplitWs sw = split_ws(ctx, p);
     { StageTimer t(ctx, ST_CONV2_FWD); launch_conv2_fwd(h1, w2t, th, 2 * G, b, h2, bf16, st); }
-    { StageTimer t(ctx, ST_CONV3_FWD); launch_conv3_fwd(h2, w3t, th, 2 * G, b, h3, bf16, st); }
+    { StageTimer t(ctx, ST_CONV3_FWD); launch_conv3_fwd(h2, w3t, th, 2 * G, b, h3, sw, bf16, st); }
     int S = 0;
     { StageTimer t(ctx, ST_FC1_FWD); S = launch_fc1_fwd(h3, th, w4f, 2 * G, b, fc1part, bf16, st); }
 
@@ -524,21 +550,21 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
                        r, term, gamma, clip_delta, h4, q, ell, coef, dz4, st);
     }
     int head_blocks = 0, s1 = 0, s2 = 0, s3 = 0;
-    const int kp3 = dz3_parts(B), kp2 = dz2_parts(B);
+    const int kp = bwd_parts(B);
     {
         StageTimer t(ctx, ST_FC1_BWD);
         head_blocks = launch_fc1_backward(dz4, on, w4b, G, h3, h4, a, coef, ell, b, A, dz3, grads_out, P,
-                                          at<float>(ctx, p.hpart), kp3, bf16, st);
+                                          at<float>(ctx, p.hpart), kp, sw, bf16, st);
     }
     {
         StageTimer t(ctx, ST_CONV3_BWD);
         s3 = launch_conv3_backward(dz3, w3d, G, h2, b, dz2, at<float>(ctx, p.part3),
-                                   bpart + 2 * BIAS_PART_STRIDE, kp3, kp2, bf16, st);
+                                   bpart + 2 * BIAS_PART_STRIDE, kp, bf16, st);
     }
     {
         StageTimer t(ctx, ST_CONV2_BWD);
         s2 = launch_conv2_backward(dz2, w2p, G, h1, b, dz1, at<float>(ctx, p.part2),
-                                   bpart + BIAS_PART_STRIDE, kp2, bf16, st);
+                                   bpart + BIAS_PART_STRIDE, kp, bf16, st);
     }
     {
         StageTimer t(ctx, ST_CONV1_WGRAD);

@@ -212,6 +212,28 @@ struct GemmShape {
     static constexpr int SMEM_FLOATS = 2 * STAGE_FLOATS;
 };
 
+// One piece of a tile whose reduction is cut into np pieces run by different
+// workgroups (np == 1: the whole tile, no hand-off).  Each piece stores its
+// accumulators to ws[piece] (tile-private, np * BM * BN floats) and counts
+// itself in *cnt; the piece that counts last adds the np partial tiles in
+// piece order, so the sum does not depend on which piece finishes last, runs
+// the epilogue and sets *cnt back to 0 for the next launch.  No piece waits
+// for another.
+//
+// All pieces of a tile run on one XCD (TailSplit places them so), whose L2 is
+// shared by its compute units and is where their vector stores land (the
+// per-unit L1 writes through).  A piece waits for its own stores to complete
+// before it counts, so the last piece finds every partial tile in that L2; it
+// has not read those addresses before in the launch, so its L1 holds no
+// stale copy.  This needs no device-wide cache write-back or invalidation,
+// which would evict every other workgroup's operands from the L2.
+constexpr int SPLIT_MAX_TILES = 32, SPLIT_MAX_PIECES = 16, SPLIT_TILE_FLOATS = 64 * 64;
+struct SplitPiece {
+    float* ws = nullptr;
+    int* cnt = nullptr;
+    int piece = 0, np = 1;
+};
+
 // Loaders: `la.init(j, row, k)` is called once per quad slot j of this thread
 // with the quad's tile coordinates; `la.load(kc, j)` returns the quad for
 // reduction chunk kc (zeros where the operand is zero-padded).
@@ -236,7 +258,8 @@ template <int BM, int BN, int WAVES_M, int AMODE, int BMODE, int PA = 0, int PB 
           class LoadB, class Epi>
 __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
                                           LoadA& la, LoadB& lb, Epi& epi,
-                                          float* rowsum_out = nullptr) {
+                                          float* rowsum_out = nullptr,
+                                          const SplitPiece& sp = SplitPiece{}) {
     using SH = GemmShape<BM, BN, AMODE, BMODE, PA, PB>;
     using LA = typename SH::LA;
     using LB = typename SH::LB;
@@ -424,6 +447,46 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
         __syncthreads();
         if (tid < BM) rowsum_out[tid] = ((smem[tid] + smem[64 + tid]) + smem[128 + tid]) + smem[192 + tid];
     }
+    // hand-off between the pieces of one tile (never with a row sum; tiles up
+    // to SPLIT_TILE_FLOATS elements)
+    constexpr int NV = TM * TN * 4;  // f32x4 per thread: 256 * NV * 4 == BM * BN
+    static_assert(256 * NV * 4 == BM * BN, "four waves hold the tile");
+    if (BM * BN <= SPLIT_TILE_FLOATS && sp.np > 1) {
+        f32x4* mine = (f32x4*)sp.ws + ((int64_t)sp.piece * 256 + tid) * NV;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    mine[(i * TN + j) * 4 + q] = f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1],
+                                                       acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        __builtin_amdgcn_s_waitcnt(0);  // the partial tile is in the L2 before it is counted
+        __syncthreads();
+        int* flag = (int*)smem;  // the LDS buffers are free after the loop's last barrier
+        if (tid == 0) flag[0] = atomicAdd(sp.cnt, 1);
+        __syncthreads();
+        if (flag[0] != sp.np - 1) return;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+                f32x16 sum{};
+                for (int p = 0; p < sp.np; ++p) {
+                    const f32x4* src = (const f32x4*)sp.ws + ((int64_t)p * 256 + tid) * NV;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const f32x4 v = p == sp.piece ? f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1],
+                                                              acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]}
+                                                      : src[(i * TN + j) * 4 + q];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) sum[4 * q + e] += v[e];
+                    }
+                }
+                acc[i][j] = sum;
+            }
+        if (tid == 0) *sp.cnt = 0;
+    }
 
     // The epilogue's element coordinates come from an opaque copy of the
     // lane index, so its address arithmetic is redone here instead of being
@@ -473,6 +536,77 @@ constexpr int NUM_XCD = 8;
 __host__ __device__ inline int pad_xcd(int n) { return (n + NUM_XCD - 1) / NUM_XCD * NUM_XCD; }
 __device__ inline int xcd_tile(int bid, int padded) {
     return (bid % NUM_XCD) * (padded / NUM_XCD) + bid / NUM_XCD;
+}
+
+// Balancing the last tiles of a launch.  When a launch of T equal tiles puts
+// k tiles on every compute unit and r = T mod CUs more on a few of them, those
+// few run a whole tile longer than the rest.  A job's TailSplit keeps its
+// first `full` tiles whole (one XCD-mapped workgroup each) and runs its last
+// `tail` tiles as `pieces` reduction pieces each (SplitPiece), dispatched
+// after the whole tiles, so the extra work is spread thinly over many units.
+// Tail tile s goes to XCD s % 8 with all of its pieces: tail block j runs on
+// XCD j % 8 and is that XCD's (j / 8)-th piece.  ws holds tail * pieces *
+// TILE_FLOATS floats of partial tiles, cnt one counter per tail tile (zero
+// between launches).
+struct TailSplit {
+    float* ws = nullptr;
+    int* cnt = nullptr;
+    int full = -1, tail = 0, pieces = 1;  // full < 0: the whole job unsplit
+    __host__ __device__ int blocks(int tiles) const {
+        return tail ? pad_xcd(full) + NUM_XCD * ((tail + NUM_XCD - 1) / NUM_XCD) * pieces
+                    : pad_xcd(tiles);
+    }
+    // Workgroup bid of the job: its tile t, chunk range [k0, k1) of `chunks`,
+    // and its piece (np == 1 for a whole tile); false for an idle workgroup.
+    __device__ bool map(int bid, int tiles, int chunks, int& t, int& k0, int& k1,
+                        SplitPiece& sp) const {
+        k0 = 0;
+        k1 = chunks;
+        if (!tail) {
+            t = xcd_tile(bid, pad_xcd(tiles));
+            return t < tiles;
+        }
+        const int head = pad_xcd(full);
+        if (bid < head) {
+            t = xcd_tile(bid, head);
+            return t < full;
+        }
+        const int j = bid - head, k = j / NUM_XCD, p = k % pieces;
+        const int s = (k / pieces) * NUM_XCD + j % NUM_XCD;  // same XCD as every other piece of s
+        if (s >= tail) return false;
+        t = full + s;
+        k0 = p * chunks / pieces;
+        k1 = (p + 1) * chunks / pieces;
+        sp.ws = ws + (int64_t)s * pieces * SPLIT_TILE_FLOATS;
+        sp.cnt = cnt + s;
+        sp.piece = p;
+        sp.np = pieces;
+        return true;
+    }
+};
+// The split for a job of job_tiles tiles of `chunks` chunks that closes a
+// launch of launch_tiles equal tiles on `cus` compute units: the r excess
+// tiles (r <= SPLIT_MAX_TILES, taken from this job) in up to 16 pieces of at
+// least two chunks, about one piece per unit.  Only when the whole tiles fit
+// in one round of four workgroups per unit (the residency of these GEMM
+// kernels), so that the pieces start alongside them: behind a full round
+// they would only start as whole tiles finish, which measured no faster.
+inline TailSplit plan_tail(float* ws, int* cnt, int cus, int launch_tiles, int job_tiles,
+                           int chunks) {
+    TailSplit ts;
+    ts.ws = ws;
+    ts.cnt = cnt;
+    if (!ws || !cnt || cus < 1 || launch_tiles < cus) return ts;
+    const int r = launch_tiles % cus;
+    if (r == 0 || r > SPLIT_MAX_TILES || r > job_tiles || launch_tiles - r > 4 * cus) return ts;
+    int p = SPLIT_MAX_PIECES;
+    if (chunks / 2 < p) p = chunks / 2;
+    if (cus / r < p) p = cus / r;
+    if (p < 2) return ts;
+    ts.full = job_tiles - r;
+    ts.tail = r;
+    ts.pieces = p;
+    return ts;
 }
 
 // Several independent jobs in one launch: blocks [0, a.blocks()) run job a,

@@ -110,10 +110,20 @@ void launch_widen_bf16(const WidenSet& set, int n_nets, int64_t count, hipStream
 // (widened to fp32) and the products run on bf16 MFMA operands (common.h).
 void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int groups, int n,
                       float* h1, bool bf16, hipStream_t st);
+// Workspace for balancing the last tiles of a launch (TailSplit): ws holds
+// SPLIT_MAX_TILES * SPLIT_MAX_PIECES partial 64x64 tiles, cnt SPLIT_MAX_TILES
+// counters that are zero between launches; ws == nullptr turns splitting
+// off.  The launches on one stream run one after another, so they share it.
+// cus is set either way (launch shapes use it).
+struct SplitWs {
+    float* ws = nullptr;
+    int* cnt = nullptr;
+    int cus = 0;  // compute units of the device
+};
 void launch_conv2_fwd(const float* h1, const GroupPtrs& w2t, const GroupPtrs& theta, int groups,
                       int n, float* h2, bool bf16, hipStream_t st);
 void launch_conv3_fwd(const float* h2, const GroupPtrs& w3t, const GroupPtrs& theta, int groups,
-                      int n, float* h3, bool bf16, hipStream_t st);
+                      int n, float* h3, const SplitWs& sw, bool bf16, hipStream_t st);
 // fc1 forward as split-K partial sums partial[g][s][b][512]; returns the
 // number of splits s (the head kernels finish the layer).  With bf16, W4 is
 // read from w4b (the sets' bf16 W4 blocks, 2-byte aligned at least), not theta.
@@ -145,16 +155,16 @@ void launch_td_head(const float* fc1part_online, const float* fc1part_target, in
 //  conv3: dz2 and split partials of dW3 / db3 (returns splits per group);
 //  conv2: dz1 and split partials of dW2 / db2 (returns splits per group).
 // kp: dz3 / dz2 partial planes, each groups * n rows long; fc1 writes kp
-// planes of dz3, conv3 reads them and writes kp_out planes of dz2, conv2
-// reads those.
+// planes of dz3, conv3 reads them and writes kp planes of dz2, conv2 reads
+// those.
 int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, const GroupPtrs16& w4b,
                         int groups, const float* h3,
                         const float* h4, const int32_t* a, const float* coef, const float* ell,
                         int n, int A, float* dz3, float* grads, int64_t grads_stride,
-                        float* hpart, int kp, bool bf16, hipStream_t st);
+                        float* hpart, int kp, const SplitWs& sw, bool bf16, hipStream_t st);
 int launch_conv3_backward(const float* dz3, const GroupPtrs& w3d, int groups, const float* h2,
-                          int n, float* dz2, float* partial, float* bias_part, int kp, int kp_out,
-                          bool bf16, hipStream_t st);
+                          int n, float* dz2, float* partial, float* bias_part, int kp, bool bf16,
+                          hipStream_t st);
 int launch_conv2_backward(const float* dz2, const GroupPtrs& w2p, int groups, const float* h1,
                           int n, float* dz1, float* partial, float* bias_part, int kp, bool bf16,
                           hipStream_t st);
@@ -206,13 +216,12 @@ constexpr int CONV3_WG_SPLITS = 114;         // 9 column tiles x 114 splits ~ 10
 constexpr int CONV2_WG_SPLITS = 64;          // 8 column tiles x 64 splits
 constexpr int CONV1_WG_MAX_SPLITS = 512;
 // Small batches split the fc1 and conv3 data gradients over the reduction:
-// with B learner rows, dz3 arrives as dz3_parts(B) and dz2 as dz2_parts(B)
-// partial planes (each already masked by the ReLU, which is linear in them)
-// that the conv3 and conv2 backward loaders add in plane order.
-// bwd_split_rows(B) >= parts * B rows are reserved per tensor; it never
-// decreases with B, so a workspace sized for a batch serves every smaller one.
-__host__ __device__ constexpr int dz3_parts(int64_t rows) { return rows <= 64 ? 4 : rows <= 128 ? 2 : 1; }
-__host__ __device__ constexpr int dz2_parts(int64_t rows) { return dz3_parts(rows); }
+// with B learner rows, dz3 and dz2 arrive as bwd_parts(B) partial planes
+// (each already masked by the ReLU, which is linear in them) that the conv3
+// and conv2 backward loaders add in plane order.  bwd_split_rows(B) >=
+// bwd_parts(B) * B rows are reserved per tensor; it never decreases with B,
+// so a workspace sized for a batch serves every smaller one.
+__host__ __device__ constexpr int bwd_parts(int64_t rows) { return rows <= 64 ? 4 : rows <= 128 ? 2 : 1; }
 __host__ __device__ constexpr int64_t bwd_split_rows(int64_t rows) {
     return rows <= 64 ? 4 * rows : rows <= 256 ? 256 : rows;
 }

@@ -130,6 +130,9 @@ struct Conv2FwdJob {
     }
 };
 
+// No TailSplit here: at batch 512 the whole tiles already fill every slot of
+// every compute unit (five per unit), so pieces could only start once whole
+// tiles finish, and measured no faster than the unsplit launch.
 void launch_conv2_fwd(const float* h1, const GroupPtrs& w2t, const GroupPtrs& theta, int groups,
                       int n, float* h2, bool bf16, hipStream_t st) {
     if (n <= 0) return;
@@ -177,28 +180,33 @@ struct Conv3FwdJob {
     GroupPtrs w3t, theta;
     float* h3;
     int n, groups;
-    static constexpr int PA = BF ? BF_WEIGHT : 0, PB = BF ? BF_ACT_FWD : 0;
+    TailSplit ts;
+    static constexpr int PA = BF ? BF_WEIGHT : 0, PB = BF ? BF_ACT_FWD : 0, CHUNKS = 18;
     using SH = GemmShape<64, 64, KMAJ, KMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return (n * P3 + 63) / 64; }
-    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
+    __host__ __device__ int blocks() const { return ts.blocks(tiles() * groups); }
     __device__ void run(int bid, float* smem) const {
-        const int t = xcd_tile(bid, blocks());
-        if (t >= tiles() * groups) return;
+        int t, k0, k1;
+        SplitPiece sp;
+        if (!ts.map(bid, tiles() * groups, CHUNKS, t, k0, k1, sp)) return;
         const int g = t / tiles(), m0 = (t % tiles()) * 64;
         const int rows = n * P3;
         WtapB<C2, C3> la{w3t.p[g]};
         Conv3FwdB lb{h2 + (int64_t)g * n * P2 * C2, rows, m0};
         Conv3FwdStore epi{h3 + (int64_t)g * n * FLAT, theta.p[g] + OFF_B3, rows, m0};
-        mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, 0, 18, la, lb, epi);
+        if (sp.np == 1) mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, 0, CHUNKS, la, lb, epi);
+        else mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, k0, k1, la, lb, epi, nullptr, sp);
     }
 };
 
 void launch_conv3_fwd(const float* h2, const GroupPtrs& w3t, const GroupPtrs& theta, int groups,
-                      int n, float* h3, bool bf16, hipStream_t st) {
+                      int n, float* h3, const SplitWs& sw, bool bf16, hipStream_t st) {
     if (n <= 0) return;
-    if (bf16) launch_jobs(st, Conv3FwdJob<1>{h2, w3t, theta, h3, n, groups});
-    else      launch_jobs(st, Conv3FwdJob<0>{h2, w3t, theta, h3, n, groups});
+    const int T = (n * P3 + 63) / 64 * groups;
+    const TailSplit ts = plan_tail(sw.ws, sw.cnt, sw.cus, T, T, Conv3FwdJob<0>::CHUNKS);
+    if (bf16) launch_jobs(st, Conv3FwdJob<1>{h2, w3t, theta, h3, n, groups, ts});
+    else      launch_jobs(st, Conv3FwdJob<0>{h2, w3t, theta, h3, n, groups, ts});
 }
 
 // ---------------------------------------------------------------------------
@@ -379,16 +387,27 @@ struct Fc1DgradJob {
     const float* h3;
     float* dz3;
     int n, groups, kp;  // kp reduction parts, each writing its own dz3 plane
-    static constexpr int PA = BF ? BF_GRAD : 0, PB = BF ? BF_WEIGHT : 0;
+    TailSplit ts;       // kp == 1 only
+    static constexpr int PA = BF ? BF_GRAD : 0, PB = BF ? BF_WEIGHT : 0, CHUNKS = HID / BK;
     using SH = GemmShape<64, 64, KMAJ, RMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return ((n + 63) / 64) * (FLAT / 64); }
-    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups * kp); }
+    __host__ __device__ int blocks() const {
+        return kp > 1 ? pad_xcd(tiles() * groups * kp) : ts.blocks(tiles() * groups);
+    }
     __device__ void run(int bid, float* smem) const {
-        int t = xcd_tile(bid, blocks());
-        if (t >= tiles() * groups * kp) return;
-        const int part = t / (tiles() * groups);
-        t -= part * tiles() * groups;
+        int t, part = 0, kc0 = 0, kc1 = CHUNKS;  // HID is a whole number of chunks
+        SplitPiece sp;
+        if (kp > 1) {
+            t = xcd_tile(bid, blocks());
+            if (t >= tiles() * groups * kp) return;
+            part = t / (tiles() * groups);
+            t -= part * tiles() * groups;
+            kc0 = part * CHUNKS / kp;
+            kc1 = (part + 1) * CHUNKS / kp;
+        } else if (!ts.map(bid, tiles() * groups, CHUNKS, t, kc0, kc1, sp)) {
+            return;
+        }
         const int g = t / tiles();
         t -= g * tiles();
         const int mt = (n + 63) / 64;
@@ -397,14 +416,21 @@ struct Fc1DgradJob {
         RowMajorK la{dz4 + rows * HID, n, r0, HID};
         Dz3NhwcStore epi{dz3 + part * (int64_t)groups * n * FLAT + rows * FLAT, h3 + rows * FLAT, n,
                          r0, c0};
-        const int kc0 = part * (HID / BK) / kp, kc1 = (part + 1) * (HID / BK) / kp;
-        // HID is a whole number of chunks
+        // small-batch parts keep runtime bounds; whole tiles compile-time ones
+        auto gemm = [&](auto& lb) {
+            if (sp.np > 1)
+                mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi, nullptr, sp);
+            else if (kp > 1)
+                mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi);
+            else
+                mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, 0, CHUNKS, la, lb, epi);
+        };
         if constexpr (BF > 0) {
             RowMajorR16 lb{w4b.p[g], c0, FLAT, HID};
-            mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi);
+            gemm(lb);
         } else {
             RowMajorR<false> lb{theta.p[g] + OFF_W4, c0, FLAT, HID};
-            mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi);
+            gemm(lb);
         }
     }
 };
@@ -518,17 +544,34 @@ int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, const GroupPtr
                         int groups, const float* h3,
                         const float* h4, const int32_t* a, const float* coef, const float* ell,
                         int n, int A, float* dz3, float* grads, int64_t grads_stride,
-                        float* hpart, int kp, bool bf16, hipStream_t st) {
+                        float* hpart, int kp, const SplitWs& sw, bool bf16, hipStream_t st) {
     if (n <= 0) return 0;
     const int rows = max(32, (n + HEAD_MAX_BLOCKS - 1) / HEAD_MAX_BLOCKS);
     const int row_blocks = (n + rows - 1) / rows;
     const HeadPartialJob hp{h4, a, coef, ell, hpart, n, A, rows, row_blocks, groups};
-    if (bf16)
-        launch_jobs(st, Fc1DgradJob<1>{dz4, theta, w4b, h3, dz3, n, groups, kp},
-                    Fc1WgradJob<1>{dz4, h3, grads, grads_stride, n, groups}, hp);
-    else
-        launch_jobs(st, Fc1DgradJob<0>{dz4, theta, w4b, h3, dz3, n, groups, kp},
-                    Fc1WgradJob<0>{dz4, h3, grads, grads_stride, n, groups}, hp);
+    // the two GEMMs balance as one launch of equal tiles when their chunk
+    // counts agree (the batch rounds up to the 512 hidden units)
+    TailSplit ts;
+    const int wt = (HID / 64) * (FLAT / 64) * groups, dt = ((n + 63) / 64) * (FLAT / 64) * groups;
+    if (kp == 1 && (n + BK - 1) / BK == HID / BK)
+        ts = plan_tail(sw.ws, sw.cnt, sw.cus, wt + dt, dt, HID / BK);
+    // Dispatch order: when the launch runs several rounds of workgroups per
+    // compute unit and the data-gradient tiles are the longer ones (many
+    // learner groups of a few rows each), those go first so that the short
+    // weight-gradient tiles fill in behind them instead of trailing them.
+    // Otherwise (one round, or equal tiles whose last data-gradient tiles are
+    // split) the weight gradient goes first, which measured faster at batches
+    // 32 and 512.
+    const bool dgrad_first = (n + BK - 1) / BK < HID / BK / kp && wt + dt > 4 * sw.cus;
+    auto go = [&](auto bf) {
+        constexpr int BF = decltype(bf)::value;
+        const Fc1WgradJob<BF> w{dz4, h3, grads, grads_stride, n, groups};
+        const Fc1DgradJob<BF> d{dz4, theta, w4b, h3, dz3, n, groups, kp, ts};
+        if (dgrad_first) launch_jobs(st, d, w, hp);
+        else launch_jobs(st, w, d, hp);
+    };
+    if (bf16) go(std::integral_constant<int, 1>{});
+    else go(std::integral_constant<int, 0>{});
     return row_blocks;
 }
 
@@ -581,9 +624,9 @@ struct Conv3DgradStore {
     }
 };
 
-// dz3 arrives as KP partial planes; KPO > 1 cuts the reduction over (tap, o)
-// into KPO parts, each writing its own masked dz2 plane.
-template <int BF, int KP, int KPO>
+// dz3 arrives as KP partial planes, and KP > 1 also cuts the reduction over
+// (tap, o) into KP parts, each writing its own masked dz2 plane.
+template <int BF, int KP>
 struct Conv3DgradJob {
     const float* dz3;
     GroupPtrs w3d;
@@ -594,10 +637,10 @@ struct Conv3DgradJob {
     using SH = GemmShape<64, 64, KMAJ, KMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return P2 * ((n + 63) / 64); }
-    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups * KPO); }
+    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups * KP); }
     __device__ void run(int bid, float* smem) const {
         int t = xcd_tile(bid, blocks());
-        if (t >= tiles() * groups * KPO) return;
+        if (t >= tiles() * groups * KP) return;
         const int part = t / (tiles() * groups);
         t -= part * tiles() * groups;
         const int g = t / tiles();
@@ -610,8 +653,8 @@ struct Conv3DgradJob {
         Conv3DgradA<KP> la{dz3 + rows * FLAT, n, b0, y, x, u0, v0, nv, plane * FLAT};
         Conv3DgradB lb{w3d.p[g], u0, v0, nv};
         Conv3DgradStore epi{dz2 + (part * plane + rows) * P2 * C2, h2 + rows * P2 * C2, n, b0, pos};
-        mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, part * 2 * taps / KPO,
-                                                 (part + 1) * 2 * taps / KPO, la, lb, epi);
+        mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, part * 2 * taps / KP, (part + 1) * 2 * taps / KP,
+                                                 la, lb, epi);
     }
 };
 
@@ -678,11 +721,11 @@ struct Conv3WgradJob {
 
 // Splits per group shrink with the group count so one launch stays near the
 // same number of workgroups; groups * splits stays within WG_MAX_SPLITS.
-template <int BF, int KP, int KPO>
+template <int BF, int KP>
 static void conv3_backward_jobs(const float* dz3, const GroupPtrs& w3d, int groups, const float* h2,
                                 int n, float* dz2, float* partial, float* bias_part, int splits,
                                 int cps, hipStream_t st) {
-    launch_jobs(st, Conv3DgradJob<BF, KP, KPO>{dz3, w3d, h2, dz2, n, groups},
+    launch_jobs(st, Conv3DgradJob<BF, KP>{dz3, w3d, h2, dz2, n, groups},
                 Conv3WgradJob<BF, KP>{dz3, h2, partial, bias_part, n, splits, cps, groups});
 }
 
@@ -695,22 +738,20 @@ static void with_parts(int k, F&& f) {
 }
 
 int launch_conv3_backward(const float* dz3, const GroupPtrs& w3d, int groups, const float* h2,
-                          int n, float* dz2, float* partial, float* bias_part, int kp, int kp_out,
-                          bool bf16, hipStream_t st) {
+                          int n, float* dz2, float* partial, float* bias_part, int kp, bool bf16,
+                          hipStream_t st) {
     if (n <= 0) return 0;
     const int nchunks = (n * P3 + BK - 1) / BK;
     int splits = min(min(WG_MAX_SPLITS / groups, nchunks), max(1, CONV3_WG_SPLITS / groups));
     const int cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
-    with_parts(kp, [&](auto ki) {
-        with_parts(kp_out, [&](auto ko) {
-            if (bf16)
-                conv3_backward_jobs<1, ki.value, ko.value>(dz3, w3d, groups, h2, n, dz2, partial,
-                                                           bias_part, splits, cps, st);
-            else
-                conv3_backward_jobs<0, ki.value, ko.value>(dz3, w3d, groups, h2, n, dz2, partial,
-                                                           bias_part, splits, cps, st);
-        });
+    with_parts(kp, [&](auto k) {
+        if (bf16)
+            conv3_backward_jobs<1, k.value>(dz3, w3d, groups, h2, n, dz2, partial, bias_part, splits,
+                                            cps, st);
+        else
+            conv3_backward_jobs<0, k.value>(dz3, w3d, groups, h2, n, dz2, partial, bias_part, splits,
+                                            cps, st);
     });
     return splits;
 }

@@ -104,6 +104,9 @@ def test_learner_step_batch512_a6(torch_cuda, g, ctx, oracle_mod):
 @pytest.mark.parametrize("B,A,clip,term_p", [
     (1, 18, 1.0, 0.5), (37, 18, math.inf, 0.5), (97, 4, 1.0, 0.0), (65, 32, 0.5, 1.0),
     (33, 1, 1.0, 0.1),  # one action: max_a' is that action's Q
+    # 774 conv3 tiles and 784 fc1 backward tiles: both launches run their last
+    # tiles as reduction pieces on 256 compute units, the last conv3 tile ragged
+    (505, 6, 1.0, 0.01),
 ])
 def test_learner_step_ragged_and_degenerate(torch_cuda, g, ctx, oracle_mod, B, A, clip, term_p):
     _say(f"learner ragged B={B} A={A} clip={clip} term_p={term_p}")
@@ -122,10 +125,13 @@ def test_learner_step_row_indices(torch_cuda, g, ctx, oracle_mod):
     _learner_case(torch_cuda, g, ctx, oracle_mod, inp)
 
 
-def test_learner_step_is_deterministic(torch_cuda, g, ctx):
-    _say("learner determinism B=128")
+@pytest.mark.parametrize("B", [128, 512])
+def test_learner_step_is_deterministic(torch_cuda, g, ctx, B):
+    """Bit-identical repeats; at 512 the tiles split into reduction pieces are
+    added in piece order whichever piece finishes last."""
+    _say(f"learner determinism B={B}")
     torch = torch_cuda
-    inp = datagen.learner_inputs(7300, 128, 18)
+    inp = datagen.learner_inputs(7300, B, 18)
     theta, tgt, idx = _dev(torch, inp.theta), _dev(torch, inp.theta_target), _dev(torch, inp.idx)
     rep = _stacked(torch, g, inp)
     g1, l1 = g.learner_step(ctx, theta, tgt, 18, rep, idx)
@@ -280,7 +286,7 @@ def test_learner_step_from_ring(torch_cuda, g, ctx, oracle_mod, ring):
 # ---------------------------------------------------------------------------
 # Actor inference
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("n", [1, 3, 37, 130])
+@pytest.mark.parametrize("n", [1, 3, 37, 130, 1010])  # 1010: 774 conv3 tiles, the last split
 def test_q_forward_ragged(torch_cuda, g, ctx, oracle_mod, n):
     _say(f"q_forward n={n}")
     torch = torch_cuda
