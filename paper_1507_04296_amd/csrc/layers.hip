@@ -12,6 +12,25 @@
 
 namespace gorila {
 
+// Output positions of an N x N data-gradient grid (kernel K taps per axis
+// over an IN x IN input, stride-1 form) in decreasing order of valid taps,
+// then raster order.  The data-gradient workgroups of a launch go longest
+// first, so the short border positions fill in at the end instead of long
+// interior ones trailing the launch.
+template <int N, int K, int IN>
+struct LongestFirst {
+    unsigned char pos[N * N];
+    static constexpr int taps(int y) {
+        return (y < K - 1 ? y : K - 1) - (y - (IN - 1) > 0 ? y - (IN - 1) : 0) + 1;
+    }
+    constexpr LongestFirst() : pos() {
+        int r = 0;
+        for (int want = K * K; want >= 1; --want)
+            for (int p = 0; p < N * N; ++p)
+                if (taps(p / N) * taps(p % N) == want) pos[r++] = (unsigned char)p;
+    }
+};
+
 // Quad at p summed over the KP partial planes p, p + ps, ... in plane order.
 template <int KP>
 __device__ __forceinline__ f32x4 ld4_parts(const float* p, int64_t ps) {
@@ -646,7 +665,8 @@ struct Conv3DgradJob {
         const int g = t / tiles();
         t -= g * tiles();
         const int64_t rows = (int64_t)g * n, plane = (int64_t)groups * n;
-        const int pos = t % P2, y = pos / H2, x = pos - y * H2, b0 = (t / P2) * 64;
+        constexpr LongestFirst<H2, K3, H3> ORDER{};
+        const int pos = ORDER.pos[t % P2], y = pos / H2, x = pos - y * H2, b0 = (t / P2) * 64;
         const int u0 = max(0, y - (H3 - 1)), u1 = min(K3 - 1, y);
         const int v0 = max(0, x - (H3 - 1)), v1 = min(K3 - 1, x);
         const int nv = v1 - v0 + 1, taps = (u1 - u0 + 1) * nv;
@@ -833,8 +853,9 @@ struct Conv2DgradJob {
         const int g = t / tiles();
         t -= g * tiles();
         const int64_t rows = (int64_t)g * n;
-        // neighbouring positions adjacent
-        const int pos = t % 100, ct = (t / 100) % NCT, b0 = (t / (100 * NCT)) * 64;
+        // the column tiles of one position adjacent, positions longest first
+        constexpr LongestFirst<10, 2, H2> ORDER{};
+        const int ct = t % NCT, pos = ORDER.pos[(t / NCT) % 100], b0 = (t / (100 * NCT)) * 64;
         const int yy = pos / 10, xx = pos % 10;
         const int du0 = max(0, yy - (H2 - 1)), du1 = min(1, yy);
         const int dv0 = max(0, xx - (H2 - 1)), dv1 = min(1, xx);
