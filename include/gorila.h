@@ -116,7 +116,7 @@ size_t gorila_workspace_bytes(int32_t max_batch, int32_t n_actions, int32_t dtyp
  * workspace of ws_bytes (>= gorila_workspace_bytes(1,1,0,1), 256-byte
  * aligned) to a new context on the current device.  The context owns only
  * host bookkeeping; destroy it before freeing the workspace.  Creation
- * zeroes the workspace's first 256 bytes (an error word and the counters of
+ * zeroes the workspace's first 1024 bytes (an error word and the counters of
  * split reductions, which every call leaves at zero) on the stream; the
  * caller must not write the workspace while the context lives, and calls on
  * one context must not overlap (one stream). */

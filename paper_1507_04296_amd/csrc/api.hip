@@ -71,21 +71,22 @@ struct Plan {
     size_t h1, h2, h3, h4, q, ell, coef;
     size_t dz4, dz3, dz2, dz1;
     size_t fc1part, part1, part2, part3, bpart, hpart;
-    size_t split;  // TailSplit partial tiles, or SIZE_MAX when the batch is too small to use them
+    size_t split;  // TailSplit partial tiles
     size_t total;
 };
 
-// The zeroed head of the workspace: the sticky error word, then the TailSplit
-// counters at SPLIT_CNT_OFFSET (zero between launches).
-constexpr size_t SPLIT_CNT_OFFSET = 128;
-static_assert(SPLIT_CNT_OFFSET + 4 * SPLIT_MAX_TILES <= ALIGN, "counters fit the zeroed head");
+// The zeroed head of the workspace (WS_HEAD bytes, cleared when a context is
+// created): the sticky error word, then the TailSplit counters at
+// SPLIT_CNT_OFFSET (every launch leaves them at zero).
+constexpr size_t WS_HEAD = 1024, SPLIT_CNT_OFFSET = 256;
+static_assert(SPLIT_CNT_OFFSET + 4 * SPLIT_MAX_TILES <= WS_HEAD, "counters fit the zeroed head");
 
 Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online = 1, int widened = 0) {
     Plan p{};
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t at = o; o += up(bytes); return at; };
     const int64_t F = fwd_rows, B = bwd_rows;
-    p.err = take(ALIGN);
+    p.err = take(WS_HEAD);
     p.ftab = take(sizeof(void*) * 2 * (size_t)(F > 2 * B ? F : 2 * B) * 4);
     p.a = take(4 * (size_t)B);
     p.r = take(4 * (size_t)B);
@@ -113,10 +114,7 @@ Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online = 1, int wi
     p.part3 = B ? take(4 * (size_t)WG_MAX_SPLITS * C3 * 9 * C2) : o;
     p.bpart = B ? take(4 * (size_t)3 * BIAS_PART_STRIDE) : o;
     p.hpart = B ? take(4 * (size_t)online * HEAD_MAX_BLOCKS * HP_STRIDE) : o;
-    // a launch needs at least one tile per compute unit before its tail is
-    // split; smaller batches never split, and leave the region out
-    p.split = F >= 128 ? take(4 * (size_t)SPLIT_MAX_TILES * SPLIT_MAX_PIECES * SPLIT_TILE_FLOATS)
-                       : SIZE_MAX;
+    p.split = take(4 * (size_t)SPLIT_MAX_SLOTS * SPLIT_TILE_FLOATS);
     p.total = o;
     return p;
 }
@@ -127,10 +125,8 @@ T* at(gorila_ctx* c, size_t off) { return (T*)(c->ws + off); }
 SplitWs split_ws(gorila_ctx* c, const Plan& p) {
     SplitWs sw;
     sw.cus = c->cus;
-    if (p.split != SIZE_MAX) {
-        sw.ws = at<float>(c, p.split);
-        sw.cnt = at<int>(c, p.err + SPLIT_CNT_OFFSET);
-    }
+    sw.ws = at<float>(c, p.split);
+    sw.cnt = at<int>(c, p.err + SPLIT_CNT_OFFSET);
     return sw;
 }
 
@@ -248,7 +244,7 @@ size_t gorila_workspace_bytes(int32_t max_batch, int32_t n_actions, int32_t dtyp
 
 int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_t ws_bytes) {
     if (!out || !workspace || !aligned16(workspace)) return GORILA_EINVAL;
-    if (ws_bytes < make_plan(1, 1, 1).err + ALIGN) return GORILA_EWORKSPACE;
+    if (ws_bytes < make_plan(1, 1, 1).err + WS_HEAD) return GORILA_EWORKSPACE;
     int dev = -1, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) return GORILA_EHIP;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -262,7 +258,7 @@ int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_
         c->cus = cus;
     }
     if (!c) return GORILA_EINVAL;
-    if (hipMemsetAsync(c->ws, 0, ALIGN, c->stream) != hipSuccess) {
+    if (hipMemsetAsync(c->ws, 0, WS_HEAD, c->stream) != hipSuccess) {
         delete c;
         return GORILA_EHIP;
     }

@@ -227,7 +227,8 @@ struct GemmShape {
 // has not read those addresses before in the launch, so its L1 holds no
 // stale copy.  This needs no device-wide cache write-back or invalidation,
 // which would evict every other workgroup's operands from the L2.
-constexpr int SPLIT_MAX_TILES = 32, SPLIT_MAX_PIECES = 16, SPLIT_TILE_FLOATS = 64 * 64;
+constexpr int SPLIT_MAX_TILES = 32, SPLIT_MAX_PIECES = 16, SPLIT_MAX_SLOTS = 512;
+constexpr int SPLIT_TILE_FLOATS = 64 * 64;
 struct SplitPiece {
     float* ws = nullptr;
     int* cnt = nullptr;
@@ -467,24 +468,33 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
         if (tid == 0) flag[0] = atomicAdd(sp.cnt, 1);
         __syncthreads();
         if (flag[0] != sp.np - 1) return;
+        // add every piece's partial tile (this one's included, read back) in
+        // piece order, two pieces' loads in flight at a time
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                f32x16 sum{};
-                for (int p = 0; p < sp.np; ++p) {
-                    const f32x4* src = (const f32x4*)sp.ws + ((int64_t)p * 256 + tid) * NV;
+            for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
+        for (int p0 = 0; p0 < sp.np; p0 += 2) {
+            f32x4 part[2][NV];
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const f32x4 v = p == sp.piece ? f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1],
-                                                              acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]}
-                                                      : src[(i * TN + j) * 4 + q];
+            for (int q = 0; q < 2; ++q)
+                if (p0 + q < sp.np) {
+                    const f32x4* src = (const f32x4*)sp.ws + ((int64_t)(p0 + q) * 256 + tid) * NV;
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) sum[4 * q + e] += v[e];
-                    }
+                    for (int v = 0; v < NV; ++v) part[q][v] = src[v];
                 }
-                acc[i][j] = sum;
-            }
+#pragma unroll
+            for (int q = 0; q < 2; ++q)
+                if (p0 + q < sp.np) {
+#pragma unroll
+                    for (int i = 0; i < TM; ++i)
+#pragma unroll
+                        for (int j = 0; j < TN; ++j)
+#pragma unroll
+                            for (int r = 0; r < 16; ++r)
+                                acc[i][j][r] += part[q][(i * TN + j) * 4 + r / 4][r % 4];
+                }
+        }
         if (tid == 0) *sp.cnt = 0;
     }
 
@@ -544,10 +554,12 @@ __device__ inline int xcd_tile(int bid, int padded) {
 // first `full` tiles whole (one XCD-mapped workgroup each) and runs its last
 // `tail` tiles as `pieces` reduction pieces each (SplitPiece), dispatched
 // after the whole tiles, so the extra work is spread thinly over many units.
+// (Splitting every tile of a small launch the same way measured slower at
+// batch 32: a workgroup's fixed latency, ~6 us, dominates its few chunks.)
 // Tail tile s goes to XCD s % 8 with all of its pieces: tail block j runs on
-// XCD j % 8 and is that XCD's (j / 8)-th piece.  ws holds tail * pieces *
-// TILE_FLOATS floats of partial tiles, cnt one counter per tail tile (zero
-// between launches).
+// XCD j % 8 and is that XCD's (j / 8)-th piece.  ws holds tail * pieces <=
+// SPLIT_MAX_SLOTS partial tiles of TILE_FLOATS floats, cnt one counter per
+// tail tile (zero between launches).
 struct TailSplit {
     float* ws = nullptr;
     int* cnt = nullptr;
@@ -591,18 +603,18 @@ struct TailSplit {
 // in one round of four workgroups per unit (the residency of these GEMM
 // kernels), so that the pieces start alongside them: behind a full round
 // they would only start as whole tiles finish, which measured no faster.
-inline TailSplit plan_tail(float* ws, int* cnt, int cus, int launch_tiles, int job_tiles,
-                           int chunks) {
+inline TailSplit plan_split(float* ws, int* cnt, int cus, int launch_tiles, int job_tiles,
+                            int chunks) {
     TailSplit ts;
     ts.ws = ws;
     ts.cnt = cnt;
     if (!ws || !cnt || cus < 1 || launch_tiles < cus) return ts;
     const int r = launch_tiles % cus;
-    if (r == 0 || r > SPLIT_MAX_TILES || r > job_tiles || launch_tiles - r > 4 * cus) return ts;
+    if (r == 0 || r > job_tiles || launch_tiles - r > 4 * cus) return ts;
     int p = SPLIT_MAX_PIECES;
     if (chunks / 2 < p) p = chunks / 2;
     if (cus / r < p) p = cus / r;
-    if (p < 2) return ts;
+    if (p < 2 || r > SPLIT_MAX_TILES || r * p > SPLIT_MAX_SLOTS) return ts;
     ts.full = job_tiles - r;
     ts.tail = r;
     ts.pieces = p;

@@ -110,10 +110,9 @@ void launch_widen_bf16(const WidenSet& set, int n_nets, int64_t count, hipStream
 // (widened to fp32) and the products run on bf16 MFMA operands (common.h).
 void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int groups, int n,
                       float* h1, bool bf16, hipStream_t st);
-// Workspace for balancing the last tiles of a launch (TailSplit): ws holds
-// SPLIT_MAX_TILES * SPLIT_MAX_PIECES partial 64x64 tiles, cnt SPLIT_MAX_TILES
-// counters that are zero between launches; ws == nullptr turns splitting
-// off.  The launches on one stream run one after another, so they share it.
+// Workspace for balancing a launch (TailSplit): ws holds SPLIT_MAX_SLOTS
+// partial 64x64 tiles, cnt SPLIT_MAX_TILES counters that are zero between
+// launches; ws == nullptr turns splitting off.  The launches on one stream run one after another, so they share it.
 // cus is set either way (launch shapes use it).
 struct SplitWs {
     float* ws = nullptr;

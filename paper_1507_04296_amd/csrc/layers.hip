@@ -193,7 +193,9 @@ struct Conv3FwdStore {  // row = o, col = pixel index within the tile
     }
 };
 
-template <int BF>
+// SPLIT: the launch runs some tiles as reduction pieces (TailSplit); the
+// unsplit instantiation carries none of the hand-off code.
+template <int BF, bool SPLIT = false>
 struct Conv3FwdJob {
     const float* h2;
     GroupPtrs w3t, theta;
@@ -204,11 +206,18 @@ struct Conv3FwdJob {
     using SH = GemmShape<64, 64, KMAJ, KMAJ, PA, PB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return (n * P3 + 63) / 64; }
-    __host__ __device__ int blocks() const { return ts.blocks(tiles() * groups); }
+    __host__ __device__ int blocks() const {
+        return SPLIT ? ts.blocks(tiles() * groups) : pad_xcd(tiles() * groups);
+    }
     __device__ void run(int bid, float* smem) const {
-        int t, k0, k1;
+        int t, k0 = 0, k1 = CHUNKS;
         SplitPiece sp;
-        if (!ts.map(bid, tiles() * groups, CHUNKS, t, k0, k1, sp)) return;
+        if constexpr (SPLIT) {
+            if (!ts.map(bid, tiles() * groups, CHUNKS, t, k0, k1, sp)) return;
+        } else {
+            t = xcd_tile(bid, blocks());
+            if (t >= tiles() * groups) return;
+        }
         const int g = t / tiles(), m0 = (t % tiles()) * 64;
         const int rows = n * P3;
         WtapB<C2, C3> la{w3t.p[g]};
@@ -223,9 +232,11 @@ void launch_conv3_fwd(const float* h2, const GroupPtrs& w3t, const GroupPtrs& th
                       int n, float* h3, const SplitWs& sw, bool bf16, hipStream_t st) {
     if (n <= 0) return;
     const int T = (n * P3 + 63) / 64 * groups;
-    const TailSplit ts = plan_tail(sw.ws, sw.cnt, sw.cus, T, T, Conv3FwdJob<0>::CHUNKS);
-    if (bf16) launch_jobs(st, Conv3FwdJob<1>{h2, w3t, theta, h3, n, groups, ts});
-    else      launch_jobs(st, Conv3FwdJob<0>{h2, w3t, theta, h3, n, groups, ts});
+    const TailSplit ts = plan_split(sw.ws, sw.cnt, sw.cus, T, T, Conv3FwdJob<0>::CHUNKS);
+    if (bf16 && ts.tail) launch_jobs(st, Conv3FwdJob<1, true>{h2, w3t, theta, h3, n, groups, ts});
+    else if (bf16) launch_jobs(st, Conv3FwdJob<1>{h2, w3t, theta, h3, n, groups, ts});
+    else if (ts.tail) launch_jobs(st, Conv3FwdJob<0, true>{h2, w3t, theta, h3, n, groups, ts});
+    else launch_jobs(st, Conv3FwdJob<0>{h2, w3t, theta, h3, n, groups, ts});
 }
 
 // ---------------------------------------------------------------------------
@@ -398,7 +409,7 @@ struct Dz3NhwcStore {
 
 // kp > 1 cuts the reduction over the 512 hidden units into kp parts, each
 // writing its masked dz3 plane (the ReLU mask is linear in the parts).
-template <int BF>
+template <int BF, bool SPLIT = false>  // SPLIT as for Conv3FwdJob (kp == 1 only)
 struct Fc1DgradJob {
     const float* dz4;
     GroupPtrs theta;
@@ -412,20 +423,20 @@ struct Fc1DgradJob {
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return ((n + 63) / 64) * (FLAT / 64); }
     __host__ __device__ int blocks() const {
-        return kp > 1 ? pad_xcd(tiles() * groups * kp) : ts.blocks(tiles() * groups);
+        return SPLIT ? ts.blocks(tiles() * groups) : pad_xcd(tiles() * groups * kp);
     }
     __device__ void run(int bid, float* smem) const {
         int t, part = 0, kc0 = 0, kc1 = CHUNKS;  // HID is a whole number of chunks
         SplitPiece sp;
-        if (kp > 1) {
+        if constexpr (SPLIT) {
+            if (!ts.map(bid, tiles() * groups, CHUNKS, t, kc0, kc1, sp)) return;
+        } else {
             t = xcd_tile(bid, blocks());
             if (t >= tiles() * groups * kp) return;
             part = t / (tiles() * groups);
             t -= part * tiles() * groups;
             kc0 = part * CHUNKS / kp;
             kc1 = (part + 1) * CHUNKS / kp;
-        } else if (!ts.map(bid, tiles() * groups, CHUNKS, t, kc0, kc1, sp)) {
-            return;
         }
         const int g = t / tiles();
         t -= g * tiles();
@@ -437,7 +448,7 @@ struct Fc1DgradJob {
                          r0, c0};
         // small-batch parts keep runtime bounds; whole tiles compile-time ones
         auto gemm = [&](auto& lb) {
-            if (sp.np > 1)
+            if (SPLIT && sp.np > 1)
                 mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi, nullptr, sp);
             else if (kp > 1)
                 mfma_gemm<64, 64, 2, KMAJ, RMAJ, PA, PB>(smem, kc0, kc1, la, lb, epi);
@@ -573,7 +584,7 @@ int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, const GroupPtr
     TailSplit ts;
     const int wt = (HID / 64) * (FLAT / 64) * groups, dt = ((n + 63) / 64) * (FLAT / 64) * groups;
     if (kp == 1 && (n + BK - 1) / BK == HID / BK)
-        ts = plan_tail(sw.ws, sw.cnt, sw.cus, wt + dt, dt, HID / BK);
+        ts = plan_split(sw.ws, sw.cnt, sw.cus, wt + dt, dt, HID / BK);
     // Dispatch order: when the launch runs several rounds of workgroups per
     // compute unit and the data-gradient tiles are the longer ones (many
     // learner groups of a few rows each), those go first so that the short
@@ -587,6 +598,7 @@ int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, const GroupPtr
         const Fc1WgradJob<BF> w{dz4, h3, grads, grads_stride, n, groups};
         const Fc1DgradJob<BF> d{dz4, theta, w4b, h3, dz3, n, groups, kp, ts};
         if (dgrad_first) launch_jobs(st, d, w, hp);
+        else if (ts.tail) launch_jobs(st, w, Fc1DgradJob<BF, true>{dz4, theta, w4b, h3, dz3, n, groups, kp, ts}, hp);
         else launch_jobs(st, w, d, hp);
     };
     if (bf16) go(std::integral_constant<int, 1>{});
@@ -666,7 +678,10 @@ struct Conv3DgradJob {
         t -= g * tiles();
         const int64_t rows = (int64_t)g * n, plane = (int64_t)groups * n;
         constexpr LongestFirst<H2, K3, H3> ORDER{};
-        const int pos = ORDER.pos[t % P2], y = pos / H2, x = pos - y * H2, b0 = (t / P2) * 64;
+        // the position is uniform over the workgroup: keep it (and what derives
+        // from it) in scalar registers
+        const int pos = __builtin_amdgcn_readfirstlane(ORDER.pos[t % P2]);
+        const int y = pos / H2, x = pos - y * H2, b0 = (t / P2) * 64;
         const int u0 = max(0, y - (H3 - 1)), u1 = min(K3 - 1, y);
         const int v0 = max(0, x - (H3 - 1)), v1 = min(K3 - 1, x);
         const int nv = v1 - v0 + 1, taps = (u1 - u0 + 1) * nv;
@@ -855,7 +870,8 @@ struct Conv2DgradJob {
         const int64_t rows = (int64_t)g * n;
         // the column tiles of one position adjacent, positions longest first
         constexpr LongestFirst<10, 2, H2> ORDER{};
-        const int ct = t % NCT, pos = ORDER.pos[(t / NCT) % 100], b0 = (t / (100 * NCT)) * 64;
+        const int ct = t % NCT, b0 = (t / (100 * NCT)) * 64;
+        const int pos = __builtin_amdgcn_readfirstlane(ORDER.pos[(t / NCT) % 100]);  // uniform
         const int yy = pos / 10, xx = pos % 10;
         const int du0 = max(0, yy - (H2 - 1)), du1 = min(1, yy);
         const int dv0 = max(0, xx - (H2 - 1)), dv1 = min(1, xx);
