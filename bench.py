@@ -167,6 +167,52 @@ def run_learner(torch, g, datagen, B, A, seed, steps, warmup, timed_stage=None, 
                 graph_ms=graph_ms)
 
 
+def run_two_learners(torch, g, datagen, B, A, seed, steps, warmup):
+    """Two independent learners (their own contexts and gradient buffers, the
+    same minibatch) stepping on two streams at once, as learners bundled on one
+    GPU would: the learner transitions/s of the pair, timed from one event on
+    the current stream to the join of both streams."""
+    inp = datagen.learner_inputs(seed, B, A)
+    dev = torch.device("cuda:0")
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    theta, tgt, idx = t(inp.theta), t(inp.theta_target), t(inp.idx)
+    rep = g.Replay.stacked(t(inp.s), t(inp.s2), t(inp.a), t(inp.r), t(inp.term))
+    streams = [torch.cuda.Stream(device=dev) for _ in range(2)]  # default priority
+    learners = []
+    for s in streams:
+        with torch.cuda.stream(s):
+            learners.append((g.Context(B, A, device=dev),
+                             torch.empty(g.param_count(A), dtype=torch.float32, device=dev),
+                             torch.empty(1, dtype=torch.float32, device=dev)))
+    def step_pair():
+        for s, (ctx, grads, loss) in zip(streams, learners):
+            with torch.cuda.stream(s):
+                g.gorila_learner_step(ctx, theta, tgt, A, rep, idx, inp.gamma, 1.0, grads, loss)
+    for _ in range(warmup):
+        step_pair()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    cur = torch.cuda.current_stream(dev)
+    start.record(cur)
+    for s in streams:
+        s.wait_event(start)
+    for _ in range(steps):
+        step_pair()
+    for s in streams:
+        cur.wait_stream(s)
+    stop.record(cur)
+    torch.cuda.synchronize()
+    for ctx, _, _ in learners:
+        ctx.check()
+        ctx.close()
+    ms_per_step = start.elapsed_time(stop) / (2 * steps)
+    return {"workload": f"learner_b{B}_a{A}_f32 x 2 learners", "streams": 2,
+            "value": round(B / (ms_per_step * 1e-3), 1), "unit": "transitions/s",
+            "ms_per_learner_step": round(ms_per_step, 4),
+            "note": "two independent learner steps in flight at once (bundled learners); "
+                    "not the headline value, which times one learner's steps back to back"}
+
+
 def run_grouped(torch, g, datagen, steps, warmup):
     """The stale-replica workload: 16 bf16 replicas x 64 transitions, 18 actions."""
     w = datagen.WORKLOADS["grouped_g16_b64_a18_bf16"]
@@ -407,6 +453,8 @@ def main():
     ap.add_argument("--no-grouped", action="store_true",
                     help="skip the 16-replica bf16 grouped-step companion line")
     ap.add_argument("--no-actor", action="store_true", help="skip the actor-inference line")
+    ap.add_argument("--no-two-learners", action="store_true",
+                    help="skip the two-learners-on-two-streams lines")
     ap.add_argument("--no-ring", action="store_true",
                     help="skip the one-million-frame ring gather / learner line")
     ap.add_argument("--no-ps", action="store_true",
@@ -481,6 +529,11 @@ def main():
                           "step_ms_p10_p50_p90": r32["pct"],
                           "hip_graph": {"ms_per_step": round(r32["graph_ms"], 4),
                                         "value": round(32 / (r32["graph_ms"] * 1e-3), 1)}}
+    if not args.no_two_learners:
+        out["two_learners"] = {
+            "b512": run_two_learners(torch, g, datagen, B, A, seed, args.steps, args.warmup),
+            "b32": run_two_learners(torch, g, datagen, 32, 18, datagen.SEED_BASE + 0,
+                                    max(args.steps, 50), args.warmup)}
     if not args.no_grouped:
         out["grouped"] = run_grouped(torch, g, datagen, max(args.steps // 2, 5), args.warmup)
     if not args.no_actor:

@@ -558,7 +558,7 @@ __device__ inline int xcd_tile(int bid, int padded) {
 // batch 32: a workgroup's fixed latency, ~6 us, dominates its few chunks.)
 // Tail tile s goes to XCD s % 8 with all of its pieces: tail block j runs on
 // XCD j % 8 and is that XCD's (j / 8)-th piece.  ws holds tail * pieces <=
-// SPLIT_MAX_SLOTS partial tiles of TILE_FLOATS floats, cnt one counter per
+// SPLIT_MAX_SLOTS partial tiles of SPLIT_TILE_FLOATS floats, cnt one counter per
 // tail tile (zero between launches).
 struct TailSplit {
     float* ws = nullptr;
