@@ -251,11 +251,24 @@ def run_grouped(torch, g, datagen, steps, warmup):
     # every parameter set is bf16, so the products run on bf16 MFMA operands
     # (forward activations as two bf16 terms) with fp32 accumulation; tflops
     # counts algorithmic FLOPs, priced against the dense bf16 peak
+    # compulsory HBM bytes of the step: both stacks of every transition, the G
+    # bf16 replicas and the bf16 target read once, the G fp32 gradients written
+    P = g.param_count(A)
+    compulsory = 2 * G * b * datagen.STATE_BYTES + (G + 1) * P * 2 + G * P * 4
+    hbm_tbs = compulsory / (ms * 1e-3) / 1e12
+    mfma_s = G * b * step_flops_per_transition(A) / (BF16_MFMA_PEAK_TFLOPS * 1e12)
+    hbm_s = compulsory / (HBM_PEAK_GBS * 1e9)
     return {"workload": "grouped_g16_b64_a18_bf16", "value": round(G * b / (ms * 1e-3), 1),
             "unit": "transitions/s", "ms_per_step": round(ms, 4), "tflops": round(tflops, 2),
             "dtype": "bf16 operands, f32 accumulation",
             "pct_mfma_peak": round(100 * tflops / BF16_MFMA_PEAK_TFLOPS, 2),
             "mfma_peak_tflops": BF16_MFMA_PEAK_TFLOPS,
+            "roofline": {"mfma_bf16": {"floor_ms": round(mfma_s * 1e3, 4),
+                                       "frac": round(tflops / BF16_MFMA_PEAK_TFLOPS, 4)},
+                         "hbm": {"compulsory_bytes": compulsory, "floor_ms": round(hbm_s * 1e3, 4),
+                                 "achieved_tb_per_s": round(hbm_tbs, 3),
+                                 "frac": round(hbm_tbs * 1e3 / HBM_PEAK_GBS, 4)},
+                         "binding": "hbm" if hbm_s > mfma_s else "mfma"},
             "stage_ms": {k: round(v[0] / n, 4) for k, v in prof.items()}}
 
 
