@@ -46,7 +46,7 @@ enum {
     GORILA_ERANGE = -2,        /* device saw an index or action out of range    */
     GORILA_EWORKSPACE = -3,    /* workspace too small for this call             */
     GORILA_EHIP = -4,          /* HIP runtime or launch error                   */
-    GORILA_EUNSUPPORTED = -5   /* valid request this build does not implement   */
+    GORILA_EUNSUPPORTED = -5   /* valid request the library does not implement */
 };
 
 enum { GORILA_F32 = 0, GORILA_BF16 = 1 };

@@ -300,7 +300,7 @@ const char* gorila_strerror(int code) {
         case GORILA_ERANGE: return "minibatch index or action out of range (seen on the device)";
         case GORILA_EWORKSPACE: return "workspace too small";
         case GORILA_EHIP: return "HIP runtime error";
-        case GORILA_EUNSUPPORTED: return "not supported by this build";
+        case GORILA_EUNSUPPORTED: return "not supported by this library";
         default: return "unknown error";
     }
 }

@@ -2,7 +2,7 @@
 
 The paper's input is the four most recent preprocessed frames (Section 5.1) and
 its replay memory stores (s, a, r, s') tuples (Section 4); the zero-fill across
-episode starts is this build's reading.  The 12-slot fixture was enumerated by
+episode starts is the reading taken here (the paper is silent).  The 12-slot fixture was enumerated by
 hand from that rule; the random-ring checks are invariants any correct gather
 satisfies.
 """
