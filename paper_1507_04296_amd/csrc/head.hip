@@ -135,67 +135,128 @@ void launch_act_head(const float* fc1part, int splits, const float* theta, int n
 // ell, coef and dz4, and rows 2gn .. 2gn+2n-1 of q (online, then target).
 // fc1part_online / fc1part_target + g * part_stride: [splits][n][512] for the
 // group's online network (on s) and the target network (on s').
+//
+// One workgroup of four waves per learner row, so the row's dependent memory
+// round trips overlap: every load that does not depend on h4 (the fc1 split
+// partials, this wave's W5 rows of both networks, the W5 row of the chosen
+// action) is issued before the first sum.  Waves 0-1 finish the online h4,
+// waves 2-3 the target's (four hidden units a thread) into LDS; wave w then
+// computes the Q values of actions w, w + 4, ... of both networks (lane l:
+// units 8l .. 8l + 7 of one W5 row, then the butterfly sum -- the same
+// arithmetic, in the same order, as one wave per row); every thread forms the
+// TD error from the Q values in LDS, and waves 0-1 write dz4.
+constexpr int TD_JB = 3;  // actions per wave whose W5 rows are loaded together (A <= 12: one round trip)
 __global__ __launch_bounds__(256) void td_head_kernel(
     const float* __restrict__ fc1part, const float* __restrict__ fc1part_t, int64_t part_stride,
     int splits, GroupPtrs thetas, const float* __restrict__ theta_t, int n, int A,
     const int32_t* __restrict__ a, const float* __restrict__ r, const uint8_t* __restrict__ term,
     float gamma, float clip, float* __restrict__ h4, float* __restrict__ q,
     float* __restrict__ ell, float* __restrict__ coef, float* __restrict__ dz4) {
-    const int lane = threadIdx.x & 63, bl = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (bl >= n) return;
-    const int grp = blockIdx.y;
+    __shared__ __attribute__((aligned(16))) float hs[2][HID];  // online, target h4
+    __shared__ float qv[2][MAX_ACTIONS];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int bl = blockIdx.x, grp = blockIdx.y;
     const float* theta = thetas.p[grp];
-    const int64_t ss = (int64_t)n * HID;
-    float h[8], ht[8];
-    finish_h4(fc1part + grp * part_stride + (int64_t)bl * HID, splits, ss, theta + OFF_B4, lane, h);
-    finish_h4(fc1part_t + grp * part_stride + (int64_t)bl * HID, splits, ss, theta_t + OFF_B4, lane,
-              ht);
     const int64_t b = (int64_t)grp * n + bl;  // learner row
-    q += (int64_t)grp * 2 * n * A;
-    float* h4row = h4 + b * HID + lane * 8;
-    *(f32x4*)h4row = f32x4{h[0], h[1], h[2], h[3]};
-    *(f32x4*)(h4row + 4) = f32x4{h[4], h[5], h[6], h[7]};
+    const int ab = a[b];
     const float* W5 = theta + OFF_W5;
     const float* b5 = theta + off_b5(A);
     const float* W5t = theta_t + OFF_W5;
     const float* b5t = theta_t + off_b5(A);
-    const int ab = a[b];
-    float q_sa = 0.0f, m = 0.0f;
-    for (int k0 = 0; k0 < A; k0 += HB) {
-        float qs[HB], qt[HB];
-        head_rows(h, W5, b5, k0, A, lane, qs);
-        head_rows(ht, W5t, b5t, k0, A, lane, qt);
+
+    // loads that do not depend on h4: this thread's network and units
+    const bool tgt = tid >= 128;
+    const int u = 4 * (tid & 127);
+    const int64_t ss = (int64_t)n * HID;
+    const float* pp = (tgt ? fc1part_t : fc1part) + grp * part_stride + (int64_t)bl * HID + u;
+    f32x4 pa[FC1_MAX_SPLITS];
 #pragma unroll
-        for (int j = 0; j < HB; ++j) {
-            const int k = k0 + j;
-            if (k >= A) break;
-            const float s = qs[j], st = qt[j];
-            if (lane == 0) {
-                q[(int64_t)bl * A + k] = s;
-                q[(int64_t)(n + bl) * A + k] = st;
-            }
-            if (k == ab) q_sa = s;
-            m = k == 0 ? st : fmaxf(m, st);  // max_a' Q(s', a'; theta-)
+    for (int s = 0; s < FC1_MAX_SPLITS; ++s)
+        if (s < splits) pa[s] = ld4(pp + s * ss);
+    const f32x4 bias = ld4((tgt ? theta_t : theta) + OFF_B4 + u);
+    const f32x4 wa = ld4(W5 + ab * HID + u);  // the chosen action's row (online units)
+    const int nk = (A - wave + 3) / 4;  // this wave's actions
+    f32x4 w0[TD_JB], w1[TD_JB], v0[TD_JB], v1[TD_JB];
+#pragma unroll
+    for (int j = 0; j < TD_JB; ++j) {
+        const int k = min(wave + 4 * j, A - 1);
+        w0[j] = ld4(W5 + k * HID + lane * 8);
+        w1[j] = ld4(W5 + k * HID + lane * 8 + 4);
+        v0[j] = ld4(W5t + k * HID + lane * 8);
+        v1[j] = ld4(W5t + k * HID + lane * 8 + 4);
+    }
+
+    // h4 = relu(b4 + sum of the split partials in split order)
+    f32x4 hv = pa[0];
+#pragma unroll
+    for (int s = 1; s < FC1_MAX_SPLITS; ++s)
+        if (s < splits) hv += pa[s];
+    hv = f32x4{fmaxf(hv[0] + bias[0], 0.f), fmaxf(hv[1] + bias[1], 0.f),
+               fmaxf(hv[2] + bias[2], 0.f), fmaxf(hv[3] + bias[3], 0.f)};
+    *(f32x4*)&hs[tgt][u] = hv;
+    if (!tgt) *(f32x4*)(h4 + b * HID + u) = hv;
+    __syncthreads();
+
+    // Q of this wave's actions for both networks
+    float h[8], hh[8];
+    {
+        const f32x4 x0 = *(const f32x4*)&hs[0][lane * 8], x1 = *(const f32x4*)&hs[0][lane * 8 + 4];
+        const f32x4 y0 = *(const f32x4*)&hs[1][lane * 8], y1 = *(const f32x4*)&hs[1][lane * 8 + 4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            h[e] = x0[e]; h[4 + e] = x1[e];
+            hh[e] = y0[e]; hh[4 + e] = y1[e];
         }
     }
+    q += (int64_t)grp * 2 * n * A;
+    for (int j0 = 0; j0 < nk; j0 += TD_JB) {
+        if (j0 > 0) {
+#pragma unroll
+            for (int j = 0; j < TD_JB; ++j) {
+                const int k = min(wave + 4 * (j0 + j), A - 1);
+                w0[j] = ld4(W5 + k * HID + lane * 8);
+                w1[j] = ld4(W5 + k * HID + lane * 8 + 4);
+                v0[j] = ld4(W5t + k * HID + lane * 8);
+                v1[j] = ld4(W5t + k * HID + lane * 8 + 4);
+            }
+        }
+        float so[TD_JB], st[TD_JB];
+#pragma unroll
+        for (int j = 0; j < TD_JB; ++j) {
+            so[j] = dot8(h, w0[j], w1[j]);
+            st[j] = dot8(hh, v0[j], v1[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < TD_JB; ++j) {
+            const int k = wave + 4 * (j0 + j);
+            const float qo = wave_sum(so[j]) + b5[min(k, A - 1)];
+            const float qt = wave_sum(st[j]) + b5t[min(k, A - 1)];
+            if (j0 + j < nk && lane == 0) {
+                qv[0][k] = qo;
+                qv[1][k] = qt;
+                q[(int64_t)bl * A + k] = qo;
+                q[(int64_t)(n + bl) * A + k] = qt;
+            }
+        }
+    }
+    __syncthreads();
+
+    // TD error, Huber loss and dLoss/dQ(s, a) (every thread, the same values)
+    float m = qv[1][0];
+    for (int k = 1; k < A; ++k) m = fmaxf(m, qv[1][k]);  // max_a' Q(s', a'; theta-)
+    const float q_sa = qv[0][ab];
     const float y = term[b] ? r[b] : r[b] + gamma * m;
     const float d = y - q_sa;
     const float ad = fabsf(d);
     const float g = fminf(fmaxf(d, -clip), clip);
     const float cf = -g / (float)n;  // d(mean loss)/dQ(s, a)
-    if (lane == 0) {
+    if (tid == 0) {
         ell[b] = ad <= clip ? 0.5f * d * d : clip * ad - 0.5f * clip * clip;
         coef[b] = cf;
     }
-    const float* w = W5 + ab * HID + lane * 8;
-    float* out = dz4 + b * HID + lane * 8;
-    const f32x4 w0 = ld4(w), w1 = ld4(w + 4);
-    const f32x4 o0 = {h[0] > 0.f ? cf * w0[0] : 0.f, h[1] > 0.f ? cf * w0[1] : 0.f,
-                      h[2] > 0.f ? cf * w0[2] : 0.f, h[3] > 0.f ? cf * w0[3] : 0.f};
-    const f32x4 o1 = {h[4] > 0.f ? cf * w1[0] : 0.f, h[5] > 0.f ? cf * w1[1] : 0.f,
-                      h[6] > 0.f ? cf * w1[2] : 0.f, h[7] > 0.f ? cf * w1[3] : 0.f};
-    *(f32x4*)out = o0;
-    *(f32x4*)(out + 4) = o1;
+    if (!tgt)
+        *(f32x4*)(dz4 + b * HID + u) = f32x4{hv[0] > 0.f ? cf * wa[0] : 0.f, hv[1] > 0.f ? cf * wa[1] : 0.f,
+                                             hv[2] > 0.f ? cf * wa[2] : 0.f, hv[3] > 0.f ? cf * wa[3] : 0.f};
 }
 
 void launch_td_head(const float* fc1part_online, const float* fc1part_target, int64_t part_stride,
@@ -204,7 +265,8 @@ void launch_td_head(const float* fc1part_online, const float* fc1part_target, in
                     float gamma, float clip, float* h4, float* q, float* ell, float* coef,
                     float* dz4, hipStream_t st) {
     if (n <= 0) return;
-    td_head_kernel<<<dim3((n + 3) / 4, groups), 256, 0, st>>>(
+    static_assert(4 * 128 == HID, "four hidden units a thread, two networks");
+    td_head_kernel<<<dim3(n, groups), 256, 0, st>>>(
         fc1part_online, fc1part_target, part_stride, splits, thetas, theta_target, n, A, a, r, term,
         gamma, clip, h4, q, ell, coef, dz4);
 }
