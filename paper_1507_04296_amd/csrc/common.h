@@ -227,7 +227,7 @@ struct GemmShape {
 // has not read those addresses before in the launch, so its L1 holds no
 // stale copy.  This needs no device-wide cache write-back or invalidation,
 // which would evict every other workgroup's operands from the L2.
-constexpr int SPLIT_MAX_TILES = 32, SPLIT_MAX_PIECES = 16, SPLIT_MAX_SLOTS = 512;
+constexpr int SPLIT_MAX_TILES = 128, SPLIT_MAX_PIECES = 16, SPLIT_MAX_SLOTS = 512;
 constexpr int SPLIT_TILE_FLOATS = 64 * 64;
 struct SplitPiece {
     float* ws = nullptr;
@@ -548,14 +548,14 @@ __device__ inline int xcd_tile(int bid, int padded) {
     return (bid % NUM_XCD) * (padded / NUM_XCD) + bid / NUM_XCD;
 }
 
-// Balancing the last tiles of a launch.  When a launch of T equal tiles puts
-// k tiles on every compute unit and r = T mod CUs more on a few of them, those
-// few run a whole tile longer than the rest.  A job's TailSplit keeps its
-// first `full` tiles whole (one XCD-mapped workgroup each) and runs its last
-// `tail` tiles as `pieces` reduction pieces each (SplitPiece), dispatched
-// after the whole tiles, so the extra work is spread thinly over many units.
-// (Splitting every tile of a small launch the same way measured slower at
-// batch 32: a workgroup's fixed latency, ~6 us, dominates its few chunks.)
+// Balancing a launch over the compute units.  When a launch of T equal tiles
+// puts k tiles on every compute unit and r = T mod CUs more on a few of them,
+// those few run a whole tile longer than the rest; when T is at most half the
+// unit count, most units idle while a few walk each tile's whole reduction.
+// A job's TailSplit keeps its first `full` tiles whole (one XCD-mapped
+// workgroup each) and runs its last `tail` tiles as `pieces` reduction pieces
+// each (SplitPiece), dispatched after the whole tiles, so that work is spread
+// over more units.
 // Tail tile s goes to XCD s % 8 with all of its pieces: tail block j runs on
 // XCD j % 8 and is that XCD's (j / 8)-th piece.  ws holds tail * pieces <=
 // SPLIT_MAX_SLOTS partial tiles of SPLIT_TILE_FLOATS floats, cnt one counter per
@@ -597,23 +597,34 @@ struct TailSplit {
     }
 };
 // The split for a job of job_tiles tiles of `chunks` chunks that closes a
-// launch of launch_tiles equal tiles on `cus` compute units: the r excess
-// tiles (r <= SPLIT_MAX_TILES, taken from this job) in up to 16 pieces of at
-// least two chunks, about one piece per unit.  Only when the whole tiles fit
-// in one round of four workgroups per unit (the residency of these GEMM
-// kernels), so that the pieces start alongside them: behind a full round
-// they would only start as whole tiles finish, which measured no faster.
+// launch of launch_tiles equal tiles on `cus` compute units, in pieces of at
+// least two chunks:
+//  - a small launch (at most half a tile per unit): every tile of the job in
+//    two pieces.  A workgroup costs ~5 us before its first chunk and after
+//    its last (per-workgroup timestamps at batch 32), and each further piece
+//    adds a round trip to the hand-off, so more pieces measured slower;
+//  - otherwise the r = launch_tiles mod cus excess tiles, taken from this
+//    job, in up to 16 pieces, about one per unit -- only when the whole tiles
+//    fit in one round of four workgroups per unit (the LDS residency of these
+//    GEMM kernels), so that the pieces start alongside them: behind a full
+//    round they would only start as whole tiles finish (measured no faster).
 inline TailSplit plan_split(float* ws, int* cnt, int cus, int launch_tiles, int job_tiles,
                             int chunks) {
     TailSplit ts;
     ts.ws = ws;
     ts.cnt = cnt;
-    if (!ws || !cnt || cus < 1 || launch_tiles < cus) return ts;
-    const int r = launch_tiles % cus;
-    if (r == 0 || r > job_tiles || launch_tiles - r > 4 * cus) return ts;
-    int p = SPLIT_MAX_PIECES;
+    if (!ws || !cnt || cus < 1 || launch_tiles < 1) return ts;
+    int r, p = SPLIT_MAX_PIECES;
     if (chunks / 2 < p) p = chunks / 2;
-    if (cus / r < p) p = cus / r;
+    if (2 * launch_tiles <= cus) {
+        r = job_tiles;
+        if (p > 2) p = 2;
+    } else {
+        if (launch_tiles < cus) return ts;
+        r = launch_tiles % cus;
+        if (r == 0 || r > job_tiles || launch_tiles - r > 4 * cus) return ts;
+        if (cus / r < p) p = cus / r;
+    }
     if (p < 2 || r > SPLIT_MAX_TILES || r * p > SPLIT_MAX_SLOTS) return ts;
     ts.full = job_tiles - r;
     ts.tail = r;

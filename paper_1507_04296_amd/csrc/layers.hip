@@ -149,9 +149,10 @@ struct Conv2FwdJob {
     }
 };
 
-// No TailSplit here: at batch 512 the whole tiles already fill every slot of
-// every compute unit (five per unit), so pieces could only start once whole
-// tiles finish, and measured no faster than the unsplit launch.
+// No TailSplit here: at batch 512 the 1296 whole tiles more than fill the
+// four LDS slots of every compute unit, so pieces could only start once whole
+// tiles finish, and measured no faster than the unsplit launch; at batch 32
+// two pieces a tile measured no faster either.
 void launch_conv2_fwd(const float* h1, const GroupPtrs& w2t, const GroupPtrs& theta, int groups,
                       int n, float* h2, bool bf16, hipStream_t st) {
     if (n <= 0) return;
