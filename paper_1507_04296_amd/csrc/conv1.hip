@@ -307,8 +307,10 @@ void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int groups
         return;
     }
     // splits per group: one round of two workgroups per CU, each over a
-    // contiguous range of units; groups * splits stays within max_splits
-    const int splits = max(1, min(n * C1W_UNITS, min(C1W_TARGET, max_splits) / groups));
+    // contiguous range of at least two units (at batch 32 one unit each left
+    // the final reduction 320 partials per element: 10 -> 8 us for it, +0.5
+    // here); groups * splits stays within max_splits
+    const int splits = max(1, min((n * C1W_UNITS + 1) / 2, min(C1W_TARGET, max_splits) / groups));
     *splits_out = splits;
     if (bf16)
         conv1_wgrad_mfma16_kernel<1><<<dim3(splits, groups), 256, 0, st>>>(dz1, ftab, n, partial, bias_part);
