@@ -220,9 +220,11 @@ struct GemmShape {
 // the epilogue and sets *cnt back to 0 for the next launch.  No piece waits
 // for another.
 //
-// All pieces of a tile run on one XCD (TailSplit places them so), whose L2 is
-// shared by its compute units and is where their vector stores land (the
-// per-unit L1 writes through).  A piece waits for its own stores to complete
+// All pieces of a tile run on one XCD (TailSplit places them so: workgroup
+// ids that agree mod 8 share an XCD whenever a partition dispatches
+// round-robin over 1, 2, 4 or 8 XCDs), whose L2 is shared by its compute
+// units and is where their vector stores land (the per-unit L1 writes
+// through).  A piece waits for its own stores to complete
 // before it counts, so the last piece finds every partial tile in that L2; it
 // has not read those addresses before in the launch, so its L1 holds no
 // stale copy.  This needs no device-wide cache write-back or invalidation,
