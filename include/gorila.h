@@ -115,11 +115,14 @@ size_t gorila_workspace_bytes(int32_t max_batch, int32_t n_actions, int32_t dtyp
 /* Bind a stream (hipStream_t, may be NULL for the null stream) and a device
  * workspace of ws_bytes (>= gorila_workspace_bytes(1,1,0,1), 256-byte
  * aligned) to a new context on the current device.  The context owns only
- * host bookkeeping; destroy it before freeing the workspace.  Creation
- * zeroes the workspace's first 1024 bytes (an error word and the counters of
- * split reductions, which every call leaves at zero) on the stream; the
- * caller must not write the workspace while the context lives, and calls on
- * one context must not overlap (one stream). */
+ * host bookkeeping; destroy it before freeing the workspace.  Creation runs
+ * one small kernel that records which XCD each of 256 workgroups runs on
+ * (split reductions are used only if ids equal mod 8 share one), waits for
+ * it (a stream synchronisation), then zeroes the workspace's first 1024 bytes
+ * (an error word and the counters of split reductions, which every call
+ * leaves at zero) on the stream; the caller must not write the workspace
+ * while the context lives, and calls on one context must not overlap (one
+ * stream). */
 int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_t ws_bytes);
 int gorila_ctx_destroy(gorila_ctx* ctx);
 /* Point the context at another stream (subsequent calls enqueue there). */

@@ -32,6 +32,7 @@ struct gorila_ctx {
     size_t ws_bytes;
     int device;
     int cus = 0;  // compute units of the device
+    bool split_ok = false;  // workgroup placement allows split reductions
     uint32_t timing_mask = 0;
     std::vector<TimingRecord> records;  // events created by timing_begin
     size_t used = 0;
@@ -125,7 +126,7 @@ T* at(gorila_ctx* c, size_t off) { return (T*)(c->ws + off); }
 SplitWs split_ws(gorila_ctx* c, const Plan& p) {
     SplitWs sw;
     sw.cus = c->cus;
-    sw.ws = at<float>(c, p.split);
+    sw.ws = c->split_ok ? at<float>(c, p.split) : nullptr;  // null: every tile whole
     sw.cnt = at<int>(c, p.err + SPLIT_CNT_OFFSET);
     return sw;
 }
@@ -242,6 +243,31 @@ size_t gorila_workspace_bytes(int32_t max_batch, int32_t n_actions, int32_t dtyp
     return make_plan(2 * B, B, n_actions, groups, widened).total;
 }
 
+// Thread 0 of workgroup b writes the XCD it runs on (hardware register
+// XCC_ID) to out[b].
+static __global__ __launch_bounds__(64) void xcd_probe_kernel(unsigned* out) {
+    if (threadIdx.x == 0) out[blockIdx.x] = __builtin_amdgcn_s_getreg((31 << 11) | 20) & 15u;
+}
+
+// The split reductions exchange partial tiles through one XCD's L2, so they
+// need every workgroup id to share an XCD with the ids equal to it mod 8
+// (round-robin dispatch over 1, 2, 4 or 8 XCDs).  Checked once per context on
+// WS_HEAD / 4 workgroups, using the workspace head as the record; where it
+// does not hold, every tile runs whole.
+static int probe_split_placement(gorila_ctx* c) {
+    constexpr int N = (int)(WS_HEAD / 4);
+    unsigned xcc[N];
+    xcd_probe_kernel<<<N, 64, 0, c->stream>>>((unsigned*)c->ws);
+    if (hipGetLastError() != hipSuccess) return GORILA_EHIP;
+    if (hipMemcpyAsync(xcc, c->ws, sizeof xcc, hipMemcpyDeviceToHost, c->stream) != hipSuccess ||
+        hipStreamSynchronize(c->stream) != hipSuccess)
+        return GORILA_EHIP;
+    c->split_ok = true;
+    for (int b = NUM_XCD; b < N; ++b)
+        if (xcc[b] != xcc[b % NUM_XCD]) c->split_ok = false;
+    return GORILA_OK;
+}
+
 int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_t ws_bytes) {
     if (!out || !workspace || !aligned16(workspace)) return GORILA_EINVAL;
     if (ws_bytes < make_plan(1, 1, 1).err + WS_HEAD) return GORILA_EWORKSPACE;
@@ -258,7 +284,8 @@ int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_
         c->cus = cus;
     }
     if (!c) return GORILA_EINVAL;
-    if (hipMemsetAsync(c->ws, 0, WS_HEAD, c->stream) != hipSuccess) {
+    const int rc = probe_split_placement(c);
+    if (rc != GORILA_OK || hipMemsetAsync(c->ws, 0, WS_HEAD, c->stream) != hipSuccess) {
         delete c;
         return GORILA_EHIP;
     }
