@@ -472,6 +472,9 @@ def main():
                     help="skip the one-million-frame ring gather / learner line")
     ap.add_argument("--no-ps", action="store_true",
                     help="skip the parameter-server apply / loss-filter line")
+    ap.add_argument("--only", choices=("actor", "grouped"), default=None,
+                    help="only run that companion measurement and print its object "
+                         "(profiles its kernels alone)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES bytes three times "
                          "(calibrates the HBM traffic counters)")
@@ -497,6 +500,14 @@ def main():
         print(json.dumps({"copy_probe_bytes": args.copy_probe}), flush=True)
         return
     g.lib()  # fails loudly if the HIP library is missing
+    if args.only == "actor":
+        print(json.dumps({"actor": run_actor(torch, g, datagen, max(args.steps, 20), args.warmup)}),
+              flush=True)
+        return
+    if args.only == "grouped":
+        print(json.dumps({"grouped": run_grouped(torch, g, datagen, max(args.steps // 2, 5),
+                                                 args.warmup)}), flush=True)
+        return
 
     B, A = args.batch, args.actions
     seed = datagen.SEED_BASE + 2

@@ -12,13 +12,15 @@
 using namespace gorila;
 
 namespace {
-// Stages of the calls, in launch order (bits of the timing mask).
+// Stages of the calls, in launch order (bits of the timing mask).  The
+// minibatch resolution (or a forward call's frame table) shares the prep
+// launch.
 enum Stage {
-    ST_RESOLVE, ST_PREP, ST_CONV1_FWD, ST_CONV2_FWD, ST_CONV3_FWD, ST_FC1_FWD, ST_HEAD,
+    ST_PREP, ST_CONV1_FWD, ST_CONV2_FWD, ST_CONV3_FWD, ST_FC1_FWD, ST_HEAD,
     ST_FC1_BWD, ST_CONV3_BWD, ST_CONV2_BWD, ST_CONV1_WGRAD, ST_GRAD_REDUCE, ST_COUNT
 };
 const char* const STAGE_NAMES[ST_COUNT] = {
-    "resolve", "prep_weights", "conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "head",
+    "prep_weights", "conv1_fwd", "conv2_fwd", "conv3_fwd", "fc1_fwd", "head",
     "fc1_bwd", "conv3_bwd", "conv2_bwd", "conv1_wgrad", "grad_reduce"};
 struct TimingRecord {
     int stage;
@@ -189,8 +191,16 @@ ReplayView view_of(const gorila_replay* rv) {
                       rv->head,     rv->action,   rv->reward};
 }
 
-// Frame table for a batch of stacked states (forward-only calls).
-__global__ void states_table_kernel(const uint8_t* states, int n, const uint8_t** ftab) {
+// Forward-only calls: the first tblocks workgroups write the frame table of
+// n stacked states, the other PREP_BLOCKS the weight transposes of one set
+// (independent, so one launch).
+__global__ __launch_bounds__(256) void states_prep_kernel(const uint8_t* states, int n,
+                                                          const uint8_t** ftab, WeightViews wv,
+                                                          int tblocks) {
+    if ((int)blockIdx.x >= tblocks) {
+        prep_weights_part(wv, blockIdx.x - tblocks, PREP_BLOCKS);
+        return;
+    }
     const int e = blockIdx.x * blockDim.x + threadIdx.x;
     if (e < n * 4) ftab[e] = states + (int64_t)(e >> 2) * STATE_BYTES + (int64_t)(e & 3) * FRAME_BYTES;
 }
@@ -201,7 +211,6 @@ int forward_one(gorila_ctx* c, const Plan& p, const gorila_params* prm, const ui
                 int n, const float** theta32, int* fc1_splits) {
     hipStream_t st = c->stream;
     const uint8_t** ftab = at<const uint8_t*>(c, p.ftab);
-    { StageTimer t(c, ST_RESOLVE); states_table_kernel<<<(n * 4 + 255) / 256, 256, 0, st>>>(states, n, ftab); }
     WidenSet ws{};
     int n_widen = 0;
     const float* theta = fp32_params(c, p, prm, ws, n_widen);
@@ -210,7 +219,8 @@ int forward_one(gorila_ctx* c, const Plan& p, const gorila_params* prm, const ui
     {
         StageTimer t(c, ST_PREP);
         if (n_widen) launch_widen_bf16(ws, n_widen, param_count(prm->n_actions), st);
-        launch_prep_weights(&wv, 1, st);
+        const int tblocks = (n * 4 + 255) / 256;
+        states_prep_kernel<<<tblocks + PREP_BLOCKS, 256, 0, st>>>(states, n, ftab, wv, tblocks);
     }
     GroupPtrs th{}, w2t{}, w3t{};
     th.p[0] = theta;
@@ -511,11 +521,8 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
         launch_resolve_prep(view_of(replay), idx, B, A, ftab, a, r, term,
                             at<unsigned>(ctx, p.err), wv, G + 1, st);
     } else {
-        {
-            StageTimer t(ctx, ST_RESOLVE);
-            launch_resolve(view_of(replay), idx, B, A, ftab, a, r, term, at<unsigned>(ctx, p.err),
-                           st);
-        }
+        // widened sets: the transposes read the widened copies, so the shared
+        // resolve + transpose launch follows the widening
         StageTimer t(ctx, ST_PREP);
         if (bf16) {
             launch_widen_bf16(widen, n_widen, OFF_W4, st);
@@ -528,7 +535,8 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
         } else {
             launch_widen_bf16(widen, n_widen, P, st);
         }
-        launch_prep_weights(wv, G + 1, st);
+        launch_resolve_prep(view_of(replay), idx, B, A, ftab, a, r, term,
+                            at<unsigned>(ctx, p.err), wv, G + 1, st);
     }
     // forward groups 0 .. G-1: online nets on s; G .. 2G-1: the target on s'
     GroupPtrs th{}, w2t{}, w3t{};

@@ -23,11 +23,6 @@ struct ReplayView {
     const float* reward;
 };
 
-// Resolve minibatch indices: frame pointers ftab[2][n][4] (s then s'; null =
-// zero-filled channel), a/r/term per row, optional frame map [n][2][4].
-void launch_resolve(const ReplayView& rv, const int64_t* idx, int n, int n_actions,
-                    const uint8_t** ftab, int32_t* a, float* r, uint8_t* term, unsigned* err,
-                    hipStream_t st);
 
 // Materialising gather: s_out / s2_out [n][4][84][84], frame_map [n][2][4]
 // (may be null), a, r, term, in one launch (one workgroup per transition).
@@ -92,8 +87,10 @@ __device__ inline void prep_weights_part(const WeightViews& v, int blk, int nblk
     }
 }
 
-// launch_resolve and launch_prep_weights in one launch (they are independent):
-// the first blocks resolve the minibatch, the rest transpose the weights.
+// Minibatch resolution and the weight transposes in one launch (they are
+// independent): the first blocks resolve the indices into frame pointers
+// ftab[2][n][4] (s then s'; null = zero-filled channel) and a/r/term per row,
+// the rest do launch_prep_weights's work.
 void launch_resolve_prep(const ReplayView& rv, const int64_t* idx, int n, int n_actions,
                          const uint8_t** ftab, int32_t* a, float* r, uint8_t* term,
                          unsigned* err, const WeightViews* nets, int n_nets, hipStream_t st);

@@ -101,30 +101,6 @@ __device__ Resolved resolve_one(const ReplayView& rv, int64_t k, int n_actions,
     return o;
 }
 
-__global__ __launch_bounds__(256) void resolve_kernel(ReplayView rv, const int64_t* __restrict__ idx,
-                                                      int n, int n_actions,
-                                                      const uint8_t** __restrict__ ftab,
-                                                      int32_t* __restrict__ a_out,
-                                                      float* __restrict__ r_out,
-                                                      uint8_t* __restrict__ term_out,
-                                                      unsigned* __restrict__ err) {
-    const int b = blockIdx.x * blockDim.x + threadIdx.x;
-    if (b >= n) return;
-    const Resolved o = resolve_one(rv, idx[b], n_actions, err);
-    for (int w = 0; w < 2; ++w)
-        for (int c = 0; c < 4; ++c) ftab[((int64_t)w * n + b) * 4 + c] = o.ptr[w][c];
-    a_out[b] = o.act;
-    r_out[b] = o.rew;
-    term_out[b] = o.term;
-}
-
-void launch_resolve(const ReplayView& rv, const int64_t* idx, int n, int n_actions,
-                    const uint8_t** ftab, int32_t* a, float* r, uint8_t* term, unsigned* err,
-                    hipStream_t st) {
-    if (n <= 0) return;
-    resolve_kernel<<<(n + 255) / 256, 256, 0, st>>>(rv, idx, n, n_actions, ftab, a, r, term, err);
-}
-
 __global__ __launch_bounds__(256) void resolve_prep_kernel(
     ReplayView rv, const int64_t* __restrict__ idx, int n, int n_actions,
     const uint8_t** __restrict__ ftab, int32_t* __restrict__ a_out, float* __restrict__ r_out,
