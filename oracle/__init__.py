@@ -97,7 +97,7 @@ def lib() -> ctypes.CDLL:
                                  ctypes.c_uint64, i32p, dp]
         L.oracle_learner_step.argtypes = [
             net_p, dp, dp, u8p, u8p, i32p, dp, u8p, ctypes.c_int32,
-            ctypes.c_double, ctypes.c_double, dp, dp, dp, dp, dp]
+            ctypes.c_double, ctypes.c_double, dp, dp, dp, dp, dp, dp]
         L.oracle_gather.argtypes = [
             u8p, u8p, i32p, f32p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32,
             ctypes.c_int64, i64p, ctypes.c_int32, u8p, u8p, i64p, i32p, f32p, u8p]
@@ -188,9 +188,11 @@ def learner_step(net: Net, theta, theta_target, s, s2, a, r, term, gamma: float,
                  clip: float = 1.0):
     """DQN loss (eq. (1)) and its gradient (eq. (2)) on one minibatch.
 
-    Returns dict(grads [P] f64, loss f64, q [B,A], q2 [B,A], margin [B]).
-    margin is each sample's smallest ReLU kink margin over the online network
-    (min |z| / (|b| + sum |w||x|)).  gamma, r and clip are float32 values
+    Returns dict(grads [P] f64, loss f64, q [B,A], q2 [B,A], margin [B],
+    max_q2 [B], y [B], delta [B], ell [B]).  margin is each sample's smallest
+    ReLU kink margin over the online network (min |z| / (|b| + sum |w||x|));
+    max_q2, y, delta and ell are the per-sample pieces of Algorithm 1's target
+    and eq. (1)'s error (max_a' Q(s',a';theta-), y, y - Q(s,a;theta), Huber).  gamma, r and clip are float32 values
     promoted exactly to fp64 (clip may be +inf)."""
     theta = _c(theta, np.float64)
     theta_target = _c(theta_target, np.float64)
@@ -206,12 +208,14 @@ def learner_step(net: Net, theta, theta_target, s, s2, a, r, term, gamma: float,
     q = np.zeros((B, net.n_actions), np.float64)
     q2 = np.zeros((B, net.n_actions), np.float64)
     margin = np.zeros(B, np.float64)
+    td = np.zeros((B, 4), np.float64)
     _check(lib().oracle_learner_step(
         ctypes.byref(net.c()), _ptr(theta), _ptr(theta_target), _ptr(s), _ptr(s2),
         _ptr(a), _ptr(r), _ptr(term), B, float(np.float32(gamma)),
         float(np.float32(clip)), _ptr(grads), _ptr(loss), _ptr(q), _ptr(q2),
-        _ptr(margin)), "learner_step")
-    return dict(grads=grads, loss=float(loss[0]), q=q, q2=q2, margin=margin)
+        _ptr(margin), _ptr(td)), "learner_step")
+    return dict(grads=grads, loss=float(loss[0]), q=q, q2=q2, margin=margin, max_q2=td[:, 0],
+                y=td[:, 1], delta=td[:, 2], ell=td[:, 3])
 
 
 def gather(frames, ep_start, action, reward, head: int, idx, hist: int = 4):

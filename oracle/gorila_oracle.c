@@ -448,7 +448,8 @@ int oracle_learner_step(const oracle_net* net, const double* theta,
                         const uint8_t* s2, const int32_t* a, const double* r,
                         const uint8_t* term, int32_t B, double gamma,
                         double clip, double* grads_out, double* loss_out,
-                        double* q_out, double* q2_out, double* margin_out) {
+                        double* q_out, double* q2_out, double* margin_out,
+                        double* td_out) {
     layout L;
     if (make_layout(net, &L) || !theta || !theta_target || !s || !s2 || !a ||
         !r || !term || B <= 0 || !grads_out || !loss_out || !(clip > 0.0))
@@ -509,6 +510,12 @@ int oracle_learner_step(const oracle_net* net, const double* theta,
             for (int k = 0; k < A; ++k) q_out[(int64_t)b * A + k] = S[b].q[k];
         if (q2_out)
             for (int k = 0; k < A; ++k) q2_out[(int64_t)b * A + k] = T.q[k];
+        if (td_out) {
+            td_out[(int64_t)b * 4 + 0] = m;
+            td_out[(int64_t)b * 4 + 1] = y;
+            td_out[(int64_t)b * 4 + 2] = delta;
+            td_out[(int64_t)b * 4 + 3] = ell[b];
+        }
     }
 
     double loss = 0.0;

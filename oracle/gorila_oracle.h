@@ -74,13 +74,17 @@ int oracle_act(const oracle_net* net, const double* theta,
  * q_out / q2_out [B, A] (may be NULL) receive Q(s;theta), Q(s';theta-).
  * margin_out [B] (may be NULL) receives each sample's smallest ReLU kink
  * margin over the online network: min |z| / (|b| + sum |w||x|) over every
- * hidden pre-activation z (units whose terms are all zero are skipped). */
+ * hidden pre-activation z (units whose terms are all zero are skipped).
+ * td_out [B, 4] (may be NULL) receives, per sample, max_a' Q(s', a'; theta-),
+ * the TD target y, the TD error delta = y - Q(s, a; theta) and its Huber
+ * loss (Algorithm 1, eq. (1)). */
 int oracle_learner_step(const oracle_net* net, const double* theta,
                         const double* theta_target, const uint8_t* s,
                         const uint8_t* s2, const int32_t* a, const double* r,
                         const uint8_t* term, int32_t B, double gamma,
                         double clip, double* grads_out, double* loss_out,
-                        double* q_out, double* q2_out, double* margin_out);
+                        double* q_out, double* q2_out, double* margin_out,
+                        double* td_out);
 
 /* Replay gather: for logical positions idx[n] build s = stack(k) and
  * s' = stack(k+1) (each hist frames of frame_bytes bytes, oldest first),

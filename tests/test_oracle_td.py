@@ -50,8 +50,14 @@ def test_bias_only_network_closed_form(oracle_mod, full):
     for b in range(B):
         y = float(r[b]) if term[b] else float(r[b]) + g * m
         d = y - v[a[b]]
-        loss += 0.5 * d * d if abs(d) <= clip else clip * abs(d) - 0.5 * clip * clip
+        ell = 0.5 * d * d if abs(d) <= clip else clip * abs(d) - 0.5 * clip * clip
+        loss += ell
         db5[a[b]] -= max(-clip, min(clip, d)) / B
+        # the per-sample pieces the oracle reports
+        assert out["max_q2"][b] == m
+        assert out["y"][b] == pytest.approx(y, rel=1e-15, abs=1e-15)
+        assert out["delta"][b] == pytest.approx(d, rel=1e-14, abs=1e-15)
+        assert out["ell"][b] == pytest.approx(ell, rel=1e-14, abs=1e-15)
     assert out["loss"] == pytest.approx(loss / B, rel=1e-14)
     np.testing.assert_allclose(out["grads"][off[9]:off[10]], db5, rtol=1e-14, atol=1e-16)
     assert not out["grads"][:off[9]].any()
@@ -74,6 +80,8 @@ def test_huber_values(oracle_mod, r, clip, loss, coef):
                                   0.99, clip)
     # terminal: y = r (the target net's 7.0 must not leak in), delta = r - 0
     assert out["loss"] == loss
+    assert out["y"][0] == r and out["delta"][0] == r and out["ell"][0] == loss
+    assert out["max_q2"][0] == 7.0
     assert out["grads"][off[9] + 1] == coef
     assert out["grads"][off[9]] == 0 and out["grads"][off[9] + 2] == 0
 
