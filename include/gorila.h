@@ -67,22 +67,25 @@ typedef struct {
  * STACKED: `rows` whole transitions; a minibatch index k in [0, rows) names
  *   s = s[k] and s' = s2[k] (uint8 [rows,4,84,84]), action[k], reward[k] and
  *   term[k] (nonzero = s' is terminal).
- * RING: a ring of `capacity` single uint8 84x84 frames; `head` is the slot of
- *   the oldest frame and logical position k lives in slot
- *   (head + k) mod capacity.  With rows = R > 1 the arrays hold R rings of
+ * RING: a ring of `capacity` single uint8 84x84 frames holding `size`
+ *   frames (0 .. capacity; capacity once the ring has wrapped); `head` is the
+ *   slot of the oldest frame and logical position k (0 <= k < size) lives in
+ *   slot (head + k) mod capacity.  With rows = R > 1 the arrays hold R rings of
  *   `capacity` slots each ([R][capacity] layout, one ring per actor of
  *   Section 4's bundled mode, filled in lockstep so they share `head`), and a
  *   minibatch index r * capacity + k names logical position k of ring r;
  *   rows 0 or 1 is a single ring.  Frame maps then report global slots
  *   r * capacity + slot.  ep_start[slot] != 0 marks the first frame of an
  *   episode; logical 0 also counts as one.  A minibatch index is a logical
- *   position k in [0, capacity-2]: s is the stack of frames k-3 .. k and s'
+ *   position k in [0, size-2]: s is the stack of frames k-3 .. k and s'
  *   of frames k-2 .. k+1 (oldest first), where any frame before the latest
  *   episode start at or before the stack's newest frame is all zeros (the
  *   paper concatenates the four most recent frames, Section 5.1; zero-fill at
  *   episode starts is this library's reading).  The transition's action and
  *   reward are action[slot(k)], reward[slot(k)]; it is terminal iff k+1
- *   starts an episode.  s, s2 and term are unused. */
+ *   starts an episode.  s, s2 and term are unused.  An index past size-2
+ *   (a slot not yet written) is out of range (GORILA_ERANGE).
+ * `reserved` is padding (set it to 0). */
 typedef struct {
     int32_t kind;
     int32_t reserved;
@@ -94,6 +97,7 @@ typedef struct {
     const uint8_t* ep_start;
     int64_t capacity;
     int64_t head;
+    int64_t size;            /* RING: frames stored per ring, 0 .. capacity */
     const int32_t* action;   /* [rows] or [capacity] */
     const float* reward;     /* [rows] or [capacity] */
 } gorila_replay;
@@ -205,6 +209,19 @@ int gorila_learner_step_grouped(const gorila_params* params, int32_t groups,
                                 const gorila_params* target_params, const gorila_replay* replay,
                                 const int64_t* idx, int32_t batch, float gamma, float clip_delta,
                                 float* grads_out, float* loss_out, gorila_ctx* ctx);
+
+/* Per-transition values of the most recent learner call on this context
+ * (gorila_learner_step or _grouped; Algorithm 1's target and eq. (1)'s
+ * error), in that call's row order (group g's rows g*batch .. g*batch+batch-1):
+ *   q_out      [rows, A] fp32: Q(s; theta) of the learner's parameters,
+ *   q_next_out [rows, A] fp32: Q(s'; theta-),
+ *   td_out     [rows, 4] fp32: max_a' Q(s', a'; theta-), the target y, the
+ *              TD error delta = y - Q(s, a; theta) and its Huber loss,
+ * with rows = groups * batch.  Any output may be NULL.  The values live in the
+ * context's workspace until a forward or act call reuses it: GORILA_EINVAL
+ * if no learner call has run since the context was made or since such a
+ * call.  Enqueued on the context's stream (device-to-device copies). */
+int gorila_learner_td(gorila_ctx* ctx, float* q_out, float* q_next_out, float* td_out);
 
 /* ---- Actor side (Algorithm 1, Section 4 actors and replay memory, Section 5.1) ---- */
 

@@ -32,7 +32,7 @@ EXPORTS = (
     "gorila_q_forward", "gorila_act", "gorila_learner_step", "gorila_learner_step_grouped",
     "gorila_ctx_timing_begin", "gorila_ctx_timing_end", "gorila_stage_name",
     "gorila_loss_filter", "gorila_ps_apply", "gorila_replay_insert", "gorila_epsilon",
-    "gorila_params_sync",
+    "gorila_params_sync", "gorila_learner_td",
 )
 
 
@@ -51,7 +51,7 @@ class _Replay(ctypes.Structure):
                 ("s", ctypes.c_void_p), ("s2", ctypes.c_void_p), ("term", ctypes.c_void_p),
                 ("rows", ctypes.c_int64), ("frames", ctypes.c_void_p),
                 ("ep_start", ctypes.c_void_p), ("capacity", ctypes.c_int64),
-                ("head", ctypes.c_int64), ("action", ctypes.c_void_p),
+                ("head", ctypes.c_int64), ("size", ctypes.c_int64), ("action", ctypes.c_void_p),
                 ("reward", ctypes.c_void_p)]
 
 
@@ -94,6 +94,7 @@ def lib() -> ctypes.CDLL:
         "gorila_params_sync": (ctypes.c_int, [vp, vp, i64, i32, i32, vp, vp, i64, vp, vp]),
         "gorila_ps_apply": (ctypes.c_int, [vp, vp, i64, vp, i32, vp, vp, vp, i64, f32, f32, vp,
                                            vp]),
+        "gorila_learner_td": (ctypes.c_int, [vp, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -222,32 +223,35 @@ class Replay:
     ep_start: object = None
     head: int = 0
     rings: int = 1
+    size: int | None = None  # RING: frames stored per ring (None: full)
 
     @staticmethod
     def stacked(s, s2, action, reward, term) -> "Replay":
         return Replay(REPLAY_STACKED, action, reward, s=s, s2=s2, term=term)
 
     @staticmethod
-    def ring(frames, ep_start, action, reward, head: int) -> "Replay":
-        """One ring: frames [capacity, 84, 84]."""
-        return Replay(REPLAY_RING, action, reward, frames=frames, ep_start=ep_start, head=head)
+    def ring(frames, ep_start, action, reward, head: int, size: int | None = None) -> "Replay":
+        """One ring: frames [capacity, 84, 84] holding `size` frames (default: full)."""
+        return Replay(REPLAY_RING, action, reward, frames=frames, ep_start=ep_start, head=head,
+                      size=size)
 
     @staticmethod
-    def rings_of(frames, ep_start, action, reward, head: int) -> "Replay":
+    def rings_of(frames, ep_start, action, reward, head: int, size: int | None = None) -> "Replay":
         """R rings filled in lockstep: frames [R, capacity, 84, 84], the others [R, capacity];
         minibatch index r * capacity + k is logical position k of ring r."""
         return Replay(REPLAY_RING, action, reward, frames=frames, ep_start=ep_start, head=head,
-                      rings=frames.shape[0])
+                      rings=frames.shape[0], size=size)
 
     def c(self) -> _Replay:
         if self.kind == REPLAY_RING:
             rows = self.rings if self.rings > 1 else 0
             cap = self.frames.shape[1] if self.rings > 1 else self.frames.shape[0]
+            size = cap if self.size is None else int(self.size)
         else:
             rows = self.s.shape[0] if self.s is not None else 0
-            cap = 0
+            cap = size = 0
         return _Replay(self.kind, 0, _ptr(self.s), _ptr(self.s2), _ptr(self.term), rows,
-                       _ptr(self.frames), _ptr(self.ep_start), cap, int(self.head),
+                       _ptr(self.frames), _ptr(self.ep_start), cap, int(self.head), size,
                        _ptr(self.action), _ptr(self.reward))
 
 
@@ -294,6 +298,23 @@ def gorila_learner_step_grouped(ctx: Context, thetas, theta_target, n_actions: i
            "gorila_learner_step_grouped")
 
 
+def gorila_learner_td(ctx: Context, q_out=None, q_next_out=None, td_out=None) -> None:
+    """Per-row Q(s), Q(s'), and (max Q(s'), y, delta, Huber) of the last learner call."""
+    _check(lib().gorila_learner_td(ctx.bind_stream(), _ptr(q_out), _ptr(q_next_out), _ptr(td_out)),
+           "gorila_learner_td")
+
+
+def learner_td(ctx: Context, rows: int, n_actions: int, device=None):
+    """Allocating wrapper of gorila_learner_td: (q [rows, A], q_next [rows, A], td [rows, 4])."""
+    import torch
+    dev = ctx.device if device is None else device
+    q = torch.empty((rows, n_actions), dtype=torch.float32, device=dev)
+    qn = torch.empty_like(q)
+    td = torch.empty((rows, 4), dtype=torch.float32, device=dev)
+    gorila_learner_td(ctx, q, qn, td)
+    return q, qn, td
+
+
 def gorila_loss_filter(ctx: Context, stats, loss, alpha: float, k: float, warmup: int,
                        keep_out) -> None:
     """stats: float64 [G, 3] device tensor (updated in place); loss [G] fp32."""
@@ -329,8 +350,9 @@ class RingSet:
     def replay(self) -> Replay:
         if self.rings == 1:
             return Replay.ring(self.frames[0], self.ep_start[0], self.action[0], self.reward[0],
-                               self.head)
-        return Replay.rings_of(self.frames, self.ep_start, self.action, self.reward, self.head)
+                               self.head, self.size)
+        return Replay.rings_of(self.frames, self.ep_start, self.action, self.reward, self.head,
+                               self.size)
 
 
 def gorila_replay_insert(ctx: Context, rs: RingSet, frames_in, ep_in, act_in, rew_in) -> None:

@@ -38,6 +38,12 @@ struct gorila_ctx {
     uint32_t timing_mask = 0;
     std::vector<TimingRecord> records;  // events created by timing_begin
     size_t used = 0;
+    // Where the most recent learner call left its per-row TD values (q of
+    // both networks, td rows); valid until a forward or act call reuses the
+    // workspace.
+    bool td_valid = false;
+    int td_b = 0, td_groups = 0, td_actions = 0;
+    size_t td_q = 0, td_rows = 0;
 };
 
 namespace {
@@ -71,7 +77,7 @@ struct Plan {
     size_t err, ftab, a, r, term;
     size_t theta32, theta32_stride;
     size_t w2t, w3t, w3d, w2p;  // bases of per-set arrays (stride W2T_BYTES / W3T_BYTES)
-    size_t h1, h2, h3, h4, q, ell, coef;
+    size_t h1, h2, h3, h4, q, ell, coef, td;
     size_t dz4, dz3, dz2, dz1;
     size_t fc1part, part1, part2, part3, bpart, hpart;
     size_t split;  // TailSplit partial tiles
@@ -108,6 +114,7 @@ Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online = 1, int wi
     p.fc1part = take(4 * (size_t)F * HID * FC1_MAX_SPLITS);
     p.ell = take(4 * (size_t)B);
     p.coef = take(4 * (size_t)B);
+    p.td = take(16 * (size_t)B);
     p.dz4 = take(4 * (size_t)B * HID);
     p.dz3 = take(4 * (size_t)bwd_split_rows(B) * FLAT);  // bwd_parts(B) partial planes
     p.dz2 = take(4 * (size_t)bwd_split_rows(B) * P2 * C2);
@@ -180,6 +187,7 @@ int check_replay(const gorila_replay* rv) {
     if (rv->kind == GORILA_REPLAY_RING) {
         if (!rv->frames || !rv->ep_start || rv->capacity < 2 || rv->rows < 0) return GORILA_EINVAL;
         if (rv->head < 0 || rv->head >= rv->capacity || !aligned16(rv->frames)) return GORILA_EINVAL;
+        if (rv->size < 0 || rv->size > rv->capacity) return GORILA_EINVAL;
         return GORILA_OK;
     }
     return GORILA_EINVAL;
@@ -188,7 +196,7 @@ int check_replay(const gorila_replay* rv) {
 ReplayView view_of(const gorila_replay* rv) {
     return ReplayView{rv->kind,     rv->s,        rv->s2,       rv->term,
                       rv->rows,     rv->frames,   rv->ep_start, rv->capacity,
-                      rv->head,     rv->action,   rv->reward};
+                      rv->head,     rv->size,     rv->action,   rv->reward};
 }
 
 // Forward-only calls: the first tblocks workgroups write the frame table of
@@ -210,6 +218,7 @@ __global__ __launch_bounds__(256) void states_prep_kernel(const uint8_t* states,
 int forward_one(gorila_ctx* c, const Plan& p, const gorila_params* prm, const uint8_t* states,
                 int n, const float** theta32, int* fc1_splits) {
     hipStream_t st = c->stream;
+    c->td_valid = false;  // the forward rows overwrite a learner call's q
     const uint8_t** ftab = at<const uint8_t*>(c, p.ftab);
     WidenSet ws{};
     int n_widen = 0;
@@ -578,8 +587,14 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
     {
         StageTimer t(ctx, ST_HEAD);
         launch_td_head(fc1part, fc1part + G * part_stride, part_stride, S, on, G, theta_t, b, A, a,
-                       r, term, gamma, clip_delta, h4, q, ell, coef, dz4, st);
+                       r, term, gamma, clip_delta, h4, q, ell, coef, at<float>(ctx, p.td), dz4, st);
     }
+    ctx->td_valid = true;
+    ctx->td_b = b;
+    ctx->td_groups = G;
+    ctx->td_actions = A;
+    ctx->td_q = p.q;
+    ctx->td_rows = p.td;
     int head_blocks = 0, s1 = 0, s2 = 0, s3 = 0;
     const int kp = bwd_parts(B);
     {
@@ -630,6 +645,26 @@ int gorila_learner_step_grouped(const gorila_params* params, int32_t groups,
                                 float* grads_out, float* loss_out, gorila_ctx* ctx) {
     return learner_steps(ctx, params, groups, true, target_params, replay, idx, batch, gamma,
                          clip_delta, grads_out, loss_out);
+}
+
+int gorila_learner_td(gorila_ctx* ctx, float* q_out, float* q_next_out, float* td_out) {
+    int rc = check_ctx(ctx);
+    if (rc) return rc;
+    if (!ctx->td_valid) return GORILA_EINVAL;
+    const size_t b = (size_t)ctx->td_b, G = (size_t)ctx->td_groups, A = (size_t)ctx->td_actions;
+    const size_t row = b * A * sizeof(float);  // one group's Q block of one network
+    // q region: [group][online, target][b][A]
+    const char* q = ctx->ws + ctx->td_q;
+    if (q_out && hipMemcpy2DAsync(q_out, row, q, 2 * row, row, G, hipMemcpyDeviceToDevice,
+                                  ctx->stream) != hipSuccess)
+        return GORILA_EHIP;
+    if (q_next_out && hipMemcpy2DAsync(q_next_out, row, q + row, 2 * row, row, G,
+                                       hipMemcpyDeviceToDevice, ctx->stream) != hipSuccess)
+        return GORILA_EHIP;
+    if (td_out && hipMemcpyAsync(td_out, ctx->ws + ctx->td_rows, 16 * b * G,
+                                 hipMemcpyDeviceToDevice, ctx->stream) != hipSuccess)
+        return GORILA_EHIP;
+    return GORILA_OK;
 }
 
 int gorila_replay_insert(uint8_t* frames, uint8_t* ep_start, int32_t* action, float* reward,

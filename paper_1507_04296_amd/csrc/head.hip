@@ -151,7 +151,8 @@ __global__ __launch_bounds__(256) void td_head_kernel(
     int splits, GroupPtrs thetas, const float* __restrict__ theta_t, int n, int A,
     const int32_t* __restrict__ a, const float* __restrict__ r, const uint8_t* __restrict__ term,
     float gamma, float clip, float* __restrict__ h4, float* __restrict__ q,
-    float* __restrict__ ell, float* __restrict__ coef, float* __restrict__ dz4) {
+    float* __restrict__ ell, float* __restrict__ coef, float* __restrict__ td,
+    float* __restrict__ dz4) {
     __shared__ __attribute__((aligned(16))) float hs[2][HID];  // online, target h4
     __shared__ float qv[2][MAX_ACTIONS];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -251,8 +252,10 @@ __global__ __launch_bounds__(256) void td_head_kernel(
     const float g = fminf(fmaxf(d, -clip), clip);
     const float cf = -g / (float)n;  // d(mean loss)/dQ(s, a)
     if (tid == 0) {
-        ell[b] = ad <= clip ? 0.5f * d * d : clip * ad - 0.5f * clip * clip;
+        const float l = ad <= clip ? 0.5f * d * d : clip * ad - 0.5f * clip * clip;
+        ell[b] = l;
         coef[b] = cf;
+        *(f32x4*)(td + 4 * b) = f32x4{m, y, d, l};
     }
     if (!tgt)
         *(f32x4*)(dz4 + b * HID + u) = f32x4{hv[0] > 0.f ? cf * wa[0] : 0.f, hv[1] > 0.f ? cf * wa[1] : 0.f,
@@ -263,12 +266,12 @@ void launch_td_head(const float* fc1part_online, const float* fc1part_target, in
                     int splits, const GroupPtrs& thetas, int groups, const float* theta_target,
                     int n, int A, const int32_t* a, const float* r, const uint8_t* term,
                     float gamma, float clip, float* h4, float* q, float* ell, float* coef,
-                    float* dz4, hipStream_t st) {
+                    float* td, float* dz4, hipStream_t st) {
     if (n <= 0) return;
     static_assert(4 * 128 == HID, "four hidden units a thread, two networks");
     td_head_kernel<<<dim3(n, groups), 256, 0, st>>>(
         fc1part_online, fc1part_target, part_stride, splits, thetas, theta_target, n, A, a, r, term,
-        gamma, clip, h4, q, ell, coef, dz4);
+        gamma, clip, h4, q, ell, coef, td, dz4);
 }
 
 }  // namespace gorila

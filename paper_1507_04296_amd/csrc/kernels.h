@@ -19,6 +19,7 @@ struct ReplayView {
     const uint8_t* ep_start;
     int64_t capacity;
     int64_t head;
+    int64_t size;  // RING: frames stored per ring (valid indices 0 .. size-2)
     const int32_t* action;
     const float* reward;
 };
@@ -132,7 +133,8 @@ void launch_q_head(const float* fc1part, int splits, const float* theta, int n, 
                    hipStream_t st);
 void launch_act_head(const float* fc1part, int splits, const float* theta, int n, int A, float eps,
                      uint64_t seed, int32_t* actions, float* q_out, hipStream_t st);
-// Writes h4 (online rows), q [2n][A], ell, coef = dLoss/dQ(s,a) and dz4.
+// Writes h4 (online rows), q [2n][A], ell, coef = dLoss/dQ(s,a), td [n][4] =
+// (max_a' Q(s',a'), y, delta, ell) per learner row, and dz4.
 // `groups` learner groups of n rows each (group g: rows g*n .. g*n+n-1, online
 // parameters thetas.p[g]); fc1part_online / fc1part_target + g * part_stride
 // each hold [splits][n][512] for group g.
@@ -140,7 +142,7 @@ void launch_td_head(const float* fc1part_online, const float* fc1part_target, in
                     int splits, const GroupPtrs& thetas, int groups, const float* theta_target,
                     int n, int A, const int32_t* a, const float* r, const uint8_t* term,
                     float gamma, float clip, float* h4, float* q, float* ell, float* coef,
-                    float* dz4, hipStream_t st);
+                    float* td, float* dz4, hipStream_t st);
 
 // Backward of `groups` learner groups of n rows each (group g: rows
 // g*n .. g*n+n-1 of every per-sample tensor, parameters of set g), three

@@ -61,7 +61,7 @@ __device__ Resolved resolve_one(const ReplayView& rv, int64_t k, int n_actions,
         const int64_t r = rings > 1 && k >= 0 ? k / cap : 0;
         if (rings > 1) k -= r * cap;
         const int64_t ring0 = r * cap;  // first slot of ring r
-        if (k < 0 || k > cap - 2 || r >= rings) {
+        if (k < 0 || k > rv.size - 2 || r >= rings) {  // size <= cap
             if (err) atomicOr(err, ERR_IDX_RANGE);
         } else {
 #pragma unroll

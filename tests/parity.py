@@ -2,14 +2,20 @@
 
 Tolerances: Q values within 1e-4 relative (max |q - q*| / max |q*|), the loss
 within 1e-4 relative, every gradient tensor within 1e-3 relative L2 for the fp32
-path and 2e-2 for bf16 operands with fp32 accumulation; integer outputs (gathered bytes, frame maps, actions) bit-exact.
+path and 2e-2 for bf16 operands with fp32 accumulation; integer outputs
+(gathered bytes, frame maps, actions) bit-exact.
 
-ReLU derivatives are a discrete choice taken from a float: a pre-activation
-within rounding of zero may be switched on in fp32 and off in fp64, and a single
-such flip moves a whole sample's backward pass by ~1/sqrt(512 B).  Gradient
-parity therefore runs on rows whose online pre-activations all clear the
-oracle's kink margin KINK_TAU (|z| / (|b| + sum |w||x|)); the batch size, and so
-the launch configuration, stays the one under test.
+Per-sample TD values (Algorithm 1's target y, eq. (1)'s error delta) are
+compared in absolute terms against the Q scale, because delta is a difference
+of two Q values: with every Q within Q_TOL * s of the oracle (s the largest
+|Q| of either network), max Q(s') and y lie within Q_TOL * s and delta within
+2 Q_TOL * s; the Huber loss of a row moves by at most
+min(|delta|, c) * e + e^2 / 2 for a delta error e.
+
+Bit-exact argmax is well posed only away from ties: an environment's greedy
+action is demanded exactly when the oracle's top-2 gap is at least
+Q_TOL * max|Q| (over a hundred times the Q error this path measures), and the
+actor workloads assert that every one of their environments clears that gap.
 """
 import numpy as np
 
@@ -20,14 +26,6 @@ LOSS_TOL = 1e-4
 GRAD_TOL = 1e-3
 GRAD_TOL_BF16 = 2e-2  # bf16 operands with fp32 accumulation
 TENSORS = ("W1", "b1", "W2", "b2", "W3", "b3", "W4", "b4", "W5", "b5")
-KINK_TAU = 1e-6
-
-
-def kink_certified(margins, want, tau=KINK_TAU):
-    """Positions of the first `want` rows whose kink margin is at least tau."""
-    ok = np.nonzero(np.asarray(margins) >= tau)[0]
-    assert ok.size >= want, f"only {ok.size} of {len(margins)} rows clear the kink margin"
-    return ok[:want]
 
 
 def q_rel_err(q, q_ref):
@@ -54,15 +52,43 @@ def assert_grads_close(g, g_ref, n_actions, tol=GRAD_TOL):
     return errs
 
 
+def assert_td_close(q, q_next, td, ref, clip, q_tol=Q_TOL):
+    """Element-by-element check of a learner call's per-row values against the
+    oracle's: q [B,A] = Q(s), q_next [B,A] = Q(s'), td [B,4] = (max Q(s'), y,
+    delta, Huber).  Returns the largest errors, each relative to the Q scale."""
+    q, q_next, td = (np.asarray(x, np.float64) for x in (q, q_next, td))
+    s = max(np.abs(ref["q"]).max(), np.abs(ref["q2"]).max(), 1e-30)
+    assert q_rel_err(q, ref["q"]) <= q_tol, ("Q(s)", q_rel_err(q, ref["q"]))
+    assert q_rel_err(q_next, ref["q2"]) <= q_tol, ("Q(s')", q_rel_err(q_next, ref["q2"]))
+    errs = {}
+    for col, name, bound in ((0, "max_q2", q_tol * s), (1, "y", q_tol * s),
+                             (2, "delta", 2 * q_tol * s)):
+        e = np.abs(td[:, col] - ref[name])
+        assert e.max() <= bound, (name, int(e.argmax()), float(e.max()), bound)
+        errs[name] = float(e.max() / s)
+    e = 2 * q_tol * s
+    d = np.minimum(np.maximum(np.abs(td[:, 2]), np.abs(ref["delta"])), clip)
+    el = np.abs(td[:, 3] - ref["ell"])
+    assert np.all(el <= d * e + 0.5 * e * e + 1e-7 * np.abs(ref["ell"])), ("ell", float(el.max()))
+    errs["ell"] = float(el.max() / s)
+    return errs
+
+
+def tie_gap(q_oracle):
+    """Top-2 gap of each row of Q, relative to max |Q| of the whole call."""
+    q = np.asarray(q_oracle, np.float64)
+    srt = np.sort(q, axis=1)
+    return (srt[:, -1] - srt[:, -2]) / max(np.abs(q).max(), 1e-30)
+
+
 def assert_actions_match(actions, q_oracle, acts_oracle, explored):
-    """Bit-exact where the greedy choice is well posed; elsewhere the GPU's
-    greedy action must be one of the oracle's near-maxima."""
+    """Bit-exact wherever the greedy choice is well posed (an explored env, or a
+    top-2 gap of at least Q_TOL * max|Q|); elsewhere the GPU's greedy action must
+    be one of the oracle's near-maxima.  Returns the number of near-tie envs."""
     q = np.asarray(q_oracle, np.float64)
     scale = np.abs(q).max()
-    srt = np.sort(q, axis=1)
-    gap = srt[:, -1] - srt[:, -2]
-    certified = explored | (gap > 4 * Q_TOL * scale)
+    certified = explored | (tie_gap(q) >= Q_TOL)
     np.testing.assert_array_equal(np.asarray(actions)[certified], acts_oracle[certified])
     for e in np.nonzero(~certified)[0]:
-        assert q[e, actions[e]] >= q[e].max() - 4 * Q_TOL * scale, e
+        assert q[e, actions[e]] >= q[e].max() - Q_TOL * scale, e
     return int((~certified).sum())

@@ -1,8 +1,8 @@
 """GPU parity of the actor side (Algorithm 1 acting and storing; Section 4
 bundled mode, one replay ring per actor; Section 5.1 epsilon schedule) against
 the oracle on the same seeded inputs: replay insert and multi-ring gathers are
-bit-exact, the learner step on per-actor rings meets the fp32 bars on
-kink-certified rows, and a closed actor loop on a synthetic game (SpriteEnv)
+bit-exact, the learner step on per-actor rings meets the fp32 bars, and a
+closed actor loop on a synthetic game (SpriteEnv)
 produces the same replay memory as the same loop run with the oracle."""
 import sys
 
@@ -147,11 +147,7 @@ def test_grouped_learner_on_actor_rings(torch_cuda, g, oracle_mod):
     net = oracle_mod.Net(n_actions=18)
     idx, refs = [], []
     for gi in range(G):
-        pool = rng.integers(0, cap - 1, 48)
-        pg = orc.gather(oracle_mod, gi, pool)
-        m = oracle_mod.learner_step(net, thetas[gi], target, pg["s"], pg["s2"], pg["a"], pg["r"],
-                                    pg["term"], 0.99, 1.0)["margin"]
-        ks = pool[parity.kink_certified(m, b)]
+        ks = rng.integers(0, cap - 1, b)
         idx.append(gi * cap + ks)
         rg = orc.gather(oracle_mod, gi, ks)
         refs.append(oracle_mod.learner_step(net, thetas[gi], target, rg["s"], rg["s2"], rg["a"],
@@ -169,9 +165,10 @@ def test_grouped_learner_on_actor_rings(torch_cuda, g, oracle_mod):
 def test_closed_actor_loop_on_sprite_games(torch_cuda, g, oracle_mod):
     """R actors play SpriteEnv for T steps with the annealed epsilon, storing
     every step in their rings; the oracle plays the same loop.  Actions must
-    agree wherever the greedy choice is well posed (the loop stops comparing at
-    the first near-tie that the two sides break differently), and the replay
-    memories must be identical up to that step."""
+    agree bit for bit wherever the greedy choice is well posed (top-2 gap of at
+    least 1e-4 max|Q|; a near-tie that the two sides broke differently would end
+    the comparison there), and the replay memories must be identical.  On this
+    seeded loop every step is compared: no near-tie is broken differently."""
     torch = torch_cuda
     R, T, cap, A = 8, 40, 64, 18
     _say(f"closed actor loop R={R} T={T}")
@@ -185,7 +182,7 @@ def test_closed_actor_loop_on_sprite_games(torch_cuda, g, oracle_mod):
     cur = np.zeros((R, 4, 84, 84), np.uint8)
     cur[:, 3] = env.frames()
     ep_now = np.ones(R, np.uint8)  # the first frame starts an episode
-    greedy_steps = 0
+    greedy_steps = compared = 0
     for t in range(T):
         eps = g.epsilon(t, 1.0, 0.3, 20)
         assert eps == oracle_mod.epsilon(t, 1.0, 0.3, 20)
@@ -196,10 +193,11 @@ def test_closed_actor_loop_on_sprite_games(torch_cuda, g, oracle_mod):
         acts = acts_d.cpu().numpy()
         explored = acts_o != np.argmax(q_o, axis=1)
         greedy_steps += int((~explored).sum())
+        parity.assert_actions_match(acts, q_o, acts_o, explored)  # exact unless near-tie
         if not np.array_equal(acts, acts_o):
-            parity.assert_actions_match(acts, q_o, acts_o, explored)  # near-ties only
             _say(f"near-tie at step {t}: stopping the comparison")
             break
+        compared += 1
         reward, done = env.step(acts)
         recs = (cur[None, :, 3], ep_now[None], acts[None].astype(np.int32), reward[None])
         _insert_both(torch, g, ctx, rs, orc, oracle_mod, recs)
@@ -210,5 +208,6 @@ def test_closed_actor_loop_on_sprite_games(torch_cuda, g, oracle_mod):
     ctx.check()
     _assert_rings_equal(rs, orc)
     assert greedy_steps > 0 and orc.ep.sum() > R  # some greedy actions, some finished episodes
+    assert compared == T
     _say(f"greedy actions compared: {greedy_steps}; ring size {rs.size}")
     ctx.close()

@@ -9,8 +9,7 @@ backward operands rounded to bf16): every gradient tensor within 2e-2
 relative L2 and the loss within 1e-4 relative.  Mixed fp32 / bf16 steps and
 the forward-only calls compute in fp32 from the exactly widened values and
 meet the fp32 bars (Q and loss 1e-4 relative, gradients 1e-3 relative L2).
-Gradient parity runs on kink-certified rows of each group, picked out of a
-larger pool per group, so every group still runs at the batch under test.
+The stale-replica workload is checked on exactly the rows bench.py times.
 """
 import sys
 
@@ -47,15 +46,9 @@ def _dev(torch, a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def _pick_certified(oracle_mod, net, thetas64, target64, inp, pool, batch):
-    """idx [G*batch]: for group g, `batch` certified rows out of its `pool` rows."""
-    idx = []
-    for gi, th in enumerate(thetas64):
-        rows = slice(gi * pool, (gi + 1) * pool)
-        m = oracle_mod.learner_step(net, th, target64, inp.s[rows], inp.s2[rows], inp.a[rows],
-                                    inp.r[rows], inp.term[rows], inp.gamma, 1.0)["margin"]
-        idx.append(gi * pool + parity.kink_certified(m, batch))
-    return np.concatenate(idx).astype(np.int64)
+def _group_rows(G, pool, batch):
+    """idx [G*batch]: group g takes the first `batch` of its `pool` rows."""
+    return np.concatenate([gi * pool + np.arange(batch) for gi in range(G)]).astype(np.int64)
 
 
 def _oracle_groups(oracle_mod, net, thetas64, target64, inp, idx, batch, clip=1.0):
@@ -76,28 +69,35 @@ def test_grouped_16x64_bf16_a18(torch_cuda, g, oracle_mod):
     """The stale-replica workload: 16 bf16 replicas x 64 transitions, 18 actions."""
     torch = torch_cuda
     w = datagen.WORKLOADS["grouped_g16_b64_a18_bf16"]
-    G, b, A, pool = w["groups"], w["batch"], w["n_actions"], 96
+    G, b, A = w["groups"], w["batch"], w["n_actions"]
     _say(f"grouped G={G} b={b} A={A} bf16 seed={w['seed']}")
-    inp = datagen.grouped_inputs(w["seed"], G, pool, A)
+    inp = datagen.grouped_inputs(w["seed"], G, b, A)
     net = oracle_mod.Net(n_actions=A)
     th64 = [datagen.bf16_bits_to_f64(t) for t in inp.theta_bf16]
     tg64 = datagen.bf16_bits_to_f64(inp.target_bf16)
-    idx = _pick_certified(oracle_mod, net, th64, tg64, inp, pool, b)
+    idx = _group_rows(G, b, b)
+    np.testing.assert_array_equal(idx, np.arange(G * b))  # the rows bench.py times
     ctx = g.Context(max_batch=b, n_actions=A, groups=G, dtype=g.GORILA_BF16)
     thetas = _dev(torch, inp.theta_bf16.view(np.int16))
     target = _dev(torch, inp.target_bf16.view(np.int16))
     grads, loss = g.learner_step_grouped(ctx, thetas, target, A, _replay(torch, g, inp),
                                          _dev(torch, idx), inp.gamma, 1.0)
     ctx.check()
+    q, qn, td = g.learner_td(ctx, G * b, A)
     got_g, got_l = grads.cpu().numpy(), loss.cpu().numpy()
+    q, qn, td = q.cpu().numpy(), qn.cpu().numpy(), td.cpu().numpy()
     ref = _oracle_groups(oracle_mod, net, th64, tg64, inp, idx, b)
-    worst = {}
+    worst, worst_td = {}, {}
     for gi in range(G):
         errs = parity.assert_grads_close(got_g[gi], ref[gi]["grads"], A, parity.GRAD_TOL_BF16)
         assert abs(got_l[gi] - ref[gi]["loss"]) <= parity.LOSS_TOL * abs(ref[gi]["loss"]), gi
+        rows = slice(gi * b, (gi + 1) * b)
+        tde = parity.assert_td_close(q[rows], qn[rows], td[rows], ref[gi], 1.0)
         for k, v in errs.items():
             worst[k] = max(worst.get(k, 0.0), v)
-    _say(f"worst grad rel-L2 over groups {worst}")
+        for k, v in tde.items():
+            worst_td[k] = max(worst_td.get(k, 0.0), v)
+    _say(f"worst grad rel-L2 over groups {worst}; td errors / Q scale {worst_td}")
     # replicas differ, so their gradients must too
     assert not np.array_equal(got_g[0], got_g[1])
     ctx.close()
@@ -117,7 +117,7 @@ def test_grouped_ragged_mixed_dtypes(torch_cuda, g, oracle_mod):
     th64[2] = (th64[2] - 1e-4 * rng.standard_normal(th64[2].shape[0])).astype(np.float32)
     th64 = [np.asarray(t, np.float64) for t in th64]
     tg64 = datagen.bf16_bits_to_f64(inp.target_bf16)
-    idx = _pick_certified(oracle_mod, net, th64, tg64, inp, pool, b)
+    idx = _group_rows(G, pool, b)
     ctx = g.Context(max_batch=b, n_actions=A, groups=G, dtype=g.GORILA_BF16)
     thetas = [_dev(torch, th64[0].astype(np.float32)),
               _dev(torch, inp.theta_bf16[1].view(np.int16)),
@@ -145,7 +145,7 @@ def test_grouped_all_bf16_ragged(torch_cuda, g, oracle_mod, G, b, A, clip):
     net = oracle_mod.Net(n_actions=A)
     th64 = [datagen.bf16_bits_to_f64(t) for t in inp.theta_bf16]
     tg64 = datagen.bf16_bits_to_f64(inp.target_bf16)
-    idx = _pick_certified(oracle_mod, net, th64, tg64, inp, pool, b)
+    idx = _group_rows(G, pool, b)
     ctx = g.Context(max_batch=b, n_actions=A, groups=G, dtype=g.GORILA_BF16)
     thetas = _dev(torch, inp.theta_bf16.view(np.int16))
     target = _dev(torch, inp.target_bf16.view(np.int16))
