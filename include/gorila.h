@@ -126,7 +126,12 @@ size_t gorila_workspace_bytes(int32_t max_batch, int32_t n_actions, int32_t dtyp
  * (an error word and the counters of split reductions, which every call
  * leaves at zero) on the stream; the caller must not write the workspace
  * while the context lives, and calls on one context must not overlap (one
- * stream). */
+ * stream).  The first context made on a device also sets up that device's
+ * no-allocation scratch (gorila_act_noalloc below).  workspace = NULL with
+ * ws_bytes = 0 makes a context without a workspace: only gorila_act_noalloc
+ * and the calls that use no workspace (replay insert, parameter sync, loss
+ * filter, parameter-server apply, gorila_ctx_check) accept it; the others
+ * return GORILA_EWORKSPACE. */
 int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_t ws_bytes);
 int gorila_ctx_destroy(gorila_ctx* ctx);
 /* Point the context at another stream (subsequent calls enqueue there). */
@@ -209,6 +214,22 @@ int gorila_learner_step_grouped(const gorila_params* params, int32_t groups,
                                 const gorila_params* target_params, const gorila_replay* replay,
                                 const int64_t* idx, int32_t batch, float gamma, float clip_delta,
                                 float* grads_out, float* loss_out, gorila_ctx* ctx);
+
+/* For callers that cannot allocate device memory at call time (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * gorila_act without a workspace.  Same arguments, semantics and results as
+ * gorila_act (the same kernels run), for n <= GORILA_NOALLOC_MAX_STATES
+ * states; larger n returns GORILA_EWORKSPACE.  Intermediate results live in
+ * a static device array of at most GORILA_NOALLOC_SCRATCH_MB MiB that each
+ * device holds until the process ends (its address is resolved when the first
+ * context is made on that device); the call allocates nothing.  Every call on
+ * one device shares that array: calls that overlap on one device, from any
+ * context or stream, race and must not be issued. */
+#define GORILA_NOALLOC_MAX_STATES 256
+#define GORILA_NOALLOC_SCRATCH_MB 44
+int gorila_act_noalloc(const gorila_params* params, const uint8_t* states_u8, int32_t n,
+                       float eps, uint64_t seed, int32_t* actions_out, float* q_out,
+                       gorila_ctx* ctx);
 
 /* Per-transition values of the most recent learner call on this context
  * (gorila_learner_step or _grouped; Algorithm 1's target and eq. (1)'s

@@ -32,8 +32,9 @@ EXPORTS = (
     "gorila_q_forward", "gorila_act", "gorila_learner_step", "gorila_learner_step_grouped",
     "gorila_ctx_timing_begin", "gorila_ctx_timing_end", "gorila_stage_name",
     "gorila_loss_filter", "gorila_ps_apply", "gorila_replay_insert", "gorila_epsilon",
-    "gorila_params_sync", "gorila_learner_td",
+    "gorila_params_sync", "gorila_learner_td", "gorila_act_noalloc",
 )
+NOALLOC_MAX_STATES = 256  # GORILA_NOALLOC_MAX_STATES
 
 
 class GorilaError(RuntimeError):
@@ -95,6 +96,7 @@ def lib() -> ctypes.CDLL:
         "gorila_ps_apply": (ctypes.c_int, [vp, vp, i64, vp, i32, vp, vp, vp, i64, f32, f32, vp,
                                            vp]),
         "gorila_learner_td": (ctypes.c_int, [vp, vp, vp, vp]),
+        "gorila_act_noalloc": (ctypes.c_int, [P, vp, i32, f32, u64, vp, vp, vp]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -138,19 +140,24 @@ class Context:
     """A gorila_ctx bound to a torch-allocated device workspace.
 
     The workspace is sized for calls with batch <= max_batch (learner step) or
-    n <= 2 * max_batch states (forward / act)."""
+    n <= 2 * max_batch states (forward / act); max_batch = 0 makes a context
+    without one (for gorila_act_noalloc and the calls that need none)."""
 
     def __init__(self, max_batch: int, n_actions: int, groups: int = 1, device=None,
                  dtype: int = GORILA_F32):
         import torch
         self.device = torch.device(device if device is not None else "cuda")
-        self.ws_bytes = workspace_bytes(max_batch, n_actions, dtype, groups)
-        if self.ws_bytes == 0:
-            raise ValueError("invalid workspace request")
+        if max_batch == 0:  # a context without a workspace (gorila_act_noalloc)
+            self.ws_bytes, self.workspace = 0, None
+        else:
+            self.ws_bytes = workspace_bytes(max_batch, n_actions, dtype, groups)
+            if self.ws_bytes == 0:
+                raise ValueError("invalid workspace request")
         with torch.cuda.device(self.device):
-            self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+            if self.ws_bytes:
+                self.workspace = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
             h = ctypes.c_void_p()
-            _check(lib().gorila_ctx_create(ctypes.byref(h), self._stream(), self.workspace.data_ptr(),
+            _check(lib().gorila_ctx_create(ctypes.byref(h), self._stream(), _ptr(self.workspace),
                                            self.ws_bytes), "gorila_ctx_create")
         self.handle = h
 
@@ -275,6 +282,15 @@ def gorila_act(ctx: Context, theta, n_actions: int, states, eps: float, seed: in
     _check(lib().gorila_act(ctypes.byref(p), _ptr(states), states.shape[0], eps,
                             ctypes.c_uint64(seed & (2 ** 64 - 1)), _ptr(actions_out), _ptr(q_out),
                             ctx.bind_stream()), "gorila_act")
+
+
+def gorila_act_noalloc(ctx: Context, theta, n_actions: int, states, eps: float, seed: int,
+                       actions_out, q_out=None) -> None:
+    """gorila_act on the library's static scratch (no workspace, n <= NOALLOC_MAX_STATES)."""
+    p = params(theta, n_actions)
+    _check(lib().gorila_act_noalloc(ctypes.byref(p), _ptr(states), states.shape[0], eps,
+                                    ctypes.c_uint64(seed & (2 ** 64 - 1)), _ptr(actions_out),
+                                    _ptr(q_out), ctx.bind_stream()), "gorila_act_noalloc")
 
 
 def gorila_learner_step(ctx: Context, theta, theta_target, n_actions: int, replay: Replay, idx,

@@ -3,6 +3,7 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -44,6 +45,7 @@ struct gorila_ctx {
     bool td_valid = false;
     int td_b = 0, td_groups = 0, td_actions = 0;
     size_t td_q = 0, td_rows = 0;
+    char* scratch = nullptr;  // this device's no-allocation scratch (device address)
 };
 
 namespace {
@@ -67,7 +69,7 @@ struct StageTimer {
 namespace {
 
 constexpr size_t ALIGN = 256;
-size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+constexpr size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 // Byte offsets of every workspace region for fwd_rows forward rows (all
 // parameter sets together), bwd_rows learner rows, `online` learner parameter
@@ -90,7 +92,8 @@ struct Plan {
 constexpr size_t WS_HEAD = 1024, SPLIT_CNT_OFFSET = 256;
 static_assert(SPLIT_CNT_OFFSET + 4 * SPLIT_MAX_TILES <= WS_HEAD, "counters fit the zeroed head");
 
-Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online = 1, int widened = 0) {
+constexpr Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online = 1,
+                         int widened = 0) {
     Plan p{};
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t at = o; o += up(bytes); return at; };
@@ -132,13 +135,16 @@ Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online = 1, int wi
 template <class T>
 T* at(gorila_ctx* c, size_t off) { return (T*)(c->ws + off); }
 
-SplitWs split_ws(gorila_ctx* c, const Plan& p) {
+// Split-reduction workspace of a plan laid out from `base` (the context's
+// workspace, or the no-allocation scratch).
+SplitWs split_ws(gorila_ctx* c, char* base, const Plan& p) {
     SplitWs sw;
     sw.cus = c->cus;
-    sw.ws = c->split_ok ? at<float>(c, p.split) : nullptr;  // null: every tile whole
-    sw.cnt = at<int>(c, p.err + SPLIT_CNT_OFFSET);
+    sw.ws = c->split_ok ? (float*)(base + p.split) : nullptr;  // null: every tile whole
+    sw.cnt = (int*)(base + p.err + SPLIT_CNT_OFFSET);
     return sw;
 }
+SplitWs split_ws(gorila_ctx* c, const Plan& p) { return split_ws(c, c->ws, p); }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -204,44 +210,99 @@ ReplayView view_of(const gorila_replay* rv) {
 // (independent, so one launch).
 __global__ __launch_bounds__(256) void states_prep_kernel(const uint8_t* states, int n,
                                                           const uint8_t** ftab, WeightViews wv,
-                                                          int tblocks) {
+                                                          int tblocks, unsigned* zero_head) {
     if ((int)blockIdx.x >= tblocks) {
         prep_weights_part(wv, blockIdx.x - tblocks, PREP_BLOCKS);
         return;
     }
+    // a scratch that other calls share starts each call with a zero head
+    // (error word, split-reduction counters); the split launches come later
+    if (zero_head && blockIdx.x == 0)
+        for (int i = threadIdx.x; i < (int)(WS_HEAD / 4); i += blockDim.x) zero_head[i] = 0u;
     const int e = blockIdx.x * blockDim.x + threadIdx.x;
     if (e < n * 4) ftab[e] = states + (int64_t)(e >> 2) * STATE_BYTES + (int64_t)(e & 3) * FRAME_BYTES;
 }
 
-// Forward pass of n states through one parameter set up to h4; *theta32
-// receives the fp32 parameters the head must use.
-int forward_one(gorila_ctx* c, const Plan& p, const gorila_params* prm, const uint8_t* states,
-                int n, const float** theta32, int* fc1_splits) {
+// Forward pass of n states through one parameter set up to h4, with the
+// plan's regions laid out from `base`; *theta32 receives the fp32 parameters
+// the head must use.  zero_head: clear the plan's head first.
+int forward_one(gorila_ctx* c, char* base, const Plan& p, const gorila_params* prm,
+                const uint8_t* states, int n, const float** theta32, int* fc1_splits,
+                bool zero_head) {
     hipStream_t st = c->stream;
-    c->td_valid = false;  // the forward rows overwrite a learner call's q
-    const uint8_t** ftab = at<const uint8_t*>(c, p.ftab);
+    auto fp = [&](size_t off) { return (float*)(base + off); };
+    const uint8_t** ftab = (const uint8_t**)(base + p.ftab);
     WidenSet ws{};
     int n_widen = 0;
-    const float* theta = fp32_params(c, p, prm, ws, n_widen);
+    const float* theta = (const float*)prm->data;
+    if (prm->dtype != GORILA_F32) {  // exact widening into the plan's fp32 slot
+        ws.src[0] = (const uint16_t*)prm->data;
+        ws.dst[0] = fp(p.theta32);
+        n_widen = 1;
+        theta = ws.dst[0];
+    }
     *theta32 = theta;
-    WeightViews wv{theta, at<float>(c, p.w2t), at<float>(c, p.w3t), nullptr, nullptr};
+    WeightViews wv{theta, fp(p.w2t), fp(p.w3t), nullptr, nullptr};
     {
         StageTimer t(c, ST_PREP);
         if (n_widen) launch_widen_bf16(ws, n_widen, param_count(prm->n_actions), st);
         const int tblocks = (n * 4 + 255) / 256;
-        states_prep_kernel<<<tblocks + PREP_BLOCKS, 256, 0, st>>>(states, n, ftab, wv, tblocks);
+        states_prep_kernel<<<tblocks + PREP_BLOCKS, 256, 0, st>>>(
+            states, n, ftab, wv, tblocks, zero_head ? (unsigned*)(base + p.err) : nullptr);
     }
     GroupPtrs th{}, w2t{}, w3t{};
     th.p[0] = theta;
     w2t.p[0] = wv.w2t;
     w3t.p[0] = wv.w3t;
     // forward-only calls compute in fp32 (bf16 parameters are widened exactly)
-    { StageTimer t(c, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 1, n, at<float>(c, p.h1), false, st); }
-    const SplitWs sw = split_ws(c, p);
-    { StageTimer t(c, ST_CONV2_FWD); launch_conv2_fwd(at<float>(c, p.h1), w2t, th, 1, n, at<float>(c, p.h2), false, st); }
-    { StageTimer t(c, ST_CONV3_FWD); launch_conv3_fwd(at<float>(c, p.h2), w3t, th, 1, n, at<float>(c, p.h3), sw, false, st); }
-    { StageTimer t(c, ST_FC1_FWD); *fc1_splits = launch_fc1_fwd(at<float>(c, p.h3), th, GroupPtrs16{}, 1, n, at<float>(c, p.fc1part), false, st); }
+    { StageTimer t(c, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 1, n, fp(p.h1), false, st); }
+    const SplitWs sw = split_ws(c, base, p);
+    { StageTimer t(c, ST_CONV2_FWD); launch_conv2_fwd(fp(p.h1), w2t, th, 1, n, fp(p.h2), false, st); }
+    { StageTimer t(c, ST_CONV3_FWD); launch_conv3_fwd(fp(p.h2), w3t, th, 1, n, fp(p.h3), sw, false, st); }
+    { StageTimer t(c, ST_FC1_FWD); *fc1_splits = launch_fc1_fwd(fp(p.h3), th, GroupPtrs16{}, 1, n, fp(p.fc1part), false, st); }
     return check_launch();
+}
+
+// ---- The no-allocation actor call's scratch ----
+// Forward rows of the largest call, one fp32 slot for a widened bf16 set and
+// the largest action count, then WS_HEAD bytes for the placement probe of
+// contexts made without a workspace.
+constexpr Plan NOALLOC_PLAN = make_plan(GORILA_NOALLOC_MAX_STATES, 0, MAX_ACTIONS, 1, 1);
+constexpr size_t NOALLOC_PROBE = NOALLOC_PLAN.total;
+constexpr size_t NOALLOC_BYTES = NOALLOC_PROBE + WS_HEAD;
+static_assert(NOALLOC_BYTES <= (size_t)GORILA_NOALLOC_SCRATCH_MB << 20, "stated scratch size");
+}  // namespace
+
+// Each device holds its own copy for the life of the process.  Host code
+// never uses this name as an address: it uses the per-device address that
+// hipGetSymbolAddress returns (noalloc_scratch below).
+static __device__ __align__(256) char scratch[NOALLOC_BYTES];
+
+namespace {
+
+// Per device ordinal: the scratch's device address, resolved once with that
+// device current, and its head zeroed.
+constexpr int NOALLOC_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+char* g_scratch[NOALLOC_MAX_DEVICES] = {};
+
+__global__ __launch_bounds__(256) void zero_words_kernel(unsigned* p, int n) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0u;
+}
+
+int noalloc_scratch(int dev, hipStream_t st, char** out) {
+    if (dev < 0 || dev >= NOALLOC_MAX_DEVICES) return GORILA_EHIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return GORILA_EHIP;
+        zero_words_kernel<<<1, 256, 0, st>>>((unsigned*)ptr, (int)(WS_HEAD / 4));
+        if (hipGetLastError() != hipSuccess || hipStreamSynchronize(st) != hipSuccess)
+            return GORILA_EHIP;
+        g_scratch[dev] = (char*)ptr;
+    }
+    *out = g_scratch[dev];
+    return GORILA_OK;
 }
 
 }  // namespace
@@ -273,12 +334,12 @@ static __global__ __launch_bounds__(64) void xcd_probe_kernel(unsigned* out) {
 // (round-robin dispatch over 1, 2, 4 or 8 XCDs).  Checked once per context on
 // WS_HEAD / 4 workgroups, using the workspace head as the record; where it
 // does not hold, every tile runs whole.
-static int probe_split_placement(gorila_ctx* c) {
+static int probe_split_placement(gorila_ctx* c, char* rec) {
     constexpr int N = (int)(WS_HEAD / 4);
     unsigned xcc[N];
-    xcd_probe_kernel<<<N, 64, 0, c->stream>>>((unsigned*)c->ws);
+    xcd_probe_kernel<<<N, 64, 0, c->stream>>>((unsigned*)rec);
     if (hipGetLastError() != hipSuccess) return GORILA_EHIP;
-    if (hipMemcpyAsync(xcc, c->ws, sizeof xcc, hipMemcpyDeviceToHost, c->stream) != hipSuccess ||
+    if (hipMemcpyAsync(xcc, rec, sizeof xcc, hipMemcpyDeviceToHost, c->stream) != hipSuccess ||
         hipStreamSynchronize(c->stream) != hipSuccess)
         return GORILA_EHIP;
     c->split_ok = true;
@@ -288,8 +349,9 @@ static int probe_split_placement(gorila_ctx* c) {
 }
 
 int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_t ws_bytes) {
-    if (!out || !workspace || !aligned16(workspace)) return GORILA_EINVAL;
-    if (ws_bytes < make_plan(1, 1, 1).err + WS_HEAD) return GORILA_EWORKSPACE;
+    if (!out || !aligned16(workspace)) return GORILA_EINVAL;
+    if (!workspace && ws_bytes != 0) return GORILA_EINVAL;
+    if (workspace && ws_bytes < make_plan(1, 1, 1).err + WS_HEAD) return GORILA_EWORKSPACE;
     int dev = -1, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) return GORILA_EHIP;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -303,8 +365,9 @@ int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_
         c->cus = cus;
     }
     if (!c) return GORILA_EINVAL;
-    const int rc = probe_split_placement(c);
-    if (rc != GORILA_OK || hipMemsetAsync(c->ws, 0, WS_HEAD, c->stream) != hipSuccess) {
+    int rc = noalloc_scratch(dev, c->stream, &c->scratch);
+    if (rc == GORILA_OK) rc = probe_split_placement(c, c->ws ? c->ws : c->scratch + NOALLOC_PROBE);
+    if (rc != GORILA_OK || (c->ws && hipMemsetAsync(c->ws, 0, WS_HEAD, c->stream) != hipSuccess)) {
         delete c;
         return GORILA_EHIP;
     }
@@ -332,6 +395,7 @@ int gorila_ctx_check(gorila_ctx* ctx) {
     int rc = check_ctx(ctx);
     if (rc) return rc;
     if (hipStreamSynchronize(ctx->stream) != hipSuccess) return GORILA_EHIP;
+    if (!ctx->ws) return GORILA_OK;  // no workspace, no device error word
     unsigned word = 0;
     if (hipMemcpy(&word, ctx->ws, sizeof(word), hipMemcpyDeviceToHost) != hipSuccess) return GORILA_EHIP;
     if (word == 0) return GORILA_OK;
@@ -416,6 +480,7 @@ int gorila_gather(const gorila_replay* replay, const int64_t* idx, int32_t n, ui
     if (n < 0 || (n > 0 && (!idx || !s_out || !s2_out || !a_out || !r_out || !term_out)))
         return GORILA_EINVAL;
     if (!aligned16(s_out) || !aligned16(s2_out)) return GORILA_EINVAL;
+    if (!ctx->ws) return GORILA_EWORKSPACE;
     if (n == 0) return GORILA_OK;
     launch_gather(view_of(replay), idx, n, 0x7fffffff, s_out, s2_out, frame_map_out, a_out, r_out,
                   term_out, at<unsigned>(ctx, make_plan(1, 0, 1).err), ctx->stream);
@@ -430,10 +495,11 @@ int gorila_q_forward(const gorila_params* params, const uint8_t* states_u8, int3
     if (n < 0 || (n > 0 && (!states_u8 || !q_out)) || !aligned16(states_u8)) return GORILA_EINVAL;
     if (n == 0) return GORILA_OK;
     const Plan p = make_plan(n, 0, params->n_actions, 1, params->dtype == GORILA_BF16);
-    if (p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
+    if (!ctx->ws || p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
     const float* theta = nullptr;
     int splits = 0;
-    if ((rc = forward_one(ctx, p, params, states_u8, n, &theta, &splits))) return rc;
+    ctx->td_valid = false;  // the forward rows overwrite a learner call's q
+    if ((rc = forward_one(ctx, ctx->ws, p, params, states_u8, n, &theta, &splits, false))) return rc;
     {
         StageTimer t(ctx, ST_HEAD);
         launch_q_head(at<float>(ctx, p.fc1part), splits, theta, n, params->n_actions, q_out,
@@ -451,14 +517,40 @@ int gorila_act(const gorila_params* params, const uint8_t* states_u8, int32_t n,
     if (!(eps >= 0.0f && eps <= 1.0f)) return GORILA_EINVAL;
     if (n == 0) return GORILA_OK;
     const Plan p = make_plan(n, 0, params->n_actions, 1, params->dtype == GORILA_BF16);
-    if (p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
+    if (!ctx->ws || p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
     const float* theta = nullptr;
     int splits = 0;
-    if ((rc = forward_one(ctx, p, params, states_u8, n, &theta, &splits))) return rc;
+    ctx->td_valid = false;  // the forward rows overwrite a learner call's q
+    if ((rc = forward_one(ctx, ctx->ws, p, params, states_u8, n, &theta, &splits, false))) return rc;
     {
         StageTimer t(ctx, ST_HEAD);
         launch_act_head(at<float>(ctx, p.fc1part), splits, theta, n, params->n_actions, eps, seed,
                         actions_out, q_out, ctx->stream);
+    }
+    return check_launch();
+}
+
+int gorila_act_noalloc(const gorila_params* params, const uint8_t* states_u8, int32_t n,
+                       float eps, uint64_t seed, int32_t* actions_out, float* q_out,
+                       gorila_ctx* ctx) {
+    int rc = check_ctx(ctx);
+    if (rc) return rc;
+    if ((rc = check_params(params, true))) return rc;
+    if (n < 0 || (n > 0 && (!states_u8 || !actions_out)) || !aligned16(states_u8)) return GORILA_EINVAL;
+    if (!(eps >= 0.0f && eps <= 1.0f)) return GORILA_EINVAL;
+    if (n > GORILA_NOALLOC_MAX_STATES) return GORILA_EWORKSPACE;
+    if (!ctx->scratch) return GORILA_EHIP;
+    if (n == 0) return GORILA_OK;
+    const Plan p = make_plan(n, 0, params->n_actions, 1, params->dtype == GORILA_BF16);
+    if (p.total > NOALLOC_PROBE) return GORILA_EWORKSPACE;  // cannot happen: the plan grows with n, A
+    const float* theta = nullptr;
+    int splits = 0;
+    if ((rc = forward_one(ctx, ctx->scratch, p, params, states_u8, n, &theta, &splits, true)))
+        return rc;
+    {
+        StageTimer t(ctx, ST_HEAD);
+        launch_act_head((const float*)(ctx->scratch + p.fc1part), splits, theta, n,
+                        params->n_actions, eps, seed, actions_out, q_out, ctx->stream);
     }
     return check_launch();
 }
@@ -493,7 +585,7 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
     // bf16 MFMA products when every parameter set is bf16, fp32 otherwise
     const bool bf16 = n_bf16 == G + 1;
     const Plan p = make_plan(2 * (int64_t)B, B, A, G, n_bf16);
-    if (p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
+    if (!ctx->ws || p.total > ctx->ws_bytes) return GORILA_EWORKSPACE;
     hipStream_t st = ctx->stream;
     const int64_t P = param_count(A);
 
