@@ -222,13 +222,22 @@ struct GemmShape {
 //
 // All pieces of a tile run on one XCD (TailSplit places them so: workgroup
 // ids that agree mod 8 share an XCD whenever a partition dispatches
-// round-robin over 1, 2, 4 or 8 XCDs), whose L2 is shared by its compute
-// units and is where their vector stores land (the per-unit L1 writes
-// through).  A piece waits for its own stores to complete
-// before it counts, so the last piece finds every partial tile in that L2; it
-// has not read those addresses before in the launch, so its L1 holds no
-// stale copy.  This needs no device-wide cache write-back or invalidation,
-// which would evict every other workgroup's operands from the L2.
+// round-robin over 1, 2, 4 or 8 XCDs, which gorila_ctx_create checks on the
+// device), so the pieces, on different compute units, share one L2: the
+// coherence point of the compiler's own protocol for workgroups whose waves
+// span compute units (workgroup scope with thread-group split), which the
+// hand-off follows:
+//  - release: every thread waits until its stores have completed (they write
+//    through the per-unit L1 to that L2), a barrier, then one atomic add on
+//    the tile's counter (performed in the L2);
+//  - acquire: the piece that counted last invalidates its compute unit's L1
+//    (buffer_inv sc0) before it loads the other pieces' tiles, so they come
+//    from the L2; the asm statement also keeps the compiler from moving the
+//    loads above it.
+// The agent-scope forms (an L2 write-back before the add and an L2
+// invalidation or L2-bypassing loads after it) would make the exchange
+// coherent across XCDs too, but they write back or drop every other
+// workgroup's lines in the L2, and measured slower (see the design notes).
 constexpr int SPLIT_MAX_TILES = 128, SPLIT_MAX_PIECES = 16, SPLIT_MAX_SLOTS = 512;
 constexpr int SPLIT_TILE_FLOATS = 64 * 64;
 struct SplitPiece {
@@ -464,12 +473,15 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
                 for (int q = 0; q < 4; ++q)
                     mine[(i * TN + j) * 4 + q] = f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1],
                                                        acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
-        __builtin_amdgcn_s_waitcnt(0);  // the partial tile is in the L2 before it is counted
+        __builtin_amdgcn_s_waitcnt(0);  // release: the partial tile is in the L2 before it is counted
         __syncthreads();
         int* flag = (int*)smem;  // the LDS buffers are free after the loop's last barrier
-        if (tid == 0) flag[0] = atomicAdd(sp.cnt, 1);
+        if (tid == 0)
+            flag[0] = __hip_atomic_fetch_add(sp.cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __syncthreads();
         if (flag[0] != sp.np - 1) return;
+        // acquire: drop this unit's L1 so every partial tile is read from the L2
+        asm volatile("buffer_inv sc0" ::: "memory");
         // add every piece's partial tile (this one's included, read back) in
         // piece order, two pieces' loads in flight at a time
 #pragma unroll
