@@ -122,9 +122,10 @@ size_t gorila_workspace_bytes(int32_t max_batch, int32_t n_actions, int32_t dtyp
  * host bookkeeping; destroy it before freeing the workspace.  Creation runs
  * one small kernel that records which XCD each of 256 workgroups runs on
  * (split reductions are used only if ids equal mod 8 share one), waits for
- * it (a stream synchronisation), then zeroes the workspace's first 1024 bytes
- * (an error word and the counters of split reductions, which every call
- * leaves at zero) on the stream; the caller must not write the workspace
+ * it (a stream synchronisation), then zeroes the workspace's first 8192 bytes
+ * (an error word, the counters of split reductions, which every call leaves
+ * at zero, and a frame of zeros that no call writes) on the stream; the
+ * caller must not write the workspace
  * while the context lives, and calls on one context must not overlap (one
  * stream).  The first context made on a device also sets up that device's
  * no-allocation scratch (gorila_act_noalloc below).  workspace = NULL with

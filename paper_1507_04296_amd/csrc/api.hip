@@ -76,7 +76,7 @@ constexpr size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 // sets plus one target set, and `widened` fp32 copies of bf16 parameter sets.
 constexpr size_t W2T_BYTES = 4 * 16 * 64 * 32, W3T_BYTES = 4 * 9 * 64 * 64;
 struct Plan {
-    size_t err, ftab, a, r, term;
+    size_t err, zero, ftab, a, r, term;
     size_t theta32, theta32_stride;
     size_t w2t, w3t, w3d, w2p;  // bases of per-set arrays (stride W2T_BYTES / W3T_BYTES)
     size_t h1, h2, h3, h4, q, ell, coef, td;
@@ -88,8 +88,11 @@ struct Plan {
 
 // The zeroed head of the workspace (WS_HEAD bytes, cleared when a context is
 // created): the sticky error word, then the TailSplit counters at
-// SPLIT_CNT_OFFSET (every launch leaves them at zero).
-constexpr size_t WS_HEAD = 1024, SPLIT_CNT_OFFSET = 256;
+// SPLIT_CNT_OFFSET (every launch leaves them at zero).  Right after it, at the
+// same offset in every plan, ZERO_BYTES that are zeroed at creation and never
+// written: a zero frame that kernels read in place of a zero-filled channel.
+constexpr size_t WS_HEAD = 1024, SPLIT_CNT_OFFSET = 256, ZERO_BYTES = 7168;
+static_assert(ZERO_BYTES >= FRAME_BYTES && ZERO_BYTES % 256 == 0, "a whole frame of zeros");
 static_assert(SPLIT_CNT_OFFSET + 4 * SPLIT_MAX_TILES <= WS_HEAD, "counters fit the zeroed head");
 
 constexpr Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online = 1,
@@ -99,6 +102,7 @@ constexpr Plan make_plan(int64_t fwd_rows, int64_t bwd_rows, int A, int online =
     auto take = [&](size_t bytes) { size_t at = o; o += up(bytes); return at; };
     const int64_t F = fwd_rows, B = bwd_rows;
     p.err = take(WS_HEAD);
+    p.zero = take(ZERO_BYTES);
     p.ftab = take(sizeof(void*) * 2 * (size_t)(F > 2 * B ? F : 2 * B) * 4);
     p.a = take(4 * (size_t)B);
     p.r = take(4 * (size_t)B);
@@ -296,7 +300,7 @@ int noalloc_scratch(int dev, hipStream_t st, char** out) {
     if (!g_scratch[dev]) {
         void* ptr = nullptr;
         if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return GORILA_EHIP;
-        zero_words_kernel<<<1, 256, 0, st>>>((unsigned*)ptr, (int)(WS_HEAD / 4));
+        zero_words_kernel<<<1, 256, 0, st>>>((unsigned*)ptr, (int)((WS_HEAD + ZERO_BYTES) / 4));
         if (hipGetLastError() != hipSuccess || hipStreamSynchronize(st) != hipSuccess)
             return GORILA_EHIP;
         g_scratch[dev] = (char*)ptr;
@@ -351,7 +355,7 @@ static int probe_split_placement(gorila_ctx* c, char* rec) {
 int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_t ws_bytes) {
     if (!out || !aligned16(workspace)) return GORILA_EINVAL;
     if (!workspace && ws_bytes != 0) return GORILA_EINVAL;
-    if (workspace && ws_bytes < make_plan(1, 1, 1).err + WS_HEAD) return GORILA_EWORKSPACE;
+    if (workspace && ws_bytes < make_plan(1, 1, 1).zero + ZERO_BYTES) return GORILA_EWORKSPACE;
     int dev = -1, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) return GORILA_EHIP;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
@@ -367,7 +371,8 @@ int gorila_ctx_create(gorila_ctx** out, void* hip_stream, void* workspace, size_
     if (!c) return GORILA_EINVAL;
     int rc = noalloc_scratch(dev, c->stream, &c->scratch);
     if (rc == GORILA_OK) rc = probe_split_placement(c, c->ws ? c->ws : c->scratch + NOALLOC_PROBE);
-    if (rc != GORILA_OK || (c->ws && hipMemsetAsync(c->ws, 0, WS_HEAD, c->stream) != hipSuccess)) {
+    if (rc != GORILA_OK ||
+        (c->ws && hipMemsetAsync(c->ws, 0, WS_HEAD + ZERO_BYTES, c->stream) != hipSuccess)) {
         delete c;
         return GORILA_EHIP;
     }
@@ -706,8 +711,8 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
     }
     {
         StageTimer t(ctx, ST_CONV1_WGRAD);
-        launch_conv1_wgrad(dz1, ftab, G, b, at<float>(ctx, p.part1), bpart, CONV1_WG_MAX_SPLITS,
-                           &s1, bf16, st);
+        launch_conv1_wgrad(dz1, ftab, at<uint8_t>(ctx, p.zero), G, b, at<float>(ctx, p.part1), bpart,
+                           CONV1_WG_MAX_SPLITS, &s1, bf16, st);
     }
     {
         StageTimer t(ctx, ST_GRAD_REDUCE);

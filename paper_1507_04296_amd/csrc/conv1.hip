@@ -152,170 +152,258 @@ void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int gr
 // dz1[pixel][o] * byte.  The bytes are exact bf16 values; dz1 enters as WP
 // bf16 planes whose sum is dz1 exactly (three for fp32 steps, as in the
 // forward kernel; one, rounded, for bf16 steps), so only the fp32
-// accumulation rounds.  The stride-4 columns are made contiguous by staging
-// each input row in LDS by phase: xs[c][r][m][s][q] = row r byte 4 (q + s) + m,
-// so the bytes of columns v = 4s + m at pixels j .. j+7 are eight consecutive
-// entries.  A unit is two output rows of one sample (40 pixels, padded to 2 x
-// 24 = 6 groups of 8, with zeros past j = 19); an MFMA step takes two groups
-// (lane half h: group 2 step + h), so a unit is three steps.  Each workgroup
-// (4 waves; wave w owns columns 64 w .. 64 w + 63) sums a contiguous range of
-// units of one parameter set into its partial [32][256]; db1 is summed from
-// the fp32 dz1 values as they are staged.  The LDS stage is double buffered
-// and the next unit's data is fetched into registers during the products.
+// accumulation rounds.
+//
+// Work is cut into units of two output rows of one sample (40 pixels, padded
+// to 2 x 24 = 6 groups of 8); an MFMA step takes two groups (lane half h:
+// group 2 step + h), so a unit is three steps.  A workgroup has eight waves:
+// waves 4 p .. 4 p + 3 own input channels 2 p, 2 p + 1 (four column tiles of
+// 32), and each of the four walks its own contiguous range of the workgroup's
+// units with a private LDS stage, with no workgroup barrier until the end.  A
+// wave splits the dz1 values of its units into planes in registers, straight
+// from their coalesced loads (lane o, h: eight pixels of channel o), and
+// multiplies them into its four tiles.  Column tile t is (c = 2 p + t / 2,
+// s = t % 2) and lane column l % 32 is (u, m) = ((l % 32) / 4, l % 4), i.e.
+// v = 4 s + m; its eight operands are the bytes at x = 4 (j + s) + m of input
+// row 4 i + u for the group's pixels j, so each input row is staged by phase:
+// xs[c][r][m][s][q] = byte 4 (q + s) + m, and a lane's eight bytes are eight
+// consecutive entries.  Entries q >= 20 are used only by the padding pixels
+// j = 20 .. 23 and hold zeros (written once), so those pixels' dz1 values,
+// loaded from a clamped in-row address, need no masking.  The next unit's dz1
+// values and bytes are fetched into registers during the products; a frame
+// pointer is loaded one unit before the fetch that uses it, and a null
+// (zero-filled) frame is read from a frame of zeros.  db1 is summed from the
+// fp32 dz1 values (by the waves of channel pair 0).  At the end the four
+// waves of each channel pair are added in a fixed order in LDS and one
+// partial [32][256] per workgroup is written.
 constexpr int C1W_UR = 2;                       // output rows per unit
 constexpr int C1W_UNITS = H1 / C1W_UR;          // 10 units per sample
-constexpr int C1W_JP = 24;                      // padded pixel columns per output row
+constexpr int C1W_Q = 24;                       // phase entries per staged row (pixels padded to 24)
+constexpr int C1W_QR = 20;                      // entries that can be non-zero (real pixels)
+// LDS stride of a staged (row, m, s) line: 28 entries = 14 dwords, so the 8
+// (u, m) lines that 8 neighbouring lanes read (lines 2 (4 u + m) + s, 28
+// dwords apart) start on 8 distinct 4-bank groups (with 24 they would share 4)
+constexpr int C1W_QS = 28;
 constexpr int C1W_XR = S1 * (C1W_UR - 1) + K1;  // 12 input rows per unit
-constexpr int C1W_DQ = C1W_UR * H1 * C1 / 4;    // 320 dz1 quads per unit
-constexpr int C1W_XW = IN_C * C1W_XR * IN_W / 4;  // 1008 input words per unit
-constexpr int C1W_TARGET = 512;                 // workgroups: two per CU
+constexpr int C1W_CPW = 2;                      // input channels per wave
+constexpr int C1W_WAVES = 8;                    // per workgroup: 4 per channel pair
+constexpr int C1W_TASKS = C1W_CPW * C1W_XR * (C1W_QR / 2);  // 240 staging tasks per unit
+constexpr int C1W_TPL = (C1W_TASKS + 63) / 64;  // 4 per lane (the last on 48 lanes)
+constexpr int C1W_WGS = 256;                    // workgroups: one per CU
 
-template <int WP>
 struct C1wStage {
-    __bf16 d[WP][C1][C1W_UR * C1W_JP];          // dz1 planes [o][(row, j)]
-    __bf16 x[IN_C][C1W_XR][4][2][C1W_JP];      // [c][r][m][s][q]
+    __bf16 x[C1W_CPW][C1W_XR][4][2][C1W_QS];  // [c][r][m][s][q], q < 24 used; 10.5 KB
 };
+constexpr int C1W_RED = 2 * C1 * 256;  // floats: two [32][256] reduction planes
+constexpr size_t C1W_SMEM = C1W_WAVES * sizeof(C1wStage) > 4 * C1W_RED
+                                ? C1W_WAVES * sizeof(C1wStage) : 4 * C1W_RED;
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 template <int WP>
-__global__ __launch_bounds__(256) void conv1_wgrad_mfma16_kernel(
-    const float* __restrict__ dz1, const uint8_t* const* __restrict__ ftab, int n,
-    float* __restrict__ partial, float* __restrict__ bias_part) {
-    __shared__ __attribute__((aligned(16))) C1wStage<WP> stg[2];
-    __shared__ float bred[256 / 8][C1];
+__global__ __launch_bounds__(64 * C1W_WAVES) void conv1_wgrad_mfma16_kernel(
+    const float* __restrict__ dz1, const uint8_t* const* __restrict__ ftab,
+    const uint8_t* __restrict__ zero_frame, int n, float* __restrict__ partial,
+    float* __restrict__ bias_part) {
+    __shared__ __attribute__((aligned(16))) char smem[C1W_SMEM];
+    __shared__ float bred[4][2][C1];
     const int g = blockIdx.y, S = gridDim.x, x = blockIdx.x;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int U = n * C1W_UNITS;
-    const int u0 = (int)((int64_t)x * U / S), u1 = (int)((int64_t)(x + 1) * U / S);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar unit walk
+    const int cp = wave >> 2, wq = wave & 3;                    // channel pair, wave within it
+    const int h = lane >> 5, o = lane & 31;
+    C1wStage& sg = ((C1wStage*)smem)[wave];
+    __bf16* xs = &sg.x[0][0][0][0][0];
 
-    for (int e = tid; e < (int)(sizeof(stg) / 16); e += 256) ((uint4*)stg)[e] = make_uint4(0, 0, 0, 0);
+    // this wave's units: a contiguous share of the workgroup's share
+    const int64_t U = (int64_t)n * C1W_UNITS, W = (int64_t)S * 4, wi = (int64_t)x * 4 + wq;
+    const int u0 = (int)(wi * U / W), u1 = (int)((wi + 1) * U / W);
 
-    // prefetch registers: two dz1 quads (pixels 2p and 2p + 1 of the unit,
-    // channels 4 (t % 8) .. +3; threads t < 160) and four input words
-    const bool dz_lane = tid < C1W_DQ / 2;
-    const int dq0 = (tid >> 3) * 16 + (tid & 7);  // quad of pixel 2p (8 quads a pixel)
-    f32x4 dq[2];
-    uint32_t xw[4];
+    // entries q >= 20 of every staged line stay zero
+    for (int e = lane; e < C1W_CPW * C1W_XR * 4 * 2 * (C1W_Q - C1W_QR); e += 64) {
+        const int line = e / (C1W_Q - C1W_QR), q = C1W_QR + e % (C1W_Q - C1W_QR);
+        xs[line * C1W_QS + q] = (__bf16)0.0f;
+    }
+
+    // staging tasks of this lane: task t = lane + 64 k is (c, r, qp) in
+    // row-major order, so neighbouring lanes read neighbouring dwords
+    int toff[C1W_TPL];  // byte offset of dword 2 qp within the frame, relative to row 4 i0
+    int tlds[C1W_TPL];  // element offset of [c][r][0][0][2 qp] in the stage
+    int tch[C1W_TPL];
+#pragma unroll
+    for (int k = 0; k < C1W_TPL; ++k) {
+        const int t = min(lane + 64 * k, C1W_TASKS - 1);
+        const int c = t / (C1W_XR * C1W_QR / 2), rq = t - c * (C1W_XR * C1W_QR / 2);
+        const int r = rq / (C1W_QR / 2), qp = rq - r * (C1W_QR / 2);
+        tch[k] = c;
+        toff[k] = r * IN_W + 8 * qp;
+        tlds[k] = ((c * C1W_XR + r) * 4) * 2 * C1W_QS + 2 * qp;
+    }
+    const float* dzg = dz1 + (int64_t)g * n * P1 * C1;
+
+    float av[3][8];            // dz1 of the next unit's three steps (this lane's pixels)
+    uint32_t xw[C1W_TPL][3];   // three input dwords per staging task of the next unit
+    uint64_t fptr = 0;         // lane l: channel 2 p + l % 2 of the next fetch's sample
+    auto load_ptrs = [&](int u) {
+        const int b = u / C1W_UNITS;
+        fptr = ((const uint64_t*)ftab)[((int64_t)g * n + b) * 4 + C1W_CPW * cp + (lane & 1)];
+    };
     auto fetch = [&](int u) {
         const int b = u / C1W_UNITS, i0 = (u - b * C1W_UNITS) * C1W_UR;
-        const float* dsrc = dz1 + (((int64_t)g * n + b) * P1 + i0 * H1) * C1;
-#pragma unroll
-        for (int k = 0; k < 2; ++k) dq[k] = ld4(dsrc + 4 * (dz_lane ? dq0 + 8 * k : 0));
-        const uint8_t* const* fr = ftab + ((int64_t)g * n + b) * 4;
-        const uint8_t* f0 = fr[0];
-        const uint8_t* f1 = fr[1];
-        const uint8_t* f2 = fr[2];
-        const uint8_t* f3 = fr[3];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int w = tid + 256 * k;  // word w: channel w / 252
-            const int c = w / (C1W_XW / IN_C);
-            const uint8_t* f = c == 0 ? f0 : c == 1 ? f1 : c == 2 ? f2 : f3;
-            const bool ok = w < C1W_XW && f != nullptr;
-            const int wi = w - c * (C1W_XW / IN_C);
-            // branch-free: a null frame or a spare lane reads dz1 instead
-            const uint32_t v = ldg_u32(ok ? f + S1 * i0 * IN_W + 4 * wi : (const uint8_t*)dsrc);
-            xw[k] = ok ? v : 0u;
-        }
-    };
-    float bsum[4] = {0.f, 0.f, 0.f, 0.f};  // db1 of o = 4 (tid % 8) + e
-    auto stage = [&](C1wStage<WP>& sg) {
-        if (dz_lane) {  // two pixels, one packed pair of columns per channel and plane
-            const int pu = 2 * (tid >> 3), o0 = 4 * (tid & 7);
-            const int col = (pu / H1) * C1W_JP + pu % H1;  // even
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                float v0 = dq[0][e], v1 = dq[1][e];
-                bsum[e] += v0;
-                bsum[e] += v1;
-#pragma unroll
-                for (int pl = 0; pl < WP; ++pl) {
-                    const __bf16 h0 = (__bf16)v0, h1 = (__bf16)v1;
-                    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-                    *(bf16x2*)&sg.d[pl][o0 + e][col] = bf16x2{h0, h1};
-                    v0 -= (float)h0;  // exact remainders
-                    v1 -= (float)h1;
-                }
-            }
-        }
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int w = tid + 256 * k;
-            if (w < C1W_XW) {
-                const int c = w / (C1W_XW / IN_C), wi = w - c * (C1W_XW / IN_C);
-                const int r = (4 * wi) / IN_W, q0 = ((4 * wi) % IN_W) / 4;
-#pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    const __bf16 h = (__bf16)(float)((xw[k] >> (8 * m)) & 255u);
-                    sg.x[c][r][m][0][q0] = h;
-                    if (q0 > 0) sg.x[c][r][m][1][q0 - 1] = h;
-                }
-            }
-        }
-    };
-
-    f32x16 acc[2] = {f32x16{}, f32x16{}};
-    const int h = lane >> 5;
-    if (u0 < u1) fetch(u0);
-    __syncthreads();  // the zero fill is complete
-    for (int u = u0; u < u1; ++u) {
-        C1wStage<WP>& sg = stg[u & 1];
-        stage(sg);
-        __syncthreads();
-        if (u + 1 < u1) fetch(u + 1);
+        const float* dsrc = dzg + ((int64_t)b * P1 + i0 * H1) * C1 + o;
 #pragma unroll
         for (int st = 0; st < 3; ++st) {
             const int grp = 2 * st + h, ir = grp / 3, j0 = 8 * (grp % 3);
+#pragma unroll
+            for (int t = 0; t < 8; ++t)  // j >= 20: a padding pixel (address clamped)
+                av[st][t] = dsrc[(ir * H1 + min(j0 + t, H1 - 1)) * C1];
+        }
+        auto lane_ptr = [&](int l) {
+            const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)fptr, l);
+            const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(fptr >> 32), l);
+            const uint8_t* f = (const uint8_t*)(((uint64_t)hi << 32) | lo);
+            return f ? f + S1 * i0 * IN_W : zero_frame;
+        };
+        const uint8_t* f0 = lane_ptr(0);
+        const uint8_t* f1 = lane_ptr(1);
+        if (u + 1 < u1) load_ptrs(u + 1);
+#pragma unroll
+        for (int k = 0; k < C1W_TPL; ++k) {
+            const uint8_t* base = (tch[k] == 0 ? f0 : f1) + toff[k];
+#pragma unroll
+            for (int d = 0; d < 3; ++d) xw[k][d] = ldg_u32(base + 4 * d);  // dwords <= 20: in the row
+        }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int k = 0; k < C1W_TPL; ++k) {
+            if (k + 1 == C1W_TPL && lane + 64 * k >= C1W_TASKS) break;  // the last task's spare lanes
+            const uint32_t w0 = xw[k][0], w1 = xw[k][1], w2 = xw[k][2];
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const __bf16 b0 = (__bf16)(float)((w0 >> (8 * m)) & 255u);
+                const __bf16 b1 = (__bf16)(float)((w1 >> (8 * m)) & 255u);
+                const __bf16 b2 = (__bf16)(float)((w2 >> (8 * m)) & 255u);
+                // s = 0: entries q, q + 1 (bytes of dwords q, q + 1); s = 1: bytes of q + 1, q + 2
+                *(bf16x2*)(xs + tlds[k] + (2 * m) * C1W_QS) = bf16x2{b0, b1};
+                *(bf16x2*)(xs + tlds[k] + (2 * m + 1) * C1W_QS) = bf16x2{b1, b2};
+            }
+        }
+    };
+
+    f32x16 acc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[t] = f32x16{};
+    float bsum = 0.0f;
+    const int col = lane & 31, uu = col >> 2, mm = col & 3;
+    if (u0 < u1) {
+        load_ptrs(u0);
+        fetch(u0);
+    }
+    for (int u = u0; u < u1; ++u) {
+        float cur[3][8];
+#pragma unroll
+        for (int st = 0; st < 3; ++st)
+#pragma unroll
+            for (int t = 0; t < 8; ++t) cur[st][t] = av[st][t];
+        stage();  // the previous unit's LDS reads were all waited for by its products
+        if (u + 1 < u1) fetch(u + 1);  // in flight during the products
+#pragma unroll
+        for (int st = 0; st < 3; ++st) {
+            const int grp = 2 * st + h, ir = grp / 3, j0 = 8 * (grp % 3);
+            // every tile's operand first, so the products below run back to back
+            bf16x8 bx[4];
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                bx[t] = *(const bf16x8*)&sg.x[t >> 1][S1 * ir + uu][mm][t & 1][j0];
+            // planes of the eight values, two at a time: a packed round to
+            // bf16, the two rounded values widened back, the exact remainders
             bf16x8 a[WP];
 #pragma unroll
-            for (int pl = 0; pl < WP; ++pl)
-                a[pl] = *(const bf16x8*)&sg.d[pl][lane & 31][ir * C1W_JP + j0];
+            for (int t = 0; t < 8; t += 2) {
+                float v0 = cur[st][t], v1 = cur[st][t + 1];
+                if (t < 4 || j0 + t < H1) {  // db1: real pixels only (j0 is 0, 8 or 16)
+                    bsum += v0;
+                    bsum += v1;
+                }
 #pragma unroll
-            for (int tt = 0; tt < 2; ++tt) {
-                const int nc = 64 * wave + 32 * tt + (lane & 31);
-                const int c = nc >> 6, uu = (nc >> 3) & 7, v = nc & 7;
-                const bf16x8 bx = *(const bf16x8*)&sg.x[c][S1 * ir + uu][v & 3][v >> 2][j0];
-#pragma unroll
-                for (int pl = 0; pl < WP; ++pl)
-                    acc[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[pl], bx, acc[tt], 0, 0, 0);
+                for (int pl = 0; pl < WP; ++pl) {
+                    const bf16x2 hp = __builtin_convertvector(f32x2{v0, v1}, bf16x2);
+                    a[pl][t] = hp[0];
+                    a[pl][t + 1] = hp[1];
+                    if (pl + 1 < WP) {
+                        const uint32_t bits = __builtin_bit_cast(uint32_t, hp);
+                        v0 -= __uint_as_float(bits << 16);
+                        v1 -= __uint_as_float(bits & 0xffff0000u);
+                    }
+                }
             }
+#pragma unroll
+            for (int pl = 0; pl < WP; ++pl)
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[pl], bx[t], acc[t], 0, 0, 0);
         }
     }
 
+    // Add the four waves of each channel pair in LDS: waves 0, 1 of the pair
+    // store to planes 0, 1, waves 2, 3 add theirs, then the workgroup writes
+    // (w0 + w2) + (w1 + w3).
+    __syncthreads();  // every wave is done with its stage
+    float* red = (float*)smem;
+    auto at = [&](int t, int r) {  // element (o, n) of accumulator t, register r
+        const int row = 8 * (r >> 2) + 4 * h + (r & 3);
+        const int c = C1W_CPW * cp + (t >> 1), s = t & 1, v = 4 * s + mm;
+        return row * 256 + c * 64 + uu * 8 + v;
+    };
+    if (wq < 2) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) red[wq * C1 * 256 + at(t, r)] = acc[t][r];
+    }
+    if (cp == 0) bred[wq][h][o] = bsum;
+    __syncthreads();
+    if (wq >= 2) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) red[(wq - 2) * C1 * 256 + at(t, r)] += acc[t][r];
+    }
+    __syncthreads();
     const int split = g * S + x;
     float* out = partial + (int64_t)split * C1 * 256;
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-            out[(8 * (r >> 2) + 4 * h + (r & 3)) * 256 + 64 * wave + 32 * tt + (lane & 31)] =
-                acc[tt][r] * (1.0f / 255.0f);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) bred[tid >> 3][4 * (tid & 7) + e] = bsum[e];
-    __syncthreads();
+    for (int e = tid; e < C1 * 256 / 4; e += 64 * C1W_WAVES) {
+        const f32x4 p0 = *(const f32x4*)(red + 4 * e), p1 = *(const f32x4*)(red + C1 * 256 + 4 * e);
+        *(f32x4*)(out + 4 * e) = (p0 + p1) * (1.0f / 255.0f);
+    }
     if (tid < C1) {
         float t = 0.0f;
-        for (int k = 0; k < 256 / 8; ++k) t += bred[k][tid];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) t += bred[w][0][tid] + bred[w][1][tid];
         bias_part[(int64_t)split * 64 + tid] = t;
     }
 }
 
-void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int groups, int n,
-                        float* partial, float* bias_part, int max_splits, int* splits_out,
-                        bool bf16, hipStream_t st) {
+void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, const uint8_t* zero_frame,
+                        int groups, int n, float* partial, float* bias_part, int max_splits,
+                        int* splits_out, bool bf16, hipStream_t st) {
     if (n <= 0) {
         *splits_out = 0;
         return;
     }
-    // splits per group: one round of two workgroups per CU, each over a
-    // contiguous range of at least two units (at batch 32 one unit each left
-    // the final reduction 320 partials per element: 10 -> 8 us for it, +0.5
-    // here); groups * splits stays within max_splits
-    const int splits = max(1, min((n * C1W_UNITS + 1) / 2, min(C1W_TARGET, max_splits) / groups));
+    // splits per group: one workgroup per CU in all, each of whose four waves
+    // per channel pair gets at least one unit; groups * splits stays within
+    // max_splits
+    const int splits = max(1, min((n * C1W_UNITS + 3) / 4, min(C1W_WGS, max_splits) / groups));
     *splits_out = splits;
     if (bf16)
-        conv1_wgrad_mfma16_kernel<1><<<dim3(splits, groups), 256, 0, st>>>(dz1, ftab, n, partial, bias_part);
+        conv1_wgrad_mfma16_kernel<1><<<dim3(splits, groups), 64 * C1W_WAVES, 0, st>>>(
+            dz1, ftab, zero_frame, n, partial, bias_part);
     else
-        conv1_wgrad_mfma16_kernel<3><<<dim3(splits, groups), 256, 0, st>>>(dz1, ftab, n, partial, bias_part);
+        conv1_wgrad_mfma16_kernel<3><<<dim3(splits, groups), 64 * C1W_WAVES, 0, st>>>(
+            dz1, ftab, zero_frame, n, partial, bias_part);
 }
 
 }  // namespace gorila

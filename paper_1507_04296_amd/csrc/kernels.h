@@ -166,8 +166,10 @@ int launch_conv3_backward(const float* dz3, const GroupPtrs& w3d, int groups, co
 int launch_conv2_backward(const float* dz2, const GroupPtrs& w2p, int groups, const float* h1,
                           int n, float* dz1, float* partial, float* bias_part, int kp, bool bf16,
                           hipStream_t st);
-// ftab: [groups * n][4] frame pointers of the online states.
-void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, int groups, int n,
+// ftab: [groups * n][4] frame pointers of the online states (null: zero-filled);
+// zero_frame: FRAME_BYTES of zeros, read in place of a null frame.
+void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, const uint8_t* zero_frame,
+                        int groups, int n,
                         float* partial, float* bias_part, int max_splits, int* splits_out,
                         bool bf16, hipStream_t st);
 // Conv weight-gradient partials [group][split][o][(tap, c)], bias partials
