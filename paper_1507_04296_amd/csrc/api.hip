@@ -261,7 +261,7 @@ int forward_one(gorila_ctx* c, char* base, const Plan& p, const gorila_params* p
     // forward-only calls compute in fp32 (bf16 parameters are widened exactly)
     { StageTimer t(c, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 1, n, fp(p.h1), false, st); }
     const SplitWs sw = split_ws(c, base, p);
-    { StageTimer t(c, ST_CONV2_FWD); launch_conv2_fwd(fp(p.h1), w2t, th, 1, n, fp(p.h2), false, st); }
+    { StageTimer t(c, ST_CONV2_FWD); launch_conv2_fwd(fp(p.h1), w2t, th, 1, n, fp(p.h2), sw, false, st); }
     { StageTimer t(c, ST_CONV3_FWD); launch_conv3_fwd(fp(p.h2), w3t, th, 1, n, fp(p.h3), sw, false, st); }
     { StageTimer t(c, ST_FC1_FWD); *fc1_splits = launch_fc1_fwd(fp(p.h3), th, GroupPtrs16{}, 1, n, fp(p.fc1part), false, st); }
     return check_launch();
@@ -661,7 +661,7 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
     float* fc1part = at<float>(ctx, p.fc1part);
     { StageTimer t(ctx, ST_CONV1_FWD); launch_conv1_fwd(ftab, th, 2 * G, b, h1, bf16, st); }
     const SplitWs sw = split_ws(ctx, p);
-    { StageTimer t(ctx, ST_CONV2_FWD); launch_conv2_fwd(h1, w2t, th, 2 * G, b, h2, bf16, st); }
+    { StageTimer t(ctx, ST_CONV2_FWD); launch_conv2_fwd(h1, w2t, th, 2 * G, b, h2, sw, bf16, st); }
     { StageTimer t(ctx, ST_CONV3_FWD); launch_conv3_fwd(h2, w3t, th, 2 * G, b, h3, sw, bf16, st); }
     int S = 0;
     { StageTimer t(ctx, ST_FC1_FWD); S = launch_fc1_fwd(h3, th, w4f, 2 * G, b, fc1part, bf16, st); }

@@ -201,7 +201,9 @@ struct Bf16Tile {
 constexpr int BF_ACT_FWD = 2, BF_WEIGHT = 1, BF_GRAD = 1, BF_ACT_WGRAD = 1;
 
 // PA, PB: bf16 planes of A and B (0 and 0: the fp32 engine).
-template <int BM, int BN, int AMODE, int BMODE, int PA = 0, int PB = 0>
+// SB: one LDS stage instead of two (half the LDS, so more workgroups are
+// resident on a compute unit, at two barriers a chunk instead of one).
+template <int BM, int BN, int AMODE, int BMODE, int PA = 0, int PB = 0, bool SB = false>
 struct GemmShape {
     static_assert((PA > 0) == (PB > 0) && PA <= 2 && PB <= 2, "both operands fp32, or both bf16");
     using LA = LdsTile<BM, AMODE>;
@@ -209,7 +211,7 @@ struct GemmShape {
     using TA = Bf16Tile<BM, PA ? PA : 1>;
     using TB = Bf16Tile<BN, PB ? PB : 1>;
     static constexpr int STAGE_FLOATS = PA ? (TA::BYTES + TB::BYTES) / 4 : LA::SIZE + LB::SIZE;
-    static constexpr int SMEM_FLOATS = 2 * STAGE_FLOATS;
+    static constexpr int SMEM_FLOATS = (SB ? 1 : 2) * STAGE_FLOATS;
 };
 
 // One piece of a tile whose reduction is cut into np pieces run by different
@@ -266,13 +268,13 @@ struct SplitPiece {
 // set of every access are compile-time constants: LDS is then addressed with
 // ds_read/ds_write, and each global load is waited for only where its data is
 // stored to LDS, one chunk later.
-template <int BM, int BN, int WAVES_M, int AMODE, int BMODE, int PA = 0, int PB = 0, class LoadA,
-          class LoadB, class Epi>
+template <int BM, int BN, int WAVES_M, int AMODE, int BMODE, int PA = 0, int PB = 0,
+          bool SB = false, class LoadA, class LoadB, class Epi>
 __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
                                           LoadA& la, LoadB& lb, Epi& epi,
                                           float* rowsum_out = nullptr,
                                           const SplitPiece& sp = SplitPiece{}) {
-    using SH = GemmShape<BM, BN, AMODE, BMODE, PA, PB>;
+    using SH = GemmShape<BM, BN, AMODE, BMODE, PA, PB, SB>;
     using LA = typename SH::LA;
     using LB = typename SH::LB;
     using TA = typename SH::TA;
@@ -425,33 +427,61 @@ __device__ __forceinline__ void mfma_gemm(float* smem, int kc_begin, int kc_end,
         }
     };
 
-    if (kc_begin < kc_end) {
-        gload(kc_begin, ra0, rb0);
-        if (kc_begin + 1 < kc_end) gload(kc_begin + 1, ra1, rb1);
-        sstore(smem, ra0, rb0);
-    }
-    // the mask loads were issued before the first chunk's, whose data is in
-    // LDS by now, so packing them here waits for nothing more
-    if constexpr (MASK) pack_mask();
-    __syncthreads();
-    // One exit, so the accumulators stay in the same registers on every trip
-    // (an exit between the two halves makes the compiler copy them).
-    int kc = kc_begin;
-    for (; kc + 1 < kc_end; kc += 2) {
-        // even chunk: LDS buffer 0, refill register set 0 with chunk kc+2
-        if (kc + 2 < kc_end) gload(kc + 2, ra0, rb0);
-        compute(smem);
-        sstore(smem + STAGE, ra1, rb1);
+    if constexpr (SB) {
+        // One LDS stage: a chunk is stored, then multiplied, with the next
+        // chunk's global loads in flight meanwhile.
+        if (kc_begin < kc_end) gload(kc_begin, ra0, rb0);
+        // the mask loads were issued before the first chunk's, so packing
+        // them here does not wait for that chunk
+        if constexpr (MASK) pack_mask();
+        int kc = kc_begin;
+        for (; kc + 1 < kc_end; kc += 2) {
+            sstore(smem, ra0, rb0);
+            gload(kc + 1, ra1, rb1);
+            __syncthreads();
+            compute(smem);
+            __syncthreads();
+            sstore(smem, ra1, rb1);
+            if (kc + 2 < kc_end) gload(kc + 2, ra0, rb0);
+            __syncthreads();
+            compute(smem);
+            __syncthreads();
+        }
+        if (kc < kc_end) {
+            sstore(smem, ra0, rb0);
+            __syncthreads();
+            compute(smem);
+            __syncthreads();
+        }
+    } else {
+        if (kc_begin < kc_end) {
+            gload(kc_begin, ra0, rb0);
+            if (kc_begin + 1 < kc_end) gload(kc_begin + 1, ra1, rb1);
+            sstore(smem, ra0, rb0);
+        }
+        // the mask loads were issued before the first chunk's, whose data is in
+        // LDS by now, so packing them here waits for nothing more
+        if constexpr (MASK) pack_mask();
         __syncthreads();
-        // odd chunk: LDS buffer 1, refill register set 1 with chunk kc+3
-        if (kc + 3 < kc_end) gload(kc + 3, ra1, rb1);
-        compute(smem + STAGE);
-        if (kc + 2 < kc_end) sstore(smem, ra0, rb0);
-        __syncthreads();
-    }
-    if (kc < kc_end) {  // an odd chunk count ends in buffer 0
-        compute(smem);
-        __syncthreads();
+        // One exit, so the accumulators stay in the same registers on every trip
+        // (an exit between the two halves makes the compiler copy them).
+        int kc = kc_begin;
+        for (; kc + 1 < kc_end; kc += 2) {
+            // even chunk: LDS buffer 0, refill register set 0 with chunk kc+2
+            if (kc + 2 < kc_end) gload(kc + 2, ra0, rb0);
+            compute(smem);
+            sstore(smem + STAGE, ra1, rb1);
+            __syncthreads();
+            // odd chunk: LDS buffer 1, refill register set 1 with chunk kc+3
+            if (kc + 3 < kc_end) gload(kc + 3, ra1, rb1);
+            compute(smem + STAGE);
+            if (kc + 2 < kc_end) sstore(smem, ra0, rb0);
+            __syncthreads();
+        }
+        if (kc < kc_end) {  // an odd chunk count ends in buffer 0
+            compute(smem);
+            __syncthreads();
+        }
     }
     if (BM <= 64 && do_rowsum) {
         // the LDS buffers are free after the loop's last barrier
@@ -619,11 +649,12 @@ struct TailSplit {
 //    adds a round trip to the hand-off, so more pieces measured slower;
 //  - otherwise the r = launch_tiles mod cus excess tiles, taken from this
 //    job, in up to 16 pieces, about one per unit -- only when the whole tiles
-//    fit in one round of four workgroups per unit (the LDS residency of these
-//    GEMM kernels), so that the pieces start alongside them: behind a full
-//    round they would only start as whole tiles finish (measured no faster).
+//    fit in one round of `slots` workgroups per unit (the residency of the
+//    kernel: four for the double-buffered GEMMs here), so that the pieces
+//    start alongside them: behind a full round they would only start as whole
+//    tiles finish (measured no faster).
 inline TailSplit plan_split(float* ws, int* cnt, int cus, int launch_tiles, int job_tiles,
-                            int chunks) {
+                            int chunks, int slots = 4) {
     TailSplit ts;
     ts.ws = ws;
     ts.cnt = cnt;
@@ -636,7 +667,7 @@ inline TailSplit plan_split(float* ws, int* cnt, int cus, int launch_tiles, int 
     } else {
         if (launch_tiles < cus) return ts;
         r = launch_tiles % cus;
-        if (r == 0 || r > job_tiles || launch_tiles - r > 4 * cus) return ts;
+        if (r == 0 || r > job_tiles || launch_tiles - r > slots * cus) return ts;
         if (cus / r < p) p = cus / r;
     }
     if (p < 2 || r > SPLIT_MAX_TILES || r * p > SPLIT_MAX_SLOTS) return ts;
@@ -655,8 +686,14 @@ struct NoJob {
     __device__ void run(int, float*) const {}
 };
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
+// A job may ask for a minimum residency (workgroups per compute unit), which
+// caps the registers the compiler gives it: `static constexpr int MIN_WGS`.
+template <class T, class = void> struct MinWgs : std::integral_constant<int, 1> {};
+template <class T>
+struct MinWgs<T, std::void_t<decltype(T::MIN_WGS)>> : std::integral_constant<int, T::MIN_WGS> {};
 template <class J1, class J2, class J3>
-__global__ __launch_bounds__(256) void jobs_kernel(J1 a, J2 b, J3 c) {
+__global__ __launch_bounds__(256, cmax(MinWgs<J1>::value, cmax(MinWgs<J2>::value, MinWgs<J3>::value)))
+void jobs_kernel(J1 a, J2 b, J3 c) {
     __shared__ __attribute__((aligned(16))) float smem[cmax(J1::SMEM, cmax(J2::SMEM, J3::SMEM))];
     int bid = blockIdx.x;
     const int na = a.blocks();

@@ -118,7 +118,7 @@ struct SplitWs {
     int cus = 0;  // compute units of the device
 };
 void launch_conv2_fwd(const float* h1, const GroupPtrs& w2t, const GroupPtrs& theta, int groups,
-                      int n, float* h2, bool bf16, hipStream_t st);
+                      int n, float* h2, const SplitWs& sw, bool bf16, hipStream_t st);
 void launch_conv3_fwd(const float* h2, const GroupPtrs& w3t, const GroupPtrs& theta, int groups,
                       int n, float* h3, const SplitWs& sw, bool bf16, hipStream_t st);
 // fc1 forward as split-K partial sums partial[g][s][b][512]; returns the

@@ -126,38 +126,56 @@ struct BiasReluStore {
     }
 };
 
-template <int BF>
+// The fp32 job keeps one LDS stage (16 KB): with 80 registers six workgroups
+// are resident on a compute unit, so at batch 512 (1296 tiles, 5 a unit and
+// 16 over) the whole tiles take one round and the last 16 tiles run as
+// reduction pieces beside them, instead of a second round on 16 units.
+template <int BF, bool SPLIT = false>
 struct Conv2FwdJob {
     const float* h1;
     GroupPtrs w2t, theta;
     float* h2;
     int n, groups;
-    static constexpr int PA = BF ? BF_ACT_FWD : 0, PB = BF ? BF_WEIGHT : 0;
-    using SH = GemmShape<64, 64, KMAJ, KMAJ, PA, PB>;
+    TailSplit ts;
+    static constexpr int PA = BF ? BF_ACT_FWD : 0, PB = BF ? BF_WEIGHT : 0, CHUNKS = 16;
+    static constexpr bool SB = BF == 0;
+    static constexpr int MIN_WGS = SB ? 6 : 1;  // 80 registers at most
+    using SH = GemmShape<64, 64, KMAJ, KMAJ, PA, PB, SB>;
     static constexpr int SMEM = SH::SMEM_FLOATS;
     __host__ __device__ int tiles() const { return (n * P2 + 63) / 64; }
-    __host__ __device__ int blocks() const { return pad_xcd(tiles() * groups); }
+    __host__ __device__ int blocks() const {
+        return SPLIT ? ts.blocks(tiles() * groups) : pad_xcd(tiles() * groups);
+    }
     __device__ void run(int bid, float* smem) const {
-        const int t = xcd_tile(bid, blocks());
-        if (t >= tiles() * groups) return;
+        int t, k0 = 0, k1 = CHUNKS;
+        SplitPiece sp;
+        if constexpr (SPLIT) {
+            if (!ts.map(bid, tiles() * groups, CHUNKS, t, k0, k1, sp)) return;
+        } else {
+            t = xcd_tile(bid, blocks());
+            if (t >= tiles() * groups) return;
+        }
         const int g = t / tiles(), m0 = (t % tiles()) * 64;
         const int rows = n * P2;
         Conv2FwdA la{h1 + (int64_t)g * n * P1 * C1, rows, m0};
         WtapB<C1, C2> lb{w2t.p[g]};
         BiasReluStore epi{h2 + (int64_t)g * n * P2 * C2, theta.p[g] + OFF_B2, rows, m0, C2};
-        mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, 0, 16, la, lb, epi);
+        if (sp.np == 1) mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB, SB>(smem, 0, CHUNKS, la, lb, epi);
+        else mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB, SB>(smem, k0, k1, la, lb, epi, nullptr, sp);
     }
 };
 
-// No TailSplit here: at batch 512 the 1296 whole tiles more than fill the
-// four LDS slots of every compute unit, so pieces could only start once whole
-// tiles finish, and measured no faster than the unsplit launch; at batch 32
-// two pieces a tile measured no faster either.
 void launch_conv2_fwd(const float* h1, const GroupPtrs& w2t, const GroupPtrs& theta, int groups,
-                      int n, float* h2, bool bf16, hipStream_t st) {
+                      int n, float* h2, const SplitWs& sw, bool bf16, hipStream_t st) {
     if (n <= 0) return;
-    if (bf16) launch_jobs(st, Conv2FwdJob<1>{h1, w2t, theta, h2, n, groups});
-    else      launch_jobs(st, Conv2FwdJob<0>{h1, w2t, theta, h2, n, groups});
+    if (bf16) {
+        launch_jobs(st, Conv2FwdJob<1>{h1, w2t, theta, h2, n, groups});
+        return;
+    }
+    const int T = (n * P2 + 63) / 64 * groups;
+    const TailSplit ts = plan_split(sw.ws, sw.cnt, sw.cus, T, T, Conv2FwdJob<0>::CHUNKS, 6);
+    if (ts.tail) launch_jobs(st, Conv2FwdJob<0, true>{h1, w2t, theta, h2, n, groups, ts});
+    else launch_jobs(st, Conv2FwdJob<0>{h1, w2t, theta, h2, n, groups, ts});
 }
 
 // ---------------------------------------------------------------------------
