@@ -62,6 +62,7 @@ def stage_flops(stage: str, B: int, A: int) -> float:
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "traffic_learner_b512_a6.json")
+STATS_PROFILE = os.path.join(ROOT, "profiles", "learner_b512_a6_kernel_stats.json")
 
 
 def library_digest() -> str:
@@ -86,6 +87,37 @@ def stored_traffic(stage: str, B: int, A: int):
     k = prof["kernels"][stage]
     return (k["fetch_kib"] / prof["copy_fetch_factor"] +
             k["write_kib"] / prof["copy_write_factor"]) * 1024.0
+
+
+def stored_launch_ms(stage: str, B: int, A: int):
+    """(average ms per launch of `stage`, profile file) from the committed
+    rocprofv3 kernel statistics, or None when the library has been rebuilt
+    differently since they were taken, or for another workload."""
+    try:
+        prof = json.load(open(STATS_PROFILE))
+    except (OSError, ValueError):
+        return None
+    if prof.get("library_sha256") != library_digest() or prof.get("batch") != B \
+            or prof.get("n_actions") != A or stage not in prof.get("stages", {}):
+        return None
+    return prof["stages"][stage]["avg_us"] / 1e3, os.path.relpath(STATS_PROFILE, ROOT)
+
+
+def host_cpu():
+    """The host's CPU model and core counts (for the CPU baseline)."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = None
+    return {"cpu_model": model, "nproc": os.cpu_count(), "usable_cpus": usable}
 
 
 def step_percentiles(torch, fn, steps):
@@ -428,7 +460,7 @@ def cpu_baseline(datagen, B, A, seed, seconds):
         if dt >= seconds:
             break
     out = {"value": steps * B / dt, "unit": "transitions/s", "cores": oracle.num_threads(),
-           "kind": "oracle",
+           "kind": "oracle", "host": host_cpu(),
            "sample": f"{steps} fp64 learner steps of the batch-{B} workload "
                      f"({steps * B} transitions, {dt:.1f} s)"}
     # one host thread, on the first 64 rows of the same workload (per-transition
@@ -472,7 +504,7 @@ def main():
                     help="skip the one-million-frame ring gather / learner line")
     ap.add_argument("--no-ps", action="store_true",
                     help="skip the parameter-server apply / loss-filter line")
-    ap.add_argument("--only", choices=("actor", "grouped"), default=None,
+    ap.add_argument("--only", choices=("actor", "grouped", "ring"), default=None,
                     help="only run that companion measurement and print its object "
                          "(profiles its kernels alone)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -508,6 +540,10 @@ def main():
         print(json.dumps({"grouped": run_grouped(torch, g, datagen, max(args.steps // 2, 5),
                                                  args.warmup)}), flush=True)
         return
+    if args.only == "ring":
+        print(json.dumps({"ring": run_ring(torch, g, datagen, max(args.steps, 20), args.warmup)}),
+              flush=True)
+        return
 
     B, A = args.batch, args.actions
     seed = datagen.SEED_BASE + 2
@@ -542,6 +578,15 @@ def main():
         "step_ms_p10_p50_p90": r["pct"],
         "stages": stages,
     }
+    # the same kernel's average from the committed rocprofv3 statistics (another
+    # box and run: boxes differ by a few percent), beside the live figure
+    prof_ms = stored_launch_ms(r["dominant"], B, A)
+    if prof_ms is not None:
+        out["roofline"]["profile"] = {
+            "file": prof_ms[1], "avg_launch_ms": round(prof_ms[0], 4),
+            "achieved": round(dom_flops / (prof_ms[0] * 1e-3) / 1e12, 2),
+            "frac": round(dom_flops / (prof_ms[0] * 1e-3) / 1e12 / FP32_MFMA_PEAK_TFLOPS, 4),
+            "live_vs_profile": round(r["dominant_ms"] / prof_ms[0], 4)}
     if not args.no_b32:
         r32 = run_learner(torch, g, datagen, 32, 18, datagen.SEED_BASE + 0, max(args.steps, 50),
                           args.warmup, graph=True)
