@@ -166,11 +166,24 @@ struct Bf16Tile {
     // are 4 reduction indices of one row, RMAJ quads 4 rows at one index.
     template <int MODE>
     __device__ static inline void put(char* s, int row, int k, f32x4 v) {
-        bf16x4 hi, lo;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            hi[e] = (__bf16)v[e];
-            if (PL == 2) lo[e] = (__bf16)(v[e] - (float)hi[e]);  // the difference is exact
+        // two values per rounding instruction; a rounded pair widens back by
+        // moving each half to the top of a word, and the residual is exact
+        typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+        typedef float f32x2 __attribute__((ext_vector_type(2)));
+        const bf16x2 h01 = __builtin_convertvector(f32x2{v[0], v[1]}, bf16x2);
+        const bf16x2 h23 = __builtin_convertvector(f32x2{v[2], v[3]}, bf16x2);
+        const bf16x4 hi = __builtin_shufflevector(h01, h23, 0, 1, 2, 3);
+        bf16x4 lo;
+        if (PL == 2) {
+            const uint32_t b01 = __builtin_bit_cast(uint32_t, h01);
+            const uint32_t b23 = __builtin_bit_cast(uint32_t, h23);
+            const bf16x2 l01 = __builtin_convertvector(
+                f32x2{v[0] - __uint_as_float(b01 << 16), v[1] - __uint_as_float(b01 & 0xffff0000u)},
+                bf16x2);
+            const bf16x2 l23 = __builtin_convertvector(
+                f32x2{v[2] - __uint_as_float(b23 << 16), v[3] - __uint_as_float(b23 & 0xffff0000u)},
+                bf16x2);
+            lo = __builtin_shufflevector(l01, l23, 0, 1, 2, 3);
         }
         if (MODE == KMAJ) {
             const int off = chunk(row, k >> 3) + ((k & 4) << 1);
