@@ -145,6 +145,23 @@ def time_region(torch, fn, steps):
     return start.elapsed_time(stop) / steps
 
 
+SETTLE_S = 0.3
+
+
+def settle(torch, fn, seconds=SETTLE_S):
+    """Untimed calls until `seconds` of wall time have passed (after the W
+    warm-up calls): the GPU's clocks ramp up over milliseconds of load, and a
+    handful of sub-millisecond warm-up steps leaves the timed steps on a GPU
+    that is still speeding up.  The figure sought is the steady-state rate of
+    a learner that runs continuously."""
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(16):
+            fn()
+        torch.cuda.synchronize()
+
+
 def run_learner(torch, g, datagen, B, A, seed, steps, warmup, timed_stage=None, graph=False):
     inp = datagen.learner_inputs(seed, B, A)
     dev = torch.device("cuda:0")
@@ -157,6 +174,7 @@ def run_learner(torch, g, datagen, B, A, seed, steps, warmup, timed_stage=None, 
     step = lambda: g.gorila_learner_step(ctx, theta, tgt, A, rep, idx, inp.gamma, 1.0, grads, loss)
     for _ in range(warmup):
         step()
+    settle(torch, step)
     ctx.check()
 
     # per-stage profile (separate pass, every stage bracketed by events)
@@ -167,9 +185,11 @@ def run_learner(torch, g, datagen, B, A, seed, steps, warmup, timed_stage=None, 
     prof = ctx.timing_end()
 
     dominant = timed_stage or max((k for k in prof if k in MFMA_STAGES), key=lambda k: prof[k][0])
-    # timed region: events only around the dominant kernel
+    # timed region: events only around the dominant kernel, on the first
+    # quarter of the timed steps (each event pair costs the step a few
+    # microseconds; the kernel's average over those launches is the figure)
     torch.cuda.synchronize()
-    ctx.timing_begin([dominant], max_records=steps)
+    ctx.timing_begin([dominant], max_records=max(1, steps // 4))
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     start.record()
@@ -559,7 +579,7 @@ def main():
         "metric": "learner transitions/sec (DQN fwd+bwd) and % MFMA peak at batch 32/512",
         "value": round(B / (r["ms_per_step"] * 1e-3), 1),
         "unit": "transitions/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "settle_s": SETTLE_S,
         "ms_per_step": round(r["ms_per_step"], 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic",
@@ -574,6 +594,7 @@ def main():
                      "frac": round(dom_tflops / FP32_MFMA_PEAK_TFLOPS, 4),
                      "traffic": stored_traffic(r["dominant"], B, A),
                      "avg_launch_ms": round(r["dominant_ms"], 4),
+                     "launches_timed": r["dominant_launches"],
                      "flops_per_launch": dom_flops},
         "step_ms_p10_p50_p90": r["pct"],
         "stages": stages,

@@ -210,11 +210,16 @@ ReplayView view_of(const gorila_replay* rv) {
 }
 
 // Forward-only calls: the first tblocks workgroups write the frame table of
-// n stacked states, the other PREP_BLOCKS the weight transposes of one set
-// (independent, so one launch).
+// n stacked states, the next PREP_BLOCKS the weight transposes of one set and
+// the rest widen a bf16 set (independent, so one launch).
 __global__ __launch_bounds__(256) void states_prep_kernel(const uint8_t* states, int n,
                                                           const uint8_t** ftab, WeightViews wv,
-                                                          int tblocks, unsigned* zero_head) {
+                                                          int tblocks, unsigned* zero_head,
+                                                          WidenJob wj, int wpn) {
+    if ((int)blockIdx.x >= tblocks + PREP_BLOCKS) {
+        widen_part(wj, 0, blockIdx.x - tblocks - PREP_BLOCKS, wpn);
+        return;
+    }
     if ((int)blockIdx.x >= tblocks) {
         prep_weights_part(wv, blockIdx.x - tblocks, PREP_BLOCKS);
         return;
@@ -236,23 +241,24 @@ int forward_one(gorila_ctx* c, char* base, const Plan& p, const gorila_params* p
     hipStream_t st = c->stream;
     auto fp = [&](size_t off) { return (float*)(base + off); };
     const uint8_t** ftab = (const uint8_t**)(base + p.ftab);
-    WidenSet ws{};
-    int n_widen = 0;
+    WidenJob wj;
     const float* theta = (const float*)prm->data;
     if (prm->dtype != GORILA_F32) {  // exact widening into the plan's fp32 slot
-        ws.src[0] = (const uint16_t*)prm->data;
-        ws.dst[0] = fp(p.theta32);
-        n_widen = 1;
-        theta = ws.dst[0];
+        wj.set.src[0] = (const uint16_t*)prm->data;
+        wj.set.dst[0] = fp(p.theta32);
+        wj.n = 1;
+        wj.hi[0] = param_count(prm->n_actions);
+        theta = wj.set.dst[0];
     }
     *theta32 = theta;
     WeightViews wv{theta, fp(p.w2t), fp(p.w3t), nullptr, nullptr};
+    if (wj.n) wv.theta16 = wj.set.src[0];
     {
         StageTimer t(c, ST_PREP);
-        if (n_widen) launch_widen_bf16(ws, n_widen, param_count(prm->n_actions), st);
-        const int tblocks = (n * 4 + 255) / 256;
-        states_prep_kernel<<<tblocks + PREP_BLOCKS, 256, 0, st>>>(
-            states, n, ftab, wv, tblocks, zero_head ? (unsigned*)(base + p.err) : nullptr);
+        const int tblocks = (n * 4 + 255) / 256, wpn = wj.blocks_per_net();
+        states_prep_kernel<<<tblocks + PREP_BLOCKS + wpn, 256, 0, st>>>(
+            states, n, ftab, wv, tblocks, zero_head ? (unsigned*)(base + p.err) : nullptr, wj,
+            wpn > 0 ? wpn : 1);
     }
     GroupPtrs th{}, w2t{}, w3t{};
     th.p[0] = theta;
@@ -620,29 +626,24 @@ int learner_steps(gorila_ctx* ctx, const gorila_params* params, int G, bool allo
     if (bf16)
         for (int g = 0; g <= G; ++g)
             w4b.p[g] = (const uint16_t*)(g < G ? params[g].data : target_params->data) + OFF_W4;
-    if (n_widen == 0) {
-        // fp32 sets: the minibatch resolution and the weight transposes are
-        // independent and share one launch
+    WidenJob wj;
+    wj.set = widen;
+    wj.n = n_widen;
+    wj.hi[0] = bf16 ? OFF_W4 : P;
+    if (bf16) {
+        wj.lo[1] = OFF_B4;
+        wj.hi[1] = P;
+    }
+    // the transposes of a widened set read its bf16 source, so the minibatch
+    // resolution, the transposes and the widening share one launch
+    for (int g = 0; g <= G; ++g) {
+        const gorila_params& src = g < G ? params[g] : *target_params;
+        if (src.dtype == GORILA_BF16) wv[g].theta16 = (const uint16_t*)src.data;
+    }
+    {
         StageTimer t(ctx, ST_PREP);
-        launch_resolve_prep(view_of(replay), idx, B, A, ftab, a, r, term,
-                            at<unsigned>(ctx, p.err), wv, G + 1, st);
-    } else {
-        // widened sets: the transposes read the widened copies, so the shared
-        // resolve + transpose launch follows the widening
-        StageTimer t(ctx, ST_PREP);
-        if (bf16) {
-            launch_widen_bf16(widen, n_widen, OFF_W4, st);
-            WidenSet tail = widen;
-            for (int i = 0; i < n_widen; ++i) {
-                tail.src[i] += OFF_B4;
-                tail.dst[i] += OFF_B4;
-            }
-            launch_widen_bf16(tail, n_widen, P - OFF_B4, st);
-        } else {
-            launch_widen_bf16(widen, n_widen, P, st);
-        }
-        launch_resolve_prep(view_of(replay), idx, B, A, ftab, a, r, term,
-                            at<unsigned>(ctx, p.err), wv, G + 1, st);
+        launch_resolve_prep(view_of(replay), idx, B, A, ftab, a, r, term, at<unsigned>(ctx, p.err), wv,
+                            G + 1, n_widen ? &wj : nullptr, st);
     }
     // forward groups 0 .. G-1: online nets on s; G .. 2G-1: the target on s'
     GroupPtrs th{}, w2t{}, w3t{};

@@ -50,58 +50,106 @@ struct WeightViews {
     float* w3t;
     float* w3d;           // may be null (forward only)
     float* w2p;           // may be null
+    // when not null: the same parameters as bf16 bit patterns, which the
+    // transposes read (and widen exactly) instead of theta, so that they need
+    // not wait for theta's widened copy
+    const uint16_t* theta16 = nullptr;
 };
 constexpr int MAX_NETS = MAX_LEARNER_GROUPS + 1;  // learner replicas + their shared target
 struct WeightViewSet {
     WeightViews v[MAX_NETS];
 };
-void launch_prep_weights(const WeightViews* nets, int n_nets, hipStream_t st);
 
 // Block `blk` of `nblk` (256 threads each) of one net's transposes.  Every
 // destination is written in index order (coalesced); the scattered reads come
 // from the 128 KB of W2 and W3, which stay in L2.
 constexpr int PREP_BLOCKS = 64;  // blocks per net
 __device__ inline void prep_weights_part(const WeightViews& v, int blk, int nblk) {
-    const float* W2 = v.theta + OFF_W2;  // [o][c][u][v], 64 x 32 x 4 x 4
-    const float* W3 = v.theta + OFF_W3;  // [o][c][u][v], 64 x 64 x 3 x 3
+    // W2 [o][c][u][v], 64 x 32 x 4 x 4; W3 [o][c][u][v], 64 x 64 x 3 x 3
+    auto W2 = [&](int i) {
+        return v.theta16 ? __uint_as_float((uint32_t)v.theta16[OFF_W2 + i] << 16) : v.theta[OFF_W2 + i];
+    };
+    auto W3 = [&](int i) {
+        return v.theta16 ? __uint_as_float((uint32_t)v.theta16[OFF_W3 + i] << 16) : v.theta[OFF_W3 + i];
+    };
     const int stride = nblk * 256;
     for (int d = blk * 256 + (int)threadIdx.x; d < 16 * 64 * 32; d += stride) {
         {  // w2t[t][o][c], t = u*4 + v
             const int c = d & 31, o = (d >> 5) & 63, t = d >> 11;
-            v.w2t[d] = W2[((o * 32 + c) * 4 + (t >> 2)) * 4 + (t & 3)];
+            v.w2t[d] = W2(((o * 32 + c) * 4 + (t >> 2)) * 4 + (t & 3));
         }
         if (v.w2p) {  // w2p[tp][phase][c][o]: tap pair (u/2, v/2), stride phase (u%2, v%2)
             const int o = d & 63, c = (d >> 6) & 31, phase = (d >> 11) & 3, tp = d >> 13;
             const int u = (tp >> 1) * 2 + (phase >> 1), vv = (tp & 1) * 2 + (phase & 1);
-            v.w2p[d] = W2[((o * 32 + c) * 4 + u) * 4 + vv];
+            v.w2p[d] = W2(((o * 32 + c) * 4 + u) * 4 + vv);
         }
     }
     for (int d = blk * 256 + (int)threadIdx.x; d < 9 * 64 * 64; d += stride) {
         {  // w3t[t][o][c], t = u*3 + v
             const int c = d & 63, o = (d >> 6) & 63, t = d >> 12;
-            v.w3t[d] = W3[(o * 64 + c) * 9 + t];
+            v.w3t[d] = W3((o * 64 + c) * 9 + t);
         }
         if (v.w3d) {  // w3d[t][c][o]
             const int o = d & 63, c = (d >> 6) & 63, t = d >> 12;
-            v.w3d[d] = W3[(o * 64 + c) * 9 + t];
+            v.w3d[d] = W3((o * 64 + c) * 9 + t);
         }
     }
 }
 
-// Minibatch resolution and the weight transposes in one launch (they are
-// independent): the first blocks resolve the indices into frame pointers
-// ftab[2][n][4] (s then s'; null = zero-filled channel) and a/r/term per row,
-// the rest do launch_prep_weights's work.
-void launch_resolve_prep(const ReplayView& rv, const int64_t* idx, int n, int n_actions,
-                         const uint8_t** ftab, int32_t* a, float* r, uint8_t* term,
-                         unsigned* err, const WeightViews* nets, int n_nets, hipStream_t st);
-
-// Widen bf16 parameter vectors (bit patterns) to fp32 exactly: dst[i][k] = src[i][k].
+// Widening of bf16 parameter vectors (bit patterns) to fp32, exact:
+// dst[i][k] = src[i][k].
 struct WidenSet {
     const uint16_t* src[MAX_NETS];
     float* dst[MAX_NETS];
 };
-void launch_widen_bf16(const WidenSet& set, int n_nets, int64_t count, hipStream_t st);
+// Elements [lo[0], hi[0]) and [lo[1], hi[1]) of n vectors, widened by extra
+// blocks of another launch: blocks_per_net() blocks for each vector.
+struct WidenJob {
+    WidenSet set;
+    int n = 0;
+    int64_t lo[2] = {0, 0}, hi[2] = {0, 0};
+    int blocks_per_net() const {
+        const int64_t c = (hi[0] - lo[0]) + (hi[1] - lo[1]);
+        return n ? (int)(c / 4096 < 1 ? 1 : c / 4096 > 256 ? 256 : c / 4096) : 0;
+    }
+};
+// Block blk of nblk (256 threads each) of vector i's widening.
+__device__ inline void widen_part(const WidenJob& wj, int i, int blk, int nblk) {
+    const uint16_t* src0 = wj.set.src[i];
+    float* dst0 = wj.set.dst[i];
+    const int64_t tid = (int64_t)blk * 256 + threadIdx.x, stride = (int64_t)nblk * 256;
+    for (int r = 0; r < 2; ++r) {
+        const int64_t count = wj.hi[r] - wj.lo[r];
+        if (count <= 0) continue;
+        const uint16_t* src = src0 + wj.lo[r];
+        float* dst = dst0 + wj.lo[r];
+        // elements before the first 8-byte boundary of the (2-byte aligned)
+        // source and after the last whole group of four go one by one
+        const int64_t head = min<int64_t>(count, ((8 - ((uintptr_t)src & 7)) & 7) >> 1);
+        const int64_t quads = (count - head) >> 2, tail = head + 4 * quads;
+        if (tid < head) dst[tid] = __uint_as_float((uint32_t)src[tid] << 16);
+        for (int64_t q = tid; q < quads; q += stride) {
+            const int64_t e = head + 4 * q;
+            const uint2 v = *(const uint2*)(src + e);
+            dst[e] = __uint_as_float(v.x << 16);
+            dst[e + 1] = __uint_as_float(v.x & 0xffff0000u);
+            dst[e + 2] = __uint_as_float(v.y << 16);
+            dst[e + 3] = __uint_as_float(v.y & 0xffff0000u);
+        }
+        if (tail + tid < count) dst[tail + tid] = __uint_as_float((uint32_t)src[tail + tid] << 16);
+    }
+}
+
+// Minibatch resolution, the weight transposes and the parameter widening in
+// one launch (they are independent: transposes of widened sets read the bf16
+// source): the first blocks resolve the indices into frame pointers
+// ftab[2][n][4] (s then s'; null = zero-filled channel) and a/r/term per row,
+// the next the weight transposes of n_nets sets (prep_weights_part), the
+// rest wj's widening (wj may be null).
+void launch_resolve_prep(const ReplayView& rv, const int64_t* idx, int n, int n_actions,
+                         const uint8_t** ftab, int32_t* a, float* r, uint8_t* term,
+                         unsigned* err, const WeightViews* nets, int n_nets, const WidenJob* wj,
+                         hipStream_t st);
 
 // Forward layers.  `groups` parameter sets; group g owns rows [g*n, (g+1)*n)
 // of every activation buffer.  bf16: the parameter sets hold bf16 values

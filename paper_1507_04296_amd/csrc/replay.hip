@@ -8,6 +8,8 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <type_traits>
+
 namespace gorila {
 
 // Frame pointers (null = zero frame) and physical slots (-1) of s = stack(k)
@@ -101,10 +103,21 @@ __device__ Resolved resolve_one(const ReplayView& rv, int64_t k, int n_actions,
     return o;
 }
 
+// W: WidenJob, or NoWiden when no set is widened (a smaller argument block)
+struct NoWiden {};
+template <class W>
 __global__ __launch_bounds__(256) void resolve_prep_kernel(
     ReplayView rv, const int64_t* __restrict__ idx, int n, int n_actions,
     const uint8_t** __restrict__ ftab, int32_t* __restrict__ a_out, float* __restrict__ r_out,
-    uint8_t* __restrict__ term_out, unsigned* __restrict__ err, WeightViewSet set, int rblocks) {
+    uint8_t* __restrict__ term_out, unsigned* __restrict__ err, WeightViewSet set, int rblocks,
+    int pblocks, W wj, int wpn) {
+    if constexpr (!std::is_same_v<W, NoWiden>) {
+        if ((int)blockIdx.x >= rblocks + pblocks) {
+            const int q = blockIdx.x - rblocks - pblocks;
+            widen_part(wj, q / wpn, q % wpn, wpn);
+            return;
+        }
+    }
     if ((int)blockIdx.x >= rblocks) {
         const int q = blockIdx.x - rblocks;
         prep_weights_part(set.v[q / PREP_BLOCKS], q % PREP_BLOCKS, PREP_BLOCKS);
@@ -122,14 +135,21 @@ __global__ __launch_bounds__(256) void resolve_prep_kernel(
 
 void launch_resolve_prep(const ReplayView& rv, const int64_t* idx, int n, int n_actions,
                          const uint8_t** ftab, int32_t* a, float* r, uint8_t* term,
-                         unsigned* err, const WeightViews* nets, int n_nets, hipStream_t st) {
+                         unsigned* err, const WeightViews* nets, int n_nets, const WidenJob* wj,
+                         hipStream_t st) {
     WeightViewSet set{};
     for (int i = 0; i < n_nets && i < MAX_NETS; ++i) set.v[i] = nets[i];
     const int rblocks = n > 0 ? (n + 255) / 256 : 0;
-    const int blocks = rblocks + PREP_BLOCKS * min(n_nets, MAX_NETS);
-    if (blocks > 0)
+    const int pblocks = PREP_BLOCKS * min(n_nets, MAX_NETS);
+    const int wpn = wj ? wj->blocks_per_net() : 0;
+    const int blocks = rblocks + pblocks + wpn * (wj ? min(wj->n, MAX_NETS) : 0);
+    if (blocks <= 0) return;
+    if (wpn > 0)
         resolve_prep_kernel<<<blocks, 256, 0, st>>>(rv, idx, n, n_actions, ftab, a, r, term, err,
-                                                    set, rblocks);
+                                                    set, rblocks, pblocks, *wj, wpn);
+    else
+        resolve_prep_kernel<<<blocks, 256, 0, st>>>(rv, idx, n, n_actions, ftab, a, r, term, err,
+                                                    set, rblocks, pblocks, NoWiden{}, 1);
 }
 
 // The materialising gather: workgroup (b, f) resolves transition b (every
