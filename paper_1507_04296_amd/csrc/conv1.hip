@@ -4,6 +4,8 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <type_traits>
+
 namespace gorila {
 
 // The layer on v_mfma_f32_32x32x16_bf16 with exact products: the bytes
@@ -151,8 +153,8 @@ void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int gr
 // dW1[o][n] for the 256 columns n = (c, u, v) is a sum over pixels of
 // dz1[pixel][o] * byte.  The bytes are exact bf16 values; dz1 enters as WP
 // bf16 planes whose sum is dz1 exactly (three for fp32 steps, as in the
-// forward kernel; one, rounded, for bf16 steps), so only the fp32
-// accumulation rounds.
+// forward kernel), so only the fp32 accumulation rounds; bf16 steps read dz1
+// already rounded to bf16 (one plane).
 //
 // Work is cut into units of two output rows of one sample (40 pixels, padded
 // to 2 x 24 = 6 groups of 8); an MFMA step takes two groups (lane half h:
@@ -173,7 +175,7 @@ void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int gr
 // values and bytes are fetched into registers during the products; a frame
 // pointer is loaded one unit before the fetch that uses it, and a null
 // (zero-filled) frame is read from a frame of zeros.  db1 is summed from the
-// fp32 dz1 values (by the waves of channel pair 0).  At the end the four
+// dz1 values as loaded (by the waves of channel pair 0).  At the end the four
 // waves of each channel pair are added in a fixed order in LDS and one
 // partial [32][256] per workgroup is written.
 constexpr int C1W_UR = 2;                       // output rows per unit
@@ -201,9 +203,16 @@ constexpr size_t C1W_SMEM = C1W_WAVES * sizeof(C1wStage) > 4 * C1W_RED
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
+// dz1 of a bf16 step (WP = 1) arrives rounded to bf16 ([n][20][20][32] bit
+// patterns); it is widened exactly as it is loaded.
+template <int WP>
+using C1wDz = std::conditional_t<WP == 1, uint16_t, float>;
+__device__ inline float c1w_value(float v) { return v; }
+__device__ inline float c1w_value(uint16_t v) { return __uint_as_float((uint32_t)v << 16); }
+
 template <int WP>
 __global__ __launch_bounds__(64 * C1W_WAVES) void conv1_wgrad_mfma16_kernel(
-    const float* __restrict__ dz1, const uint8_t* const* __restrict__ ftab,
+    const C1wDz<WP>* __restrict__ dz1, const uint8_t* const* __restrict__ ftab,
     const uint8_t* __restrict__ zero_frame, int n, float* __restrict__ partial,
     float* __restrict__ bias_part) {
     __shared__ __attribute__((aligned(16))) char smem[C1W_SMEM];
@@ -240,7 +249,7 @@ __global__ __launch_bounds__(64 * C1W_WAVES) void conv1_wgrad_mfma16_kernel(
         toff[k] = r * IN_W + 8 * qp;
         tlds[k] = ((c * C1W_XR + r) * 4) * 2 * C1W_QS + 2 * qp;
     }
-    const float* dzg = dz1 + (int64_t)g * n * P1 * C1;
+    const C1wDz<WP>* dzg = dz1 + (int64_t)g * n * P1 * C1;
 
     float av[3][8];            // dz1 of the next unit's three steps (this lane's pixels)
     uint32_t xw[C1W_TPL][3];   // three input dwords per staging task of the next unit
@@ -251,13 +260,13 @@ __global__ __launch_bounds__(64 * C1W_WAVES) void conv1_wgrad_mfma16_kernel(
     };
     auto fetch = [&](int u) {
         const int b = u / C1W_UNITS, i0 = (u - b * C1W_UNITS) * C1W_UR;
-        const float* dsrc = dzg + ((int64_t)b * P1 + i0 * H1) * C1 + o;
+        const C1wDz<WP>* dsrc = dzg + ((int64_t)b * P1 + i0 * H1) * C1 + o;
 #pragma unroll
         for (int st = 0; st < 3; ++st) {
             const int grp = 2 * st + h, ir = grp / 3, j0 = 8 * (grp % 3);
 #pragma unroll
             for (int t = 0; t < 8; ++t)  // j >= 20: a padding pixel (address clamped)
-                av[st][t] = dsrc[(ir * H1 + min(j0 + t, H1 - 1)) * C1];
+                av[st][t] = c1w_value(dsrc[(ir * H1 + min(j0 + t, H1 - 1)) * C1]);
         }
         auto lane_ptr = [&](int l) {
             const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)fptr, l);
@@ -400,7 +409,7 @@ void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, const uint
     *splits_out = splits;
     if (bf16)
         conv1_wgrad_mfma16_kernel<1><<<dim3(splits, groups), 64 * C1W_WAVES, 0, st>>>(
-            dz1, ftab, zero_frame, n, partial, bias_part);
+            (const uint16_t*)dz1, ftab, zero_frame, n, partial, bias_part);
     else
         conv1_wgrad_mfma16_kernel<3><<<dim3(splits, groups), 64 * C1W_WAVES, 0, st>>>(
             dz1, ftab, zero_frame, n, partial, bias_part);

@@ -211,11 +211,14 @@ int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, const GroupPtr
 int launch_conv3_backward(const float* dz3, const GroupPtrs& w3d, int groups, const float* h2,
                           int n, float* dz2, float* partial, float* bias_part, int kp, bool bf16,
                           hipStream_t st);
+// dz1: fp32, or (bf16) the values rounded to bf16 in the same [n][20][20][32]
+// order, as the conv1 weight gradient below reads it.
 int launch_conv2_backward(const float* dz2, const GroupPtrs& w2p, int groups, const float* h1,
                           int n, float* dz1, float* partial, float* bias_part, int kp, bool bf16,
                           hipStream_t st);
 // ftab: [groups * n][4] frame pointers of the online states (null: zero-filled);
-// zero_frame: FRAME_BYTES of zeros, read in place of a null frame.
+// zero_frame: FRAME_BYTES of zeros, read in place of a null frame; dz1 as
+// launch_conv2_backward wrote it (bf16 bit patterns when bf16).
 void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, const uint8_t* zero_frame,
                         int groups, int n,
                         float* partial, float* bias_part, int max_splits, int* splits_out,

@@ -10,6 +10,8 @@
 #include "common.h"
 #include "kernels.h"
 
+#include <type_traits>
+
 namespace gorila {
 
 // Output positions of an N x N data-gradient grid (kernel K taps per axis
@@ -31,12 +33,26 @@ struct LongestFirst {
     }
 };
 
+// Gradients handed from one backward launch to the next (dz3, dz2): fp32, or
+// in bf16 steps whose reductions are not cut into parts (KP = 1) bf16,
+// rounded once by the producer to the precision the consumer's products take
+// them in (half the bytes written and read).
+template <int BF, int KP> using GradT = std::conditional_t<BF == 1 && KP == 1, uint16_t, float>;
+__device__ inline f32x4 ldq(const float* p) { return ld4(p); }
+__device__ inline f32x4 ldq(const uint16_t* p) {  // four bf16 values, widened exactly
+    const uint2 v = *(const uint2*)p;
+    return f32x4{__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                 __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u)};
+}
+__device__ inline void stg(float* p, float v) { *p = v; }
+__device__ inline void stg(uint16_t* p, float v) { *p = __builtin_bit_cast(uint16_t, (__bf16)v); }
+
 // Quad at p summed over the KP partial planes p, p + ps, ... in plane order.
-template <int KP>
-__device__ __forceinline__ f32x4 ld4_parts(const float* p, int64_t ps) {
-    f32x4 v = ld4(p);
+template <int KP, class T>
+__device__ __forceinline__ f32x4 ld4_parts(const T* p, int64_t ps) {
+    f32x4 v = ldq(p);
 #pragma unroll
-    for (int s = 1; s < KP; ++s) v += ld4(p + s * ps);
+    for (int s = 1; s < KP; ++s) v += ldq(p + s * ps);
     return v;
 }
 
@@ -369,7 +385,8 @@ struct RowMajorR16 {  // RowMajorR<false> over a bf16 matrix
 // conv3 backward kernels read it in 16-byte quads.
 struct Dz3NhwcStore {
     static constexpr bool MASK = true;
-    float* dz3;
+    float* dz3;       // fp32 dz3, or null
+    uint16_t* dz3h;   // bf16 dz3 (bf16 steps, one part), or null
     const float* h3;
     int rows, r0, c0;
     __device__ float pre(int row, int col) const {
@@ -380,7 +397,9 @@ struct Dz3NhwcStore {
         const int b = r0 + row;
         if (b >= rows) return;
         const int k = c0 + col, o = k / P3, p = k - o * P3;
-        dz3[(int64_t)b * FLAT + p * C3 + o] = m > 0.0f ? v : 0.0f;
+        const float r = m > 0.0f ? v : 0.0f;
+        if (dz3h) stg(dz3h + (int64_t)b * FLAT + p * C3 + o, r);
+        else stg(dz3 + (int64_t)b * FLAT + p * C3 + o, r);
     }
 };
 
@@ -421,8 +440,9 @@ struct Fc1DgradJob {
         const int r0 = (t % mt) * 64, c0 = (t / mt) * 64;  // row tiles of one W4 column block adjacent
         const int64_t rows = (int64_t)g * n;
         RowMajorK la{dz4 + rows * HID, n, r0, HID};
-        Dz3NhwcStore epi{dz3 + part * (int64_t)groups * n * FLAT + rows * FLAT, h3 + rows * FLAT, n,
-                         r0, c0};
+        const bool half = BF == 1 && kp == 1;  // dz3 as GradT<BF, kp>
+        Dz3NhwcStore epi{half ? nullptr : dz3 + part * (int64_t)groups * n * FLAT + rows * FLAT,
+                         half ? (uint16_t*)dz3 + rows * FLAT : nullptr, h3 + rows * FLAT, n, r0, c0};
         // small-batch parts keep runtime bounds; whole tiles compile-time ones
         auto gemm = [&](auto& lb) {
             if (SPLIT && sp.np > 1)
@@ -591,12 +611,12 @@ int launch_fc1_backward(const float* dz4, const GroupPtrs& theta, const GroupPtr
 // the reduction: only the 1..9 valid taps x 64 channels are multiplied.
 // rows b, cols c (64), reduction (valid tap, o) in chunks of 32 o.
 // ---------------------------------------------------------------------------
-template <int KP>
+template <int KP, class T>
 struct Conv3DgradA {  // KMAJ quads dz3[b][p][o..o+3] at p = (y-u)*7 + (x-v)
-    const float* dz3;
+    const T* dz3;
     int n, b0, y, x, u0, v0, nv;
-    int64_t ps;  // KP planes of dz3, ps floats apart
-    const float* base[MAXQ];
+    int64_t ps;  // KP planes of dz3, ps elements apart
+    const T* base[MAXQ];
     __device__ void init(int j, int row, int k) {
         const int b = b0 + row;
         base[j] = dz3 + (int64_t)(b < n ? b : 0) * FLAT + k;  // rows past n: never stored
@@ -616,9 +636,10 @@ struct Conv3DgradB {  // w3d[(u,v)][c][o], rows c, quads along o
         return ld4(base[j] + tap * C2 * C3 + (kc & 1) * BK);
     }
 };
+template <class T>
 struct Conv3DgradStore {
     static constexpr bool MASK = true;
-    float* dz2;
+    T* dz2;
     const float* h2;
     int n, b0, pos;
     __device__ float pre(int row, int col) const {
@@ -628,7 +649,7 @@ struct Conv3DgradStore {
     __device__ void operator()(int row, int col, float v, float m) const {
         const int b = b0 + row;
         if (b >= n) return;
-        dz2[((int64_t)b * P2 + pos) * C2 + col] = m > 0.0f ? v : 0.0f;
+        stg(dz2 + ((int64_t)b * P2 + pos) * C2 + col, m > 0.0f ? v : 0.0f);
     }
 };
 
@@ -662,9 +683,10 @@ struct Conv3DgradJob {
         const int u0 = max(0, y - (H3 - 1)), u1 = min(K3 - 1, y);
         const int v0 = max(0, x - (H3 - 1)), v1 = min(K3 - 1, x);
         const int nv = v1 - v0 + 1, taps = (u1 - u0 + 1) * nv;
-        Conv3DgradA<KP> la{dz3 + rows * FLAT, n, b0, y, x, u0, v0, nv, plane * FLAT};
+        using G = GradT<BF, KP>;
+        Conv3DgradA<KP, G> la{(const G*)dz3 + rows * FLAT, n, b0, y, x, u0, v0, nv, plane * FLAT};
         Conv3DgradB lb{w3d.p[g], u0, v0, nv};
-        Conv3DgradStore epi{dz2 + (part * plane + rows) * P2 * C2, h2 + rows * P2 * C2, n, b0, pos};
+        Conv3DgradStore<G> epi{(G*)dz2 + (part * plane + rows) * P2 * C2, h2 + rows * P2 * C2, n, b0, pos};
         mfma_gemm<64, 64, 2, KMAJ, KMAJ, PA, PB>(smem, part * 2 * taps / KP, (part + 1) * 2 * taps / KP,
                                                  la, lb, epi);
     }
@@ -676,11 +698,11 @@ struct Conv3DgradJob {
 // reduction over the n*49 output pixels, split across workgroups.
 // partial[s][o][tap*64 + c].
 // ---------------------------------------------------------------------------
-template <int KP>
+template <int KP, class T>
 struct Conv3WgradA {  // RMAJ quads dz3[b][p][o0..o0+3] at one output pixel m = (b, p)
-    const float* dz3;
+    const T* dz3;
     int npix;
-    int64_t ps;  // KP planes of dz3, ps floats apart
+    int64_t ps;  // KP planes of dz3, ps elements apart
     int o0[MAXQ], kk[MAXQ];
     __device__ void init(int j, int row, int k) { o0[j] = row; kk[j] = k; }
     __device__ f32x4 load(int kc, int j) const {
@@ -723,7 +745,8 @@ struct Conv3WgradJob {
         const int npix = n * P3, nchunks = (npix + BK - 1) / BK;
         const int64_t rows = (int64_t)g * n;
         const int ks = s - g * splits;
-        Conv3WgradA<KP> la{dz3 + rows * FLAT, npix, (int64_t)groups * n * FLAT};
+        using G = GradT<BF, KP>;
+        Conv3WgradA<KP, G> la{(const G*)dz3 + rows * FLAT, npix, (int64_t)groups * n * FLAT};
         Conv3WgradB lb{h2 + rows * P2 * C2, npix, tap};
         PartialEpi epi{partial + (int64_t)s * C3 * 9 * C2, 9 * C2, tap * C2, 1.0f};
         float* rs = tap == 0 ? bias_part + (int64_t)s * 64 : nullptr;
@@ -778,12 +801,12 @@ int launch_conv3_backward(const float* dz3, const GroupPtrs& w3d, int groups, co
 // for every row and column and are skipped.  Reduction (valid tap, o) in
 // chunks of 32 o; dz1 = dh1 * [h1 > 0].
 // ---------------------------------------------------------------------------
-template <int KP>
+template <int KP, class T>
 struct Conv2DgradA {  // KMAJ quads dz2[b][i][j][o..o+3]
-    const float* dz2;
+    const T* dz2;
     int n, b0, yy, xx, du0, dv0, ndv;
-    int64_t ps;  // KP planes of dz2, ps floats apart
-    const float* base[MAXQ];
+    int64_t ps;  // KP planes of dz2, ps elements apart
+    const T* base[MAXQ];
     __device__ void init(int j, int row, int k) {
         const int b = b0 + row;
         base[j] = dz2 + (int64_t)(b < n ? b : 0) * P2 * C2 + k;  // rows past n: never stored
@@ -803,9 +826,13 @@ struct Conv2DgradB {  // w2p[(du,dv)][phase][c][o], rows (phase, c), quads along
         return ld4(base[j] + tp * 4 * C1 * C2 + (kc & 1) * BK);
     }
 };
+// bf16 steps store dz1 rounded to bf16 (the precision the conv1 weight
+// gradient multiplies it in), half the bytes of the fp32 steps' dz1.
+template <int BF>
 struct Conv2DgradStore {
     static constexpr bool MASK = true;
-    float* dz1;
+    using T = std::conditional_t<BF == 1, uint16_t, float>;
+    T* dz1;
     const float* h1;
     int n, b0, yy, xx, c0;  // c0: the tile's first column (phase, c)
     __device__ int64_t at(int b, int col) const {
@@ -820,7 +847,9 @@ struct Conv2DgradStore {
     __device__ void operator()(int row, int col, float v, float m) const {
         const int b = b0 + row;
         if (b >= n) return;
-        dz1[at(b, col)] = m > 0.0f ? v : 0.0f;
+        const float r = m > 0.0f ? v : 0.0f;
+        if constexpr (BF == 1) dz1[at(b, col)] = __builtin_bit_cast(uint16_t, (__bf16)r);
+        else dz1[at(b, col)] = r;
     }
 };
 
@@ -853,10 +882,12 @@ struct Conv2DgradJob {
         const int du0 = max(0, yy - (H2 - 1)), du1 = min(1, yy);
         const int dv0 = max(0, xx - (H2 - 1)), dv1 = min(1, xx);
         const int ndv = dv1 - dv0 + 1, taps = (du1 - du0 + 1) * ndv;
-        Conv2DgradA<KP> la{dz2 + rows * P2 * C2, n, b0, yy, xx, du0, dv0, ndv,
-                           (int64_t)groups * n * P2 * C2};
+        using G = GradT<BF, KP>;
+        Conv2DgradA<KP, G> la{(const G*)dz2 + rows * P2 * C2, n, b0, yy, xx, du0, dv0, ndv,
+                              (int64_t)groups * n * P2 * C2};
         Conv2DgradB lb{w2p.p[g] + ct * BN * C2, du0, dv0, ndv};
-        Conv2DgradStore epi{dz1 + rows * P1 * C1, h1 + rows * P1 * C1, n, b0, yy, xx, ct * BN};
+        Conv2DgradStore<BF> epi{(typename Conv2DgradStore<BF>::T*)dz1 + rows * P1 * C1, h1 + rows * P1 * C1,
+                                n, b0, yy, xx, ct * BN};
         mfma_gemm<64, BN, 2, KMAJ, KMAJ, PA, PB>(smem, 0, 2 * taps, la, lb, epi);
     }
 };
@@ -866,11 +897,11 @@ struct Conv2DgradJob {
 // rows o (64), cols (tap, c) with two taps per 64-column tile, reduction over
 // the n*81 output pixels split across workgroups.  partial[s][o][tap*32 + c].
 // ---------------------------------------------------------------------------
-template <int KP>
+template <int KP, class T>
 struct Conv2WgradA {  // dz2 quads along o at one pixel
-    const float* dz2;
+    const T* dz2;
     int npix;
-    int64_t ps;  // KP planes of dz2, ps floats apart
+    int64_t ps;  // KP planes of dz2, ps elements apart
     int o0[MAXQ], kk[MAXQ];
     __device__ void init(int j, int row, int k) { o0[j] = row; kk[j] = k; }
     __device__ f32x4 load(int kc, int j) const {
@@ -916,7 +947,8 @@ struct Conv2WgradJob {
         const int npix = n * P2, nchunks = (npix + BK - 1) / BK;
         const int64_t rows = (int64_t)g * n;
         const int ks = s - g * splits;
-        Conv2WgradA<KP> la{dz2 + rows * P2 * C2, npix, (int64_t)groups * n * P2 * C2};
+        using G = GradT<BF, KP>;
+        Conv2WgradA<KP, G> la{(const G*)dz2 + rows * P2 * C2, npix, (int64_t)groups * n * P2 * C2};
         Conv2WgradB lb{h1 + rows * P1 * C1, npix, tap0};
         PartialEpi epi{partial + (int64_t)s * C2 * 16 * C1, 16 * C1, tap0 * C1, 1.0f};
         float* rs = tap0 == 0 ? bias_part + (int64_t)s * 64 : nullptr;
