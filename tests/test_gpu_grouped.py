@@ -134,10 +134,13 @@ def test_grouped_ragged_mixed_dtypes(torch_cuda, g, oracle_mod):
     ctx.close()
 
 
-@pytest.mark.parametrize("G,b,A,clip", [(3, 37, 7, 0.5), (1, 100, 4, 1.0)])
+@pytest.mark.parametrize("G,b,A,clip", [(3, 37, 7, 0.5), (1, 100, 4, 1.0), (2, 24, 5, 1.0),
+                                          (5, 53, 6, 1.0)])
 def test_grouped_all_bf16_ragged(torch_cuda, g, oracle_mod, G, b, A, clip):
     """All-bf16 steps (bf16 MFMA operands) at ragged batch sizes: partial
-    row tiles, one group on its own."""
+    row tiles, one group on its own; 48 learner rows cut the fc1 and conv3
+    data-gradient reductions into four parts (fp32 partial planes), 265 rows
+    into none (gradients handed on as bf16)."""
     torch = torch_cuda
     pool = b + b // 2 + 8
     _say(f"grouped all-bf16 G={G} b={b} A={A}")
