@@ -109,11 +109,21 @@ def test_learner_step_as_benchmarked(torch_cuda, g, ctx, oracle_mod, workload):
     # 774 conv3 tiles and 784 fc1 backward tiles: both launches run their last
     # tiles as reduction pieces on 256 compute units, the last conv3 tile ragged
     (505, 6, 1.0, 0.01),
+    # four times the benchmarked batch, ragged: several rounds of whole tiles
+    # in every launch, 256 conv1 weight-gradient splits
+    (2000, 18, 1.0, 0.01),
 ])
 def test_learner_step_ragged_and_degenerate(torch_cuda, g, ctx, oracle_mod, B, A, clip, term_p):
     _say(f"learner ragged B={B} A={A} clip={clip} term_p={term_p}")
     inp = datagen.learner_inputs(7100 + B, B, A, term_p=term_p)
-    _learner_case(torch_cuda, g, ctx, oracle_mod, inp, clip)
+    if B <= 512:
+        _learner_case(torch_cuda, g, ctx, oracle_mod, inp, clip)
+        return
+    big = g.Context(max_batch=B, n_actions=A)
+    try:
+        _learner_case(torch_cuda, g, big, oracle_mod, inp, clip)
+    finally:
+        big.close()
 
 
 def test_learner_step_row_indices(torch_cuda, g, ctx, oracle_mod):
