@@ -170,12 +170,13 @@ void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int gr
 // row 4 i + u for the group's pixels j, so each input row is staged by phase:
 // xs[c][r][m][s][q] = byte 4 (q + s) + m, and a lane's eight bytes are eight
 // consecutive entries.  Entries q >= 20 are used only by the padding pixels
-// j = 20 .. 23 and hold zeros (written once), so those pixels' dz1 values,
-// loaded from a clamped in-row address, need no masking.  The next unit's dz1
-// values and bytes are fetched into registers during the products; a frame
-// pointer is loaded one unit before the fetch that uses it, and a null
-// (zero-filled) frame is read from a frame of zeros.  db1 is summed from the
-// dz1 values as loaded (by the waves of channel pair 0).  At the end the four
+// j = 20 .. 23 and hold zeros (written once), so those pixels' dz1 operands
+// (pixels 16 .. 19 read again) need no masking.  The next unit's dz1 values
+// and bytes are fetched into registers during the products; the frame
+// pointers (wave-uniform, scalar loads) one unit before the fetch that uses
+// them, and a null (zero-filled) frame is read from a frame of zeros.  db1 is
+// summed from the dz1 values as loaded (by the waves of channel pair 0).  At
+// the end the four
 // waves of each channel pair are added in a fixed order in LDS and one
 // partial [32][256] per workgroup is written.
 constexpr int C1W_UR = 2;                       // output rows per unit
@@ -189,13 +190,13 @@ constexpr int C1W_QS = 28;
 constexpr int C1W_XR = S1 * (C1W_UR - 1) + K1;  // 12 input rows per unit
 constexpr int C1W_CPW = 2;                      // input channels per wave
 constexpr int C1W_WAVES = 8;                    // per workgroup: 4 per channel pair
-constexpr int C1W_TASKS = C1W_CPW * C1W_XR * (C1W_QR / 2);  // 240 staging tasks per unit
-constexpr int C1W_TPL = (C1W_TASKS + 63) / 64;  // 4 per lane (the last on 48 lanes)
+constexpr int C1W_TASKS = C1W_XR * (C1W_QR / 2);  // 120 staging tasks per channel and unit
 constexpr int C1W_WGS = 256;                    // workgroups: one per CU
 
 struct C1wStage {
     __bf16 x[C1W_CPW][C1W_XR][4][2][C1W_QS];  // [c][r][m][s][q], q < 24 used; 10.5 KB
 };
+constexpr int C1W_CH = C1W_XR * 4 * 2 * C1W_QS;  // stage elements per channel
 constexpr int C1W_RED = 2 * C1 * 256;  // floats: two [32][256] reduction planes
 constexpr size_t C1W_SMEM = C1W_WAVES * sizeof(C1wStage) > 4 * C1W_RED
                                 ? C1W_WAVES * sizeof(C1wStage) : 4 * C1W_RED;
@@ -235,68 +236,77 @@ __global__ __launch_bounds__(64 * C1W_WAVES) void conv1_wgrad_mfma16_kernel(
         xs[line * C1W_QS + q] = (__bf16)0.0f;
     }
 
-    // staging tasks of this lane: task t = lane + 64 k is (c, r, qp) in
-    // row-major order, so neighbouring lanes read neighbouring dwords
-    int toff[C1W_TPL];  // byte offset of dword 2 qp within the frame, relative to row 4 i0
-    int tlds[C1W_TPL];  // element offset of [c][r][0][0][2 qp] in the stage
-    int tch[C1W_TPL];
+    // Staging slots: slot k of this lane is (c, r, qp) = (k / 2, rq / 10,
+    // rq % 10) with rq = lane + 64 (k % 2), so a slot's bytes come from one
+    // frame for the whole wave (channel 2 p + c); rq >= 120 (lanes 56..63 of
+    // the odd slots) repeat task 119: the same bytes to the same place.
+    uint32_t toff[2];  // byte offset of dword 2 qp of row r, relative to row 4 i0
+    int tlds[2];       // element offset of [0][r][0][0][2 qp] in the stage
 #pragma unroll
-    for (int k = 0; k < C1W_TPL; ++k) {
-        const int t = min(lane + 64 * k, C1W_TASKS - 1);
-        const int c = t / (C1W_XR * C1W_QR / 2), rq = t - c * (C1W_XR * C1W_QR / 2);
+    for (int k = 0; k < 2; ++k) {
+        const int rq = min(lane + 64 * k, C1W_TASKS - 1);
         const int r = rq / (C1W_QR / 2), qp = rq - r * (C1W_QR / 2);
-        tch[k] = c;
-        toff[k] = r * IN_W + 8 * qp;
-        tlds[k] = ((c * C1W_XR + r) * 4) * 2 * C1W_QS + 2 * qp;
+        toff[k] = (uint32_t)(r * IN_W + 8 * qp);
+        tlds[k] = (r * 4) * 2 * C1W_QS + 2 * qp;
     }
-    const C1wDz<WP>* dzg = dz1 + (int64_t)g * n * P1 * C1;
+    // dz1 byte offsets (relative to the unit's first pixel) of this lane's
+    // eight pixels in step st: pixel p0 + t, where (ir, j0) is the lane half's
+    // pixel group; a group with j0 = 16 has padding pixels t >= 4, which read
+    // pixels 16..19 again (finite values that meet zero bytes).
+    using T = C1wDz<WP>;
+    uint32_t dlo[3], dhi[3];
+#pragma unroll
+    for (int st = 0; st < 3; ++st) {
+        const int grp = 2 * st + h, ir = grp / 3, j0 = 8 * (grp % 3);
+        const int p0 = ir * H1 + j0;
+        dlo[st] = (uint32_t)((p0 * C1 + o) * sizeof(T));
+        dhi[st] = (uint32_t)(((j0 + 8 > H1 ? p0 : p0 + 4) * C1 + o) * sizeof(T));
+    }
+    const T* dzg = dz1 + (int64_t)g * n * P1 * C1;
 
-    float av[3][8];            // dz1 of the next unit's three steps (this lane's pixels)
-    uint32_t xw[C1W_TPL][3];   // three input dwords per staging task of the next unit
-    uint64_t fptr = 0;         // lane l: channel 2 p + l % 2 of the next fetch's sample
+    float av[3][8];          // dz1 of a unit's three steps (this lane's pixels)
+    uint32_t xw[4][3];       // three input dwords per staging slot of the next unit
+    const uint8_t* fnext[C1W_CPW];  // wave-uniform: frames 2 p, 2 p + 1 of the next fetch's sample
     auto load_ptrs = [&](int u) {
         const int b = u / C1W_UNITS;
-        fptr = ((const uint64_t*)ftab)[((int64_t)g * n + b) * 4 + C1W_CPW * cp + (lane & 1)];
+        const uint8_t* const* fp = ftab + ((int64_t)g * n + b) * IN_C + C1W_CPW * cp;
+#pragma unroll
+        for (int c = 0; c < C1W_CPW; ++c) fnext[c] = fp[c];
     };
-    auto fetch = [&](int u) {
+    auto fetch_dz = [&](int u, int st) {
         const int b = u / C1W_UNITS, i0 = (u - b * C1W_UNITS) * C1W_UR;
-        const C1wDz<WP>* dsrc = dzg + ((int64_t)b * P1 + i0 * H1) * C1 + o;
+        const char* d = (const char*)(dzg + ((int64_t)b * P1 + i0 * H1) * C1);  // wave-uniform
 #pragma unroll
-        for (int st = 0; st < 3; ++st) {
-            const int grp = 2 * st + h, ir = grp / 3, j0 = 8 * (grp % 3);
-#pragma unroll
-            for (int t = 0; t < 8; ++t)  // j >= 20: a padding pixel (address clamped)
-                av[st][t] = c1w_value(dsrc[(ir * H1 + min(j0 + t, H1 - 1)) * C1]);
+        for (int t = 0; t < 4; ++t) {
+            av[st][t] = c1w_value(*(const T*)(d + dlo[st] + t * C1 * sizeof(T)));
+            av[st][t + 4] = c1w_value(*(const T*)(d + dhi[st] + t * C1 * sizeof(T)));
         }
-        auto lane_ptr = [&](int l) {
-            const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)fptr, l);
-            const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(fptr >> 32), l);
-            const uint8_t* f = (const uint8_t*)(((uint64_t)hi << 32) | lo);
-            return f ? f + S1 * i0 * IN_W : zero_frame;
-        };
-        const uint8_t* f0 = lane_ptr(0);
-        const uint8_t* f1 = lane_ptr(1);
-        if (u + 1 < u1) load_ptrs(u + 1);
+    };
+    auto fetch_bytes = [&](int u) {
+        const int i0 = (u % C1W_UNITS) * C1W_UR;
+        const uint8_t* fr[C1W_CPW];
 #pragma unroll
-        for (int k = 0; k < C1W_TPL; ++k) {
-            const uint8_t* base = (tch[k] == 0 ? f0 : f1) + toff[k];
+        for (int c = 0; c < C1W_CPW; ++c) fr[c] = fnext[c] ? fnext[c] + S1 * i0 * IN_W : zero_frame;
+        load_ptrs(min(u + 1, u1 - 1));
 #pragma unroll
-            for (int d = 0; d < 3; ++d) xw[k][d] = ldg_u32(base + 4 * d);  // dwords <= 20: in the row
-        }
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int dd = 0; dd < 3; ++dd)  // dwords <= 20: in the row
+                xw[k][dd] = ldg_u32(fr[k >> 1] + toff[k & 1] + 4 * dd);
     };
     auto stage = [&]() {
 #pragma unroll
-        for (int k = 0; k < C1W_TPL; ++k) {
-            if (k + 1 == C1W_TPL && lane + 64 * k >= C1W_TASKS) break;  // the last task's spare lanes
+        for (int k = 0; k < 4; ++k) {
             const uint32_t w0 = xw[k][0], w1 = xw[k][1], w2 = xw[k][2];
+            __bf16* dst = xs + (k >> 1) * C1W_CH + tlds[k & 1];
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
                 const __bf16 b0 = (__bf16)(float)((w0 >> (8 * m)) & 255u);
                 const __bf16 b1 = (__bf16)(float)((w1 >> (8 * m)) & 255u);
                 const __bf16 b2 = (__bf16)(float)((w2 >> (8 * m)) & 255u);
                 // s = 0: entries q, q + 1 (bytes of dwords q, q + 1); s = 1: bytes of q + 1, q + 2
-                *(bf16x2*)(xs + tlds[k] + (2 * m) * C1W_QS) = bf16x2{b0, b1};
-                *(bf16x2*)(xs + tlds[k] + (2 * m + 1) * C1W_QS) = bf16x2{b1, b2};
+                *(bf16x2*)(dst + (2 * m) * C1W_QS) = bf16x2{b0, b1};
+                *(bf16x2*)(dst + (2 * m + 1) * C1W_QS) = bf16x2{b1, b2};
             }
         }
     };
@@ -306,54 +316,95 @@ __global__ __launch_bounds__(64 * C1W_WAVES) void conv1_wgrad_mfma16_kernel(
     for (int t = 0; t < 4; ++t) acc[t] = f32x16{};
     float bsum = 0.0f;
     const int col = lane & 31, uu = col >> 2, mm = col & 3;
-    if (u0 < u1) {
-        load_ptrs(u0);
-        fetch(u0);
-    }
-    for (int u = u0; u < u1; ++u) {
-        float cur[3][8];
+
+    // One MFMA step: the operands of its four column tiles from the stage,
+    // and the planes of its eight dz1 values (summed into db1 on the way:
+    // real pixels only; j0 is 0, 8 or 16).
+    auto read_bx = [&](int st, bf16x8 (&bx)[4]) {
+        const int grp = 2 * st + h, ir = grp / 3, j0 = 8 * (grp % 3);
 #pragma unroll
-        for (int st = 0; st < 3; ++st)
+        for (int t = 0; t < 4; ++t)
+            bx[t] = *(const bf16x8*)&sg.x[t >> 1][S1 * ir + uu][mm][t & 1][j0];
+    };
+    // planes of the eight values, two at a time: a packed round to bf16, the
+    // two rounded values widened back, the exact remainders
+    auto planes = [&](int st, bf16x8 (&a)[WP]) {
+        const int j0 = 8 * ((2 * st + h) % 3);
 #pragma unroll
-            for (int t = 0; t < 8; ++t) cur[st][t] = av[st][t];
-        stage();  // the previous unit's LDS reads were all waited for by its products
-        if (u + 1 < u1) fetch(u + 1);  // in flight during the products
-#pragma unroll
-        for (int st = 0; st < 3; ++st) {
-            const int grp = 2 * st + h, ir = grp / 3, j0 = 8 * (grp % 3);
-            // every tile's operand first, so the products below run back to back
-            bf16x8 bx[4];
-#pragma unroll
-            for (int t = 0; t < 4; ++t)
-                bx[t] = *(const bf16x8*)&sg.x[t >> 1][S1 * ir + uu][mm][t & 1][j0];
-            // planes of the eight values, two at a time: a packed round to
-            // bf16, the two rounded values widened back, the exact remainders
-            bf16x8 a[WP];
-#pragma unroll
-            for (int t = 0; t < 8; t += 2) {
-                float v0 = cur[st][t], v1 = cur[st][t + 1];
-                if (t < 4 || j0 + t < H1) {  // db1: real pixels only (j0 is 0, 8 or 16)
-                    bsum += v0;
-                    bsum += v1;
-                }
-#pragma unroll
-                for (int pl = 0; pl < WP; ++pl) {
-                    const bf16x2 hp = __builtin_convertvector(f32x2{v0, v1}, bf16x2);
-                    a[pl][t] = hp[0];
-                    a[pl][t + 1] = hp[1];
-                    if (pl + 1 < WP) {
-                        const uint32_t bits = __builtin_bit_cast(uint32_t, hp);
-                        v0 -= __uint_as_float(bits << 16);
-                        v1 -= __uint_as_float(bits & 0xffff0000u);
-                    }
-                }
+        for (int t = 0; t < 8; t += 2) {
+            float v0 = av[st][t], v1 = av[st][t + 1];
+            if (t < 4 || j0 + t < H1) {
+                bsum += v0;
+                bsum += v1;
             }
 #pragma unroll
-            for (int pl = 0; pl < WP; ++pl)
-#pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[pl], bx[t], acc[t], 0, 0, 0);
+            for (int pl = 0; pl < WP; ++pl) {
+                const bf16x2 hp = __builtin_convertvector(f32x2{v0, v1}, bf16x2);
+                a[pl][t] = hp[0];
+                a[pl][t + 1] = hp[1];
+                if (pl + 1 < WP) {
+                    const uint32_t bits = __builtin_bit_cast(uint32_t, hp);
+                    v0 -= __uint_as_float(bits << 16);
+                    v1 -= __uint_as_float(bits & 0xffff0000u);
+                }
+            }
         }
+    };
+    auto products = [&](const bf16x8 (&a)[WP], const bf16x8 (&bx)[4]) {
+#pragma unroll
+        for (int pl = 0; pl < WP; ++pl)
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[pl], bx[t], acc[t], 0, 0, 0);
+    };
+
+    // Software pipeline over the steps: while a step's products run, the next
+    // step's operands are read and its planes split, and each dz1 register is
+    // refilled with the next unit's value right after its split (one set of
+    // dz1 registers, no copies).  Unit u enters with its step 0 operands and
+    // planes ready and leaves with unit u + 1's; the next unit's bytes are
+    // staged beside the last step's products, after every operand read of
+    // this unit (LDS serves a wave in order).  Fetches past the wave's last
+    // unit read that unit again (in bounds, unused).
+    if (u0 < u1) {
+        const int last = u1 - 1;
+        load_ptrs(u0);
+#pragma unroll
+        for (int st = 0; st < 3; ++st) fetch_dz(u0, st);
+        fetch_bytes(u0);
+        stage();
+        fetch_bytes(min(u0 + 1, last));
+        bf16x8 a0[WP], b0[4], a1[WP], b1[4];  // planes and operands of two steps
+        read_bx(0, b0);
+        planes(0, a0);
+        fetch_dz(min(u0 + 1, last), 0);
+        // Each region between scheduling barriers runs one step's products
+        // beside the next step's operand reads and split; the refills close
+        // their region, so they are issued as early as their registers allow.
+        auto unit = [&](int u, auto more) {
+            constexpr bool MORE = decltype(more)::value;
+            products(a0, b0);
+            read_bx(1, b1);
+            planes(1, a1);
+            fetch_dz(min(u + 1, last), 1);
+            __builtin_amdgcn_sched_barrier(0);
+            products(a1, b1);
+            read_bx(2, b0);
+            planes(2, a0);
+            fetch_dz(min(u + 1, last), 2);
+            __builtin_amdgcn_sched_barrier(0);
+            products(a0, b0);
+            if constexpr (MORE) {
+                stage();  // unit u + 1
+                fetch_bytes(min(u + 2, last));
+                read_bx(0, b0);
+                planes(0, a0);
+                fetch_dz(min(u + 2, last), 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+        for (int u = u0; u < last; ++u) unit(u, std::true_type{});
+        unit(last, std::false_type{});
     }
 
     // Add the four waves of each channel pair in LDS: waves 0, 1 of the pair
