@@ -158,13 +158,13 @@ void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int gr
 //
 // Work is cut into units of two output rows of one sample (40 pixels, padded
 // to 2 x 24 = 6 groups of 8); an MFMA step takes two groups (lane half h:
-// group 2 step + h), so a unit is three steps.  A workgroup has eight waves:
-// waves 4 p .. 4 p + 3 own input channels 2 p, 2 p + 1 (four column tiles of
-// 32), and each of the four walks its own contiguous range of the workgroup's
-// units with a private LDS stage, with no workgroup barrier until the end.  A
-// wave splits the dz1 values of its units into planes in registers, straight
-// from their coalesced loads (lane o, h: eight pixels of channel o), and
-// multiplies them into its four tiles.  Column tile t is (c = 2 p + t / 2,
+// group 2 step + h), so a unit is three steps.  Workgroups come in pairs that
+// share a range of units, one per channel pair p (input channels 2 p, 2 p + 1:
+// four column tiles of 32); each of a workgroup's eight waves walks its own
+// contiguous part of the range with a private LDS stage, with no workgroup
+// barrier until the end.  A wave splits the dz1 values of its units into
+// planes in registers, straight from their coalesced loads (lane o, h: eight
+// pixels of channel o), and multiplies them into its four tiles.  Column tile t is (c = 2 p + t / 2,
 // s = t % 2) and lane column l % 32 is (u, m) = ((l % 32) / 4, l % 4), i.e.
 // v = 4 s + m; its eight operands are the bytes at x = 4 (j + s) + m of input
 // row 4 i + u for the group's pixels j, so each input row is staged by phase:
@@ -175,10 +175,9 @@ void launch_conv1_fwd(const uint8_t* const* ftab, const GroupPtrs& theta, int gr
 // and bytes are fetched into registers during the products; the frame
 // pointers (wave-uniform, scalar loads) one unit before the fetch that uses
 // them, and a null (zero-filled) frame is read from a frame of zeros.  db1 is
-// summed from the dz1 values as loaded (by the waves of channel pair 0).  At
-// the end the four
-// waves of each channel pair are added in a fixed order in LDS and one
-// partial [32][256] per workgroup is written.
+// summed from the dz1 values as loaded (kept by the workgroup of channel pair
+// 0).  At the end the eight waves are added in a fixed order in LDS and each
+// workgroup writes its channel pair's half of one partial [32][256].
 constexpr int C1W_UR = 2;                       // output rows per unit
 constexpr int C1W_UNITS = H1 / C1W_UR;          // 10 units per sample
 constexpr int C1W_Q = 24;                       // phase entries per staged row (pixels padded to 24)
@@ -189,7 +188,7 @@ constexpr int C1W_QR = 20;                      // entries that can be non-zero 
 constexpr int C1W_QS = 28;
 constexpr int C1W_XR = S1 * (C1W_UR - 1) + K1;  // 12 input rows per unit
 constexpr int C1W_CPW = 2;                      // input channels per wave
-constexpr int C1W_WAVES = 8;                    // per workgroup: 4 per channel pair
+constexpr int C1W_WAVES = 8;                    // per workgroup, all on one channel pair
 constexpr int C1W_TASKS = C1W_XR * (C1W_QR / 2);  // 120 staging tasks per channel and unit
 constexpr int C1W_WGS = 256;                    // workgroups: one per CU
 
@@ -197,9 +196,9 @@ struct C1wStage {
     __bf16 x[C1W_CPW][C1W_XR][4][2][C1W_QS];  // [c][r][m][s][q], q < 24 used; 10.5 KB
 };
 constexpr int C1W_CH = C1W_XR * 4 * 2 * C1W_QS;  // stage elements per channel
-constexpr int C1W_RED = 2 * C1 * 256;  // floats: two [32][256] reduction planes
-constexpr size_t C1W_SMEM = C1W_WAVES * sizeof(C1wStage) > 4 * C1W_RED
-                                ? C1W_WAVES * sizeof(C1wStage) : 4 * C1W_RED;
+constexpr int C1W_PLANE = 4 * 16 * 64;  // floats: one wave's accumulators
+constexpr size_t C1W_SMEM = C1W_WAVES * sizeof(C1wStage) > 4 * C1W_WAVES * C1W_PLANE
+                                ? C1W_WAVES * sizeof(C1wStage) : 4 * C1W_WAVES * C1W_PLANE;
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
@@ -217,17 +216,18 @@ __global__ __launch_bounds__(64 * C1W_WAVES) void conv1_wgrad_mfma16_kernel(
     const uint8_t* __restrict__ zero_frame, int n, float* __restrict__ partial,
     float* __restrict__ bias_part) {
     __shared__ __attribute__((aligned(16))) char smem[C1W_SMEM];
-    __shared__ float bred[4][2][C1];
-    const int g = blockIdx.y, S = gridDim.x, x = blockIdx.x;
+    __shared__ float bred[C1W_WAVES][2][C1];
+    const int g = blockIdx.y, SP = gridDim.x >> 1;
+    const int cp = blockIdx.x & 1, xp = blockIdx.x >> 1;  // channel pair, workgroup pair
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar unit walk
-    const int cp = wave >> 2, wq = wave & 3;                    // channel pair, wave within it
     const int h = lane >> 5, o = lane & 31;
     C1wStage& sg = ((C1wStage*)smem)[wave];
     __bf16* xs = &sg.x[0][0][0][0][0];
 
-    // this wave's units: a contiguous share of the workgroup's share
-    const int64_t U = (int64_t)n * C1W_UNITS, W = (int64_t)S * 4, wi = (int64_t)x * 4 + wq;
+    // this wave's units: a contiguous share of the workgroup pair's share
+    const int64_t U = (int64_t)n * C1W_UNITS, W = (int64_t)SP * C1W_WAVES;
+    const int64_t wi = (int64_t)xp * C1W_WAVES + wave;
     const int u0 = (int)(wi * U / W), u1 = (int)((wi + 1) * U / W);
 
     // entries q >= 20 of every staged line stay zero
@@ -407,41 +407,36 @@ __global__ __launch_bounds__(64 * C1W_WAVES) void conv1_wgrad_mfma16_kernel(
         unit(last, std::false_type{});
     }
 
-    // Add the four waves of each channel pair in LDS: waves 0, 1 of the pair
-    // store to planes 0, 1, waves 2, 3 add theirs, then the workgroup writes
-    // (w0 + w2) + (w1 + w3).
+    // Add the eight waves in LDS: each stores its accumulators as one plane
+    // laid out [tile][register][lane] (every store 64 consecutive floats),
+    // then each thread sums one quad of four columns over the planes in a
+    // fixed order and writes it; the two workgroups of a pair write the two
+    // column halves of one partial [32][256].
     __syncthreads();  // every wave is done with its stage
     float* red = (float*)smem;
-    auto at = [&](int t, int r) {  // element (o, n) of accumulator t, register r
-        const int row = 8 * (r >> 2) + 4 * h + (r & 3);
-        const int c = C1W_CPW * cp + (t >> 1), s = t & 1, v = 4 * s + mm;
-        return row * 256 + c * 64 + uu * 8 + v;
-    };
-    if (wq < 2) {
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
+    for (int t = 0; t < 4; ++t)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) red[wq * C1 * 256 + at(t, r)] = acc[t][r];
-    }
-    if (cp == 0) bred[wq][h][o] = bsum;
+        for (int r = 0; r < 16; ++r) red[wave * C1W_PLANE + (t * 16 + r) * 64 + lane] = acc[t][r];
+    bred[wave][h][o] = bsum;
     __syncthreads();
-    if (wq >= 2) {
+    const int split = g * SP + xp;
+    float* out = partial + (int64_t)split * C1 * 256 + cp * 128;
+    for (int e = tid; e < C1 * 128 / 4; e += 64 * C1W_WAVES) {
+        // quad e: row (filter o), column tile c of the pair, quad q = (u, s);
+        // register r and lane half of that row in the accumulator layout
+        const int row = e >> 5, c = (e >> 4) & 1, q = e & 15, ue = q >> 1, s = q & 1;
+        const int r = 4 * (row >> 3) + (row & 3), hh = (row >> 2) & 1;
+        const int off = ((2 * c + s) * 16 + r) * 64 + hh * 32 + ue * 4;
+        f32x4 sum = *(const f32x4*)(red + off);
 #pragma unroll
-        for (int t = 0; t < 4; ++t)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) red[(wq - 2) * C1 * 256 + at(t, r)] += acc[t][r];
+        for (int w = 1; w < C1W_WAVES; ++w) sum += *(const f32x4*)(red + w * C1W_PLANE + off);
+        *(f32x4*)(out + row * 256 + c * 64 + ue * 8 + 4 * s) = sum * (1.0f / 255.0f);
     }
-    __syncthreads();
-    const int split = g * S + x;
-    float* out = partial + (int64_t)split * C1 * 256;
-    for (int e = tid; e < C1 * 256 / 4; e += 64 * C1W_WAVES) {
-        const f32x4 p0 = *(const f32x4*)(red + 4 * e), p1 = *(const f32x4*)(red + C1 * 256 + 4 * e);
-        *(f32x4*)(out + 4 * e) = (p0 + p1) * (1.0f / 255.0f);
-    }
-    if (tid < C1) {
+    if (cp == 0 && tid < C1) {
         float t = 0.0f;
 #pragma unroll
-        for (int w = 0; w < 4; ++w) t += bred[w][0][tid] + bred[w][1][tid];
+        for (int w = 0; w < C1W_WAVES; ++w) t += bred[w][0][tid] + bred[w][1][tid];
         bias_part[(int64_t)split * 64 + tid] = t;
     }
 }
@@ -453,16 +448,17 @@ void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, const uint
         *splits_out = 0;
         return;
     }
-    // splits per group: one workgroup per CU in all, each of whose four waves
-    // per channel pair gets at least one unit; groups * splits stays within
-    // max_splits
-    const int splits = max(1, min((n * C1W_UNITS + 3) / 4, min(C1W_WGS, max_splits) / groups));
+    // workgroup pairs (one workgroup per channel pair) per group: one
+    // workgroup per CU in all, each of whose waves gets at least one unit;
+    // groups * pairs stays within max_splits (a pair writes one partial)
+    const int splits = max(1, min((n * C1W_UNITS + C1W_WAVES - 1) / C1W_WAVES,
+                                  min(C1W_WGS / 2, max_splits) / groups));
     *splits_out = splits;
     if (bf16)
-        conv1_wgrad_mfma16_kernel<1><<<dim3(splits, groups), 64 * C1W_WAVES, 0, st>>>(
+        conv1_wgrad_mfma16_kernel<1><<<dim3(2 * splits, groups), 64 * C1W_WAVES, 0, st>>>(
             (const uint16_t*)dz1, ftab, zero_frame, n, partial, bias_part);
     else
-        conv1_wgrad_mfma16_kernel<3><<<dim3(splits, groups), 64 * C1W_WAVES, 0, st>>>(
+        conv1_wgrad_mfma16_kernel<3><<<dim3(2 * splits, groups), 64 * C1W_WAVES, 0, st>>>(
             dz1, ftab, zero_frame, n, partial, bias_part);
 }
 
