@@ -213,12 +213,15 @@ __device__ inline float c1w_value(uint16_t v) { return __uint_as_float((uint32_t
 template <int WP>
 __global__ __launch_bounds__(64 * C1W_WAVES) void conv1_wgrad_mfma16_kernel(
     const C1wDz<WP>* __restrict__ dz1, const uint8_t* const* __restrict__ ftab,
-    const uint8_t* __restrict__ zero_frame, int n, float* __restrict__ partial,
+    const uint8_t* __restrict__ zero_frame, int n, int SP, float* __restrict__ partial,
     float* __restrict__ bias_part) {
     __shared__ __attribute__((aligned(16))) char smem[C1W_SMEM];
     __shared__ float bred[C1W_WAVES][2][C1];
-    const int g = blockIdx.y, SP = gridDim.x >> 1;
-    const int cp = blockIdx.x & 1, xp = blockIdx.x >> 1;  // channel pair, workgroup pair
+    // block b runs on XCD b % 8, so the two workgroups of pair xp (channel
+    // pairs 0 and 1, blocks 8 apart) share an L2 and read dz1 from HBM once
+    const int g = blockIdx.y, b8 = blockIdx.x / NUM_XCD;
+    const int cp = b8 & 1, xp = (b8 >> 1) * NUM_XCD + blockIdx.x % NUM_XCD;  // channel pair, pair
+    if (xp >= SP) return;  // padding of the last group of eight pairs
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar unit walk
     const int h = lane >> 5, o = lane & 31;
@@ -454,12 +457,14 @@ void launch_conv1_wgrad(const float* dz1, const uint8_t* const* ftab, const uint
     const int splits = max(1, min((n * C1W_UNITS + C1W_WAVES - 1) / C1W_WAVES,
                                   min(C1W_WGS / 2, max_splits) / groups));
     *splits_out = splits;
+    // the pairs in groups of eight: 16 blocks each, the kernel's block order
+    const int blocks = 2 * pad_xcd(splits);
     if (bf16)
-        conv1_wgrad_mfma16_kernel<1><<<dim3(2 * splits, groups), 64 * C1W_WAVES, 0, st>>>(
-            (const uint16_t*)dz1, ftab, zero_frame, n, partial, bias_part);
+        conv1_wgrad_mfma16_kernel<1><<<dim3(blocks, groups), 64 * C1W_WAVES, 0, st>>>(
+            (const uint16_t*)dz1, ftab, zero_frame, n, splits, partial, bias_part);
     else
-        conv1_wgrad_mfma16_kernel<3><<<dim3(2 * splits, groups), 64 * C1W_WAVES, 0, st>>>(
-            dz1, ftab, zero_frame, n, partial, bias_part);
+        conv1_wgrad_mfma16_kernel<3><<<dim3(blocks, groups), 64 * C1W_WAVES, 0, st>>>(
+            dz1, ftab, zero_frame, n, splits, partial, bias_part);
 }
 
 }  // namespace gorila
