@@ -110,7 +110,7 @@ def test_learner_step_as_benchmarked(torch_cuda, g, ctx, oracle_mod, workload):
     # tiles as reduction pieces on 256 compute units, the last conv3 tile ragged
     (505, 6, 1.0, 0.01),
     # four times the benchmarked batch, ragged: several rounds of whole tiles
-    # in every launch, 256 conv1 weight-gradient splits
+    # in every launch, 128 conv1 weight-gradient workgroup pairs
     (2000, 18, 1.0, 0.01),
 ])
 def test_learner_step_ragged_and_degenerate(torch_cuda, g, ctx, oracle_mod, B, A, clip, term_p):
