@@ -126,6 +126,37 @@ def test_learner_step_ragged_and_degenerate(torch_cuda, g, ctx, oracle_mod, B, A
         big.close()
 
 
+def test_gradient_is_batch_additive(torch_cuda, g):
+    """At 16 times the benchmarked batch (8192 rows: several rounds of tiles in
+    every launch, every split and reduction at full width) the loss and every
+    gradient tensor of the whole batch are the means of those of its two
+    halves, since the loss is a mean over transitions (eq. (2)).  The property
+    holds at any size, so it needs no oracle run at this one; the halves take
+    other launch shapes and split orders, and a row whose ReLU input sits at a
+    kink may flip between them, hence the 1e-3 per-tensor bar of the oracle
+    comparisons."""
+    torch = torch_cuda
+    B, A = 8192, 6
+    _say(f"batch additivity B={B} A={A}")
+    inp = datagen.learner_inputs(9100, B, A)
+    big = g.Context(max_batch=B, n_actions=A)
+    try:
+        theta, tgt = _dev(torch, inp.theta), _dev(torch, inp.theta_target)
+        rep = _stacked(torch, g, inp)
+        idx = _dev(torch, inp.idx)
+        out = []
+        for part in (idx, idx[: B // 2].contiguous(), idx[B // 2:].contiguous()):
+            grads, loss = g.learner_step(big, theta, tgt, A, rep, part, inp.gamma, 1.0)
+            out.append((grads.cpu().numpy().astype(np.float64), float(loss.cpu()[0])))
+        big.check()
+    finally:
+        big.close()
+    (full, lf), (ga, la), (gb, lb) = out
+    errs = parity.assert_grads_close(full, (ga + gb) / 2, A)
+    _say(f"batch additivity errors {errs}")
+    assert abs(lf - (la + lb) / 2) <= 1e-5 * abs(lf), (lf, la, lb)
+
+
 def test_learner_step_row_indices(torch_cuda, g, ctx, oracle_mod):
     """Minibatch rows picked by idx out of a larger stacked replay, with repeats."""
     _say("learner indexed rows")
